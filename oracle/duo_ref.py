@@ -1,0 +1,384 @@
+"""Float64 reference ("oracle") for DuoGPT's layer-wise calibration solver.
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke entry point and the
+CPU-baseline leg of the benchmark may import this module.  The product path
+(the HIP library and its Python binding) never calls it and shares no code with
+it.
+
+Everything here is plain numpy in float64, written from the DuoGPT paper
+(arXiv 2506.20194) to be checked against the paper by eye:
+
+* activation sparsification, section "Preliminaries / Activation Sparsity";
+* the asymmetric objective and its Lagrangian, section 4.2, Eq. 2;
+* the single-weight closed form (loss and update), Eq. 3, proof in App. A.1;
+* the decomposed score and its a, b, c terms, Eq. 5-7, App. A.2-A.4;
+* Algorithm 1 (blocked column sweep with lazy batch updates).
+
+Notation follows the paper: W is n x k (out x in), the paper's calibration
+matrix X is k x m.  In memory (and in this module) activations are stored
+token-major, m x k, i.e. the transpose of the paper's X.  X_dense is the
+paper's X-tilde (dense stream), Xh is X-hat (the sparsified stream) and
+dX = X_dense - Xh is the paper's Delta X.
+
+Readings taken where the paper is silent or ambiguous (each is listed in the
+design notes of the repository):
+
+R-act   exactly floor(p_x*k + 0.5) activations are zeroed per token, those with
+        the smallest (|x|, channel index) key; -0.0 counts as 0.
+R-damp  lambda = damp * mean(diag(H)) with H = Xh^T Xh undamped; H + lambda*I
+        replaces H everywhere (equivalently, a ridge term lambda*|dw|^2 is
+        added to the layer objective).
+R-mask  the weight mask of each B-column block is chosen globally over the
+        n x B block; the count uses cumulative rounding so that blocks 0..b
+        hold floor(p_w*n*(j0+B_b) + 0.5) zeros in total; ties in the score are
+        broken by (score, column, row) ascending.
+R-lazy  the residual-correction term of the lazy batch update uses the value
+        each column had when it was processed (before it was pruned).  This is
+        the only reading under which the blocked sweep equals the column-by-
+        column (eager) sweep.
+R-sign  the residual is R = W (X_dense - Xh); Eq. 4 prints the opposite sign,
+        which contradicts Eq. 3 and the update rule of Algorithm 1.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "act_zero_count",
+    "sparsify_tokens",
+    "hessian_terms",
+    "inverse_cholesky",
+    "score_terms",
+    "block_prune_counts",
+    "select_block_mask",
+    "sweep_eager",
+    "sweep_blocked",
+    "prune_layer",
+    "objective",
+    "sparsegpt_layer",
+    "magnitude_layer",
+    "obs_closed_form",
+    "obs_bruteforce",
+]
+
+_TOKEN_CHUNK = 8192
+
+
+def _f64(a):
+    return np.asarray(a, dtype=np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Activation sparsification (Preliminaries, "Activation Sparsity")
+# ---------------------------------------------------------------------------
+
+def act_zero_count(k: int, p_x: float) -> int:
+    """Number of activations zeroed per token (reading R-act)."""
+    return int(np.floor(p_x * k + 0.5))
+
+
+def sparsify_tokens(X, p_x: float):
+    """Per-token magnitude sparsification.
+
+    Each token (a column of the paper's X, a row here) keeps all but the
+    ``act_zero_count(k, p_x)`` entries of smallest |x|; equal magnitudes are
+    ordered by channel index, so the lower channel is zeroed first.
+
+    Returns (Xh, keep) with Xh = X * keep, both m x k.
+    """
+    X = _f64(X)
+    m, k = X.shape
+    z = act_zero_count(k, p_x)
+    keep = np.ones((m, k), dtype=bool)
+    if z > 0:
+        for t0 in range(0, m, _TOKEN_CHUNK):
+            t1 = min(m, t0 + _TOKEN_CHUNK)
+            # stable sort: ascending |x|, equal keys stay in channel order
+            order = np.argsort(np.abs(X[t0:t1]), axis=1, kind="stable")
+            rows = np.arange(t1 - t0)[:, None]
+            keep[t0:t1][rows, order[:, :z]] = False
+    return np.where(keep, X, 0.0), keep
+
+
+# ---------------------------------------------------------------------------
+# Hessian and residual terms (Alg. 1 first two lines; Sec. 4.3 "a")
+# ---------------------------------------------------------------------------
+
+def hessian_terms(X_src, p_x: float, X_dense=None):
+    """H = Xh Xh^T, G = dX Xh^T and a = diag(dX dX^T) in the paper's orientation.
+
+    X_src is the stream that gets sparsified (the pruned model's input); X_dense
+    is the dense model's input (defaults to X_src, the single-layer case).
+    All inputs are token-major m x k.  Returns (H, G, a) with H, G k x k.
+    """
+    X_src = _f64(X_src)
+    X_dense = X_src if X_dense is None else _f64(X_dense)
+    m, k = X_src.shape
+    H = np.zeros((k, k))
+    G = np.zeros((k, k))
+    a = np.zeros(k)
+    for t0 in range(0, m, _TOKEN_CHUNK):
+        t1 = min(m, t0 + _TOKEN_CHUNK)
+        Xh, _ = sparsify_tokens(X_src[t0:t1], p_x)
+        dX = X_dense[t0:t1] - Xh
+        H += Xh.T @ Xh          # sum_t xh_t^T xh_t
+        G += dX.T @ Xh          # G[p, q] = sum_t dX[t, p] * Xh[t, q]
+        a += np.sum(dX * dX, axis=0)
+    return H, G, a
+
+
+# ---------------------------------------------------------------------------
+# Damped inverse Cholesky (Sec. 4.3, Alg. 1 "Inverse_Cholesky")
+# ---------------------------------------------------------------------------
+
+def inverse_cholesky(H, damp: float):
+    """L lower-triangular with L L^T = (H + lambda I)^-1, lambda = damp*mean(diag H).
+
+    The plain route: explicit inverse, symmetrised, then a Cholesky
+    factorisation.  Returns (L, lambda).
+    """
+    H = _f64(H)
+    k = H.shape[0]
+    lam = damp * float(np.mean(np.diag(H)))
+    Hl = H + lam * np.eye(k)
+    Hinv = np.linalg.inv(Hl)
+    Hinv = 0.5 * (Hinv + Hinv.T)
+    L = np.linalg.cholesky(Hinv)
+    return L, lam
+
+
+# ---------------------------------------------------------------------------
+# Score factor and residual-update matrix (Eq. 7; App. A.2-A.4)
+# ---------------------------------------------------------------------------
+
+def score_terms(G, L, a):
+    """Precompute of Alg. 1: Q = G L, U = Q * M_u (strictly upper),
+    b = diag(U U^T), c = diag(Q) / diag(L), D = U L^T and the per-column score
+    factor fac = 1/diag(L)^2 + a - b + 2c (Eq. 7), so that S = W^2 * fac.
+
+    Returns (fac, D, (a, b, c)).
+    """
+    G = _f64(G)
+    L = _f64(L)
+    a = _f64(a)
+    Q = G @ L
+    U = np.triu(Q, 1)
+    b = np.sum(U * U, axis=1)
+    dL = np.diag(L)
+    c = np.diag(Q) / dL
+    D = U @ L.T
+    fac = 1.0 / dL ** 2 + a - b + 2.0 * c
+    return fac, D, (a, b, c)
+
+
+# ---------------------------------------------------------------------------
+# Weight-mask selection (Alg. 1, mask line; caption: each block p_w sparse)
+# ---------------------------------------------------------------------------
+
+def block_prune_counts(n: int, k: int, p_w: float, B: int):
+    """Zeros per block under cumulative rounding (reading R-mask)."""
+    counts = []
+    prev = 0
+    for j0 in range(0, k, B):
+        j1 = min(k, j0 + B)
+        cum = int(np.floor(p_w * n * j1 + 0.5))
+        counts.append(cum - prev)
+        prev = cum
+    return counts
+
+
+def select_block_mask(S, z: int):
+    """Keep-mask of an n x Bb score block with the z lowest scores removed.
+
+    Order: ascending score, then column, then row (reading R-mask).
+    """
+    S = _f64(S)
+    n, Bb = S.shape
+    flat = S.T.reshape(-1)                  # index = column * n + row
+    order = np.argsort(flat, kind="stable")
+    keep = np.ones(n * Bb, dtype=bool)
+    keep[order[:z]] = False
+    return keep.reshape(Bb, n).T
+
+
+# ---------------------------------------------------------------------------
+# Column sweep: definition (eager) and Algorithm 1 (blocked, lazy batches)
+# ---------------------------------------------------------------------------
+
+def _check_mask_in(mask_in, n, k):
+    if mask_in is None:
+        return None
+    mask_in = np.asarray(mask_in, dtype=bool)
+    assert mask_in.shape == (n, k)
+    return mask_in
+
+
+def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None):
+    """Column sweep with every column's update applied to all later columns at once.
+
+    Processing column j: w0 = W[:, j]; p = w0 * m_j; e = (w0 - p) / L_jj and
+    every later column j' gets  W[:, j'] -= e * L[j', j] - w0 * D[j, j'].
+    The mask of each block is chosen when the sweep reaches the block, from
+    S = W[:, blk]^2 * fac[blk].  Returns (W_hat, keep).
+    """
+    W = _f64(W).copy()
+    L = _f64(L)
+    D = _f64(D)
+    fac = _f64(fac)
+    n, k = W.shape
+    mask_in = _check_mask_in(mask_in, n, k)
+    keep = np.ones((n, k), dtype=bool)
+    counts = block_prune_counts(n, k, p_w, B)
+    for bi, j0 in enumerate(range(0, k, B)):
+        j1 = min(k, j0 + B)
+        S = W[:, j0:j1] ** 2 * fac[j0:j1]
+        if scores_out is not None:
+            scores_out.append(S.copy())
+        keep[:, j0:j1] = select_block_mask(S, counts[bi]) if mask_in is None else mask_in[:, j0:j1]
+        for j in range(j0, j1):
+            w0 = W[:, j].copy()
+            p = w0 * keep[:, j]
+            e = (w0 - p) / L[j, j]
+            W[:, j] = p
+            W[:, j + 1:] -= np.outer(e, L[j + 1:, j]) - np.outer(w0, D[j, j + 1:])
+    return W * keep, keep
+
+
+def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None):
+    """Algorithm 1: in-block sequential updates, then one lazy batch update
+    W[:, rest] -= E L[rest, blk]^T - W0 D[blk, rest] per block (reading R-lazy:
+    W0 holds each column's value at the time it was processed).
+    Returns (W_hat, keep).
+    """
+    W = _f64(W).copy()
+    L = _f64(L)
+    D = _f64(D)
+    fac = _f64(fac)
+    n, k = W.shape
+    mask_in = _check_mask_in(mask_in, n, k)
+    keep = np.ones((n, k), dtype=bool)
+    counts = block_prune_counts(n, k, p_w, B)
+    for bi, j0 in enumerate(range(0, k, B)):
+        j1 = min(k, j0 + B)
+        Bb = j1 - j0
+        S = W[:, j0:j1] ** 2 * fac[j0:j1]
+        if scores_out is not None:
+            scores_out.append(S.copy())
+        keep[:, j0:j1] = select_block_mask(S, counts[bi]) if mask_in is None else mask_in[:, j0:j1]
+        E = np.zeros((n, Bb))
+        W0 = np.zeros((n, Bb))
+        for j in range(j0, j1):
+            w0 = W[:, j].copy()
+            p = w0 * keep[:, j]
+            e = (w0 - p) / L[j, j]
+            E[:, j - j0] = e
+            W0[:, j - j0] = w0
+            W[:, j] = p
+            W[:, j + 1:j1] -= np.outer(e, L[j + 1:j1, j]) - np.outer(w0, D[j, j + 1:j1])
+        if j1 < k:
+            W[:, j1:] -= E @ L[j1:, j0:j1].T - W0 @ D[j0:j1, j1:]
+    return W * keep, keep
+
+
+# ---------------------------------------------------------------------------
+# Whole layer, objective and comparators
+# ---------------------------------------------------------------------------
+
+def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 128,
+                X_dense=None, mask_in=None, blocked: bool = True, scores_out=None):
+    """DuoGPT on one linear layer: Alg. 1 end to end.  Returns a dict."""
+    H, G, a = hessian_terms(X_src, p_x, X_dense)
+    L, lam = inverse_cholesky(H, damp)
+    fac, D, (_, b, c) = score_terms(G, L, a)
+    sweep = sweep_blocked if blocked else sweep_eager
+    W_hat, keep = sweep(W, L, D, fac, p_w, B, mask_in=mask_in, scores_out=scores_out)
+    return dict(W_hat=W_hat, keep=keep, H=H, G=G, a=a, b=b, c=c, L=L, lam=lam, fac=fac, D=D)
+
+
+def objective(W, W_hat, X_src, p_x: float, X_dense=None):
+    """Layer objective |W X_dense - W_hat Xh|_F^2 (Sec. 4.2), undamped, f64."""
+    W = _f64(W)
+    W_hat = _f64(W_hat)
+    X_src = _f64(X_src)
+    X_dense = X_src if X_dense is None else _f64(X_dense)
+    total = 0.0
+    for t0 in range(0, X_src.shape[0], _TOKEN_CHUNK):
+        t1 = min(X_src.shape[0], t0 + _TOKEN_CHUNK)
+        Xh, _ = sparsify_tokens(X_src[t0:t1], p_x)
+        R = X_dense[t0:t1] @ W.T - Xh @ W_hat.T
+        total += float(np.sum(R * R))
+    return total
+
+
+def sparsegpt_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 128):
+    """Comparator: the same sweep on the same sparse Hessian without the
+    residual terms (a = b = c = 0, D = 0), i.e. the OBS update of Eq. 1."""
+    W = _f64(W)
+    H, _, _ = hessian_terms(X_src, p_x)
+    L, _ = inverse_cholesky(H, damp)
+    k = W.shape[1]
+    fac = 1.0 / np.diag(L) ** 2
+    W_hat, keep = sweep_blocked(W, L, np.zeros((k, k)), fac, p_w, B)
+    return W_hat, keep
+
+
+def magnitude_layer(W, p_w: float, B: int = 128):
+    """Comparator: magnitude pruning with the same per-block counts and tie
+    order (|w|, column, row); no weight update."""
+    W = _f64(W)
+    n, k = W.shape
+    keep = np.ones((n, k), dtype=bool)
+    for bi, (j0, z) in enumerate(zip(range(0, k, B), block_prune_counts(n, k, p_w, B))):
+        j1 = min(k, j0 + B)
+        keep[:, j0:j1] = select_block_mask(np.abs(W[:, j0:j1]), z)
+    return W * keep, keep
+
+
+# ---------------------------------------------------------------------------
+# Single-weight closed form (Eq. 3) and its brute-force counterpart
+# ---------------------------------------------------------------------------
+
+def obs_closed_form(w, Xh, X_dense, lam: float, p: int):
+    """Eq. 3 for one row w (length k) and candidate p, with H = Xh^T Xh + lam I.
+
+    r = w (X_dense - Xh) is the row's output residual (a length-m vector here).
+    Returns (L_p, dw) with
+      L_p = w_p^2/h + r r^T - r Xh^T H^-1_{-p} Xh r^T + (2 w_p / h) r Xh^T H^-1_{:,p}
+      dw  = -(w_p / h) H^-1_{p,:} + r Xh^T H^-1_{-p}
+    where h = [H^-1]_pp and H^-1_{-p} is the Gaussian-eliminated inverse.
+    """
+    w = _f64(w)
+    Xh = _f64(Xh)
+    X_dense = _f64(X_dense)
+    k = w.shape[0]
+    Hinv = np.linalg.inv(Xh.T @ Xh + lam * np.eye(k))
+    h = Hinv[p, p]
+    Hm = Hinv - np.outer(Hinv[:, p], Hinv[p, :]) / h
+    r = (X_dense - Xh) @ w
+    rX = Xh.T @ r
+    Lp = w[p] ** 2 / h + r @ r - rX @ Hm @ rX + 2.0 * w[p] / h * (rX @ Hinv[:, p])
+    dw = -(w[p] / h) * Hinv[p, :] + rX @ Hm
+    return float(Lp), dw
+
+
+def obs_bruteforce(w, Xh, X_dense, lam: float, p: int, frozen=()):
+    """Direct constrained ridge least squares for removing weight p of row w:
+    minimise |dw Xh - r|^2 + lam |dw|^2 subject to dw_p = -w_p and dw_f = 0 for
+    every frozen index f.  Returns (loss, dw).  No closed form is used."""
+    w = _f64(w)
+    Xh = _f64(Xh)
+    X_dense = _f64(X_dense)
+    k = w.shape[0]
+    r = (X_dense - Xh) @ w
+    free = [j for j in range(k) if j != p and j not in set(frozen)]
+    target = r + w[p] * Xh[:, p]            # residual left after dw_p = -w_p
+    A = np.vstack([Xh[:, free], np.sqrt(lam) * np.eye(len(free))])
+    t = np.concatenate([target, np.zeros(len(free))])
+    dw = np.zeros(k)
+    dw[p] = -w[p]
+    if free:
+        v, *_ = np.linalg.lstsq(A, t, rcond=None)
+        dw[free] = v
+    loss = float(np.sum((Xh @ dw - r) ** 2) + lam * np.sum(dw * dw))
+    return loss, dw

@@ -1,0 +1,416 @@
+"""Pins of the float64 oracle against facts that do not come from the oracle
+itself: brute-force least squares, closed forms derived from the paper's
+appendix, hand-worked examples, counting and invariance properties.
+
+Each test names the passage of the DuoGPT paper it follows.  A plausible slip
+in the oracle (a dropped a/b/c term, a wrong sign of the residual, a transposed
+G, the wrong column feeding the lazy residual update, a wrong tie order)
+fails at least one of them.
+"""
+
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import duo_ref as R
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
+
+
+def _layer(seed, n, k, m, scale_sigma=0.5, outliers=0):
+    rng = np.random.default_rng(seed)
+    s = np.exp(scale_sigma * rng.standard_normal(k))
+    if outliers:
+        s[rng.choice(k, outliers, replace=False)] *= 20.0
+    X = rng.standard_normal((m, k)) * s
+    W = 0.02 * rng.standard_normal((n, k))
+    return W, X
+
+
+def _ridge(A, y, lam):
+    """argmin_v |A v - y|^2 + lam |v|^2 and its value, by lstsq on the stacked
+    system (no normal equations)."""
+    q = A.shape[1]
+    if q == 0:
+        return np.zeros(0), float(y @ y)
+    M = np.vstack([A, np.sqrt(lam) * np.eye(q)])
+    t = np.concatenate([y, np.zeros(q)])
+    v, *_ = np.linalg.lstsq(M, t, rcond=None)
+    return v, float(np.sum((A @ v - y) ** 2) + lam * v @ v)
+
+
+# ---------------------------------------------------------------------------
+# Activation rule (Preliminaries, "Activation Sparsity")
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("k,p_x", [(7, 0.5), (16, 0.6), (10, 0.0), (9, 0.99), (12, 0.25)])
+def test_sparsify_bruteforce_keys(k, p_x):
+    rng = np.random.default_rng(k)
+    # coarse values: many exact magnitude ties, signed zeros
+    X = rng.integers(-3, 4, size=(40, k)).astype(np.float64)
+    X[X == 0] = np.where(rng.random((X == 0).sum()) < 0.5, 0.0, -0.0)
+    Xh, keep = R.sparsify_tokens(X, p_x)
+    z = int(np.floor(p_x * k + 0.5))
+    for t in range(X.shape[0]):
+        assert (~keep[t]).sum() == z
+        dropped = [(abs(X[t, c]), c) for c in range(k) if not keep[t, c]]
+        kept = [(abs(X[t, c]), c) for c in range(k) if keep[t, c]]
+        if dropped and kept:
+            assert max(dropped) < min(kept)      # lexicographic (|x|, channel)
+    assert np.array_equal(Xh, np.where(keep, X, 0.0))
+
+
+def test_zero_count_rounding():
+    assert R.act_zero_count(11008, 0.6) == 6605          # 6604.8
+    assert R.act_zero_count(4096, 0.5) == 2048
+    assert R.act_zero_count(2, 0.5) == 1                 # 1.5 rounds half up
+    assert R.act_zero_count(3, 0.5) == 2
+
+
+# ---------------------------------------------------------------------------
+# Eq. 3 against direct constrained ridge least squares (App. A.1)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_eq3_closed_form_equals_bruteforce(seed):
+    rng = np.random.default_rng(seed)
+    k, m = 8, 30
+    X = rng.standard_normal((m, k)) * np.exp(rng.standard_normal(k))
+    Xh, _ = R.sparsify_tokens(X, 0.5)
+    w = rng.standard_normal(k)
+    lam = 0.3
+    for p in range(k):
+        Lp, dw = R.obs_closed_form(w, Xh, X, lam, p)
+        Lb, dwb = R.obs_bruteforce(w, Xh, X, lam, p)
+        assert abs(Lp - Lb) <= 1e-9 * max(1.0, abs(Lb))
+        np.testing.assert_allclose(dw, dwb, rtol=1e-8, atol=1e-10)
+        assert abs(dw[p] + w[p]) < 1e-10                 # constraint dw e_p^T + w_p = 0
+
+
+@pytest.mark.parametrize("k", [4, 6, 10])
+def test_bruteforce_over_masks_single_weight(k):
+    """Tiny layer: trying every one-weight mask by least squares finds the
+    same optimum as minimising the Eq. 3 loss over p."""
+    rng = np.random.default_rng(100 + k)
+    X = rng.standard_normal((3 * k, k)) * np.exp(0.7 * rng.standard_normal(k))
+    Xh, _ = R.sparsify_tokens(X, 0.5)
+    w = rng.standard_normal(k)
+    lam = 0.1
+    closed = [R.obs_closed_form(w, Xh, X, lam, p)[0] for p in range(k)]
+    brute = [R.obs_bruteforce(w, Xh, X, lam, p)[0] for p in range(k)]
+    assert int(np.argmin(closed)) == int(np.argmin(brute))
+    assert abs(min(closed) - min(brute)) <= 1e-9 * max(1.0, min(brute))
+
+
+def test_theorem1_single_step_gain():
+    """Theorem 1 (proof in App. A.5): for one step the DuoGPT loss is below the
+    SparseGPT loss by r Xh^T H^-1_{-p} Xh r^T >= 0."""
+    rng = np.random.default_rng(7)
+    k, m, lam = 6, 25, 0.2
+    X = rng.standard_normal((m, k))
+    Xh, _ = R.sparsify_tokens(X, 0.5)
+    w = rng.standard_normal(k)
+    Hl = Xh.T @ Xh + lam * np.eye(k)
+    Hinv = np.linalg.inv(Hl)
+    r = (X - Xh) @ w
+    for p in range(k):
+        h = Hinv[p, p]
+        dw_s = -(w[p] / h) * Hinv[p, :]
+        loss_s = np.sum((Xh @ dw_s - r) ** 2) + lam * dw_s @ dw_s
+        loss_d, _ = R.obs_closed_form(w, Xh, X, lam, p)
+        Hm = Hinv - np.outer(Hinv[:, p], Hinv[p, :]) / h
+        gain = (Xh.T @ r) @ Hm @ (Xh.T @ r)
+        assert gain >= 0
+        assert abs((loss_s - loss_d) - gain) <= 1e-9 * max(1.0, loss_s)
+
+
+# ---------------------------------------------------------------------------
+# Score factor, D and the Cholesky identities (Eq. 7, App. A.2-A.4)
+# ---------------------------------------------------------------------------
+
+def _terms(seed, k=9, m=40, p_x=0.5, damp=0.05):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((m, k)) * np.exp(0.8 * rng.standard_normal(k))
+    H, G, a = R.hessian_terms(X, p_x)
+    L, lam = R.inverse_cholesky(H, damp)
+    fac, D, (aa, b, c) = R.score_terms(G, L, a)
+    Xh, _ = R.sparsify_tokens(X, p_x)
+    return X, Xh, H, G, a, L, lam, fac, D
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_score_factor_is_constrained_ridge(seed):
+    """With columns < p frozen, removing w_p costs w_p^2 * fac_p where
+    fac_p = lam + min_v |Xh_{>p} v - X_dense_p|^2 + lam |v|^2 (the residual of
+    regressing the dense column p on the later sparse columns), and the optimal
+    correction of the later weights is w_p * v*.  In the sweep that correction
+    is w_p * (D[p, j] - L[j, p] / L[p, p])."""
+    X, Xh, H, G, a, L, lam, fac, D = _terms(seed)
+    k = X.shape[1]
+    for p in range(k):
+        v, val = _ridge(Xh[:, p + 1:], X[:, p], lam)
+        assert abs(fac[p] - (lam + val)) <= 1e-8 * max(1.0, abs(fac[p]))
+        step = D[p, p + 1:] - L[p + 1:, p] / L[p, p]
+        np.testing.assert_allclose(step, v, rtol=1e-7, atol=1e-9)
+        assert fac[p] >= lam * (1 - 1e-12)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_D_is_residual_regression(seed):
+    """A kept weight w_p still moves the later weights by w_p * D[p, >p], the
+    ridge regression of dX_p on the later sparse columns (Eq. 3 update term,
+    App. A.4)."""
+    X, Xh, H, G, a, L, lam, fac, D = _terms(seed)
+    k = X.shape[1]
+    dX = X - Xh
+    for p in range(k):
+        u, _ = _ridge(Xh[:, p + 1:], dX[:, p], lam)
+        np.testing.assert_allclose(D[p, p + 1:], u, rtol=1e-7, atol=1e-9)
+        assert np.all(D[p, :p + 1] == 0.0)
+
+
+def test_last_column_closed_form():
+    X, Xh, H, G, a, L, lam, fac, D = _terms(5)
+    k = X.shape[1]
+    assert abs(fac[k - 1] - (X[:, k - 1] @ X[:, k - 1] + lam)) <= 1e-10 * fac[k - 1]
+    # k = 1: the score of the only weight is w^2 (|x|^2 + lam)
+    x = np.array([[3.0], [-2.0], [0.5]])
+    H, G, a = R.hessian_terms(x, 0.0)
+    L, lam = R.inverse_cholesky(H, 0.1)
+    fac1, _, _ = R.score_terms(G, L, a)
+    assert abs(fac1[0] - (x[:, 0] @ x[:, 0] + lam)) < 1e-12
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_cholesky_identities(seed):
+    """App. A.2: L_{p+1:,p+1:} L_{p+1:,p+1:}^T is the inverse of the trailing
+    block of H.  App. A.3: after Gaussian elimination of columns < p (the
+    update of Sec. 3), column p of H^-1 divided by its diagonal equals
+    L[:, p] / L[p, p]."""
+    X, Xh, H, G, a, L, lam, fac, D = _terms(seed)
+    k = X.shape[1]
+    Hl = H + lam * np.eye(k)
+    for p in range(k - 1):
+        np.testing.assert_allclose(L[p + 1:, p + 1:] @ L[p + 1:, p + 1:].T,
+                                   np.linalg.inv(Hl[p + 1:, p + 1:]), rtol=1e-8, atol=1e-14)
+    Hinv = np.linalg.inv(Hl)
+    for p in range(k):
+        np.testing.assert_allclose(Hinv[:, p] / Hinv[p, p], L[:, p] / L[p, p], rtol=1e-8, atol=1e-12)
+        Hinv = Hinv - np.outer(Hinv[:, p], Hinv[p, :]) / Hinv[p, p]
+
+
+def test_bc_terms_explicit():
+    """b and c as first defined in Sec. 4.3 (before the Cholesky rewrite)."""
+    X, Xh, H, G, a, L, lam, fac, D = _terms(11)
+    k = X.shape[1]
+    dX = X - Xh
+    Hl = H + lam * np.eye(k)
+    _, _, (aa, b, c) = R.score_terms(G, L, a)
+    Hinv = np.linalg.inv(Hl)
+    for p in range(k):
+        z = dX[:, p] @ Xh                          # dX_p Xh^T
+        Hm = np.zeros((k, k))
+        Hm[p + 1:, p + 1:] = np.linalg.inv(Hl[p + 1:, p + 1:])
+        assert abs(b[p] - z @ Hm @ z) <= 1e-8 * max(1.0, abs(b[p]))
+        # c_p = dX_p Xh^T H^-1_{:,p} / [H^-1]_pp with the inverse after eliminating < p
+        Hp = np.zeros((k, k))
+        Hp[p:, p:] = np.linalg.inv(Hl[p:, p:])
+        assert abs(c[p] - z @ Hp[:, p] / Hp[p, p]) <= 1e-8 * max(1.0, abs(c[p]))
+    np.testing.assert_allclose(aa, np.sum(dX * dX, axis=0))
+
+
+# ---------------------------------------------------------------------------
+# Hand-worked examples
+# ---------------------------------------------------------------------------
+
+def _golden():
+    with open(GOLDEN) as f:
+        return json.load(f)["examples"]
+
+
+@pytest.mark.parametrize("ex", _golden(), ids=lambda e: e["name"])
+def test_hand_examples(ex):
+    X = np.array(ex["X"])
+    W = np.array(ex["W"])
+    e = ex["expect"]
+    _, keep_x = R.sparsify_tokens(X, ex["p_x"])
+    assert keep_x.tolist() == e["keep_x"]
+    out = R.prune_layer(W, X, ex["p_x"], ex["p_w"], damp=ex["damp"], B=ex["B"])
+    tol = dict(rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(out["H"], e["H"], **tol)
+    np.testing.assert_allclose(out["G"], e["G"], **tol)
+    np.testing.assert_allclose(out["a"], e["a"], **tol)
+    assert abs(out["lam"] - e["lam"]) < 1e-12
+    np.testing.assert_allclose(out["L"], e["L"], **tol)
+    np.testing.assert_allclose(out["b"], e["b"], **tol)
+    np.testing.assert_allclose(out["c"], e["c"], **tol)
+    np.testing.assert_allclose(out["D"], e["D"], **tol)
+    np.testing.assert_allclose(out["fac"], e["fac"], **tol)
+    assert out["keep"].tolist() == e["keep_w"]
+    np.testing.assert_allclose(out["W_hat"], e["W_hat"], **tol)
+    J = R.objective(W, out["W_hat"], X, ex["p_x"])
+    assert abs(J - e["objective"]) < 1e-9
+
+
+# ---------------------------------------------------------------------------
+# Sweep: counts, special cases, lazy == eager, objective, invariances
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n,k,p_w,B", [(7, 50, 0.5, 16), (5, 33, 0.6, 8), (3, 10, 0.37, 4), (4, 12, 0.0, 5)])
+def test_mask_counts_exact(n, k, p_w, B):
+    W, X = _layer(n * k, n, k, 4 * k)
+    out = R.prune_layer(W, X, 0.5, p_w, damp=0.01, B=B)
+    keep = out["keep"]
+    counts = R.block_prune_counts(n, k, p_w, B)
+    for bi, j0 in enumerate(range(0, k, B)):
+        assert (~keep[:, j0:j0 + B]).sum() == counts[bi]
+        assert abs(counts[bi] - p_w * n * min(B, k - j0)) <= 1.0
+    assert (~keep).sum() == int(np.floor(p_w * n * k + 0.5))
+    assert np.all(out["W_hat"][~keep] == 0.0)
+
+
+def test_selected_scores_are_lowest():
+    W, X = _layer(3, 12, 40, 160)
+    scores = []
+    out = R.prune_layer(W, X, 0.5, 0.5, B=16, scores_out=scores)
+    for bi, j0 in enumerate(range(0, 40, 16)):
+        S = scores[bi]
+        keep = out["keep"][:, j0:j0 + 16]
+        assert S[~keep].max() <= S[keep].min()
+
+
+def test_zero_sparsity_returns_weights_bit_unchanged():
+    W, X = _layer(9, 6, 24, 80)
+    out = R.prune_layer(W, X, 0.0, 0.0, B=8)
+    assert np.array_equal(out["W_hat"], W)
+    assert np.all(out["D"] == 0.0) and np.all(out["a"] == 0.0)
+
+
+def test_weight_sparsity_zero_still_corrects():
+    W, X = _layer(10, 6, 24, 80)
+    out = R.prune_layer(W, X, 0.5, 0.0, B=8)
+    assert out["keep"].all()
+    assert np.max(np.abs(out["W_hat"] - W)) > 1e-6
+    J_duo = R.objective(W, out["W_hat"], X, 0.5)
+    J_id = R.objective(W, W, X, 0.5)
+    assert J_duo < J_id
+
+
+def test_no_activation_sparsity_is_sparsegpt():
+    W, X = _layer(12, 8, 40, 120)
+    out = R.prune_layer(W, X, 0.0, 0.5, B=16)
+    Ws, ks = R.sparsegpt_layer(W, X, 0.0, 0.5, B=16)
+    assert np.array_equal(out["keep"], ks)
+    np.testing.assert_allclose(out["W_hat"], Ws, rtol=0, atol=1e-15)
+    assert np.all(out["D"] == 0.0)
+
+
+@pytest.mark.parametrize("B", [1, 3, 8, 16, 64])
+def test_lazy_equals_eager(B):
+    W, X = _layer(20 + B, 9, 45, 150, outliers=2)
+    H, G, a = R.hessian_terms(X, 0.5)
+    L, _ = R.inverse_cholesky(H, 0.01)
+    fac, D, _ = R.score_terms(G, L, a)
+    We, ke = R.sweep_eager(W, L, D, fac, 0.5, B)
+    Wb, kb = R.sweep_blocked(W, L, D, fac, 0.5, B)
+    assert np.array_equal(ke, kb)
+    np.testing.assert_allclose(Wb, We, rtol=0, atol=1e-12 * np.abs(We).max())
+    # forced mask: the result no longer depends on the block size
+    W1, _ = R.sweep_blocked(W, L, D, fac, 0.5, 5, mask_in=ke)
+    np.testing.assert_allclose(W1, We, rtol=0, atol=1e-12 * np.abs(We).max())
+
+
+def test_lazy_uses_preprune_values():
+    """Reading R-lazy is what makes blocked == eager; the post-prune reading
+    (lazy update fed with the pruned columns) does not match."""
+    W, X = _layer(31, 6, 32, 120)
+    H, G, a = R.hessian_terms(X, 0.5)
+    L, _ = R.inverse_cholesky(H, 0.01)
+    fac, D, _ = R.score_terms(G, L, a)
+    We, ke = R.sweep_eager(W, L, D, fac, 0.5, 8)
+    # post-prune variant, written out here only to show the difference
+    Wp = W.copy()
+    for j0 in range(0, 32, 8):
+        j1 = j0 + 8
+        E = np.zeros((6, 8))
+        for j in range(j0, j1):
+            w0 = Wp[:, j].copy()
+            p = w0 * ke[:, j]
+            E[:, j - j0] = (w0 - p) / L[j, j]
+            Wp[:, j] = p
+            Wp[:, j + 1:j1] -= np.outer(E[:, j - j0], L[j + 1:j1, j]) - np.outer(w0, D[j, j + 1:j1])
+        Wp[:, j1:] -= E @ L[j1:, j0:j1].T - Wp[:, j0:j1] @ D[j0:j1, j1:]
+    assert np.max(np.abs(Wp * ke - We)) > 1e-6
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_objective_below_magnitude(seed):
+    W, X = _layer(40 + seed, 16, 64, 256, scale_sigma=1.0, outliers=2)
+    out = R.prune_layer(W, X, 0.5, 0.5, B=16)
+    Wm, _ = R.magnitude_layer(W, 0.5, B=16)
+    J_duo = R.objective(W, out["W_hat"], X, 0.5)
+    J_mag = R.objective(W, Wm, X, 0.5)
+    assert J_duo < J_mag
+
+
+def test_beats_single_mask_bruteforce_bound():
+    """Tiny layer, two weights removed from one row: the greedy sweep cannot
+    beat the exhaustive optimum over all masks (each solved by least squares
+    with the same ridge term), and it should not be far from it."""
+    rng = np.random.default_rng(77)
+    k, m = 6, 30
+    X = rng.standard_normal((m, k)) * np.exp(0.5 * rng.standard_normal(k))
+    W = rng.standard_normal((1, k))
+    out = R.prune_layer(W, X, 0.5, 2.0 / k, damp=0.01, B=k)
+    Xh, _ = R.sparsify_tokens(X, 0.5)
+    lam = out["lam"]
+    J_sweep = float(np.sum((X @ W[0] - Xh @ out["W_hat"][0]) ** 2))
+    best = np.inf
+    for pair in itertools.combinations(range(k), 2):
+        free = [j for j in range(k) if j not in pair]
+        v, _ = _ridge(Xh[:, free], X @ W[0], lam)
+        wnew = np.zeros(k)
+        wnew[free] = v
+        best = min(best, float(np.sum((X @ W[0] - Xh @ wnew) ** 2)))
+    assert J_sweep >= best * (1 - 1e-9)
+    assert J_sweep <= 20.0 * best
+
+
+def test_input_scale_invariance():
+    W, X = _layer(50, 10, 48, 160)
+    a = R.prune_layer(W, X, 0.5, 0.5, B=16)
+    b = R.prune_layer(W, 4.0 * X, 0.5, 0.5, B=16)
+    assert np.array_equal(a["keep"], b["keep"])
+    np.testing.assert_allclose(b["W_hat"], a["W_hat"], rtol=1e-9, atol=1e-13)
+
+
+def test_row_permutation_equivariance():
+    W, X = _layer(51, 10, 48, 160)
+    perm = np.random.default_rng(0).permutation(10)
+    a = R.prune_layer(W, X, 0.5, 0.5, B=16)
+    b = R.prune_layer(W[perm], X, 0.5, 0.5, B=16)
+    assert np.array_equal(a["keep"][perm], b["keep"])
+    np.testing.assert_allclose(b["W_hat"], a["W_hat"][perm], rtol=1e-12, atol=1e-15)
+
+
+def test_two_stream_residual():
+    """Multi-layer case (Sec. 4.2): X_src (pruned model's input) differs from
+    X_dense.  H depends only on the sparsified X_src; dX = X_dense - Xh; the
+    last-column closed form becomes fac_{k-1} = |X_dense_{k-1}|^2 + lam."""
+    rng = np.random.default_rng(60)
+    k, m = 9, 50
+    Xd = rng.standard_normal((m, k))
+    Xs = Xd + 0.1 * rng.standard_normal((m, k))
+    H, G, a = R.hessian_terms(Xs, 0.5, Xd)
+    Xh, _ = R.sparsify_tokens(Xs, 0.5)
+    np.testing.assert_allclose(H, Xh.T @ Xh)
+    np.testing.assert_allclose(G, (Xd - Xh).T @ Xh)
+    L, lam = R.inverse_cholesky(H, 0.05)
+    fac, D, _ = R.score_terms(G, L, a)
+    assert abs(fac[-1] - (Xd[:, -1] @ Xd[:, -1] + lam)) < 1e-9 * fac[-1]
+    for p in range(k):
+        v, val = _ridge(Xh[:, p + 1:], Xd[:, p], lam)
+        assert abs(fac[p] - (lam + val)) <= 1e-8 * fac[p]
