@@ -1,0 +1,221 @@
+/*
+ * duo.h - C ABI of the MI355X (gfx950) DuoGPT layer solver.
+ *
+ * The library computes, for one linear layer, the activation-sparsity-aware
+ * OBC pruning of DuoGPT (arXiv 2506.20194):
+ *
+ *   stage 1  duo_hessian_accum / duo_residual_term
+ *            per-token magnitude sparsification of the calibration input and
+ *            accumulation of H = Xh Xh^T, G = dX Xh^T and a = diag(dX dX^T)
+ *            (Sec. 4.2-4.3, Algorithm 1 first two lines);
+ *   stage 2  duo_chol_inv
+ *            damping and the lower Cholesky factor L of the inverse Hessian,
+ *            (H + lambda I)^-1 = L L^T (Sec. 4.3, "Inverse_Cholesky");
+ *   stage 3  duo_score_terms + duo_sweep (together: duo_prune_layer)
+ *            Q = G L, b, c, D = U L^T and the score factor of Eq. 7, then the
+ *            blocked column sweep of Algorithm 1 with lazy batch updates.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Orientation.  The paper's calibration matrix X is k x m (channels x tokens).
+ *   In memory activations are token-major: an m x k row-major array with row
+ *   stride ldx >= k elements (PyTorch's activation layout), i.e. X^T.
+ *   W is n x k row-major (out x in, PyTorch's Linear layout).  H, G, L and D are
+ *   k x k row-major fp32 with a row stride >= k.  H[p][q] = sum_t Xh[t][p] Xh[t][q];
+ *   G[p][q] = sum_t dX[t][p] Xh[t][q] (paper: dX Xh^T).
+ * Streams X_src / X_dense.  X_src is the stream that is sparsified (the pruned
+ *   model's input); X_dense is the dense model's input (the paper's X-tilde).
+ *   For a single layer they are the same array; pass X_dense = NULL.
+ * Pointers.  Every array argument is a DEVICE pointer owned by the caller,
+ *   except where a comment says "host".  The library never allocates or frees
+ *   device memory: scratch memory comes from the caller's workspace (ws,
+ *   ws_bytes), sized by duo_workspace_size() and aligned to 256 bytes.
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Work is
+ *   enqueued on it in order; a call returns before the work finishes unless
+ *   stated otherwise.  Calls that share a workspace must not overlap.
+ * Errors.  Each call returns a duo_status.  Argument errors are detected on
+ *   the host before anything is enqueued; nothing is written then.  Numerical
+ *   failures detected on the device (non-positive pivot, non-finite input)
+ *   are reported by duo_chol_inv.  No C++ exception crosses this interface.
+ * Precision.  Inputs are fp32 or bf16; every product of two inputs is formed
+ *   exactly (bf16) or in fp32, and every accumulation is fp32.  Results are
+ *   deterministic: the same inputs give bitwise identical outputs.
+ * Limits.  1 <= k <= 32768 (per-token selection keeps a token in registers),
+ *   n >= 1, m >= 0, block in [1, 128].
+ */
+#ifndef DUO_H
+#define DUO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t duo_status;
+enum {
+  DUO_OK = 0,
+  DUO_ERR_INVALID_ARG = 1,  /* null pointer, bad size/stride/ratio/dtype */
+  DUO_ERR_UNSUPPORTED = 2,  /* valid but outside this build's limits      */
+  DUO_ERR_WORKSPACE = 3,    /* workspace missing, too small or misaligned  */
+  DUO_ERR_NOT_PD = 4,       /* damped Hessian not positive definite        */
+  DUO_ERR_NONFINITE = 5,    /* NaN/Inf met where a finite value is needed  */
+  DUO_ERR_HIP = 6,          /* a HIP runtime call failed                   */
+  DUO_ERR_NO_DEVICE = 7     /* no gfx950 device is current                 */
+};
+
+/* element types of X and W */
+enum { DUO_F32 = 0, DUO_BF16 = 1 };
+
+/* Activation sparsification rule (Preliminaries, "Activation Sparsity").
+ * DUO_ACT_TOPK_MAG_PER_TOKEN: every token keeps all but z = floor(p*k + 0.5)
+ * of its k entries; the entries zeroed are those with the smallest key
+ * (|x|, channel index), so on equal magnitude the lower channel goes first and
+ * -0.0 counts as 0.  DUO_ACT_NONE keeps everything (p ignored). */
+enum { DUO_ACT_NONE = 0, DUO_ACT_TOPK_MAG_PER_TOKEN = 1 };
+typedef struct {
+  int32_t kind;
+  double sparsity; /* p^x in [0, 1] */
+} duo_act_rule;
+
+/* operations, for duo_workspace_size */
+enum {
+  DUO_OP_HESSIAN = 0,     /* duo_hessian_accum and duo_residual_term (uses m, k) */
+  DUO_OP_CHOL_INV = 1,    /* duo_chol_inv (uses k)                               */
+  DUO_OP_SCORE_TERMS = 2, /* duo_score_terms (uses k)                            */
+  DUO_OP_SWEEP = 3,       /* duo_sweep (uses n, k, block)                        */
+  DUO_OP_PRUNE_LAYER = 4  /* duo_prune_layer (uses n, k, block)                  */
+};
+
+/* Result record of duo_chol_inv (host memory). */
+typedef struct {
+  double lambda;      /* damping added to the diagonal                        */
+  int64_t fail_index; /* a column whose pivot was not positive, else -1      */
+  int32_t status;     /* DUO_OK, DUO_ERR_NOT_PD or DUO_ERR_NONFINITE          */
+} duo_chol_info;
+
+/* Bytes of workspace an operation needs (0 for a bad op).  Pure host
+ * arithmetic; safe to call without a device. */
+size_t duo_workspace_size(int32_t op, int64_t n, int64_t k, int64_t m, int32_t block);
+
+/* Human-readable text of a status code (static storage). */
+const char* duo_status_string(duo_status s);
+
+/* Library version string, e.g. "duo 0.1.0 gfx950". */
+const char* duo_version(void);
+
+/*
+ * duo_act_sparsify_mask - the activation mask alone (test and inspection hook).
+ *   X (m x k, ldx, x_dtype) is sparsified per token with `rule`; bit c of
+ *   token t is written to mask_out[t * ceil(k/32) + c/32] bit (c % 32),
+ *   1 = kept.  mask_out must hold m * ceil(k/32) uint32 words.
+ *   Workspace: DUO_OP_HESSIAN with the same m and k.
+ */
+duo_status duo_act_sparsify_mask(const void* X, int32_t x_dtype, int64_t m, int64_t k, int64_t ldx,
+                                 duo_act_rule rule, uint32_t* mask_out, void* ws, size_t ws_bytes,
+                                 void* stream);
+
+/*
+ * duo_hessian_accum - stage 1 (Algorithm 1, H <- Xh Xh^T; Sec. 4.3 a-term).
+ *   X_src    m x k, ldx, x_dtype: the input to sparsify (Xh = sparsify(X_src)).
+ *   X_dense  m x k, ldx, x_dtype, or NULL (= X_src): the dense stream.
+ *   H        k x k fp32, ldh: H += Xh^T Xh over the m tokens (both triangles).
+ *   G, a     optional (both NULL or both set): G += dX^T Xh with dX = X_dense - Xh,
+ *            a[p] += sum_t dX[t][p]^2.  G is k x k fp32 with row stride ldg.
+ *   The caller zeroes H, G and a before the first token chunk; further calls
+ *   add more tokens (raw sums, no 1/m scaling).  For X_src != X_dense, dX is
+ *   represented to ~16 significant bits inside the product (exact when the
+ *   two streams' values are within a factor of 2^7 of each other or the entry
+ *   is dropped); a is accumulated from exact fp32 differences.
+ *   Workspace: DUO_OP_HESSIAN with the same m and k.
+ */
+duo_status duo_hessian_accum(const void* X_src, const void* X_dense, int32_t x_dtype, int64_t m,
+                             int64_t k, int64_t ldx, duo_act_rule rule, float* H, int64_t ldh,
+                             float* G, int64_t ldg, float* a, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/*
+ * duo_residual_term - stage 1, residual part only (Sec. 4.3: G = dX Xh^T,
+ *   a = diag(dX dX^T)).  Same arguments and accumulation as duo_hessian_accum
+ *   without H; X_src = NULL means X_src = X_dense (single-layer case).
+ */
+duo_status duo_residual_term(const void* X_dense, const void* X_src, int32_t x_dtype, int64_t m,
+                             int64_t k, int64_t ldx, duo_act_rule rule, float* G, int64_t ldg,
+                             float* a, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * duo_chol_inv - stage 2 (Sec. 4.3 Hessian synchronisation; Algorithm 1
+ *   "Inverse_Cholesky"; App. A.2).
+ *   H_inout  k x k fp32, ldh, symmetric (both triangles read as written by
+ *            duo_hessian_accum; only the upper triangle is used).  On return
+ *            it holds L: lower triangular with a positive diagonal and
+ *            L L^T = (H + lambda I)^-1, lambda = damp_ratio * mean(diag H);
+ *            the strictly upper triangle is set to 0.
+ *   info     host pointer or NULL.  NULL: fully asynchronous, device-side
+ *            failures are not reported.  Non-NULL: the call waits for the
+ *            stream, fills *info and returns its status (DUO_ERR_NOT_PD when a
+ *            pivot was not positive, DUO_ERR_NONFINITE when mean(diag H) is
+ *            not finite or not positive).
+ *   Workspace: DUO_OP_CHOL_INV with the same k.
+ */
+duo_status duo_chol_inv(float* H_inout, int64_t k, int64_t ldh, double damp_ratio,
+                        duo_chol_info* info, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * duo_score_terms - stage 3 precompute (Eq. 7; App. A.3-A.4; Algorithm 1
+ *   lines Q, U, a, b, c, D).
+ *   L (ldl, strictly upper triangle zero), G (ldg), a (k) -> D (k x k, ldd)
+ *   and fac (k):  Q = G L, U = strict upper(Q), b = diag(U U^T),
+ *   c = diag(Q) / diag(L), D = U L^T (strictly upper; its lower triangle and
+ *   diagonal are written as 0 inside the diagonal 128 x 128 tiles and are not
+ *   written elsewhere), fac = 1/diag(L)^2 + a - b + 2c.  The score of weight
+ *   W[r][p] is S = W[r][p]^2 * fac[p].
+ *   Workspace: DUO_OP_SCORE_TERMS with the same k.
+ */
+duo_status duo_score_terms(const float* L, int64_t ldl, const float* G, int64_t ldg, const float* a,
+                           int64_t k, float* D, int64_t ldd, float* fac, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/*
+ * duo_sweep - stage 3 sweep (Algorithm 1 outer/inner loops, lazy updates).
+ *   W        n x k, ldw, w_dtype: dense weights (not modified).
+ *   L, D     from duo_chol_inv / duo_score_terms; fac from duo_score_terms.
+ *   w_sparsity  p^w in [0, 1].  Blocks are columns [j0, j0+B_b), B_b =
+ *            min(block, k - j0); blocks 0..b hold floor(p^w*n*(j0+B_b) + 0.5)
+ *            zeros in total.  Within a block the weights with the smallest key
+ *            (S, column, row) are pruned.
+ *   The correction term of the lazy batch update uses each column's value at
+ *   the moment it is processed (before pruning), so the blocked sweep equals
+ *   the column-by-column sweep.
+ *   mask_in  NULL, or an n x ceil(k/32) bit mask (1 = keep) that replaces the
+ *            selection (forced-mask mode; counts are then not enforced).
+ *   W_out    n x k fp32, row stride k: the pruned, compensated weights.
+ *   W_out_lowp  NULL or n x k (row stride k) in w_dtype (round to nearest even).
+ *   mask_out NULL or n x ceil(k/32) uint32 words, 1 = kept.
+ *   block_scores_out  NULL or n x k fp32: each weight's score S at the time
+ *            its block was selected.
+ *   Workspace: DUO_OP_SWEEP with the same n, k, block.
+ */
+duo_status duo_sweep(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw,
+                     const float* L, int64_t ldl, const float* D, int64_t ldd, const float* fac,
+                     double w_sparsity, int32_t block, const uint32_t* mask_in, float* W_out,
+                     void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws,
+                     size_t ws_bytes, void* stream);
+
+/*
+ * duo_prune_layer - stage 3 in one call: duo_score_terms then duo_sweep, with
+ *   D and fac kept in the workspace.  Arguments as in those two calls.
+ *   Workspace: DUO_OP_PRUNE_LAYER with the same n, k, block.
+ */
+duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw,
+                           const float* L, int64_t ldl, const float* G, int64_t ldg, const float* a,
+                           double w_sparsity, int32_t block, const uint32_t* mask_in, float* W_out,
+                           void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws,
+                           size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DUO_H */

@@ -1,0 +1,259 @@
+// Stage 2 of the DuoGPT layer solver on gfx950: damping and the lower
+// Cholesky factor of the inverse Hessian (paper Sec. 4.3, Algorithm 1
+// "Inverse_Cholesky"; App. A.2).
+//
+// Route.  If (H + lambda I) = V V^T with V upper triangular (a Cholesky
+// factorisation that eliminates from the last column backwards), then
+// (H + lambda I)^-1 = V^-T V^-1, so L = V^-T is lower triangular with
+// L L^T = (H + lambda I)^-1.  This needs one factorisation (k^3/3) and one
+// triangular inverse (k^3/3) instead of an explicit inverse followed by a
+// second factorisation.
+//
+//   1. damp: lambda = damp * mean(diag H) (fixed-order double sum), H += lambda I.
+//   2. blocked factorisation from the bottom-right, 128 columns at a time:
+//      diagonal block V_bb and its inverse in one workgroup (LDS), panel
+//      V[0:r0, b] = H[0:r0, b] V_bb^-T and symmetric update of the leading
+//      block, both on the fp32 MFMA GEMM.  V lives in the upper triangle.
+//   3. N = V^-1 by recursive halving: N12 = -N11 V12 N22 (two GEMMs per node).
+//   4. L = N^T written to the lower triangle; the strict upper set to zero.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace duo {
+
+namespace {
+
+__global__ __launch_bounds__(256) void damp_kernel(float* H, int64_t ldh, int k, double damp, CholStatus* st) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < k; i += 256) s += (double)H[(int64_t)i * ldh + i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  const double mean = red[0] / (double)k;
+  const double lam = damp * mean;
+  if (threadIdx.x == 0) {
+    st->lambda = lam;
+    st->fail = -1;
+    st->status = DUO_OK;
+    if (!(mean == mean) || mean > 1e300 || mean < -1e300)
+      st->status = DUO_ERR_NONFINITE;
+    else if (!(mean > 0.0))
+      st->status = DUO_ERR_NOT_PD;
+  }
+  const float lf = (float)lam;
+  for (int i = threadIdx.x; i < k; i += 256) H[(int64_t)i * ldh + i] += lf;
+}
+
+// Factor the s x s diagonal block at (r0, r0) from its upper triangle:
+// A = V V^T with V upper, eliminating the last column first.  V overwrites
+// the block's upper triangle (lower set to 0); V^-1 goes to `vinv`
+// (128 x 128, row-major, zeros below the diagonal).
+__global__ __launch_bounds__(256) void diag_factor_kernel(float* H, int64_t ldh, int r0, int s, float* vinv,
+                                                          CholStatus* st) {
+  __shared__ float A[kTile][kTile + 1];
+  __shared__ float N[kTile][kTile + 1];
+  __shared__ float invd[kTile];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < kTile * kTile; e += 256) {
+    const int r = e / kTile, c = e % kTile;
+    float v = 0.f;
+    if (r < s && c < s) v = r <= c ? H[(int64_t)(r0 + r) * ldh + r0 + c] : H[(int64_t)(r0 + c) * ldh + r0 + r];
+    A[r][c] = v;
+    N[r][c] = 0.f;
+  }
+  __syncthreads();
+  for (int c = s - 1; c >= 0; --c) {
+    const float piv = A[c][c];
+    const float d = sqrtf(piv);
+    if (tid == 0 && !(piv > 0.f) && st->status == DUO_OK) {
+      st->status = DUO_ERR_NOT_PD;
+      st->fail = r0 + c;
+    }
+    __syncthreads();  // everyone has read the pivot
+    if (tid < c) A[tid][c] = A[tid][c] / d;
+    if (tid == 0) A[c][c] = d;
+    __syncthreads();
+    for (int e = tid; e < c * c; e += 256) {
+      const int r = e / c, q = e % c;
+      if (r <= q) A[r][q] -= A[r][c] * A[q][c];
+    }
+    __syncthreads();
+  }
+  // N = V^-1, row by row from the bottom; two threads per column
+  if (tid < s) invd[tid] = 1.0f / A[tid][tid];
+  __syncthreads();
+  const int col = tid >> 1, half = tid & 1;
+  for (int r = s - 1; r >= 0; --r) {
+    float part = 0.f;
+    if (col > r && col < s)
+      for (int q = r + 1 + half; q <= col; q += 2) part += A[r][q] * N[q][col];
+    part += __shfl_xor(part, 1);
+    if (half == 0 && col < s) {
+      if (col == r)
+        N[r][col] = invd[r];
+      else if (col > r)
+        N[r][col] = -part * invd[r];
+    }
+    __syncthreads();
+  }
+  for (int e = tid; e < kTile * kTile; e += 256) {
+    const int r = e / kTile, c = e % kTile;
+    vinv[e] = (r < s && c < s) ? N[r][c] : 0.f;
+    if (r < s && c < s) H[(int64_t)(r0 + r) * ldh + r0 + c] = r <= c ? A[r][c] : 0.f;
+  }
+}
+
+// Copy the inverted diagonal blocks into place (full 128 x 128 incl. zeros).
+__global__ __launch_bounds__(256) void place_diag_kernel(float* H, int64_t ldh, int k, const float* vinv) {
+  const int b = blockIdx.x;
+  const float* src = vinv + (int64_t)b * kTile * kTile;
+  for (int e = threadIdx.x; e < kTile * kTile; e += 256) {
+    const int r = b * kTile + e / kTile, c = b * kTile + e % kTile;
+    if (r < k && c < k) H[(int64_t)r * ldh + c] = src[e];
+  }
+}
+
+// L = N^T: tile pair (ti <= tj): upper tile (ti, tj) -> lower tile (tj, ti); upper zeroed.
+__global__ __launch_bounds__(256) void transpose_upper_kernel(float* H, int64_t ldh, int k) {
+  __shared__ float t[64][65];
+  int ti, tj;
+  tri_pair(blockIdx.x, &tj, &ti);  // ti <= tj, tiles of 64
+  const int i0 = ti * 64, j0 = tj * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int r = e / 64, c = e % 64;
+    const int gi = i0 + r, gj = j0 + c;
+    float v = 0.f;
+    if (gi < k && gj < k && gi <= gj) v = H[(int64_t)gi * ldh + gj];
+    t[r][c] = v;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int r = e / 64, c = e % 64;
+    // destination (j0 + r, i0 + c) takes source (i0 + c, j0 + r)
+    const int gi = j0 + r, gj = i0 + c;
+    if (gi < k && gj < k) {
+      if (gi >= gj)
+        H[(int64_t)gi * ldh + gj] = t[c][r];
+      else
+        H[(int64_t)gi * ldh + gj] = 0.f;
+    }
+    // zero the strictly upper source entries of off-diagonal tiles
+    const int si = i0 + r, sj = j0 + c;
+    if (ti != tj && si < k && sj < k) H[(int64_t)si * ldh + sj] = 0.f;
+  }
+}
+
+struct CholWs {
+  CholStatus* st;
+  float* vinv;
+  float* X;
+  size_t bytes;
+};
+
+CholWs carve(void* ws, int64_t k) {
+  const int64_t T = cdiv(k, kTile);
+  const int64_t half = cdiv(T, 2) * kTile;
+  Carver c(ws);
+  CholWs w;
+  w.st = c.take<CholStatus>(1);
+  w.vinv = c.take<float>((size_t)T * kTile * kTile);
+  w.X = c.take<float>((size_t)half * half);
+  w.bytes = c.off;
+  return w;
+}
+
+// N = V^-1 on the block range [lo, hi) (units of 128 columns); the diagonal
+// blocks already hold their inverses.
+duo_status trinv(float* H, int64_t ldh, int64_t k, int lo, int hi, float* X, hipStream_t s) {
+  if (hi - lo <= 1) return DUO_OK;
+  const int mid = lo + (hi - lo) / 2;
+  duo_status st = trinv(H, ldh, k, lo, mid, X, s);
+  if (st != DUO_OK) return st;
+  st = trinv(H, ldh, k, mid, hi, X, s);
+  if (st != DUO_OK) return st;
+  const int64_t r_lo = (int64_t)lo * kTile, r_mid = (int64_t)mid * kTile;
+  const int64_t r_hi = (int64_t)hi * kTile < k ? (int64_t)hi * kTile : k;
+  const int m1 = (int)(r_mid - r_lo), m2 = (int)(r_hi - r_mid);
+  // X = V12 N22 (N22 upper: for output column tile j only l < j-tile end)
+  GemmDesc a{};
+  a.M = m1;
+  a.N = m2;
+  a.C = X;
+  a.ldc = m2;
+  a.beta = 0.f;
+  a.tri = TRI_ALL;
+  a.nterms = 1;
+  a.t[0] = GemmTerm{H + r_lo * ldh + r_mid, ldh, 1, H + r_mid * ldh + r_mid, ldh, 1, m2, 1.f, KLO_ZERO, KHI_COL};
+  st = gemm_f32(a, s);
+  if (st != DUO_OK) return st;
+  // V12 <- -N11 X (N11 upper: for output row tile i only l >= i-tile start)
+  GemmDesc b{};
+  b.M = m1;
+  b.N = m2;
+  b.C = H + r_lo * ldh + r_mid;
+  b.ldc = ldh;
+  b.beta = 0.f;
+  b.tri = TRI_ALL;
+  b.nterms = 1;
+  b.t[0] = GemmTerm{H + r_lo * ldh + r_lo, ldh, 1, X, m2, 1, m1, -1.f, KLO_ROW, KHI_FULL};
+  return gemm_f32(b, s);
+}
+
+}  // namespace
+
+size_t chol_ws_bytes(int64_t k) { return carve(nullptr, k).bytes; }
+
+duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hipStream_t s, CholStatus** status_dev) {
+  const CholWs w = carve(ws, k);
+  *status_dev = w.st;
+  const int T = (int)cdiv(k, kTile);
+  hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, H, ldh, (int)k, damp, w.st);
+  DUO_LAUNCH_CHECK();
+  for (int b = T - 1; b >= 0; --b) {
+    const int r0 = b * kTile;
+    const int sz = (int)((int64_t)r0 + kTile <= k ? kTile : k - r0);
+    hipLaunchKernelGGL(diag_factor_kernel, dim3(1), dim3(256), 0, s, H, ldh, r0, sz,
+                       w.vinv + (int64_t)b * kTile * kTile, w.st);
+    DUO_LAUNCH_CHECK();
+    if (r0 == 0) break;
+    // panel: H[0:r0, r0:r0+sz] <- H[0:r0, r0:r0+sz] * Vinv_bb^T   (in place: one tile column)
+    GemmDesc p{};
+    p.M = r0;
+    p.N = sz;
+    p.C = H + r0;
+    p.ldc = ldh;
+    p.beta = 0.f;
+    p.tri = TRI_ALL;
+    p.nterms = 1;
+    p.t[0] = GemmTerm{H + r0, ldh, 1, w.vinv + (int64_t)b * kTile * kTile, kTile, 0, sz, 1.f, KLO_ZERO, KHI_FULL};
+    duo_status st = gemm_f32(p, s);
+    if (st != DUO_OK) return st;
+    // leading block (upper tiles): H[0:r0, 0:r0] -= P P^T
+    GemmDesc u{};
+    u.M = r0;
+    u.N = r0;
+    u.C = H;
+    u.ldc = ldh;
+    u.beta = 1.f;
+    u.tri = TRI_UPPER;
+    u.nterms = 1;
+    u.t[0] = GemmTerm{H + r0, ldh, 1, H + r0, ldh, 0, sz, -1.f, KLO_ZERO, KHI_FULL};
+    st = gemm_f32(u, s);
+    if (st != DUO_OK) return st;
+  }
+  hipLaunchKernelGGL(place_diag_kernel, dim3(T), dim3(256), 0, s, H, ldh, (int)k, (const float*)w.vinv);
+  DUO_LAUNCH_CHECK();
+  duo_status st = trinv(H, ldh, k, 0, T, w.X, s);
+  if (st != DUO_OK) return st;
+  const int T64 = (int)cdiv(k, 64);
+  hipLaunchKernelGGL(transpose_upper_kernel, dim3(T64 * (T64 + 1) / 2), dim3(256), 0, s, H, ldh, (int)k);
+  DUO_LAUNCH_CHECK();
+  return DUO_OK;
+}
+
+}  // namespace duo

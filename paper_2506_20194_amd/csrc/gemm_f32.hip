@@ -1,0 +1,222 @@
+// fp32 MFMA GEMM for gfx950 used by the dense k^3 stages (inverse Cholesky,
+// Q = G L, D = U L^T) and by the lazy trailing update of the column sweep.
+//
+// 128 x 128 output tile per 256-thread workgroup, 2 x 2 waves of 64 x 64,
+// v_mfma_f32_16x16x4_f32; K staged 16 at a time through LDS with one stage
+// of register prefetch.  Triangular operands are handled by restricting each
+// tile's K range (tile-granular) and by tile filters (lower/upper only); the
+// zeros inside diagonal tiles must be stored explicitly.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace duo {
+
+namespace {
+
+constexpr int KT = 16;          // K per stage
+constexpr int LS = kTile + 16;  // LDS row stride (floats): conflict-free fragment reads
+
+struct Stage {
+  float4 a[2];
+  float4 b[2];
+};
+
+__device__ inline int64_t lo_of(int mode, int i0, int j0) {
+  return mode == KLO_ROW ? i0 : mode == KLO_COL ? j0 : 0;
+}
+__device__ inline int64_t hi_of(int mode, int i0, int j0, int K) {
+  const int64_t v = mode == KHI_ROW ? (int64_t)i0 + kTile : mode == KHI_COL ? (int64_t)j0 + kTile : K;
+  return v < K ? v : K;
+}
+
+// Load 4 consecutive elements p[0..3] of a line whose valid index range is
+// [lo, hi), starting at index `idx`; vector load when fully inside and aligned.
+__device__ inline float4 load4(const float* p, int64_t idx, int64_t lo, int64_t hi, bool line_ok) {
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (!line_ok) return v;
+  if (idx >= lo && idx + 3 < hi && ((reinterpret_cast<uintptr_t>(p) & 15) == 0)) return *(const float4*)p;
+  if (idx + 0 >= lo && idx + 0 < hi) v.x = p[0];
+  if (idx + 1 >= lo && idx + 1 < hi) v.y = p[1];
+  if (idx + 2 >= lo && idx + 2 < hi) v.z = p[2];
+  if (idx + 3 >= lo && idx + 3 < hi) v.w = p[3];
+  return v;
+}
+
+template <bool AR, bool BR>
+__device__ inline void load_stage(const GemmTerm& t, int M, int N, int i0, int j0, int64_t k0, int64_t klo,
+                                  int64_t khi, Stage& st) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    if (AR) {  // A(i,l) = A[i*lda + l]: 4 consecutive l of one row
+      const int row = (tid >> 2) + 64 * q, l4 = (tid & 3) * 4;
+      const int64_t i = i0 + row, l = k0 + l4;
+      st.a[q] = load4(t.A + i * t.lda + l, l, klo, khi, i < M);
+    } else {  // A(i,l) = A[l*lda + i]: 4 consecutive i of one l
+      const int lr = (tid >> 5) + 8 * q, i4 = (tid & 31) * 4;
+      const int64_t i = i0 + i4, l = k0 + lr;
+      const bool ok = l >= klo && l < khi;
+      st.a[q] = load4(t.A + l * t.lda + i, i, 0, M, ok);
+    }
+    if (BR) {  // B(l,j) = B[l*ldb + j]: 4 consecutive j of one l
+      const int lr = (tid >> 5) + 8 * q, j4 = (tid & 31) * 4;
+      const int64_t j = j0 + j4, l = k0 + lr;
+      const bool ok = l >= klo && l < khi;
+      st.b[q] = load4(t.B + l * t.ldb + j, j, 0, N, ok);
+    } else {  // B(l,j) = B[j*ldb + l]: 4 consecutive l of one j
+      const int col = (tid >> 2) + 64 * q, l4 = (tid & 3) * 4;
+      const int64_t j = j0 + col, l = k0 + l4;
+      st.b[q] = load4(t.B + j * t.ldb + l, l, klo, khi, j < N);
+    }
+  }
+}
+
+template <bool AR, bool BR>
+__device__ inline void store_stage(float* sA, float* sB, const Stage& st, float alpha) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const float4 a = st.a[q];
+    if (AR) {
+      const int row = (tid >> 2) + 64 * q, l4 = (tid & 3) * 4;
+      sA[(l4 + 0) * LS + row] = alpha * a.x;
+      sA[(l4 + 1) * LS + row] = alpha * a.y;
+      sA[(l4 + 2) * LS + row] = alpha * a.z;
+      sA[(l4 + 3) * LS + row] = alpha * a.w;
+    } else {
+      const int lr = (tid >> 5) + 8 * q, i4 = (tid & 31) * 4;
+      *(float4*)&sA[lr * LS + i4] = make_float4(alpha * a.x, alpha * a.y, alpha * a.z, alpha * a.w);
+    }
+    const float4 b = st.b[q];
+    if (BR) {
+      const int lr = (tid >> 5) + 8 * q, j4 = (tid & 31) * 4;
+      *(float4*)&sB[lr * LS + j4] = b;
+    } else {
+      const int col = (tid >> 2) + 64 * q, l4 = (tid & 3) * 4;
+      sB[(l4 + 0) * LS + col] = b.x;
+      sB[(l4 + 1) * LS + col] = b.y;
+      sB[(l4 + 2) * LS + col] = b.z;
+      sB[(l4 + 3) * LS + col] = b.w;
+    }
+  }
+}
+
+template <bool AR, bool BR>
+__device__ inline void run_term(const GemmTerm& t, int M, int N, int i0, int j0, float* smem, f4 (&acc)[4][4]) {
+  const int64_t klo = lo_of(t.klo, i0, j0);
+  const int64_t khi = hi_of(t.khi, i0, j0, t.K);
+  if (klo >= khi) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wi = wave >> 1, wj = wave & 1;
+  float* bufs[2][2] = {{smem, smem + KT * LS}, {smem + 2 * KT * LS, smem + 3 * KT * LS}};
+  Stage st;
+  load_stage<AR, BR>(t, M, N, i0, j0, klo, klo, khi, st);
+  __syncthreads();  // previous users of the LDS buffers are done
+  store_stage<AR, BR>(bufs[0][0], bufs[0][1], st, t.alpha);
+  __syncthreads();
+  int buf = 0;
+  for (int64_t k0 = klo; k0 < khi; k0 += KT) {
+    const bool more = k0 + KT < khi;
+    if (more) load_stage<AR, BR>(t, M, N, i0, j0, k0 + KT, klo, khi, st);
+    const float* sA = bufs[buf][0];
+    const float* sB = bufs[buf][1];
+#pragma unroll
+    for (int ks = 0; ks < KT / 4; ++ks) {
+      const int kr = ks * 4 + (lane >> 4);
+      float av[4], bv[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        av[a] = sA[kr * LS + wi * 64 + a * 16 + (lane & 15)];
+        bv[a] = sB[kr * LS + wj * 64 + a * 16 + (lane & 15)];
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
+    }
+    if (more) {
+      store_stage<AR, BR>(bufs[buf ^ 1][0], bufs[buf ^ 1][1], st, t.alpha);
+      __syncthreads();
+      buf ^= 1;
+    }
+  }
+}
+
+__device__ inline int xcd_remap_g(int b, int nblocks) {
+  const int per = (nblocks + 7) / 8;
+  return (b % 8) * per + b / 8;
+}
+
+template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmDesc d, int ntiles) {
+  __shared__ __attribute__((aligned(16))) float smem[4 * KT * LS];
+  const int id = xcd_remap_g(blockIdx.x, gridDim.x);
+  if (id >= ntiles) return;
+  int ti, tj;
+  if (d.tri == TRI_ALL) {
+    const int tn = (int)cdiv(d.N, kTile);
+    ti = id / tn;
+    tj = id % tn;
+  } else if (d.tri == TRI_LOWER) {
+    tri_pair(id, &ti, &tj);
+  } else {
+    tri_pair(id, &tj, &ti);
+  }
+  const int i0 = ti * kTile, j0 = tj * kTile;
+  f4 acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
+  run_term<A1R, B1R>(d.t[0], d.M, d.N, i0, j0, smem, acc);
+  if (TWO) run_term<A2R, B2R>(d.t[1], d.M, d.N, i0, j0, smem, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wi = wave >> 1, wj = wave & 1;
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t i = i0 + wi * 64 + a * 16 + (lane >> 4) * 4 + r;
+        const int64_t j = j0 + wj * 64 + b * 16 + (lane & 15);
+        if (i < d.M && j < d.N) {
+          float* c = d.C + i * d.ldc + j;
+          *c = d.beta != 0.f ? d.beta * *c + acc[a][b][r] : acc[a][b][r];
+        }
+      }
+}
+
+template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
+duo_status launch(const GemmDesc& d, hipStream_t s) {
+  const int tm = (int)cdiv(d.M, kTile), tn = (int)cdiv(d.N, kTile);
+  int ntiles = d.tri == TRI_ALL ? tm * tn : tm * (tm + 1) / 2;
+  if (ntiles <= 0) return DUO_OK;
+  const int grid = (int)rup(ntiles, 8);
+  hipLaunchKernelGGL((gemm_kernel<A1R, B1R, A2R, B2R, TWO>), dim3(grid), dim3(256), 0, s, d, ntiles);
+  DUO_LAUNCH_CHECK();
+  return DUO_OK;
+}
+
+}  // namespace
+
+duo_status gemm_f32(const GemmDesc& d, hipStream_t s) {
+  if (d.M <= 0 || d.N <= 0) return DUO_OK;
+  if (d.tri != TRI_ALL && d.M != d.N) return DUO_ERR_UNSUPPORTED;
+  const int c1 = d.t[0].a_row * 2 + d.t[0].b_row;
+  if (d.nterms == 1) {
+    switch (c1) {
+      case 0: return launch<false, false, false, false, false>(d, s);
+      case 1: return launch<false, true, false, false, false>(d, s);
+      case 2: return launch<true, false, false, false, false>(d, s);
+      default: return launch<true, true, false, false, false>(d, s);
+    }
+  }
+  const int c2 = d.t[1].a_row * 2 + d.t[1].b_row;
+  if (c1 == 2 && c2 == 3) return launch<true, false, true, true, true>(d, s);
+  return DUO_ERR_UNSUPPORTED;
+}
+
+}  // namespace duo

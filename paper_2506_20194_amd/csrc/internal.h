@@ -1,0 +1,71 @@
+// Declarations shared between the translation units of the library.
+#pragma once
+
+#include "common.h"
+
+namespace duo {
+
+// ---- stage 1 (hessian.hip) ----
+int64_t hessian_chunk_tokens(int64_t m, int64_t k);
+int gram_split(int64_t npairs);
+size_t hessian_ws_bytes(int64_t m, int64_t k);
+duo_status hessian_run(const void* Xs, const void* Xd, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z,
+                       float* H, int64_t ldh, float* G, int64_t ldg, float* a, void* ws, bool want_h,
+                       hipStream_t s);
+duo_status act_mask_run(const void* X, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z, uint32_t* mask,
+                        void* ws, hipStream_t s);
+
+// ---- fp32 MFMA GEMM (gemm_f32.hip) ----
+// C[i][j] = beta * C[i][j] + sum_terms alpha * sum_{l in range} A(i, l) B(l, j)
+// over the tiles selected by `tri`.
+enum { KLO_ZERO = 0, KLO_ROW = 1, KLO_COL = 2 };  // range start: 0 / tile-row start / tile-col start
+enum { KHI_FULL = 0, KHI_ROW = 1, KHI_COL = 2 };  // range end: K / tile-row end / tile-col end
+enum { TRI_ALL = 0, TRI_LOWER = 1, TRI_UPPER = 2 };
+
+struct GemmTerm {
+  const float* A;
+  int64_t lda;
+  int a_row;  // 1: A(i,l) = A[i*lda + l]; 0: A(i,l) = A[l*lda + i]
+  const float* B;
+  int64_t ldb;
+  int b_row;  // 1: B(l,j) = B[l*ldb + j]; 0: B(l,j) = B[j*ldb + l]
+  int K;
+  float alpha;
+  int klo, khi;
+};
+
+struct GemmDesc {
+  int M, N;
+  float* C;
+  int64_t ldc;
+  float beta;
+  int tri;
+  int nterms;
+  GemmTerm t[2];
+};
+
+duo_status gemm_f32(const GemmDesc& d, hipStream_t s);
+
+// ---- stage 2 (chol.hip) ----
+struct CholStatus {
+  double lambda;
+  long long fail;
+  int status;
+  int pad;
+};
+size_t chol_ws_bytes(int64_t k);
+duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hipStream_t s,
+                    CholStatus** status_dev);
+
+// ---- stage 3 (score.hip, sweep.hip) ----
+size_t score_ws_bytes(int64_t k);
+duo_status score_run(const float* L, int64_t ldl, const float* G, int64_t ldg, const float* a, int64_t k,
+                     float* D, int64_t ldd, float* fac, void* ws, hipStream_t s);
+
+size_t sweep_ws_bytes(int64_t n, int64_t k, int B);
+duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L,
+                     int64_t ldl, const float* D, int64_t ldd, const float* fac, double p_w, int B,
+                     const uint32_t* mask_in, float* W_out, void* W_out_lowp, uint32_t* mask_out,
+                     float* scores_out, void* ws, hipStream_t s);
+
+}  // namespace duo

@@ -1,0 +1,332 @@
+"""Thin Python binding of libduo.so (the gfx950 DuoGPT layer solver).
+
+The functions carry the names of the C entry points in include/duo.h and only
+marshal arguments: tensors become device pointers, the current torch stream
+becomes the HIP stream, workspaces are allocated from torch's caching
+allocator.  Every computation happens in the HIP library; if the library is
+missing or no gfx950 device is present the calls raise.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libduo.so")
+
+DUO_OK, DUO_ERR_INVALID_ARG, DUO_ERR_UNSUPPORTED, DUO_ERR_WORKSPACE = 0, 1, 2, 3
+DUO_ERR_NOT_PD, DUO_ERR_NONFINITE, DUO_ERR_HIP, DUO_ERR_NO_DEVICE = 4, 5, 6, 7
+DUO_F32, DUO_BF16 = 0, 1
+DUO_ACT_NONE, DUO_ACT_TOPK_MAG_PER_TOKEN = 0, 1
+DUO_OP_HESSIAN, DUO_OP_CHOL_INV, DUO_OP_SCORE_TERMS, DUO_OP_SWEEP, DUO_OP_PRUNE_LAYER = 0, 1, 2, 3, 4
+
+EXPORTED = (
+    "duo_workspace_size", "duo_status_string", "duo_version", "duo_act_sparsify_mask",
+    "duo_hessian_accum", "duo_residual_term", "duo_chol_inv", "duo_score_terms", "duo_sweep",
+    "duo_prune_layer",
+)
+
+
+class DuoError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+class ActRule(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("sparsity", ctypes.c_double)]
+
+
+class CholInfo(ctypes.Structure):
+    _fields_ = [("lam", ctypes.c_double), ("fail_index", ctypes.c_int64), ("status", ctypes.c_int32)]
+
+
+_lib = None
+P = ctypes.c_void_p
+I64 = ctypes.c_int64
+I32 = ctypes.c_int32
+F64 = ctypes.c_double
+SZ = ctypes.c_size_t
+
+
+def lib():
+    """The loaded library (raises when libduo.so has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        L.duo_workspace_size.restype = SZ
+        L.duo_workspace_size.argtypes = [I32, I64, I64, I64, I32]
+        L.duo_status_string.restype = ctypes.c_char_p
+        L.duo_status_string.argtypes = [I32]
+        L.duo_version.restype = ctypes.c_char_p
+        L.duo_version.argtypes = []
+        L.duo_act_sparsify_mask.restype = I32
+        L.duo_act_sparsify_mask.argtypes = [P, I32, I64, I64, I64, ActRule, P, P, SZ, P]
+        L.duo_hessian_accum.restype = I32
+        L.duo_hessian_accum.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, I64, P, P, SZ, P]
+        L.duo_residual_term.restype = I32
+        L.duo_residual_term.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, P, SZ, P]
+        L.duo_chol_inv.restype = I32
+        L.duo_chol_inv.argtypes = [P, I64, I64, F64, ctypes.POINTER(CholInfo), P, SZ, P]
+        L.duo_score_terms.restype = I32
+        L.duo_score_terms.argtypes = [P, I64, P, I64, P, I64, P, I64, P, P, SZ, P]
+        L.duo_sweep.restype = I32
+        L.duo_sweep.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, P, P, P, P, P, P, SZ, P]
+        L.duo_prune_layer.restype = I32
+        L.duo_prune_layer.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, P, P, P, P, P, P, SZ, P]
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().duo_status_string(int(status)).decode()
+
+
+def version() -> str:
+    return lib().duo_version().decode()
+
+
+def _check(status: int, where: str):
+    if status != DUO_OK:
+        raise DuoError(status, where)
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return DUO_F32
+    if t.dtype == torch.bfloat16:
+        return DUO_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _ld(t: torch.Tensor) -> int:
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a 2-d tensor with unit column stride")
+    return t.stride(0)
+
+
+def _stream(device) -> ctypes.c_void_p:
+    if torch.device(device).type != "cuda":
+        raise ValueError("duo: tensors must live on a CUDA (HIP) device")
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _same_device(*ts):
+    devs = {t.device for t in ts if t is not None}
+    if len(devs) != 1 or next(iter(devs)).type != "cuda":
+        raise ValueError("duo: all tensors must be on one CUDA (HIP) device")
+
+
+def _shape(t, shape, name):
+    if t is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"duo: {name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _contig(t, name):
+    if t is not None and not t.is_contiguous():
+        raise ValueError(f"duo: {name} must be contiguous")
+
+
+def act_rule(sparsity: float | None) -> ActRule:
+    if sparsity is None:
+        return ActRule(DUO_ACT_NONE, 0.0)
+    return ActRule(DUO_ACT_TOPK_MAG_PER_TOKEN, float(sparsity))
+
+
+def duo_workspace_size(op: int, n: int, k: int, m: int, block: int) -> int:
+    return int(lib().duo_workspace_size(op, n, k, m, block))
+
+
+def workspace(op: int, n: int, k: int, m: int, block: int, device) -> torch.Tensor:
+    """A workspace tensor for `op` (256-byte aligned by torch's allocator)."""
+    nbytes = duo_workspace_size(op, n, k, m, block)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+def duo_act_sparsify_mask(X, act_sparsity, mask_out=None, ws=None):
+    m, k = X.shape
+    _same_device(X, mask_out, ws)
+    _shape(mask_out, (m, (k + 31) // 32), "mask_out")
+    _contig(mask_out, "mask_out")
+    if mask_out is None:
+        mask_out = torch.empty((m, (k + 31) // 32), dtype=torch.int32, device=X.device)
+    if ws is None:
+        ws = workspace(DUO_OP_HESSIAN, 0, k, m, 0, X.device)
+    st = lib().duo_act_sparsify_mask(_ptr(X), _dtype(X), m, k, _ld(X), act_rule(act_sparsity), _ptr(mask_out),
+                                     _ptr(ws), ws.numel(), _stream(X.device))
+    _check(st, "duo_act_sparsify_mask")
+    return mask_out
+
+
+def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=None):
+    m, k = X_src.shape
+    _same_device(X_src, X_dense, H, G, a, ws)
+    _shape(H, (k, k), "H")
+    _shape(G, (k, k), "G")
+    _shape(a, (k,), "a")
+    _contig(a, "a")
+    if ws is None:
+        ws = workspace(DUO_OP_HESSIAN, 0, k, m, 0, X_src.device)
+    if X_dense is not None and (X_dense.shape != X_src.shape or X_dense.stride() != X_src.stride()):
+        raise ValueError("X_dense must have the shape and strides of X_src")
+    st = lib().duo_hessian_accum(_ptr(X_src), _ptr(X_dense), _dtype(X_src), m, k, _ld(X_src), act_rule(act_sparsity),
+                                 _ptr(H), _ld(H), _ptr(G), _ld(G) if G is not None else k, _ptr(a), _ptr(ws),
+                                 ws.numel(), _stream(X_src.device))
+    _check(st, "duo_hessian_accum")
+
+
+def duo_residual_term(X_dense, G, a, act_sparsity, X_src=None, ws=None):
+    m, k = X_dense.shape
+    _same_device(X_dense, X_src, G, a, ws)
+    _shape(X_src, (m, k), "X_src")
+    _shape(G, (k, k), "G")
+    _shape(a, (k,), "a")
+    _contig(a, "a")
+    if X_src is not None and X_src.stride() != X_dense.stride():
+        raise ValueError("X_src must have the strides of X_dense")
+    if ws is None:
+        ws = workspace(DUO_OP_HESSIAN, 0, k, m, 0, X_dense.device)
+    st = lib().duo_residual_term(_ptr(X_dense), _ptr(X_src), _dtype(X_dense), m, k, _ld(X_dense),
+                                 act_rule(act_sparsity), _ptr(G), _ld(G), _ptr(a), _ptr(ws), ws.numel(),
+                                 _stream(X_dense.device))
+    _check(st, "duo_residual_term")
+
+
+def duo_chol_inv(H, damp, ws=None, sync=True):
+    """In place: H becomes L.  Returns (lambda, fail_index) when sync, else None."""
+    k = H.shape[0]
+    _same_device(H, ws)
+    _shape(H, (k, k), "H")
+    if ws is None:
+        ws = workspace(DUO_OP_CHOL_INV, 0, k, 0, 0, H.device)
+    info = CholInfo()
+    st = lib().duo_chol_inv(_ptr(H), k, _ld(H), float(damp), ctypes.byref(info) if sync else None, _ptr(ws),
+                            ws.numel(), _stream(H.device))
+    _check(st, "duo_chol_inv")
+    return (info.lam, info.fail_index) if sync else None
+
+
+def duo_score_terms(L, G, a, D=None, fac=None, ws=None):
+    k = L.shape[0]
+    _same_device(L, G, a, D, fac, ws)
+    for t, nm in ((L, "L"), (G, "G"), (D, "D")):
+        _shape(t, (k, k), nm)
+    _shape(a, (k,), "a")
+    _shape(fac, (k,), "fac")
+    _contig(a, "a")
+    _contig(fac, "fac")
+    if D is None:
+        D = torch.zeros((k, k), dtype=torch.float32, device=L.device)
+    if fac is None:
+        fac = torch.empty(k, dtype=torch.float32, device=L.device)
+    if ws is None:
+        ws = workspace(DUO_OP_SCORE_TERMS, 0, k, 0, 0, L.device)
+    _shape(D, (k, k), "D")
+    _shape(fac, (k,), "fac")
+    st = lib().duo_score_terms(_ptr(L), _ld(L), _ptr(G), _ld(G), _ptr(a), k, _ptr(D), _ld(D), _ptr(fac), _ptr(ws),
+                               ws.numel(), _stream(L.device))
+    _check(st, "duo_score_terms")
+    return D, fac
+
+
+def _check_outputs(out, W):
+    n, k = W.shape
+    W_out, lowp, mask, scores = out
+    _same_device(W, W_out, lowp, mask, scores)
+    _shape(W_out, (n, k), "W_out")
+    _shape(lowp, (n, k), "W_out_lowp")
+    _shape(mask, (n, (k + 31) // 32), "mask_out")
+    _shape(scores, (n, k), "block_scores_out")
+    for t, nm in ((W_out, "W_out"), (lowp, "W_out_lowp"), (mask, "mask_out"), (scores, "block_scores_out")):
+        _contig(t, nm)
+    if W_out is None or W_out.dtype != torch.float32 or (lowp is not None and lowp.dtype != W.dtype):
+        raise ValueError("duo: W_out must be fp32 and W_out_lowp in W's dtype")
+
+
+def _sweep_outputs(W, want_lowp, want_mask, want_scores):
+    n, k = W.shape
+    dev = W.device
+    W_out = torch.empty((n, k), dtype=torch.float32, device=dev)
+    lowp = torch.empty((n, k), dtype=W.dtype, device=dev) if want_lowp else None
+    mask = torch.empty((n, (k + 31) // 32), dtype=torch.int32, device=dev) if want_mask else None
+    scores = torch.empty((n, k), dtype=torch.float32, device=dev) if want_scores else None
+    return W_out, lowp, mask, scores
+
+
+def duo_sweep(W, L, D, fac, w_sparsity, block=128, mask_in=None, want_lowp=False, want_mask=True,
+              want_scores=False, ws=None, out=None):
+    n, k = W.shape
+    _same_device(W, L, D, fac, mask_in, ws)
+    _shape(L, (k, k), "L")
+    _shape(D, (k, k), "D")
+    _shape(fac, (k,), "fac")
+    _contig(fac, "fac")
+    _shape(mask_in, (n, (k + 31) // 32), "mask_in")
+    _contig(mask_in, "mask_in")
+    if ws is None:
+        ws = workspace(DUO_OP_SWEEP, n, k, 0, block, W.device)
+    W_out, lowp, mask, scores = out if out is not None else _sweep_outputs(W, want_lowp, want_mask, want_scores)
+    _check_outputs((W_out, lowp, mask, scores), W)
+    st = lib().duo_sweep(_ptr(W), _dtype(W), n, k, _ld(W), _ptr(L), _ld(L), _ptr(D), _ld(D), _ptr(fac),
+                         float(w_sparsity), int(block), _ptr(mask_in), _ptr(W_out), _ptr(lowp), _ptr(mask),
+                         _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
+    _check(st, "duo_sweep")
+    return W_out, lowp, mask, scores
+
+
+def duo_prune_layer(W, L, G, a, w_sparsity, block=128, mask_in=None, want_lowp=False, want_mask=True,
+                    want_scores=False, ws=None, out=None):
+    n, k = W.shape
+    _same_device(W, L, G, a, mask_in, ws)
+    _shape(L, (k, k), "L")
+    _shape(G, (k, k), "G")
+    _shape(a, (k,), "a")
+    _contig(a, "a")
+    _shape(mask_in, (n, (k + 31) // 32), "mask_in")
+    _contig(mask_in, "mask_in")
+    if ws is None:
+        ws = workspace(DUO_OP_PRUNE_LAYER, n, k, 0, block, W.device)
+    W_out, lowp, mask, scores = out if out is not None else _sweep_outputs(W, want_lowp, want_mask, want_scores)
+    _check_outputs((W_out, lowp, mask, scores), W)
+    st = lib().duo_prune_layer(_ptr(W), _dtype(W), n, k, _ld(W), _ptr(L), _ld(L), _ptr(G), _ld(G), _ptr(a),
+                               float(w_sparsity), int(block), _ptr(mask_in), _ptr(W_out), _ptr(lowp), _ptr(mask),
+                               _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
+    _check(st, "duo_prune_layer")
+    return W_out, lowp, mask, scores
+
+
+def unpack_mask(words: torch.Tensor, k: int) -> torch.Tensor:
+    """Bit-packed (rows x ceil(k/32) int32) mask -> bool rows x k (device-side
+    bit extraction by torch; used for inspection only)."""
+    w = words.to(torch.int64) & 0xFFFFFFFF
+    bits = (w.unsqueeze(-1) >> torch.arange(32, device=words.device)) & 1
+    return bits.reshape(words.shape[0], -1)[:, :k].bool()
+
+
+def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=None, want_lowp=True):
+    """DuoGPT on one linear layer (stages 1-3 on the device).
+
+    W: n x k (out x in), X: m x k token-major calibration input of the pruned
+    stream (sparsified per token), X_dense: the dense stream (defaults to X).
+    Returns dict(W_out fp32, W_lowp in W's dtype, mask (bool n x k), lam).
+    """
+    n, k = W.shape
+    dev = W.device
+    H = torch.zeros((k, k), dtype=torch.float32, device=dev)
+    G = torch.zeros((k, k), dtype=torch.float32, device=dev)
+    a = torch.zeros(k, dtype=torch.float32, device=dev)
+    duo_hessian_accum(X, H, act_sparsity, X_dense=X_dense, G=G, a=a)
+    lam, _ = duo_chol_inv(H, damp)
+    W_out, lowp, mask, _ = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp)
+    return dict(W_out=W_out, W_lowp=lowp, mask=unpack_mask(mask, k), lam=lam)

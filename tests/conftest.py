@@ -16,3 +16,15 @@ def pytest_configure(config):
 @pytest.fixture(scope="session")
 def rng_seed():
     return 1234
+
+
+@pytest.fixture(scope="session")
+def duo_lib():
+    """The built library; builds it once if it is missing."""
+    from paper_2506_20194_amd import duo
+
+    if not os.path.exists(duo.LIB_PATH):
+        from paper_2506_20194_amd import build
+
+        build.build()
+    return duo

@@ -1,0 +1,129 @@
+"""Host-side checks of the C ABI (no GPU needed): every symbol declared in
+include/duo.h is exported, workspace sizes are sane, and argument errors are
+rejected before any device work (a call with valid arguments reports
+DUO_ERR_NO_DEVICE here, proving it got past validation)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "duo.h")
+FAKE = ctypes.c_void_p(1 << 20)      # never dereferenced on the host
+WS = ctypes.c_void_p(256 << 20)      # 256-byte aligned fake workspace
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(duo_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_named_entry_points():
+    names = declared_functions()
+    for n in ("duo_hessian_accum", "duo_residual_term", "duo_chol_inv", "duo_prune_layer"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(duo_lib):
+    L = duo_lib.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    assert set(duo_lib.EXPORTED) == set(declared_functions())
+
+
+def test_status_strings_and_version(duo_lib):
+    for s in range(8):
+        assert duo_lib.status_string(s) not in ("", "unknown status")
+    assert duo_lib.status_string(99) == "unknown status"
+    assert "gfx950" in duo_lib.version()
+
+
+def test_workspace_sizes(duo_lib):
+    ws = duo_lib.duo_workspace_size
+    assert ws(duo_lib.DUO_OP_HESSIAN, 0, 512, 2048, 0) > 0
+    assert ws(duo_lib.DUO_OP_HESSIAN, 0, 4096, 131072, 0) >= ws(duo_lib.DUO_OP_HESSIAN, 0, 4096, 1024, 0)
+    assert ws(duo_lib.DUO_OP_CHOL_INV, 0, 4096, 0, 0) >= 4096 * 4096 // 4 * 4
+    assert ws(duo_lib.DUO_OP_PRUNE_LAYER, 4096, 4096, 0, 128) > ws(duo_lib.DUO_OP_SWEEP, 4096, 4096, 0, 128)
+    assert ws(duo_lib.DUO_OP_SWEEP, 16, 16, 0, 0) == 0          # bad block
+    assert ws(duo_lib.DUO_OP_SWEEP, 16, 16, 0, 129) == 0
+    assert ws(duo_lib.DUO_OP_CHOL_INV, 0, 0, 0, 0) == 0         # bad k
+    assert ws(duo_lib.DUO_OP_CHOL_INV, 0, 40000, 0, 0) == 0     # beyond the k limit
+    assert ws(99, 1, 1, 1, 1) == 0
+
+
+def _rule(p=0.5, kind=1):
+    from paper_2506_20194_amd.duo import ActRule
+
+    return ActRule(kind, p)
+
+
+def test_hessian_argument_errors(duo_lib):
+    L = duo_lib.lib()
+    E, NODEV = duo_lib.DUO_ERR_INVALID_ARG, duo_lib.DUO_ERR_NO_DEVICE
+    big = 10 ** 10
+
+    def call(X=FAKE, Xd=None, dt=1, m=64, k=32, ldx=32, rule=None, H=FAKE, ldh=32, G=None, ldg=32, a=None, ws=WS,
+             wsb=big):
+        return L.duo_hessian_accum(X, Xd, dt, m, k, ldx, rule or _rule(), H, ldh, G, ldg, a, ws, wsb, None)
+
+    assert call() == NODEV
+    assert call(X=None) == E
+    assert call(H=None) == E
+    assert call(dt=7) == E
+    assert call(m=-1) == E
+    assert call(k=0) == E
+    assert call(k=40000, ldx=40000, ldh=40000) == duo_lib.DUO_ERR_UNSUPPORTED
+    assert call(ldx=31) == E
+    assert call(ldh=31) == E
+    assert call(G=FAKE) == E                     # G without a
+    assert call(G=FAKE, a=FAKE, ldg=8) == E
+    assert call(rule=_rule(1.5)) == E
+    assert call(rule=_rule(float("nan"))) == E
+    assert call(rule=_rule(0.5, kind=9)) == E
+    assert call(ws=None) == duo_lib.DUO_ERR_WORKSPACE
+    assert call(wsb=16) == duo_lib.DUO_ERR_WORKSPACE
+    assert call(ws=ctypes.c_void_p((256 << 20) + 8)) == duo_lib.DUO_ERR_WORKSPACE
+    assert call(m=0) == duo_lib.DUO_OK           # nothing to do, nothing enqueued
+    assert L.duo_residual_term(None, None, 1, 64, 32, 32, _rule(), FAKE, 32, FAKE, WS, big, None) == E
+    assert L.duo_residual_term(FAKE, None, 1, 64, 32, 32, _rule(), FAKE, 32, FAKE, WS, big, None) == NODEV
+
+
+def test_chol_and_sweep_argument_errors(duo_lib):
+    L = duo_lib.lib()
+    E, NODEV = duo_lib.DUO_ERR_INVALID_ARG, duo_lib.DUO_ERR_NO_DEVICE
+    big = 10 ** 10
+    assert L.duo_chol_inv(FAKE, 64, 64, 0.01, None, WS, big, None) == NODEV
+    assert L.duo_chol_inv(None, 64, 64, 0.01, None, WS, big, None) == E
+    assert L.duo_chol_inv(FAKE, 64, 63, 0.01, None, WS, big, None) == E
+    assert L.duo_chol_inv(FAKE, 64, 64, -1.0, None, WS, big, None) == E
+    assert L.duo_chol_inv(FAKE, 64, 64, float("inf"), None, WS, big, None) == E
+    assert L.duo_chol_inv(FAKE, 64, 64, 0.01, None, WS, 8, None) == duo_lib.DUO_ERR_WORKSPACE
+    assert L.duo_score_terms(FAKE, 64, FAKE, 64, FAKE, 64, FAKE, 64, FAKE, WS, big, None) == NODEV
+    assert L.duo_score_terms(FAKE, 64, None, 64, FAKE, 64, FAKE, 64, FAKE, WS, big, None) == E
+
+    def sweep(W=FAKE, dt=1, n=32, k=64, ldw=64, p=0.5, B=16, Wo=FAKE, fn=L.duo_sweep):
+        return fn(W, dt, n, k, ldw, FAKE, 64, FAKE, 64, FAKE, p, B, None, Wo, None, None, None, WS, big, None)
+
+    for fn in (L.duo_sweep, L.duo_prune_layer):
+        assert sweep(fn=fn) == NODEV
+        assert sweep(W=None, fn=fn) == E
+        assert sweep(Wo=None, fn=fn) == E
+        assert sweep(n=0, fn=fn) == E
+        assert sweep(ldw=60, fn=fn) == E
+        assert sweep(p=-0.1, fn=fn) == E
+        assert sweep(p=1.01, fn=fn) == E
+        assert sweep(B=0, fn=fn) == E
+        assert sweep(B=129, fn=fn) == E
+        assert sweep(dt=3, fn=fn) == E
+
+
+def test_binding_refuses_host_tensors(duo_lib):
+    import torch
+
+    H = torch.zeros((8, 8))
+    with pytest.raises(ValueError):
+        duo_lib.duo_chol_inv(H, 0.01, ws=torch.zeros(1 << 20, dtype=torch.uint8))
+    with pytest.raises(ValueError):
+        duo_lib.prune_linear(torch.zeros(4, 8), torch.zeros(16, 8), 0.5, 0.5)
