@@ -1,0 +1,188 @@
+#!/usr/bin/env python3
+"""Benchmark of the DuoGPT layer solver on one MI355X.
+
+One step = the whole per-layer path on the device: activation sparsification
+and H/G/a accumulation, damped inverse Cholesky, score terms and the blocked
+column sweep with lazy updates, for one LLaMA-shaped linear layer with its
+calibration tokens already resident in HBM.  Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X dense fp32 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="llama2_7b_q_proj")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(W, X, c):
+    """The float64 oracle, untuned, on a bounded sample of the same layer:
+    stage 1 on the first 1024 tokens, stages 2-3 precompute at full width,
+    the sweep on the first 64 rows; each part scaled to the full layer."""
+    import numpy as np
+
+    from oracle import duo_ref as R
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    n, k, m = c["n"], c["k"], c["m"]
+    ms, ns = min(1024, m), min(64, n)
+    Xs = X[:ms].float().cpu().numpy()
+    Ws = W[:ns].float().cpu().numpy()
+    t = time.perf_counter()
+    H, G, a = R.hessian_terms(Xs, c["p_x"])
+    t1 = time.perf_counter() - t
+    t = time.perf_counter()
+    L, _ = R.inverse_cholesky(H, c["damp"])
+    t2 = time.perf_counter() - t
+    t = time.perf_counter()
+    fac, D, _ = R.score_terms(G, L, a)
+    t3 = time.perf_counter() - t
+    t = time.perf_counter()
+    R.sweep_blocked(Ws, L, D, fac, c["p_w"], c["block"])
+    t4 = time.perf_counter() - t
+    est = t1 * (m / ms) + t2 + t3 + t4 * (n / ns)
+    return {
+        "value": est, "unit": "s/layer", "cores": cores, "kind": "oracle",
+        "sample": f"stage 1 on {ms} of {m} tokens (x{m / ms:g}), inverse Cholesky and score terms at full k={k}, "
+                  f"sweep on {ns} of {n} rows (x{n / ns:g}); measured {t1 + t2 + t3 + t4:.1f} s of CPU work",
+        "stage_s": {"hessian": t1 * (m / ms), "chol_inv": t2, "score_terms": t3, "sweep": t4 * (n / ns)},
+        "cpu": platform.processor() or platform.machine(),
+        "blas": str(np.__config__.CONFIG.get("Build Dependencies", {}).get("blas", {}).get("name", "?")),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the multi-GPU path is a design note, not implemented", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2506_20194_amd import duo
+    from workloads import synth
+
+    c = synth.CONFIGS[args.workload]
+    n, k, m, B = c["n"], c["k"], c["m"], c["block"]
+    dev = torch.device("cuda:0")
+    W, X = synth.config_inputs(args.workload, device=dev)
+    H = torch.zeros((k, k), dtype=torch.float32, device=dev)
+    G = torch.zeros((k, k), dtype=torch.float32, device=dev)
+    a = torch.zeros(k, dtype=torch.float32, device=dev)
+    ws_h = duo.workspace(duo.DUO_OP_HESSIAN, 0, k, m, 0, dev)
+    ws_c = duo.workspace(duo.DUO_OP_CHOL_INV, 0, k, 0, 0, dev)
+    ws_p = duo.workspace(duo.DUO_OP_PRUNE_LAYER, n, k, 0, B, dev)
+    W_out = torch.empty((n, k), dtype=torch.float32, device=dev)
+    lowp = torch.empty((n, k), dtype=W.dtype, device=dev)
+    mask = torch.empty((n, (k + 31) // 32), dtype=torch.int32, device=dev)
+
+    def step(check=False):
+        H.zero_()
+        G.zero_()
+        a.zero_()
+        duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h)
+        info = duo.duo_chol_inv(H, c["damp"], ws=ws_c, sync=check)
+        duo.duo_prune_layer(W, H, G, a, c["p_w"], B, ws=ws_p, out=(W_out, lowp, mask, None))
+        return info
+
+    lam, fail = step(check=True)  # also checks that the damped Hessian factors
+    assert fail == -1
+    for _ in range(max(0, args.warmup - 1)):
+        step()
+    torch.cuda.synchronize()
+    duo.duo_profile_enable(True)
+    for name in duo.PROF:
+        duo.duo_profile_read(name)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    duo.duo_profile_enable(False)
+    ms_step = e0.elapsed_time(e1) / args.steps
+    prof = {name: duo.duo_profile_read(name) for name in duo.PROF}
+
+    # sanity: exact number of pruned weights
+    kept = int(duo.unpack_mask(mask, k).sum().item())
+    expect_pruned = int((c["p_w"] * n * k) + 0.5)
+    assert n * k - kept == expect_pruned, (n * k - kept, expect_pruned)
+
+    per = lambda name: prof[name][0] / max(prof[name][1], 1)     # ms per launch
+    per_step = lambda name: prof[name][0] / args.steps              # ms per layer
+    gram_flop_step = (k * (k + 1) + 2 * k * k) * m                  # H lower triangle + G
+    gram_launches = prof["gram"][1] / args.steps
+    gram_tflops = gram_flop_step / gram_launches / (per("gram") * 1e-3) / 1e12
+    hess_flop = (3 * k * k + k) * m
+    hess_tflops = hess_flop / (per_step("hessian") * 1e-3) / 1e12
+    sweep_bytes = 16 * n * k
+    sweep_ms = per_step("select") + per_step("inblock")
+    sweep_gbs = sweep_bytes / (sweep_ms * 1e-3) / 1e9
+    trail_flop = 2 * n * k * (k - B)
+    trail_tflops = trail_flop / (per_step("trail") * 1e-3) / 1e12
+    chol_score_flop = 8 * k ** 3 / 3
+    line = {
+        "metric": "s/layer for OBC prune of LLaMA-shaped linears; Hessian TFLOP/s; sweep GB/s",
+        "value": ms_step / 1e3,
+        "unit": "s/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 MFMA (H, G) + fp32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "n": n, "k": k, "m": m, "p_x": c["p_x"], "p_w": c["p_w"],
+                   "block": B, "damp": c["damp"], "x_dtype": str(c["x_dtype"]).replace("torch.", ""),
+                   "inputs": c["kind"], "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "gram_kernel (H, G)", "achieved": gram_tflops,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": gram_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": None, "ms_per_launch": per("gram"), "flop_per_launch": gram_flop_step / gram_launches},
+        "hessian_tflops": hess_tflops,
+        "hessian_frac": hess_tflops / PEAK_BF16_TFLOPS,
+        "sweep_gbs": sweep_gbs,
+        "sweep_frac": sweep_gbs / PEAK_HBM_GBS,
+        "trailing_tflops": trail_tflops,
+        "trailing_frac": trail_tflops / PEAK_FP32_TFLOPS,
+        "chol_score_tflops": chol_score_flop / ((per_step("chol") + per_step("score")) * 1e-3) / 1e12,
+        "stage_ms": {name: per_step(name) for name in duo.PROF},
+        "wall_s_timed": wall,
+        "lambda": lam,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(W, X, c)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

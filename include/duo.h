@@ -214,6 +214,27 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
                            void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws,
                            size_t ws_bytes, void* stream);
 
+/*
+ * Kernel timing for benchmarks (not part of the method).  With profiling on,
+ * every launch of the tracked kernels is bracketed by HIP events on the
+ * stream it runs on.  duo_profile_read waits for the recorded events and
+ * returns the summed time (milliseconds) and the number of launches since the
+ * last read, then resets them.  Single-threaded use only.
+ */
+enum {
+  DUO_PROF_GRAM = 0,     /* stage 1: MFMA Gram kernel (H, G)                   */
+  DUO_PROF_HESSIAN = 1,  /* stage 1: whole duo_hessian_accum call              */
+  DUO_PROF_CHOL = 2,     /* stage 2: whole duo_chol_inv call                   */
+  DUO_PROF_SCORE = 3,    /* stage 3: Q, fac, D                                 */
+  DUO_PROF_SWEEP = 4,    /* stage 3: whole sweep (select, in-block, lazy)      */
+  DUO_PROF_INBLOCK = 5,  /* stage 3: in-block kernel, one launch per block     */
+  DUO_PROF_TRAIL = 6,    /* stage 3: lazy trailing-update GEMM, one per block  */
+  DUO_PROF_SELECT = 7,   /* stage 3: mask selection passes of one block        */
+  DUO_PROF_COUNT = 8
+};
+duo_status duo_profile_enable(int32_t on);
+duo_status duo_profile_read(int32_t kernel, double* total_ms, int64_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

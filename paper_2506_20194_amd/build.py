@@ -11,12 +11,15 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libduo.so")
-SOURCES = ["abi.hip", "hessian.hip", "gemm_f32.hip", "chol.hip", "score.hip", "sweep.hip"]
+SOURCES = ["abi.hip", "hessian.hip", "gemm_f32.hip", "chol.hip", "score.hip", "sweep.hip", "profile.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep MFMA accumulators in VGPRs: the AGPR form made the compiler copy every
+    # accumulator between register files on each pipeline stage
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I", INCLUDE, "-I", CSRC,
 ]
 

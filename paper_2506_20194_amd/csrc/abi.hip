@@ -137,8 +137,11 @@ static duo_status hessian_common(const void* X_src, const void* X_dense, int32_t
   if (!ws_ok(ws, ws_bytes, hessian_ws_bytes(m, k))) return DUO_ERR_WORKSPACE;
   duo_status d = device_ok();
   if (d != DUO_OK) return d;
-  return hessian_run(X_src, X_dense, x_dtype, m, k, ldx, zero_count(rule, k), H, ldh, G, ldg, a, ws, want_h,
-                     (hipStream_t)stream);
+  prof_begin(DUO_PROF_HESSIAN, (hipStream_t)stream);
+  duo_status r = hessian_run(X_src, X_dense, x_dtype, m, k, ldx, zero_count(rule, k), H, ldh, G, ldg, a, ws,
+                             want_h, (hipStream_t)stream);
+  prof_end(DUO_PROF_HESSIAN, (hipStream_t)stream);
+  return r;
 }
 
 duo_status duo_hessian_accum(const void* X_src, const void* X_dense, int32_t x_dtype, int64_t m, int64_t k,
@@ -165,7 +168,9 @@ duo_status duo_chol_inv(float* H_inout, int64_t k, int64_t ldh, double damp_rati
   if (d != DUO_OK) return d;
   CholStatus* st = nullptr;
   const hipStream_t s = (hipStream_t)stream;
+  prof_begin(DUO_PROF_CHOL, s);
   duo_status r = chol_run(H_inout, k, ldh, damp_ratio, ws, s, &st);
+  prof_end(DUO_PROF_CHOL, s);
   if (r != DUO_OK) return r;
   if (!info) return DUO_OK;
   CholStatus h;
@@ -185,7 +190,10 @@ duo_status duo_score_terms(const float* L, int64_t ldl, const float* G, int64_t 
   if (!ws_ok(ws, ws_bytes, score_ws_bytes(k))) return DUO_ERR_WORKSPACE;
   duo_status d = device_ok();
   if (d != DUO_OK) return d;
-  return score_run(L, ldl, G, ldg, a, k, D, ldd, fac, ws, (hipStream_t)stream);
+  prof_begin(DUO_PROF_SCORE, (hipStream_t)stream);
+  duo_status r = score_run(L, ldl, G, ldg, a, k, D, ldd, fac, ws, (hipStream_t)stream);
+  prof_end(DUO_PROF_SCORE, (hipStream_t)stream);
+  return r;
 }
 
 static duo_status sweep_args(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, double w_sparsity,
@@ -208,8 +216,11 @@ duo_status duo_sweep(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   if (!ws_ok(ws, ws_bytes, sweep_ws_bytes(n, k, block))) return DUO_ERR_WORKSPACE;
   duo_status d = device_ok();
   if (d != DUO_OK) return d;
-  return sweep_run(W, w_dtype, n, k, ldw, L, ldl, D, ldd, fac, w_sparsity, block, mask_in, W_out, W_out_lowp,
-                   mask_out, block_scores_out, ws, (hipStream_t)stream);
+  prof_begin(DUO_PROF_SWEEP, (hipStream_t)stream);
+  duo_status r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, D, ldd, fac, w_sparsity, block, mask_in, W_out,
+                           W_out_lowp, mask_out, block_scores_out, ws, (hipStream_t)stream);
+  prof_end(DUO_PROF_SWEEP, (hipStream_t)stream);
+  return r;
 }
 
 duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L,
@@ -225,10 +236,15 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   if (d != DUO_OK) return d;
   const PruneWs w = carve_prune(ws, n, k, block);
   const hipStream_t s = (hipStream_t)stream;
+  prof_begin(DUO_PROF_SCORE, s);
   duo_status r = score_run(L, ldl, G, ldg, a, k, w.D, k, w.fac, w.score, s);
+  prof_end(DUO_PROF_SCORE, s);
   if (r != DUO_OK) return r;
-  return sweep_run(W, w_dtype, n, k, ldw, L, ldl, w.D, k, w.fac, w_sparsity, block, mask_in, W_out, W_out_lowp,
-                   mask_out, block_scores_out, w.sweep, s);
+  prof_begin(DUO_PROF_SWEEP, s);
+  r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, w.D, k, w.fac, w_sparsity, block, mask_in, W_out, W_out_lowp,
+                mask_out, block_scores_out, w.sweep, s);
+  prof_end(DUO_PROF_SWEEP, s);
+  return r;
 }
 
 }  // extern "C"

@@ -18,6 +18,8 @@
 //   4. L = N^T written to the lower triangle; the strict upper set to zero.
 #include <hip/hip_runtime.h>
 
+#include <utility>
+
 #include "internal.h"
 
 namespace duo {
@@ -49,63 +51,125 @@ __global__ __launch_bounds__(256) void damp_kernel(float* H, int64_t ldh, int k,
   for (int i = threadIdx.x; i < k; i += 256) H[(int64_t)i * ldh + i] += lf;
 }
 
-// Factor the s x s diagonal block at (r0, r0) from its upper triangle:
-// A = V V^T with V upper, eliminating the last column first.  V overwrites
-// the block's upper triangle (lower set to 0); V^-1 goes to `vinv`
-// (128 x 128, row-major, zeros below the diagonal).
-__global__ __launch_bounds__(256) void diag_factor_kernel(float* H, int64_t ldh, int r0, int s, float* vinv,
+// Factor the s x s diagonal block at (r0, r0), s <= 128, read from its upper
+// triangle: A = V V^T with V upper, eliminating the last column first, and
+// return N = V^-1 (upper; zeros below the diagonal) in `vinv` (128 x 128,
+// row-major).  V itself is not needed by the callers and is not stored.
+//
+// 192 threads; thread (h, q) keeps rows 64h..64h+63 of column q in registers
+// (h = 0 for q < 64; h = 0, 1 for q >= 64: the lower-left quadrant is never
+// needed).  Step c (c = s-1 .. 0) broadcasts column c of the working matrix
+// and row c of N through LDS (one barrier per step):
+//   columns q < c:  A[r][q] -= A[r][c] A[q][c] / A[c][c]       (factorisation)
+//   column  q = c:  N[r][c]  = -A[r][c] / A[c][c], N[c][c] = 1 / sqrt(A[c][c])
+//   columns q > c:  N[c][q] /= V[c][c]; N[r][q] -= V[r][c] N[c][q]  (r < c)
+// The last two are back substitution of V N = I, driven by the same column c.
+// Padding rows/columns beyond s are an identity block.
+struct DiagCtx {
+  float* colbuf;  // [2][128]
+  float* rowbuf;  // [2][128]
+  float* pivbuf;  // [2]
+  CholStatus* st;
+  int tid, h, q, r0, hh, buf;
+};
+
+// One elimination step for column c = 64*hh + I0 (I0 a compile-time constant so
+// that every register index below is static).
+template <int I0>
+__device__ __forceinline__ void diag_step(float (&x)[64], DiagCtx& d) {
+  const int hh = d.hh, h = d.h, q = d.q;
+  const int c = 64 * hh + I0;
+  float* colbuf = d.colbuf + d.buf * kTile;
+  float* rowbuf = d.rowbuf + d.buf * kTile;
+  if (q == c) {
+    float4* cb = (float4*)&colbuf[64 * h];
+    if (h < hh) {
+#pragma unroll
+      for (int i = 0; i < 64; i += 4) cb[i / 4] = make_float4(x[i], x[i + 1], x[i + 2], x[i + 3]);
+    } else if (h > hh) {
+#pragma unroll
+      for (int i = 0; i < 64; i += 4) cb[i / 4] = make_float4(0.f, 0.f, 0.f, 0.f);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 64; ++i) colbuf[64 * h + i] = i < I0 ? x[i] : 0.f;
+      d.pivbuf[d.buf] = x[I0];
+    }
+  }
+  if (h == hh && q > c) rowbuf[q] = x[I0];
+  __syncthreads();
+  const float piv = d.pivbuf[d.buf];
+  if (d.tid == 0 && !(piv > 0.f) && d.st->status == DUO_OK) {
+    d.st->status = DUO_ERR_NOT_PD;
+    d.st->fail = d.r0 + c;
+  }
+  const float inv = 1.0f / sqrtf(piv);
+  const float inv2 = inv * inv;
+  if (q == c) {
+    // column c of N: N[r][c] = -A[r][c] / A[c][c] for r < c (x[i] holds A[r][c])
+    if (h < hh) {
+#pragma unroll
+      for (int i = 0; i < 64; ++i) x[i] = -x[i] * inv2;
+    } else if (h == hh) {
+#pragma unroll
+      for (int i = 0; i < I0; ++i) x[i] = -x[i] * inv2;
+    }
+  } else if (64 * h < c) {
+    // columns q < c (factorisation) and q > c (back substitution) share one
+    // FMA stream; colbuf rows >= c are zero
+    const float coef = q < c ? inv2 * colbuf[q] : inv2 * rowbuf[q];
+    const float4* cb = (const float4*)&colbuf[64 * h];
+#pragma unroll
+    for (int i = 0; i < 64; i += 4) {
+      const float4 v = cb[i / 4];
+      x[i] = fmaf(-v.x, coef, x[i]);
+      x[i + 1] = fmaf(-v.y, coef, x[i + 1]);
+      x[i + 2] = fmaf(-v.z, coef, x[i + 2]);
+      x[i + 3] = fmaf(-v.w, coef, x[i + 3]);
+    }
+  }
+  if (h == hh) {
+    if (q > c) x[I0] = x[I0] * inv;
+    if (q == c) x[I0] = inv;
+  }
+  d.buf ^= 1;
+}
+
+template <int... Is>
+__device__ __forceinline__ void diag_steps(float (&x)[64], DiagCtx& d, std::integer_sequence<int, Is...>) {
+  (diag_step<63 - Is>(x, d), ...);  // columns 64*hh + 63 down to 64*hh
+}
+
+__global__ __launch_bounds__(192) void diag_factor_kernel(const float* H, int64_t ldh, int r0, int s, float* vinv,
                                                           CholStatus* st) {
-  __shared__ float A[kTile][kTile + 1];
-  __shared__ float N[kTile][kTile + 1];
-  __shared__ float invd[kTile];
+  __shared__ __attribute__((aligned(16))) float colbuf[2][kTile];
+  __shared__ float rowbuf[2][kTile];
+  __shared__ float pivbuf[2];
   const int tid = threadIdx.x;
-  for (int e = tid; e < kTile * kTile; e += 256) {
-    const int r = e / kTile, c = e % kTile;
+  const int w = tid >> 6, lane = tid & 63;
+  const int h = w == 2 ? 1 : 0;
+  const int q = w == 0 ? lane : 64 + lane;
+  float x[64];
+#pragma unroll
+  for (int i = 0; i < 64; ++i) {
+    const int r = 64 * h + i;
     float v = 0.f;
-    if (r < s && c < s) v = r <= c ? H[(int64_t)(r0 + r) * ldh + r0 + c] : H[(int64_t)(r0 + c) * ldh + r0 + r];
-    A[r][c] = v;
-    N[r][c] = 0.f;
+    if (r < s && q < s)
+      v = r <= q ? H[(int64_t)(r0 + r) * ldh + r0 + q] : H[(int64_t)(r0 + q) * ldh + r0 + r];
+    else if (r == q)
+      v = 1.f;
+    x[i] = v;
   }
-  __syncthreads();
-  for (int c = s - 1; c >= 0; --c) {
-    const float piv = A[c][c];
-    const float d = sqrtf(piv);
-    if (tid == 0 && !(piv > 0.f) && st->status == DUO_OK) {
-      st->status = DUO_ERR_NOT_PD;
-      st->fail = r0 + c;
-    }
-    __syncthreads();  // everyone has read the pivot
-    if (tid < c) A[tid][c] = A[tid][c] / d;
-    if (tid == 0) A[c][c] = d;
-    __syncthreads();
-    for (int e = tid; e < c * c; e += 256) {
-      const int r = e / c, q = e % c;
-      if (r <= q) A[r][q] -= A[r][c] * A[q][c];
-    }
-    __syncthreads();
+  DiagCtx d{&colbuf[0][0], &rowbuf[0][0], pivbuf, st, tid, h, q, r0, 1, 0};
+  diag_steps(x, d, std::make_integer_sequence<int, 64>{});
+  d.hh = 0;
+  diag_steps(x, d, std::make_integer_sequence<int, 64>{});
+  // N (upper, rows <= q) to vinv; everything else 0
+#pragma unroll
+  for (int i = 0; i < 64; ++i) {
+    const int r = 64 * h + i;
+    vinv[r * kTile + q] = (r <= q && r < s && q < s) ? x[i] : 0.f;
   }
-  // N = V^-1, row by row from the bottom; two threads per column
-  if (tid < s) invd[tid] = 1.0f / A[tid][tid];
-  __syncthreads();
-  const int col = tid >> 1, half = tid & 1;
-  for (int r = s - 1; r >= 0; --r) {
-    float part = 0.f;
-    if (col > r && col < s)
-      for (int q = r + 1 + half; q <= col; q += 2) part += A[r][q] * N[q][col];
-    part += __shfl_xor(part, 1);
-    if (half == 0 && col < s) {
-      if (col == r)
-        N[r][col] = invd[r];
-      else if (col > r)
-        N[r][col] = -part * invd[r];
-    }
-    __syncthreads();
-  }
-  for (int e = tid; e < kTile * kTile; e += 256) {
-    const int r = e / kTile, c = e % kTile;
-    vinv[e] = (r < s && c < s) ? N[r][c] : 0.f;
-    if (r < s && c < s) H[(int64_t)(r0 + r) * ldh + r0 + c] = r <= c ? A[r][c] : 0.f;
-  }
+  for (int e = tid; e < 64 * 64; e += 192) vinv[(64 + e / 64) * kTile + (e % 64)] = 0.f;  // lower-left quadrant
 }
 
 // Copy the inverted diagonal blocks into place (full 128 x 128 incl. zeros).
@@ -217,7 +281,7 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
   for (int b = T - 1; b >= 0; --b) {
     const int r0 = b * kTile;
     const int sz = (int)((int64_t)r0 + kTile <= k ? kTile : k - r0);
-    hipLaunchKernelGGL(diag_factor_kernel, dim3(1), dim3(256), 0, s, H, ldh, r0, sz,
+    hipLaunchKernelGGL(diag_factor_kernel, dim3(1), dim3(192), 0, s, (const float*)H, ldh, r0, sz,
                        w.vinv + (int64_t)b * kTile * kTile, w.st);
     DUO_LAUNCH_CHECK();
     if (r0 == 0) break;

@@ -690,6 +690,7 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
     A.ldg = ldg;
     A.part = w.part;
     const int nunits = npairs * nseg;
+    prof_begin(DUO_PROF_GRAM, s);
     constexpr bool kLoOk = sizeof(T) == 2;  // the low part of dX exists for bf16 only
     if (want_h && want_g) {
       if constexpr (kLoOk)
@@ -704,6 +705,7 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
       else
         st = launch_gram<T, false, true, false>(A, nunits, s);
     }
+    prof_end(DUO_PROF_GRAM, s);
     if (st != DUO_OK) return st;
     if (nseg > 1) {
       hipLaunchKernelGGL(gram_reduce_kernel<T>, dim3(npairs * 3, (kTile * kTile) / (256 * 16)), dim3(256), 0, s, A,

@@ -5,6 +5,10 @@
 
 namespace duo {
 
+// ---- optional event timing (profile.hip) ----
+void prof_begin(int id, hipStream_t s);
+void prof_end(int id, hipStream_t s);
+
 // ---- stage 1 (hessian.hip) ----
 int64_t hessian_chunk_tokens(int64_t m, int64_t k);
 int gram_split(int64_t npairs);

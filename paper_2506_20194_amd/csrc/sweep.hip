@@ -363,6 +363,7 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     else if (z >= total)
       mode = MODE_PRUNE_ALL;
     const int pgrid = (int)(cdiv(total, 256 * 8) < 1024 ? cdiv(total, 256 * 8) : 1024);
+    prof_begin(DUO_PROF_SELECT, s);
     if (mode == MODE_SELECT) {
       hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist, (uint32_t)z);
       DUO_LAUNCH_CHECK();
@@ -376,9 +377,12 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
                          fac, w.st, w.hist, 0, 0, scores_out);
       DUO_LAUNCH_CHECK();
     }
+    prof_end(DUO_PROF_SELECT, s);
+    prof_begin(DUO_PROF_INBLOCK, s);
     hipLaunchKernelGGL(inblock_kernel, dim3((unsigned)cdiv(n, RPB)), dim3(256), lds, s, W_out, (int)n, (int)k, (int)j0,
                        Bb, B, L, ldl, D, ldd, fac, (const SelState*)w.st, mode, mask_in, w.EW, w.bmask);
     DUO_LAUNCH_CHECK();
+    prof_end(DUO_PROF_INBLOCK, s);
     if (j1 < k) {
       GemmDesc g{};
       g.M = (int)n;
@@ -390,7 +394,9 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
       g.nterms = 2;
       g.t[0] = GemmTerm{w.EW, 2 * B, 1, L + j1 * ldl + j0, ldl, 0, Bb, -1.f, KLO_ZERO, KHI_FULL};
       g.t[1] = GemmTerm{w.EW + B, 2 * B, 1, D + j0 * ldd + j1, ldd, 1, Bb, 1.f, KLO_ZERO, KHI_FULL};
+      prof_begin(DUO_PROF_TRAIL, s);
       duo_status st = gemm_f32(g, s);
+      prof_end(DUO_PROF_TRAIL, s);
       if (st != DUO_OK) return st;
     }
   }

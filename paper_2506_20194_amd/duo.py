@@ -26,8 +26,9 @@ DUO_OP_HESSIAN, DUO_OP_CHOL_INV, DUO_OP_SCORE_TERMS, DUO_OP_SWEEP, DUO_OP_PRUNE_
 EXPORTED = (
     "duo_workspace_size", "duo_status_string", "duo_version", "duo_act_sparsify_mask",
     "duo_hessian_accum", "duo_residual_term", "duo_chol_inv", "duo_score_terms", "duo_sweep",
-    "duo_prune_layer",
+    "duo_prune_layer", "duo_profile_enable", "duo_profile_read",
 )
+PROF = dict(gram=0, hessian=1, chol=2, score=3, sweep=4, inblock=5, trail=6, select=7)
 
 
 class DuoError(RuntimeError):
@@ -79,6 +80,10 @@ def lib():
         L.duo_sweep.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, P, P, P, P, P, P, SZ, P]
         L.duo_prune_layer.restype = I32
         L.duo_prune_layer.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, P, P, P, P, P, P, SZ, P]
+        L.duo_profile_enable.restype = I32
+        L.duo_profile_enable.argtypes = [I32]
+        L.duo_profile_read.restype = I32
+        L.duo_profile_read.argtypes = [I32, ctypes.POINTER(F64), ctypes.POINTER(I64)]
         _lib = L
     return _lib
 
@@ -304,6 +309,17 @@ def duo_prune_layer(W, L, G, a, w_sparsity, block=128, mask_in=None, want_lowp=F
                                _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
     _check(st, "duo_prune_layer")
     return W_out, lowp, mask, scores
+
+
+def duo_profile_enable(on: bool = True):
+    _check(lib().duo_profile_enable(1 if on else 0), "duo_profile_enable")
+
+
+def duo_profile_read(kernel: str):
+    """(total milliseconds, launches) of a tracked kernel since the last read."""
+    ms, n = F64(), I64()
+    _check(lib().duo_profile_read(PROF[kernel], ctypes.byref(ms), ctypes.byref(n)), "duo_profile_read")
+    return ms.value, n.value
 
 
 def unpack_mask(words: torch.Tensor, k: int) -> torch.Tensor:

@@ -140,7 +140,8 @@ def _oracle_stage(k, m, seed, p_x=0.5, damp=0.01, dtype=torch.bfloat16):
 @pytest.mark.parametrize("k", [1, 100, 128, 300, 512, 1000])
 def test_chol_inv(duo, k):
     say("chol_inv", k)
-    _, H, _, _ = _oracle_stage(k, 4 * k + 64, seed=k)
+    # k = 1 with p_x = 0.5 drops the only channel (H = 0): use dense input there
+    _, H, _, _ = _oracle_stage(k, 4 * k + 64, seed=k, p_x=0.0 if k == 1 else 0.5)
     Hd = torch.tensor(H, dtype=torch.float32, device=DEV)
     lam, fail = duo.duo_chol_inv(Hd, 0.01)
     L = f64(Hd)
