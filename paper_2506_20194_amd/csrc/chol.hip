@@ -69,8 +69,8 @@ struct DiagCtx {
   float* colbuf;  // [2][128]
   float* rowbuf;  // [2][128]
   float* pivbuf;  // [2]
-  CholStatus* st;
-  int tid, h, q, r0, hh, buf;
+  int tid, h, q, hh, buf;
+  int fail;  // first column (from the bottom) with a non-positive pivot, or -1
 };
 
 // One elimination step for column c = 64*hh + I0 (I0 a compile-time constant so
@@ -98,10 +98,7 @@ __device__ __forceinline__ void diag_step(float (&x)[64], DiagCtx& d) {
   if (h == hh && q > c) rowbuf[q] = x[I0];
   __syncthreads();
   const float piv = d.pivbuf[d.buf];
-  if (d.tid == 0 && !(piv > 0.f) && d.st->status == DUO_OK) {
-    d.st->status = DUO_ERR_NOT_PD;
-    d.st->fail = d.r0 + c;
-  }
+  if (!(piv > 0.f) && d.fail < 0) d.fail = c;  // uniform: every thread sees the same pivot
   const float inv = 1.0f / sqrtf(piv);
   const float inv2 = inv * inv;
   if (q == c) {
@@ -159,10 +156,14 @@ __global__ __launch_bounds__(192) void diag_factor_kernel(const float* H, int64_
       v = 1.f;
     x[i] = v;
   }
-  DiagCtx d{&colbuf[0][0], &rowbuf[0][0], pivbuf, st, tid, h, q, r0, 1, 0};
+  DiagCtx d{&colbuf[0][0], &rowbuf[0][0], pivbuf, tid, h, q, 1, 0, -1};
   diag_steps(x, d, std::make_integer_sequence<int, 64>{});
   d.hh = 0;
   diag_steps(x, d, std::make_integer_sequence<int, 64>{});
+  if (tid == 0 && d.fail >= 0 && d.fail < s && st->status == DUO_OK) {
+    st->status = DUO_ERR_NOT_PD;
+    st->fail = r0 + d.fail;
+  }
   // N (upper, rows <= q) to vinv; everything else 0
 #pragma unroll
   for (int i = 0; i < 64; ++i) {
