@@ -278,49 +278,68 @@ __global__ void a_reduce_kernel(const float* __restrict__ apart, int nblk, int k
 }
 
 // ---------------------------------------------------------------------------
-// gram: MFMA over a pair of 128-channel tiles (ti >= tj).
+// gram: C = [Xh ; Z] Xh^T restricted to the tiles the method needs.
+// 256 x 256 output tiles; row block I < T is an H tile (I, J) with J <= I,
+// row block I >= T is a G tile (I - T, J) for every J.  H and G together cost
+// 1.5 k^2 m multiply-adds (H's upper triangle is never computed, except inside
+// the T diagonal tiles).
 // ---------------------------------------------------------------------------
+constexpr int GT = 256;  // gram tile edge (channels)
+
 template <typename T>
 struct GramArgs {
-  const T* Ph;
-  const T* Pz;
-  const T* Pl;
-  int kp, k, ntile, npairs, nseg, seg_len, ntb;
+  const T* Ph;  // packed Xh
+  const T* Pz;  // packed dX (single stream) or its high part (two streams)
+  const T* Pl;  // packed low part of dX (two bf16 streams), else unused
+  int kp, k, nt;     // padded channels, channels, kp / 256
+  int nh, ntiles;    // H tiles (0 when H is not wanted) and H + G tiles
+  int nseg, seg_len, ntb;
   float* H;
   int64_t ldh;
   float* G;
   int64_t ldg;
-  float* part;  // [nseg][npairs][3][128*128] when nseg > 1
+  float* part;  // [nseg][ntiles][256 * 256] when nseg > 1
 };
 
-// Pair order: bands of 8 tile-rows; inside a band, column by column.  Neighbouring
-// ids share operand tiles, and the XCD remap below gives each XCD a contiguous
-// id range, so concurrently resident workgroups of one XCD reuse its L2.
-__device__ inline void band_pair(int q, int T, int* ti, int* tj) {
-  constexpr int GB = 8;
-  for (int b0 = 0; b0 < T; b0 += GB) {
-    const int b1 = min(T, b0 + GB), h = b1 - b0;
-    const int cnt = b0 * h + h * (h + 1) / 2;  // columns < b0: h rows each; then a triangle
-    if (q < cnt) {
-      if (q < b0 * h) {
-        *tj = q / h;
-        *ti = b0 + q % h;
-        return;
-      }
-      q -= b0 * h;
-      for (int c = b0; c < b1; ++c) {
-        const int nr = b1 - c;
-        if (q < nr) {
-          *tj = c;
-          *ti = c + q;
+// Tiles are numbered H first, then G.  Within each kind, bands of 4 row blocks
+// are walked column by column, so neighbouring ids share operand tiles; the
+// XCD remap below gives each XCD a contiguous id range (and so its own L2 set).
+__device__ inline void gram_tile(int t, int nh, int nt, int* isg, int* I, int* J) {
+  constexpr int GB = 4;
+  if (t < nh) {  // lower triangle of nt x nt, bands of GB rows
+    *isg = 0;
+    for (int b0 = 0; b0 < nt; b0 += GB) {
+      const int b1 = min(nt, b0 + GB), h = b1 - b0;
+      const int cnt = b0 * h + h * (h + 1) / 2;
+      if (t < cnt) {
+        if (t < b0 * h) {
+          *J = t / h;
+          *I = b0 + t % h;
           return;
         }
-        q -= nr;
+        t -= b0 * h;
+        for (int c = b0; c < b1; ++c) {
+          const int nr = b1 - c;
+          if (t < nr) {
+            *J = c;
+            *I = c + t;
+            return;
+          }
+          t -= nr;
+        }
       }
+      t -= cnt;
     }
-    q -= cnt;
+    *I = *J = 0;
+    return;
   }
-  *ti = *tj = 0;
+  t -= nh;
+  *isg = 1;
+  const int b0 = (t / (GB * nt)) * GB;
+  const int h = min(GB, nt - b0);
+  const int r = t - b0 * nt;
+  *J = r / h;
+  *I = b0 + r % h;
 }
 
 __device__ inline int xcd_remap(int b, int nblocks) {
@@ -334,7 +353,7 @@ template <typename T>
 struct MfmaOp;
 template <>
 struct MfmaOp<uint16_t> {
-  // one 16x16x32 bf16 MFMA per 16-row fragment pair per 32-token stage
+  // one 16x16x32 bf16 MFMA per fragment pair per 32-token stage
   static constexpr int kFrags = 1;
   __device__ static inline f4 mma(const v4u& a, const v4u& b, f4 c) {
     bf16x8 av, bv;
@@ -345,7 +364,9 @@ struct MfmaOp<uint16_t> {
 };
 template <>
 struct MfmaOp<float> {
-  // eight 16x16x4 fp32 MFMAs: fragment s holds tokens of group s*4 + lane/16
+  // two fragments per stage, four 16x16x4 fp32 MFMAs each; in fragment f, lane
+  // group l/16 holds the 4 tokens of group 4f + l/16 (the same tokens on both
+  // operands, so the sum runs over all 32 tokens of the stage)
   static constexpr int kFrags = 2;
   __device__ static inline f4 mma(const v4u& a, const v4u& b, f4 c) {
     const float* x = (const float*)&a;
@@ -358,217 +379,169 @@ struct MfmaOp<float> {
   }
 };
 
-template <typename T, bool WANT_H, bool WANT_G, bool HAS_LO>
-__global__ __launch_bounds__(256, 1) void gram_kernel(GramArgs<T> A) {
+// Wait until at most N of this wave's vector-memory operations (here: the
+// direct global->LDS loads) are still in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// Workgroup barrier without the memory fence of __syncthreads (whose fence
+// would also wait for every prefetch in flight).  LDS traffic of this wave is
+// drained first; the empty asm statements keep the compiler from moving memory
+// accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// 512 threads = 8 waves in a 2 x 4 grid; each wave owns 128 rows x 64 columns
+// of the tile (8 x 4 accumulator blocks of 16 x 16).  Operand tiles stream
+// through a ring of NS LDS stages (one 32-token block each) filled by direct
+// global->LDS loads (global_load_lds_dwordx4: each lane moves 16 bytes, a wave
+// 1 KB), issued NS - 1 stages ahead.  LDS layout of one operand tile:
+// [group][256 rows][16 bytes], identical to the packed global layout.
+template <typename T, bool HAS_LO>
+__global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
   constexpr int EPG = 16 / (int)sizeof(T);
   constexpr int NG = kTokBlk / EPG;
-  constexpr int TILE_B = kTile * kTokBlk * (int)sizeof(T);  // bytes of one operand tile
-  constexpr int NOPS = 2 + (HAS_LO ? 1 : 0);               // Xh, Zhi, Zlo per side
-  constexpr int STAGE_B = 2 * NOPS * TILE_B;
+  constexpr int TILE_B = GT * kTokBlk * (int)sizeof(T);
+  constexpr int NOP = HAS_LO ? 3 : 2;  // operand slots: B, A (hi), A lo
+  constexpr int STAGE_B = NOP * TILE_B;
+  constexpr int CHUNKS = TILE_B / 16;           // 16-byte chunks per operand tile
+  constexpr int DPW = NOP * CHUNKS / 64 / 8;    // wave-wide loads per wave per stage
+  constexpr int NS = STAGE_B * 3 <= 160 * 1024 ? 3 : 2;
+  static_assert(CHUNKS % 64 == 0 && (NOP * CHUNKS / 64) % 8 == 0, "load split");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
-  const int nunits = A.npairs * A.nseg;
   const int u = xcd_remap(blockIdx.x, gridDim.x);
-  if (u >= nunits) return;
-  const int seg = u / A.npairs;
-  const int pair = u % A.npairs;
-  int ti, tj;
-  band_pair(pair, A.ntile, &ti, &tj);
-  const bool diag = ti == tj;
+  if (u >= A.ntiles * A.nseg) return;
+  const int seg = u / A.ntiles;
+  const int tile = u % A.ntiles;
+  int isg, I, J;
+  gram_tile(tile, A.nh, A.nt, &isg, &I, &J);
   const int tb0 = seg * A.seg_len;
   const int tb1 = min(A.ntb, tb0 + A.seg_len);
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wi = wave >> 1, wj = wave & 1;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wi = wave >> 2, wj = wave & 3;
 
-  // One operand tile = NG planes of 128 rows x 16 bytes; the plane stride in
-  // global memory is kp * 16 bytes, in LDS 128 * 16 bytes.
-  constexpr int CHUNKS = TILE_B / 16;
-  constexpr int PER_T = CHUNKS / 256;
-  const v4u* gbase[2][NOPS];
+  // this lane's share of every stage: DPW chunks, each in its operand tile
+  const int64_t tbs = (int64_t)NG * A.kp * 16;  // bytes per token block in a packed operand
+  const uint8_t* src[DPW];
+  uint32_t ldso[DPW];  // wave-uniform LDS offset of each load within a stage
 #pragma unroll
-  for (int side = 0; side < 2; ++side)
-#pragma unroll
-    for (int o = 0; o < NOPS; ++o) {
-      const T* b = o == 0 ? A.Ph : o == 1 ? A.Pz : A.Pl;
-      gbase[side][o] = (const v4u*)(b + (int64_t)(side ? tj : ti) * kTile * EPG);
-    }
-  const int64_t tb_stride = (int64_t)NG * A.kp;  // v4u per token block
-  int64_t goff[PER_T];
-#pragma unroll
-  for (int q = 0; q < PER_T; ++q) {
-    const int ch = q * 256 + tid;
-    goff[q] = (int64_t)(ch / kTile) * A.kp + ch % kTile;
+  for (int j = 0; j < DPW; ++j) {
+    const int c0 = (wave * DPW + j) * 64;  // first chunk of this wave-wide load
+    const int op = c0 / CHUNKS, c = c0 % CHUNKS + lane;
+    const T* base = op == 0 ? A.Ph : (op == 1 ? (isg ? A.Pz : A.Ph) : A.Pl);
+    const int blk = op == 0 ? J : I;
+    src[j] = (const uint8_t*)base + ((int64_t)(c / GT) * A.kp + (int64_t)blk * GT + c % GT) * 16;
+    ldso[j] = (uint32_t)(op * CHUNKS + c0 % CHUNKS) * 16;
   }
-  v4u pre0[NOPS][PER_T], pre1[NOPS][PER_T];
+  auto issue = [&](int t) {
+    uint8_t* stage = smem + ((t - tb0) % NS) * STAGE_B;
+#pragma unroll
+    for (int j = 0; j < DPW; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(src[j] + (int64_t)t * tbs),
+                                       (__attribute__((address_space(3))) void*)(stage + ldso[j]), 16, 0, 0);
+  };
 
-  f4 accH[4][4], accG1[4][4], accG2[4][4];
+  f4 acc[8][4];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 8; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      accH[a][b] = f4{0.f, 0.f, 0.f, 0.f};
-      accG1[a][b] = accH[a][b];
-      accG2[a][b] = accH[a][b];
-    }
+    for (int b = 0; b < 4; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
 
-#define DUO_LOAD_STAGE(TB)                                                          \
-  {                                                                                 \
-    const int64_t tbo_ = (int64_t)(TB) * tb_stride;                                 \
-    _Pragma("unroll") for (int o = 0; o < NOPS; ++o)                                \
-    _Pragma("unroll") for (int q = 0; q < PER_T; ++q)                               \
-      pre0[o][q] = gbase[0][o][tbo_ + goff[q]];                                     \
-    if (!diag) {                                                                    \
-      _Pragma("unroll") for (int o = 0; o < NOPS; ++o)                              \
-      _Pragma("unroll") for (int q = 0; q < PER_T; ++q)                             \
-        pre1[o][q] = gbase[1][o][tbo_ + goff[q]];                                   \
-    }                                                                               \
-  }
-#define DUO_STORE_STAGE(BUF)                                                        \
-  {                                                                                 \
-    v4u* dst_ = (v4u*)(smem + (BUF) * STAGE_B);                                  \
-    _Pragma("unroll") for (int o = 0; o < NOPS; ++o)                                \
-    _Pragma("unroll") for (int q = 0; q < PER_T; ++q)                               \
-      dst_[o * CHUNKS + q * 256 + tid] = pre0[o][q];                                \
-    if (!diag) {                                                                    \
-      _Pragma("unroll") for (int o = 0; o < NOPS; ++o)                              \
-      _Pragma("unroll") for (int q = 0; q < PER_T; ++q)                             \
-        dst_[(NOPS + o) * CHUNKS + q * 256 + tid] = pre1[o][q];                     \
-    }                                                                               \
-  }
-
-  const int side_j = diag ? 0 : 1;
-  if (tb0 < tb1) {
-    DUO_LOAD_STAGE(tb0);
-    DUO_STORE_STAGE(0);
-    __syncthreads();
-    int buf = 0;
-    for (int tb = tb0; tb < tb1; ++tb) {
-      const bool more = tb + 1 < tb1;
-      if (more) {
-        DUO_LOAD_STAGE(tb + 1);
-      }
-      const v4u* lds = (const v4u*)(smem + buf * STAGE_B);
+  for (int t = tb0; t < min(tb1, tb0 + NS - 1); ++t) issue(t);
+  for (int t = tb0; t < tb1; ++t) {
+    // stage t complete (younger stages may still be in flight)
+    if (t + NS - 2 < tb1 && NS == 3)
+      wait_vmem<DPW>();
+    else
+      wait_vmem<0>();
+    lds_barrier();  // every wave's part of stage t has landed; stage t-1 is free
+    if (t + NS - 1 < tb1) issue(t + NS - 1);
+    const v4u* l_ = (const v4u*)(smem + ((t - tb0) % NS) * STAGE_B);
 #pragma unroll
-      for (int f = 0; f < MfmaOp<T>::kFrags; ++f) {
-        const int fo = (f * 4 + (lane >> 4)) * kTile + (lane & 15);
-        v4u hi_[4], hj_[4];
+    for (int f = 0; f < MfmaOp<T>::kFrags; ++f) {
+      const int fo = (f * 4 + (lane >> 4)) * GT + (lane & 15);
+      v4u bf[4];
 #pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          hi_[a] = lds[(0 * NOPS + 0) * CHUNKS + fo + wi * 64 + a * 16];
-          hj_[a] = lds[(side_j * NOPS + 0) * CHUNKS + fo + wj * 64 + a * 16];
-        }
-        if (WANT_H) {
+      for (int b = 0; b < 4; ++b) bf[b] = l_[fo + wj * 64 + b * 16];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        v4u af[4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a) af[a] = l_[CHUNKS + fo + wi * 128 + (4 * h2 + a) * 16];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) acc[4 * h2 + a][b] = MfmaOp<T>::mma(af[a], bf[b], acc[4 * h2 + a][b]);
+        if (HAS_LO && isg) {
+#pragma unroll
+          for (int a = 0; a < 4; ++a) af[a] = l_[2 * CHUNKS + fo + wi * 128 + (4 * h2 + a) * 16];
 #pragma unroll
           for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int b = 0; b < 4; ++b) accH[a][b] = MfmaOp<T>::mma(hi_[a], hj_[b], accH[a][b]);
+            for (int b = 0; b < 4; ++b) acc[4 * h2 + a][b] = MfmaOp<T>::mma(af[a], bf[b], acc[4 * h2 + a][b]);
         }
-        if (WANT_G) {
-#pragma unroll
-          for (int o = 1; o < NOPS; ++o) {
-            v4u zi[4];
-#pragma unroll
-            for (int a = 0; a < 4; ++a) zi[a] = lds[(0 * NOPS + o) * CHUNKS + fo + wi * 64 + a * 16];
-#pragma unroll
-            for (int a = 0; a < 4; ++a)
-#pragma unroll
-              for (int b = 0; b < 4; ++b) accG1[a][b] = MfmaOp<T>::mma(zi[a], hj_[b], accG1[a][b]);
-            if (!diag) {
-              v4u zj[4];
-#pragma unroll
-              for (int a = 0; a < 4; ++a) zj[a] = lds[(1 * NOPS + o) * CHUNKS + fo + wj * 64 + a * 16];
-#pragma unroll
-              for (int a = 0; a < 4; ++a)
-#pragma unroll
-                for (int b = 0; b < 4; ++b) accG2[a][b] = MfmaOp<T>::mma(zj[a], hi_[b], accG2[a][b]);
-            }
-          }
-        }
-      }
-      if (more) {
-        DUO_STORE_STAGE(buf ^ 1);
-        __syncthreads();
-        buf ^= 1;
       }
     }
   }
-#undef DUO_LOAD_STAGE
-#undef DUO_STORE_STAGE
 
   // epilogue.  Accumulator element r of block (a, b) sits at row
-  // 16a + 4*(lane/16) + r, column 16b + lane%16 of the wave's 64 x 64 sub-tile.
-  const int i0 = ti * kTile, j0 = tj * kTile;
+  // 16a + 4*(lane/16) + r, column 16b + lane%16 of the wave's 128 x 64 part.
   const int rq = (lane >> 4) * 4, cc = lane & 15;
   if (A.nseg > 1) {
-    float* base = A.part + ((int64_t)seg * A.npairs + pair) * 3 * kTile * kTile;
+    float* base = A.part + ((int64_t)seg * A.ntiles + tile) * GT * GT;
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < 8; ++a)
 #pragma unroll
       for (int b = 0; b < 4; ++b)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int rowl = wi * 64 + a * 16 + rq + r, coll = wj * 64 + b * 16 + cc;
-          if (WANT_H) base[rowl * kTile + coll] = accH[a][b][r];
-          if (WANT_G) {
-            base[kTile * kTile + rowl * kTile + coll] = accG1[a][b][r];
-            // G_ji block: rows are j channels (wj half), columns i channels (wi half)
-            const int rowj = wj * 64 + a * 16 + rq + r, coli = wi * 64 + b * 16 + cc;
-            base[2 * kTile * kTile + rowj * kTile + coli] = accG2[a][b][r];
-          }
-        }
+        for (int r = 0; r < 4; ++r)
+          base[(wi * 128 + a * 16 + rq + r) * GT + wj * 64 + b * 16 + cc] = acc[a][b][r];
     return;
   }
+  float* C = isg ? A.G : A.H;
+  const int64_t ldc = isg ? A.ldg : A.ldh;
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 8; ++a)
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = i0 + wi * 64 + a * 16 + rq + r, col = j0 + wj * 64 + b * 16 + cc;
+        const int row = I * GT + wi * 128 + a * 16 + rq + r, col = J * GT + wj * 64 + b * 16 + cc;
         if (row < A.k && col < A.k) {
-          if (WANT_H) {
-            A.H[(int64_t)row * A.ldh + col] += accH[a][b][r];
-            if (!diag) A.H[(int64_t)col * A.ldh + row] += accH[a][b][r];
-          }
-          if (WANT_G) A.G[(int64_t)row * A.ldg + col] += accG1[a][b][r];
-        }
-        if (WANT_G && !diag) {
-          const int rowj = j0 + wj * 64 + a * 16 + rq + r, coli = i0 + wi * 64 + b * 16 + cc;
-          if (rowj < A.k && coli < A.k) A.G[(int64_t)rowj * A.ldg + coli] += accG2[a][b][r];
+          C[(int64_t)row * ldc + col] += acc[a][b][r];
+          if (!isg && I != J) A.H[(int64_t)col * A.ldh + row] += acc[a][b][r];
         }
       }
 }
 
 // Fixed-order sum of the per-segment partial tiles into H and G.
 template <typename T>
-__global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A, int want_h, int want_g) {
-  const int pair = blockIdx.x / 3, which = blockIdx.x % 3;
-  int ti, tj;
-  band_pair(pair, A.ntile, &ti, &tj);
-  const bool diag = ti == tj;
-  if ((which == 0 && !want_h) || (which > 0 && !want_g) || (which == 2 && diag)) return;
-  const int64_t stride = (int64_t)A.npairs * 3 * kTile * kTile;
-  const float* p0 = A.part + ((int64_t)pair * 3 + which) * kTile * kTile;
-  for (int e = threadIdx.x + blockIdx.y * 256 * 16; e < min(kTile * kTile, (int)(blockIdx.y + 1) * 256 * 16);
-       e += 256) {
+__global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A) {
+  const int tile = blockIdx.x;
+  int isg, I, J;
+  gram_tile(tile, A.nh, A.nt, &isg, &I, &J);
+  const int64_t stride = (int64_t)A.ntiles * GT * GT;
+  const float* p0 = A.part + (int64_t)tile * GT * GT;
+  float* C = isg ? A.G : A.H;
+  const int64_t ldc = isg ? A.ldg : A.ldh;
+  const int e0 = blockIdx.y * 4096;
+  for (int e = e0 + threadIdx.x; e < e0 + 4096; e += 256) {
     float s = 0.f;
     for (int sg = 0; sg < A.nseg; ++sg) s += p0[sg * stride + e];
-    const int rl = e / kTile, cl = e % kTile;
-    if (which == 0) {
-      const int row = ti * kTile + rl, col = tj * kTile + cl;
-      if (row < A.k && col < A.k) {
-        A.H[(int64_t)row * A.ldh + col] += s;
-        if (!diag) A.H[(int64_t)col * A.ldh + row] += s;
-      }
-    } else if (which == 1) {
-      const int row = ti * kTile + rl, col = tj * kTile + cl;
-      if (row < A.k && col < A.k) A.G[(int64_t)row * A.ldg + col] += s;
-    } else {
-      const int row = tj * kTile + rl, col = ti * kTile + cl;
-      if (row < A.k && col < A.k) A.G[(int64_t)row * A.ldg + col] += s;
+    const int row = I * GT + e / GT, col = J * GT + e % GT;
+    if (row < A.k && col < A.k) {
+      C[(int64_t)row * ldc + col] += s;
+      if (!isg && I != J) A.H[(int64_t)col * A.ldh + row] += s;
     }
   }
 }
@@ -577,7 +550,7 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A, int wan
 // host side
 // ---------------------------------------------------------------------------
 int64_t hessian_chunk_tokens(int64_t m, int64_t k) {
-  const int64_t kp = rup(k, kTile);
+  const int64_t kp = rup(k, GT);
   int64_t ch = (int64_t)12e9 / (kp * 8);
   ch = ch < 4096 ? 4096 : ch;
   ch = ch > 131072 ? 131072 : ch;
@@ -585,11 +558,11 @@ int64_t hessian_chunk_tokens(int64_t m, int64_t k) {
   return m < ch ? (m < 1 ? 1 : m) : ch;
 }
 
-int gram_split(int64_t npairs) {
+int gram_split(int64_t ntiles) {
   int best = 1;
   double best_cost = 1e30;
   for (int s = 1; s <= 8; ++s) {
-    const double cost = (double)cdiv(npairs * s, 256) / s + (s > 1 ? 0.03 * s : 0.0);
+    const double cost = (double)cdiv(ntiles * s, 256) / s + (s > 1 ? 0.03 * s : 0.0);
     if (cost < best_cost - 1e-12) {
       best_cost = cost;
       best = s;
@@ -610,11 +583,11 @@ struct HessWs {
 
 static HessWs carve_hessian(void* ws, int64_t m, int64_t k) {
   const int64_t ch = hessian_chunk_tokens(m, k);
-  const int64_t kp = rup(k, kTile);
+  const int64_t kp = rup(k, GT);
   const int64_t tokp = rup(ch, 256);
-  const int64_t T = kp / kTile;
-  const int64_t npairs = T * (T + 1) / 2;
-  const int nseg = gram_split(npairs);
+  const int64_t T = kp / GT;
+  const int64_t ntiles = T * (T + 1) / 2 + T * T;
+  const int nseg = gram_split(ntiles);
   Carver c(ws);
   HessWs h;
   h.thr = c.take<int64_t>(tokp);
@@ -622,55 +595,55 @@ static HessWs carve_hessian(void* ws, int64_t m, int64_t k) {
   h.Pz = c.take<uint8_t>((size_t)tokp * kp * 4);
   h.Pl = c.take<uint8_t>((size_t)tokp * kp * 2);  // low part exists for bf16 only
   h.apart = c.take<float>((size_t)(tokp / 256) * kp);
-  h.part = c.take<float>(nseg > 1 ? (size_t)nseg * npairs * 3 * kTile * kTile : 1);
+  h.part = c.take<float>(nseg > 1 ? (size_t)nseg * ntiles * GT * GT : 1);
   h.bytes = c.off;
   return h;
 }
 
 size_t hessian_ws_bytes(int64_t m, int64_t k) { return carve_hessian(nullptr, m, k).bytes; }
 
-template <typename T, bool WH, bool WG, bool LO>
-static duo_status launch_gram(const GramArgs<T>& A, int nunits, hipStream_t s) {
-  constexpr int NOPS = 2 + (LO ? 1 : 0);
-  const size_t lds = 2 * 2 * NOPS * (size_t)kTile * kTokBlk * sizeof(T);
-  auto kern = gram_kernel<T, WH, WG, LO>;
+template <typename T, bool LO>
+static duo_status launch_gram(const GramArgs<T>& A, hipStream_t s) {
+  constexpr int NOP = LO ? 3 : 2;
+  const size_t stage = NOP * (size_t)GT * kTokBlk * sizeof(T);
+  const size_t lds = (stage * 3 <= 160 * 1024 ? 3 : 2) * stage;
+  auto kern = gram_kernel<T, LO>;
   DUO_HIP_TRY(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-  const int grid = (int)rup(nunits, 8);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, s, A);
+  const int grid = (int)rup((int64_t)A.ntiles * A.nseg, 8);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(512), lds, s, A);
   DUO_LAUNCH_CHECK();
   return DUO_OK;
 }
 
 template <typename T>
-static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, int64_t ldx, int z,
-                                float* H, int64_t ldh, float* G, int64_t ldg, float* a, void* ws,
-                                bool want_h, hipStream_t s) {
+static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, int64_t ldx, int z, float* H,
+                                int64_t ldh, float* G, int64_t ldg, float* a, void* ws, bool want_h, hipStream_t s) {
   const bool want_g = G != nullptr;
   const bool two = Xd != nullptr && Xd != Xs;
   const bool lo = two && sizeof(T) == 2;
   const HessWs w = carve_hessian(ws, m, k);
   const int64_t ch = hessian_chunk_tokens(m, k);
-  const int64_t kp = rup(k, kTile);
-  const int T_ = (int)(kp / kTile);
-  const int npairs = T_ * (T_ + 1) / 2;
-  const int nseg = gram_split(npairs);
+  const int64_t kp = rup(k, GT);
+  const int nt = (int)(kp / GT);
+  const int nh_all = nt * (nt + 1) / 2;
+  const int nseg = gram_split(nh_all + nt * nt);  // the same split the workspace was sized for
   for (int64_t t0 = 0; t0 < m; t0 += ch) {
     const int mc = (int)(m - t0 < ch ? m - t0 : ch);
     const T* xs = Xs + t0 * ldx;
     const T* xd = two ? Xd + t0 * ldx : nullptr;
     duo_status st = launch_act_select<T>(xs, ldx, mc, (int)k, z, w.thr, s);
     if (st != DUO_OK) return st;
-    dim3 pg((unsigned)cdiv(kp, 256), (unsigned)cdiv(mc, 256));
+    dim3 pg((unsigned)(kp / 256), (unsigned)cdiv(mc, 256));
     if (two)
-      hipLaunchKernelGGL((pack_kernel<T, true>), pg, dim3(256), 0, s, xs, xd, ldx, mc, (int)k, (int)kp,
-                         w.thr, (T*)w.Ph, (T*)w.Pz, (T*)w.Pl, want_g ? w.apart : nullptr);
+      hipLaunchKernelGGL((pack_kernel<T, true>), pg, dim3(256), 0, s, xs, xd, ldx, mc, (int)k, (int)kp, w.thr,
+                         (T*)w.Ph, (T*)w.Pz, (T*)w.Pl, want_g ? w.apart : nullptr);
     else
-      hipLaunchKernelGGL((pack_kernel<T, false>), pg, dim3(256), 0, s, xs, xs, ldx, mc, (int)k, (int)kp,
-                         w.thr, (T*)w.Ph, (T*)w.Pz, (T*)w.Pl, want_g ? w.apart : nullptr);
+      hipLaunchKernelGGL((pack_kernel<T, false>), pg, dim3(256), 0, s, xs, xs, ldx, mc, (int)k, (int)kp, w.thr,
+                         (T*)w.Ph, (T*)w.Pz, (T*)w.Pl, want_g ? w.apart : nullptr);
     DUO_LAUNCH_CHECK();
     if (want_g) {
-      hipLaunchKernelGGL(a_reduce_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.apart,
-                         (int)cdiv(mc, 256), (int)kp, (int)k, a);
+      hipLaunchKernelGGL(a_reduce_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.apart, (int)cdiv(mc, 256),
+                         (int)kp, (int)k, a);
       DUO_LAUNCH_CHECK();
     }
     GramArgs<T> A;
@@ -679,8 +652,9 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
     A.Pl = (const T*)w.Pl;
     A.kp = (int)kp;
     A.k = (int)k;
-    A.ntile = T_;
-    A.npairs = npairs;
+    A.nt = nt;
+    A.nh = want_h ? nh_all : 0;
+    A.ntiles = A.nh + (want_g ? nt * nt : 0);
     A.nseg = nseg;
     A.ntb = (int)cdiv(mc, kTokBlk);
     A.seg_len = (int)cdiv(A.ntb, nseg);
@@ -689,27 +663,15 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
     A.G = G;
     A.ldg = ldg;
     A.part = w.part;
-    const int nunits = npairs * nseg;
     prof_begin(DUO_PROF_GRAM, s);
-    constexpr bool kLoOk = sizeof(T) == 2;  // the low part of dX exists for bf16 only
-    if (want_h && want_g) {
-      if constexpr (kLoOk)
-        st = lo ? launch_gram<T, true, true, true>(A, nunits, s) : launch_gram<T, true, true, false>(A, nunits, s);
-      else
-        st = launch_gram<T, true, true, false>(A, nunits, s);
-    } else if (want_h) {
-      st = launch_gram<T, true, false, false>(A, nunits, s);
-    } else {
-      if constexpr (kLoOk)
-        st = lo ? launch_gram<T, false, true, true>(A, nunits, s) : launch_gram<T, false, true, false>(A, nunits, s);
-      else
-        st = launch_gram<T, false, true, false>(A, nunits, s);
-    }
+    if constexpr (sizeof(T) == 2)
+      st = lo ? launch_gram<T, true>(A, s) : launch_gram<T, false>(A, s);
+    else
+      st = launch_gram<T, false>(A, s);
     prof_end(DUO_PROF_GRAM, s);
     if (st != DUO_OK) return st;
     if (nseg > 1) {
-      hipLaunchKernelGGL(gram_reduce_kernel<T>, dim3(npairs * 3, (kTile * kTile) / (256 * 16)), dim3(256), 0, s, A,
-                         (int)want_h, (int)want_g);
+      hipLaunchKernelGGL(gram_reduce_kernel<T>, dim3(A.ntiles, (GT * GT) / 4096), dim3(256), 0, s, A);
       DUO_LAUNCH_CHECK();
     }
   }
