@@ -232,18 +232,18 @@ CholWs carve(void* ws, int64_t k) {
   return w;
 }
 
-// N = V^-1 on the block range [lo, hi) (units of 128 columns); the diagonal
-// blocks already hold their inverses.
-duo_status trinv(float* H, int64_t ldh, int64_t k, int lo, int hi, float* X, hipStream_t s) {
-  if (hi - lo <= 1) return DUO_OK;
-  const int mid = lo + (hi - lo) / 2;
-  duo_status st = trinv(H, ldh, k, lo, mid, X, s);
-  if (st != DUO_OK) return st;
-  st = trinv(H, ldh, k, mid, hi, X, s);
-  if (st != DUO_OK) return st;
-  const int64_t r_lo = (int64_t)lo * kTile, r_mid = (int64_t)mid * kTile;
-  const int64_t r_hi = (int64_t)hi * kTile < k ? (int64_t)hi * kTile : k;
+// N = V^-1 by bottom-up merging (units of 128 columns; the diagonal blocks
+// already hold their inverses).  At level L every node [lo, lo + 2^L) whose
+// halves [lo, mid) and [mid, hi) are inverted becomes
+//   N12 = -N11 V12 N22,  as X = V12 N22 then N12 = -N11 X.
+// All complete nodes of a level share one batched launch per product; a node
+// containing the ragged last block gets its own.
+duo_status merge_nodes(float* H, int64_t ldh, int64_t k, int64_t span, int64_t half, int64_t q0, int nodes,
+                       float* X, hipStream_t s) {
+  const int64_t r_lo = q0 * span * kTile, r_mid = r_lo + half * kTile;
+  const int64_t r_hi = r_lo + span * kTile < k ? r_lo + span * kTile : k;
   const int m1 = (int)(r_mid - r_lo), m2 = (int)(r_hi - r_mid);
+  const int64_t diag_step = span * kTile * (ldh + 1);  // next node along the diagonal
   // X = V12 N22 (N22 upper: for output column tile j only l < j-tile end)
   GemmDesc a{};
   a.M = m1;
@@ -254,7 +254,11 @@ duo_status trinv(float* H, int64_t ldh, int64_t k, int lo, int hi, float* X, hip
   a.tri = TRI_ALL;
   a.nterms = 1;
   a.t[0] = GemmTerm{H + r_lo * ldh + r_mid, ldh, 1, H + r_mid * ldh + r_mid, ldh, 1, m2, 1.f, KLO_ZERO, KHI_COL};
-  st = gemm_f32(a, s);
+  a.batch = nodes;
+  a.sC = (int64_t)m1 * m2;
+  a.sA[0] = diag_step;
+  a.sB[0] = diag_step;
+  duo_status st = gemm_f32(a, s);
   if (st != DUO_OK) return st;
   // V12 <- -N11 X (N11 upper: for output row tile i only l >= i-tile start)
   GemmDesc b{};
@@ -266,7 +270,27 @@ duo_status trinv(float* H, int64_t ldh, int64_t k, int lo, int hi, float* X, hip
   b.tri = TRI_ALL;
   b.nterms = 1;
   b.t[0] = GemmTerm{H + r_lo * ldh + r_lo, ldh, 1, X, m2, 1, m1, -1.f, KLO_ROW, KHI_FULL};
+  b.batch = nodes;
+  b.sC = diag_step;
+  b.sA[0] = diag_step;
+  b.sB[0] = (int64_t)m1 * m2;
   return gemm_f32(b, s);
+}
+
+duo_status trinv(float* H, int64_t ldh, int64_t k, int T, float* X, hipStream_t s) {
+  for (int64_t half = 1; half < T; half *= 2) {
+    const int64_t span = 2 * half;
+    const int64_t full = k / (span * kTile);  // nodes with both halves complete (no ragged block)
+    if (full > 0) {
+      duo_status st = merge_nodes(H, ldh, k, span, half, 0, (int)full, X, s);
+      if (st != DUO_OK) return st;
+    }
+    if (full * span + half < T) {  // the node holding the tail
+      duo_status st = merge_nodes(H, ldh, k, span, half, full, 1, X, s);
+      if (st != DUO_OK) return st;
+    }
+  }
+  return DUO_OK;
 }
 
 }  // namespace
@@ -313,7 +337,7 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
   }
   hipLaunchKernelGGL(place_diag_kernel, dim3(T), dim3(256), 0, s, H, ldh, (int)k, (const float*)w.vinv);
   DUO_LAUNCH_CHECK();
-  duo_status st = trinv(H, ldh, k, 0, T, w.X, s);
+  duo_status st = trinv(H, ldh, k, T, w.X, s);
   if (st != DUO_OK) return st;
   const int T64 = (int)cdiv(k, 64);
   hipLaunchKernelGGL(transpose_upper_kernel, dim3(T64 * (T64 + 1) / 2), dim3(256), 0, s, H, ldh, (int)k);

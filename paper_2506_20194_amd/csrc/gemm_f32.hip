@@ -2,8 +2,9 @@
 // Q = G L, D = U L^T) and by the lazy trailing update of the column sweep.
 //
 // 128 x 128 output tile per 256-thread workgroup, 2 x 2 waves of 64 x 64,
-// v_mfma_f32_16x16x4_f32; K staged 16 at a time through LDS with one stage
-// of register prefetch.  Triangular operands are handled by restricting each
+// v_mfma_f32_16x16x4_f32; K staged 32 at a time through LDS, with the global
+// loads of the stage after next in flight during each multiply (fence-free
+// barriers, so the prefetch is not drained at every stage).  Triangular operands are handled by restricting each
 // tile's K range (tile-granular) and by tile filters (lower/upper only); the
 // zeros inside diagonal tiles must be stored explicitly.
 #include <hip/hip_runtime.h>
@@ -14,12 +15,13 @@ namespace duo {
 
 namespace {
 
-constexpr int KT = 16;          // K per stage
+constexpr int KT = 32;          // K per stage
 constexpr int LS = kTile + 16;  // LDS row stride (floats): conflict-free fragment reads
+constexpr int PQ = KT / 8;      // float4 loads per thread per operand per stage
 
 struct Stage {
-  float4 a[2];
-  float4 b[2];
+  float4 a[PQ];
+  float4 b[PQ];
 };
 
 __device__ inline int64_t lo_of(int mode, int i0, int j0) {
@@ -43,14 +45,26 @@ __device__ inline float4 load4(const float* p, int64_t idx, int64_t lo, int64_t 
   return v;
 }
 
+// Workgroup barrier without the memory fence of __syncthreads: that fence
+// would wait for the global prefetches in flight.  This wave's LDS traffic is
+// drained first; the empty asm statements keep memory accesses on their side.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// One stage = KT values of K for 128 rows of A and 128 columns of B; each of
+// the 256 threads moves PQ float4 of each operand.
 template <bool AR, bool BR>
 __device__ inline void load_stage(const GemmTerm& t, int M, int N, int i0, int j0, int64_t k0, int64_t klo,
                                   int64_t khi, Stage& st) {
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
+  for (int q = 0; q < PQ; ++q) {
     if (AR) {  // A(i,l) = A[i*lda + l]: 4 consecutive l of one row
-      const int row = (tid >> 2) + 64 * q, l4 = (tid & 3) * 4;
+      const int row = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
       const int64_t i = i0 + row, l = k0 + l4;
       st.a[q] = load4(t.A + i * t.lda + l, l, klo, khi, i < M);
     } else {  // A(i,l) = A[l*lda + i]: 4 consecutive i of one l
@@ -64,22 +78,23 @@ __device__ inline void load_stage(const GemmTerm& t, int M, int N, int i0, int j
       const int64_t j = j0 + j4, l = k0 + lr;
       const bool ok = l >= klo && l < khi;
       st.b[q] = load4(t.B + l * t.ldb + j, j, 0, N, ok);
-    } else {  // B(l,j) = B[j*ldb + l]: 4 consecutive l of one j
-      const int col = (tid >> 2) + 64 * q, l4 = (tid & 3) * 4;
+    } else {  // B(l,j) = B[j*ldb + l]: 4 consecutive l of one column
+      const int col = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
       const int64_t j = j0 + col, l = k0 + l4;
       st.b[q] = load4(t.B + j * t.ldb + l, l, klo, khi, j < N);
     }
   }
 }
 
+// LDS layout of both operands: [k][128 + 16] (k-major), alpha folded into A.
 template <bool AR, bool BR>
 __device__ inline void store_stage(float* sA, float* sB, const Stage& st, float alpha) {
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
+  for (int q = 0; q < PQ; ++q) {
     const float4 a = st.a[q];
     if (AR) {
-      const int row = (tid >> 2) + 64 * q, l4 = (tid & 3) * 4;
+      const int row = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
       sA[(l4 + 0) * LS + row] = alpha * a.x;
       sA[(l4 + 1) * LS + row] = alpha * a.y;
       sA[(l4 + 2) * LS + row] = alpha * a.z;
@@ -93,7 +108,7 @@ __device__ inline void store_stage(float* sA, float* sB, const Stage& st, float 
       const int lr = (tid >> 5) + 8 * q, j4 = (tid & 31) * 4;
       *(float4*)&sB[lr * LS + j4] = b;
     } else {
-      const int col = (tid >> 2) + 64 * q, l4 = (tid & 3) * 4;
+      const int col = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
       sB[(l4 + 0) * LS + col] = b.x;
       sB[(l4 + 1) * LS + col] = b.y;
       sB[(l4 + 2) * LS + col] = b.z;
@@ -102,44 +117,52 @@ __device__ inline void store_stage(float* sA, float* sB, const Stage& st, float 
   }
 }
 
+__device__ inline void compute_stage(const float* sA, const float* sB, f4 (&acc)[4][4]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wi = wave >> 1, wj = wave & 1;
+#pragma unroll
+  for (int ks = 0; ks < KT / 4; ++ks) {
+    const int kr = ks * 4 + (lane >> 4);
+    float av[4], bv[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      av[a] = sA[kr * LS + wi * 64 + a * 16 + (lane & 15)];
+      bv[a] = sB[kr * LS + wj * 64 + a * 16 + (lane & 15)];
+    }
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
+  }
+}
+
+// K loop of one term: stage s sits in LDS buffer s & 1; the global loads of
+// stage s + 2 are in flight while stage s is multiplied (two register slots,
+// the loop unrolled by two so that every slot index is static).
 template <bool AR, bool BR>
 __device__ inline void run_term(const GemmTerm& t, int M, int N, int i0, int j0, float* smem, f4 (&acc)[4][4]) {
   const int64_t klo = lo_of(t.klo, i0, j0);
   const int64_t khi = hi_of(t.khi, i0, j0, t.K);
   if (klo >= khi) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wi = wave >> 1, wj = wave & 1;
-  float* bufs[2][2] = {{smem, smem + KT * LS}, {smem + 2 * KT * LS, smem + 3 * KT * LS}};
-  Stage st;
-  load_stage<AR, BR>(t, M, N, i0, j0, klo, klo, khi, st);
-  __syncthreads();  // previous users of the LDS buffers are done
-  store_stage<AR, BR>(bufs[0][0], bufs[0][1], st, t.alpha);
-  __syncthreads();
-  int buf = 0;
-  for (int64_t k0 = klo; k0 < khi; k0 += KT) {
-    const bool more = k0 + KT < khi;
-    if (more) load_stage<AR, BR>(t, M, N, i0, j0, k0 + KT, klo, khi, st);
-    const float* sA = bufs[buf][0];
-    const float* sB = bufs[buf][1];
-#pragma unroll
-    for (int ks = 0; ks < KT / 4; ++ks) {
-      const int kr = ks * 4 + (lane >> 4);
-      float av[4], bv[4];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        av[a] = sA[kr * LS + wi * 64 + a * 16 + (lane & 15)];
-        bv[a] = sB[kr * LS + wj * 64 + a * 16 + (lane & 15)];
-      }
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
-    }
-    if (more) {
-      store_stage<AR, BR>(bufs[buf ^ 1][0], bufs[buf ^ 1][1], st, t.alpha);
-      __syncthreads();
-      buf ^= 1;
-    }
+  const int nst = (int)((khi - klo + KT - 1) / KT);
+  float* sa[2] = {smem, smem + 2 * KT * LS};
+  float* sb[2] = {smem + KT * LS, smem + 3 * KT * LS};
+  Stage st0, st1;
+  load_stage<AR, BR>(t, M, N, i0, j0, klo, klo, khi, st0);
+  if (nst > 1) load_stage<AR, BR>(t, M, N, i0, j0, klo + KT, klo, khi, st1);
+  lds_barrier();  // earlier users of the LDS buffers are done
+  store_stage<AR, BR>(sa[0], sb[0], st0, t.alpha);
+  lds_barrier();
+  for (int s = 0; s < nst; s += 2) {
+    if (s + 2 < nst) load_stage<AR, BR>(t, M, N, i0, j0, klo + (int64_t)(s + 2) * KT, klo, khi, st0);
+    compute_stage(sa[0], sb[0], acc);
+    if (s + 1 < nst) store_stage<AR, BR>(sa[1], sb[1], st1, t.alpha);
+    lds_barrier();
+    if (s + 1 >= nst) break;
+    if (s + 3 < nst) load_stage<AR, BR>(t, M, N, i0, j0, klo + (int64_t)(s + 3) * KT, klo, khi, st1);
+    compute_stage(sa[1], sb[1], acc);
+    if (s + 2 < nst) store_stage<AR, BR>(sa[0], sb[0], st0, t.alpha);
+    lds_barrier();
   }
 }
 
@@ -150,9 +173,17 @@ __device__ inline int xcd_remap_g(int b, int nblocks) {
 
 template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmDesc d, int ntiles) {
-  __shared__ __attribute__((aligned(16))) float smem[4 * KT * LS];
+  __shared__ __attribute__((aligned(16))) float smem[4 * KT * LS];  // 2 buffers x (A, B)
   const int id = xcd_remap_g(blockIdx.x, gridDim.x);
   if (id >= ntiles) return;
+  if (blockIdx.y) {
+    const int64_t z = blockIdx.y;
+    d.C += z * d.sC;
+    d.t[0].A += z * d.sA[0];
+    d.t[0].B += z * d.sB[0];
+    d.t[1].A += z * d.sA[1];
+    d.t[1].B += z * d.sB[1];
+  }
   int ti, tj;
   if (d.tri == TRI_ALL) {
     const int tn = (int)cdiv(d.N, kTile);
@@ -195,7 +226,8 @@ duo_status launch(const GemmDesc& d, hipStream_t s) {
   int ntiles = d.tri == TRI_ALL ? tm * tn : tm * (tm + 1) / 2;
   if (ntiles <= 0) return DUO_OK;
   const int grid = (int)rup(ntiles, 8);
-  hipLaunchKernelGGL((gemm_kernel<A1R, B1R, A2R, B2R, TWO>), dim3(grid), dim3(256), 0, s, d, ntiles);
+  const int nb = d.batch > 1 ? d.batch : 1;
+  hipLaunchKernelGGL((gemm_kernel<A1R, B1R, A2R, B2R, TWO>), dim3(grid, nb), dim3(256), 0, s, d, ntiles);
   DUO_LAUNCH_CHECK();
   return DUO_OK;
 }

@@ -46,6 +46,9 @@ struct GemmDesc {
   int tri;
   int nterms;
   GemmTerm t[2];
+  // batched launches: problem z (blockIdx.y) uses C + z*sC, A_i + z*sA[i], B_i + z*sB[i]
+  int batch;  // 0 or 1: a single problem
+  int64_t sC, sA[2], sB[2];
 };
 
 duo_status gemm_f32(const GemmDesc& d, hipStream_t s);

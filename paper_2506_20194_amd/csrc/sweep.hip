@@ -362,7 +362,9 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
       mode = MODE_KEEP_ALL;
     else if (z >= total)
       mode = MODE_PRUNE_ALL;
-    const int pgrid = (int)(cdiv(total, 256 * 8) < 1024 ? cdiv(total, 256 * 8) : 1024);
+    // few workgroups: each pushes its local histogram to the global one with
+    // integer atomics, and hot bins serialise across workgroups
+    const int pgrid = (int)(cdiv(total, 8192) < 128 ? cdiv(total, 8192) : 128);
     prof_begin(DUO_PROF_SELECT, s);
     if (mode == MODE_SELECT) {
       hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist, (uint32_t)z);
