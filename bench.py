@@ -23,6 +23,33 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3    # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
+# HBM bytes per gram_kernel launch on this workload, from rocprofv3 --pmc
+# FETCH_SIZE and WRITE_SIZE runs (profiles/gram_kernel_llama2_7b_q_proj_hbm_traffic.md),
+# each scaled by what the same counter reads for a plain 1 GiB streaming kernel
+# (FETCH_SIZE x2.0, WRITE_SIZE x1.0).  Valid only for the kernel source they
+# were taken on: any change to that file makes the figure unknown (null).
+GRAM_TRAFFIC = {
+    "source": "paper_2506_20194_amd/csrc/hessian.hip",
+    "sha256": "26600e3902511106842e0ba4c88d4f243469cc611057de9afc7670740c6c1642",
+    "workload": "llama2_7b_q_proj",
+    "fetch_kib": 5626304.3, "fetch_scale": 2.0,
+    "write_kib": 501792.7, "write_scale": 1.0,
+}
+
+
+def gram_traffic(workload):
+    import hashlib
+
+    t = GRAM_TRAFFIC
+    try:
+        with open(os.path.join(ROOT, t["source"]), "rb") as f:
+            same = hashlib.sha256(f.read()).hexdigest() == t["sha256"]
+    except OSError:
+        same = False
+    if not same or workload != t["workload"]:
+        return None
+    return 1024.0 * (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"])
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -31,13 +58,38 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama2_7b_q_proj")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a device-to-device copy of MIB MiB (calibrates HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_probe(mib):
+    """A plain streaming kernel of known size (y = -x over MIB MiB of fp32):
+    its FETCH_SIZE / WRITE_SIZE counters give the factor that turns those
+    counters into HBM bytes."""
+    import torch
+
+    n = mib << 20
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 3
+    print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "ms_per_copy": ms,
+                      "GBs": 2 * n / (ms * 1e-3) / 1e9}), flush=True)
 
 
 def cpu_baseline(W, X, c):
     """The float64 oracle, untuned, on a bounded sample of the same layer:
-    stage 1 on the first 1024 tokens, stages 2-3 precompute at full width,
-    the sweep on the first 64 rows; each part scaled to the full layer."""
+    stage 1 on the first 8192 tokens, stages 2-3 precompute at full width,
+    the sweep on the first 512 rows; each part scaled to the full layer."""
     import numpy as np
 
     from oracle import duo_ref as R
@@ -49,7 +101,7 @@ def cpu_baseline(W, X, c):
     except Exception:  # pragma: no cover
         cores = len(os.sched_getaffinity(0))
     n, k, m = c["n"], c["k"], c["m"]
-    ms, ns = min(1024, m), min(64, n)
+    ms, ns = min(8192, m), min(512, n)
     Xs = X[:ms].float().cpu().numpy()
     Ws = W[:ns].float().cpu().numpy()
     t = time.perf_counter()
@@ -81,6 +133,9 @@ def main():
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the multi-GPU path is a design note, not implemented", file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     import torch
 
     from paper_2506_20194_amd import duo
@@ -167,7 +222,7 @@ def main():
                    "inputs": c["kind"], "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "gram_kernel (H, G)", "achieved": gram_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": gram_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": None, "ms_per_launch": per("gram"), "flop_per_launch": gram_flop_step / gram_launches},
+                     "traffic": gram_traffic(args.workload), "ms_per_launch": per("gram"), "flop_per_launch": gram_flop_step / gram_launches},
         "hessian_tflops": hess_tflops,
         "hessian_frac": hess_tflops / PEAK_BF16_TFLOPS,
         "sweep_gbs": sweep_gbs,
