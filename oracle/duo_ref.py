@@ -48,8 +48,10 @@ __all__ = [
     "act_zero_count",
     "sparsify_tokens",
     "hessian_terms",
+    "hessian_entries",
     "inverse_cholesky",
     "score_terms",
+    "window_terms",
     "block_prune_counts",
     "select_block_mask",
     "sweep_eager",
@@ -128,6 +130,55 @@ def hessian_terms(X_src, p_x: float, X_dense=None):
     return H, G, a
 
 
+def _token_keep(X, z: int):
+    """Keep-mask of reading R-act for a block of tokens, through selection
+    rather than a full sort: the z-th smallest magnitude v of each token is
+    found; entries below v are zeroed, and of the entries equal to v the
+    lowest-channel ones are zeroed until z entries are gone."""
+    m, k = X.shape
+    if z <= 0:
+        return np.ones((m, k), dtype=bool)
+    if z >= k:
+        return np.zeros((m, k), dtype=bool)
+    mag = np.abs(X)
+    v = np.partition(mag, z - 1, axis=1)[:, z - 1:z]
+    below = mag < v
+    tied = mag == v
+    need = z - np.sum(below, axis=1, keepdims=True)      # zeros still to place among the ties
+    zero_tied = tied & (np.cumsum(tied, axis=1) <= need)   # channel order
+    return ~(below | zero_tied)
+
+
+def hessian_entries(X_src, p_x: float, idx, X_dense=None, t0: int = 0, t1: int | None = None):
+    """Selected entries of the stage-1 terms, summed over tokens t0..t1-1.
+
+    Returns dict(H=H[idx][:, idx], G=G[idx][:, idx], a=a (all k), diag=diag(H)
+    (all k)) with the same definitions as ``hessian_terms``, for layers whose
+    full k x k terms are too large to form in float64.  Tokens are taken in
+    chunks; results over disjoint token ranges add up.
+    """
+    idx = np.asarray(idx)
+    m, k = X_src.shape
+    t1 = m if t1 is None else t1
+    z = act_zero_count(k, p_x)
+    s = len(idx)
+    H = np.zeros((s, s))
+    G = np.zeros((s, s))
+    a = np.zeros(k)
+    diag = np.zeros(k)
+    for c0 in range(t0, t1, 1024):
+        c1 = min(t1, c0 + 1024)
+        Xs = _f64(X_src[c0:c1])
+        Xd = Xs if X_dense is None else _f64(X_dense[c0:c1])
+        Xh = np.where(_token_keep(Xs, z), Xs, 0.0)
+        dX = Xd - Xh
+        H += Xh[:, idx].T @ Xh[:, idx]
+        G += dX[:, idx].T @ Xh[:, idx]
+        a += np.sum(dX * dX, axis=0)
+        diag += np.sum(Xh * Xh, axis=0)
+    return dict(H=H, G=G, a=a, diag=diag)
+
+
 # ---------------------------------------------------------------------------
 # Damped inverse Cholesky (Sec. 4.3, Alg. 1 "Inverse_Cholesky")
 # ---------------------------------------------------------------------------
@@ -170,6 +221,25 @@ def score_terms(G, L, a):
     D = U @ L.T
     fac = 1.0 / dL ** 2 + a - b + 2.0 * c
     return fac, D, (a, b, c)
+
+
+def window_terms(H_win, G_win, a_win, lam: float):
+    """L, fac and D restricted to a trailing window of columns T = [k-t, k).
+
+    Write H + lambda I = V V^T with V = L^-T upper triangular.  Because V is
+    upper triangular, the trailing t x t block satisfies
+    (H + lambda I)[T, T] = V[T, T] V[T, T]^T, so L[T, T] is the inverse
+    Cholesky factor of that block alone.  Q = G L, b, c and D = U L^T restricted
+    to T only involve L[T, T] and G[T, T] (L is lower, U strictly upper), so the
+    window is self-contained once lambda (from the whole diagonal) is known.
+    Returns (L_win, fac_win, D_win).
+    """
+    H_win = _f64(H_win)
+    t = H_win.shape[0]
+    Hinv = np.linalg.inv(H_win + lam * np.eye(t))
+    L = np.linalg.cholesky(0.5 * (Hinv + Hinv.T))
+    fac, D, _ = score_terms(G_win, L, a_win)
+    return L, fac, D
 
 
 # ---------------------------------------------------------------------------

@@ -414,3 +414,48 @@ def test_two_stream_residual():
     for p in range(k):
         v, val = _ridge(Xh[:, p + 1:], Xd[:, p], lam)
         assert abs(fac[p] - (lam + val)) <= 1e-8 * fac[p]
+
+
+@pytest.mark.parametrize("m,k,p_x", [(300, 37, 0.5), (200, 64, 0.0), (100, 20, 1.0), (257, 129, 0.6)])
+def test_hessian_entries_match_full_terms(m, k, p_x):
+    """Reading R-act through a selection (hessian_entries) and through a
+    stable sort (hessian_terms) give the same stage-1 entries, with planted
+    magnitude ties and signed zeros; token ranges add up."""
+    rng = np.random.default_rng(k)
+    X = np.round(rng.standard_normal((m, k)) * 4) / 4
+    X[::5, ::3] = -0.0
+    Xd = X + 0.1 * rng.standard_normal((m, k))
+    H, G, a = R.hessian_terms(X, p_x, Xd)
+    idx = np.sort(rng.choice(k, min(k, 9), replace=False))
+    e = R.hessian_entries(X, p_x, idx, Xd)
+    np.testing.assert_allclose(e["H"], H[np.ix_(idx, idx)], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(e["G"], G[np.ix_(idx, idx)], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(e["a"], a, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(e["diag"], np.diag(H), rtol=1e-12, atol=1e-12)
+    lo = R.hessian_entries(X, p_x, idx, Xd, 0, m // 2)
+    hi = R.hessian_entries(X, p_x, idx, Xd, m // 2, m)
+    np.testing.assert_allclose(lo["H"] + hi["H"], e["H"], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("t", [1, 5, 16])
+def test_window_terms_trailing_block(t):
+    """Trailing-window self-containment (the UL structure of Sec. 4.3's
+    Cholesky of the inverse): L, fac and D on the last t columns follow from
+    the window's H, G, a and the global lambda alone.  Checked against the
+    full-matrix oracle and, independently, against the ridge characterisation
+    fac_p = lambda + min |v Xh_{>p} - X_dense_p|^2 + lambda |v|^2 (App. A)."""
+    W, X = _layer(70 + t, 1, 24, 120)
+    Xd = X + 0.05 * np.random.default_rng(t).standard_normal(X.shape)
+    H, G, a = R.hessian_terms(X, 0.5, Xd)
+    L, lam = R.inverse_cholesky(H, 0.05)
+    fac, D, _ = R.score_terms(G, L, a)
+    k = H.shape[0]
+    T = slice(k - t, k)
+    Lw, facw, Dw = R.window_terms(H[T, T], G[T, T], a[T], lam)
+    np.testing.assert_allclose(Lw, L[T, T], rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(facw, fac[T], rtol=1e-9)
+    np.testing.assert_allclose(Dw, D[T, T], rtol=1e-8, atol=1e-10)
+    Xh, _ = R.sparsify_tokens(X, 0.5)
+    for i, p in enumerate(range(k - t, k)):
+        _, val = _ridge(Xh[:, p + 1:], Xd[:, p], lam)
+        assert abs(facw[i] - (lam + val)) <= 1e-8 * facw[i]
