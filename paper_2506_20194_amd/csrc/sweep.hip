@@ -2,20 +2,27 @@
 // Algorithm 1, inner and outer loops; scores from Eq. 7).
 //
 // Per block of B columns [j0, j0+Bb):
-//   select   S = W[:, blk]^2 * fac[blk]; the z lowest by (S, column, row)
-//            are pruned.  Three radix passes (11/11/10 bits) over the
-//            order-preserving bits of S find the threshold value; the last
-//            workgroup of each pass resolves the bucket (integer atomics
-//            only, so the result is deterministic); exact ties at the
-//            threshold are ordered by (column, row).
-//   in-block one row per 8 lanes, each lane owning 16 columns (c = lane%8 +
-//            8i); L[blk, blk] and D[blk, blk] sit in LDS.  Column j: w0 =
-//            W[:, j], p = w0 * m_j, e = (w0 - p) / L_jj; later columns get
-//            w -= e L[c][j] - w0 D[j][c].  E and W0 are kept for the lazy
-//            update.
+//   select   S = W[:, blk]^2 * fac[blk]; the z lowest by (S, column, row) are
+//            pruned.  Every element has the unique key (bits of S,
+//            column*n + row).  One launch histograms the top 13 key bits over
+//            the block; the next gathers the elements of the bucket that
+//            holds the z-th key (normally a few thousand) and its last
+//            workgroup finds the exact threshold among them by a radix select
+//            in LDS (a bucket larger than kSelCap is read from the block
+//            itself).  Counting uses integer atomics only, so the result is
+//            deterministic.
+//   in-block one row per 16 lanes (one DPP row), each lane owning the 8 columns
+//            c = lane%16 + 16i; L[blk, blk] and D[blk, blk] sit in LDS.  For
+//            column j the owner's current value w0 reaches the other 15 lanes
+//            by a DPP row broadcast; p = w0 * m_j, e = (w0 - p) / L_jj, and
+//            later columns get w -= e L[c][j] - w0 D[j][c].  The 128 steps are
+//            unrolled so that every register index is static.  E and W0 are
+//            kept for the lazy update.
 //   lazy     W[:, rest] += -E L[rest, blk]^T + W0 D[blk, rest] as one two-term
 //            fp32 MFMA GEMM (W0 = the columns' values before pruning).
 #include <hip/hip_runtime.h>
+
+#include <utility>
 
 #include "internal.h"
 
@@ -24,148 +31,318 @@ namespace duo {
 namespace {
 
 enum { MODE_SELECT = 0, MODE_FORCED = 1, MODE_KEEP_ALL = 2, MODE_PRUNE_ALL = 3 };
-constexpr int kBins = 2048;
+constexpr int kShift0 = 19;                 // launch 0 histograms key bits 31..19
+constexpr int kBins0 = 1 << (32 - kShift0); // 8192 bins
+constexpr int kDigit = 8;                   // radix digit of the final select
+constexpr int kSelCap = 8192;               // largest bucket gathered into LDS
+constexpr int kSelWG = 128;                 // workgroups of a selection launch (at most)
+constexpr int kRowU = 16;                   // rows loaded per batch by one thread
 
 struct SelState {
-  uint32_t prefix;   // key bits found so far (the full threshold key after pass 2)
-  uint32_t rank;     // rank of the z-th key inside the current bucket (1-based)
-  uint32_t counter;  // workgroups finished in the current pass
-  uint32_t cnt_eq;   // number of keys equal to the threshold
-  long long tie_idx; // ties with (column*n + row) <= tie_idx are pruned
+  uint32_t ncand;    // candidates gathered for the current block
+  uint32_t key;      // threshold: an element is pruned iff
+  uint32_t tie;      //   (key, column*n + row) <= (key, tie)
+  uint32_t pad;
 };
 
-__global__ void sel_init_kernel(SelState* st, uint32_t* hist, uint32_t z) {
-  for (int i = threadIdx.x; i < kBins; i += blockDim.x) hist[i] = 0;
-  if (threadIdx.x == 0) {
-    st->prefix = 0;
-    st->rank = z;
-    st->counter = 0;
-    st->cnt_eq = 0;
-    st->tie_idx = -1;
-  }
+__global__ void sel_reset_kernel(SelState* st, uint32_t* hist) {
+  for (int i = threadIdx.x; i < kBins0; i += blockDim.x) hist[i] = 0;
+  if (threadIdx.x < (int)(sizeof(SelState) / 4)) ((uint32_t*)st)[threadIdx.x] = 0;
 }
 
-__device__ inline uint32_t atomic_ld(const uint32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// One radix pass.  pass 0 also writes the scores when requested; with
-// do_hist == 0 it only writes scores.
-__global__ __launch_bounds__(256) void sel_pass_kernel(const float* __restrict__ W, int64_t ldw, int n, int Bb, int j0,
-                                                       const float* __restrict__ fac, SelState* st, uint32_t* hist,
-                                                       int pass, int do_hist, float* scores_out) {
-  __shared__ uint32_t lh[kBins];
-  __shared__ uint32_t wsum[4];
-  __shared__ int last;
-  const int shift = pass == 0 ? 21 : pass == 1 ? 10 : 0;
-  const uint32_t nb = pass == 2 ? 1024u : 2048u;
-  const uint32_t pmask = pass == 0 ? 0u : pass == 1 ? 0xffe00000u : 0xfffffc00u;
-  const uint32_t prefix = do_hist ? st->prefix : 0u;
-  for (int i = threadIdx.x; i < kBins; i += 256) lh[i] = 0;
-  __syncthreads();
-  const int64_t total = (int64_t)n * Bb;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
-    const int r = (int)(e / Bb), c = (int)(e % Bb);
-    const float S = weight_score(W[(int64_t)r * ldw + j0 + c], fac[j0 + c]);
-    if (scores_out && pass == 0) scores_out[(int64_t)r * ldw + j0 + c] = S;
-    if (do_hist) {
-      const uint32_t key = orderable(S);
-      if ((key & pmask) == prefix) atomicAdd(&lh[(key >> shift) & (nb - 1)], 1u);
-    }
-  }
-  if (!do_hist) return;
-  __syncthreads();
-  for (int i = threadIdx.x; i < (int)nb; i += 256)
-    if (lh[i]) atomicAdd(&hist[i], lh[i]);
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) last = atomicAdd(&st->counter, 1u) == gridDim.x - 1;
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  // last workgroup: locate the bucket holding the rank-th key
-  const uint32_t rank = st->rank;
-  const int per = (int)nb / 256;
-  uint32_t h[8];
-  uint32_t mine = 0;
-  for (int q = 0; q < per; ++q) {
-    h[q] = atomic_ld(&hist[threadIdx.x * per + q]);
-    mine += h[q];
-  }
-  // exclusive scan of `mine` over the 256 threads (bins in ascending order)
-  uint32_t incl = mine;
-  const int lane = threadIdx.x & 63;
+// Inclusive sum over the 256 threads of a workgroup; `tot` gets the total.
+__device__ inline uint32_t block_incl_scan(uint32_t v, uint32_t* wsum, uint32_t& tot) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint32_t incl = v;
+#pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const uint32_t y = __shfl_up(incl, o);
     if (lane >= o) incl += y;
   }
-  if (lane == 63) wsum[threadIdx.x >> 6] = incl;
+  __syncthreads();
+  if (lane == 63) wsum[wv] = incl;
   __syncthreads();
   uint32_t base = 0;
-  for (int w = 0; w < (int)(threadIdx.x >> 6); ++w) base += wsum[w];
-  const uint32_t excl = base + incl - mine;
-  if (excl < rank && rank <= excl + mine) {
+  tot = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (w < wv) base += wsum[w];
+    tot += wsum[w];
+  }
+  return base + incl;
+}
+
+// Bin of a histogram h[0 .. 256*PER) holding the rank-th element (1-based),
+// the rank inside that bin and the bin's count.  Called by all 256 threads;
+// every thread gets the result.
+template <int PER>
+__device__ void find_bucket(const uint32_t* h, uint32_t rank, uint32_t* sh, uint32_t& bin, uint32_t& rank_in,
+                            uint32_t& cnt) {
+  const int b0 = threadIdx.x * PER;
+  uint32_t hv[PER];
+  uint32_t mine = 0;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) hv[q] = h[b0 + q];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) mine += hv[q];
+  uint32_t tot;
+  const uint32_t incl = block_incl_scan(mine, sh + 4, tot);
+  const uint32_t excl = incl - mine;
+  if (excl < rank && rank <= incl) {
     uint32_t cum = excl;
-    for (int q = 0; q < per; ++q) {
-      if (rank <= cum + h[q]) {
-        const uint32_t bin = (uint32_t)(threadIdx.x * per + q);
-        st->prefix = prefix | (bin << shift);
-        st->rank = rank - cum;
-        st->cnt_eq = h[q];
-        break;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      if (rank > cum && rank <= cum + hv[q]) {
+        sh[0] = (uint32_t)(b0 + q);
+        sh[1] = rank - cum;
+        sh[2] = hv[q];
       }
-      cum += h[q];
+      cum += hv[q];
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < kBins; i += 256) hist[i] = 0;
-  if (threadIdx.x == 0) st->counter = 0;
-  if (pass != 2) return;
-  __threadfence();
+  bin = sh[0];
+  rank_in = sh[1];
+  cnt = sh[2];
   __syncthreads();
-  // ties at the threshold: prune the first `rank` of them in (column, row) order
-  const uint32_t T = atomic_ld(&st->prefix);
-  const uint32_t need = atomic_ld(&st->rank);
-  const uint32_t eq = atomic_ld(&st->cnt_eq);
-  if (need >= eq) {
-    if (threadIdx.x == 0) st->tie_idx = 0x7fffffffffffffffLL;
-    return;
-  }
-  __shared__ uint32_t found;
-  uint32_t seen = 0;
-  for (int64_t b0 = 0; b0 < total; b0 += 256) {
-    const int64_t idx = b0 + threadIdx.x;  // idx = column * n + row
-    uint32_t is = 0;
-    if (idx < total) {
-      const int c = (int)(idx / n), r = (int)(idx % n);
-      is = orderable(weight_score(W[(int64_t)r * ldw + j0 + c], fac[j0 + c])) == T;
+}
+
+// f(row, w) for rows r0+rs, r0+rs+2, ... < r1 of one column.  Loads are
+// issued kRowU at a time, unconditionally (clamped to a valid row), so that
+// they are all in flight together; the trip count is uniform per wave.
+template <class F>
+__device__ __forceinline__ void for_rows(const float* Wc, int64_t ldw, int r0, int r1, int rs, bool cv, F&& f) {
+  for (int rb = r0 + rs; rb < r1; rb += 2 * kRowU) {
+    float v[kRowU];
+#pragma unroll
+    for (int u = 0; u < kRowU; ++u) {
+      const int r = rb + 2 * u < r1 ? rb + 2 * u : rb;
+      v[u] = Wc[(int64_t)r * ldw];
     }
-    uint32_t inc = is;
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t y = __shfl_up(inc, o);
-      if (lane >= o) inc += y;
+#pragma unroll
+    for (int u = 0; u < kRowU; ++u)
+      if (cv && rb + 2 * u < r1) f(rb + 2 * u, v[u]);
+  }
+}
+
+// Selection of one block in three launches (see the file comment); kernel
+// boundaries are the only synchronisation, so no cache-wide fences are needed.
+//
+// Workgroup b of the first two owns rows [b*rpw, (b+1)*rpw); thread t handles
+// column t % 128 (clamped to Bb - 1 and masked) of every second row.
+
+// 1. histogram of key bits 31..19 over the block (optionally writing S)
+__global__ __launch_bounds__(256) void sel_hist_kernel(const float* __restrict__ W, int64_t ldw, int n, int Bb, int j0,
+                                                       const float* __restrict__ fac, uint32_t* hist,
+                                                       float* scores_out, int do_hist) {
+  __shared__ uint32_t lh[kBins0];
+  const int tid = threadIdx.x;
+  const int rpw = (n + gridDim.x - 1) / gridDim.x;
+  const int r0 = blockIdx.x * rpw, r1 = min(n, r0 + rpw);
+  const int c = min(tid & 127, Bb - 1), rs = tid >> 7;
+  const bool cv = (tid & 127) < Bb;
+  const float fc = fac[j0 + c];
+  const float* Wc = W + j0 + c;
+  if (do_hist)
+    for (int i = tid; i < kBins0; i += 256) lh[i] = 0;
+  __syncthreads();
+  for_rows(Wc, ldw, r0, r1, rs, cv, [&](int r, float w) {
+    const float S = weight_score(w, fc);
+    if (scores_out) scores_out[(int64_t)r * ldw + j0 + c] = S;
+    if (do_hist) atomicAdd(&lh[orderable(S) >> kShift0], 1u);
+  });
+  if (!do_hist) return;
+  __syncthreads();
+  for (int i = tid; i < kBins0; i += 256)
+    if (lh[i]) atomicAdd(&hist[i], lh[i]);
+}
+
+// 2. every workgroup locates the bucket of the z-th key in the histogram and
+//    appends its elements of that bucket as (low 19 key bits, index)
+//    composites; one atomic per workgroup reserves its slots
+__global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict__ W, int64_t ldw, int n, int Bb, int j0,
+                                                         const float* __restrict__ fac, uint32_t z, int idx_bits,
+                                                         const uint32_t* hist, SelState* st,
+                                                         unsigned long long* cand) {
+  __shared__ uint32_t sh[16];
+  const int tid = threadIdx.x;
+  uint32_t bin, rank, cnt;
+  find_bucket<kBins0 / 256>(hist, z, sh, bin, rank, cnt);
+  if (cnt > (uint32_t)kSelCap) return;  // the resolving launch reads the block itself
+  const int rpw = (n + gridDim.x - 1) / gridDim.x;
+  const int r0 = blockIdx.x * rpw, r1 = min(n, r0 + rpw);
+  const int c = min(tid & 127, Bb - 1), rs = tid >> 7;
+  const bool cv = (tid & 127) < Bb;
+  const float fc = fac[j0 + c];
+  const float* Wc = W + j0 + c;
+  uint32_t mine = 0;
+  for_rows(Wc, ldw, r0, r1, rs, cv, [&](int, float w) { mine += (orderable(weight_score(w, fc)) >> kShift0) == bin; });
+  uint32_t tot;
+  const uint32_t incl = block_incl_scan(mine, sh + 4, tot);
+  if (tid == 0) sh[9] = tot ? atomicAdd(&st->ncand, tot) : 0u;
+  __syncthreads();
+  uint32_t pos = sh[9] + incl - mine;
+  for_rows(Wc, ldw, r0, r1, rs, cv, [&](int r, float w) {
+    const uint32_t key = orderable(weight_score(w, fc));
+    if ((key >> kShift0) == bin) {
+      if (pos < (uint32_t)kSelCap)
+        cand[pos] = ((unsigned long long)(key & ((1u << kShift0) - 1u)) << idx_bits) |
+                    (unsigned long long)((uint32_t)c * (uint32_t)n + (uint32_t)r);
+      ++pos;
+    }
+  });
+}
+
+// 3. one workgroup: radix select of the rank-th composite of the bucket, from
+//    the gathered candidates in LDS (or, for a bucket larger than kSelCap,
+//    straight from the block); then clears the histogram for the next block
+__global__ __launch_bounds__(256) void sel_resolve_kernel(const float* __restrict__ W, int64_t ldw, int n, int Bb,
+                                                          int j0, const float* __restrict__ fac, uint32_t z,
+                                                          int idx_bits, uint32_t* hist, SelState* st,
+                                                          const unsigned long long* cand) {
+  extern __shared__ __attribute__((aligned(16))) uint32_t sel_sm[];
+  uint32_t* sh = sel_sm;                                          // [16]
+  uint32_t* lh = sel_sm + 16;                                     // [1 << kDigit]
+  unsigned long long* lc = (unsigned long long*)(lh + (1 << kDigit));  // [kSelCap]
+  const int tid = threadIdx.x;
+  uint32_t bin, rank, cnt;
+  find_bucket<kBins0 / 256>(hist, z, sh, bin, rank, cnt);
+  const bool gather = cnt <= (uint32_t)kSelCap;
+  if (gather)
+    for (uint32_t i0 = 0; i0 < cnt; i0 += 256 * 8) {
+      unsigned long long v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i = i0 + 256 * u + tid;
+        v[u] = cand[i < cnt ? i : 0];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i = i0 + 256 * u + tid;
+        if (i < cnt) lc[i] = v[u];
+      }
+    }
+  const int c = min(tid & 127, Bb - 1), rs = tid >> 7;
+  const bool cv = (tid & 127) < Bb;
+  const float fc = fac[j0 + c];
+  const float* Wc = W + j0 + c;
+  const int tb = kShift0 + idx_bits;
+  const int start = (tb + kDigit - 1) / kDigit * kDigit;
+  unsigned long long pref = 0;
+  uint32_t rk = rank;
+  for (int s = start - kDigit; s >= 0; s -= kDigit) {
+    for (int i = tid; i < (1 << kDigit); i += 256) lh[i] = 0;
+    __syncthreads();
+    const int hs = s + kDigit;
+    auto add = [&](unsigned long long v) {
+      if ((v >> hs) == (pref >> hs)) atomicAdd(&lh[(uint32_t)(v >> s) & ((1u << kDigit) - 1u)], 1u);
+    };
+    if (gather) {
+#pragma unroll 8
+      for (uint32_t i = tid; i < cnt; i += 256) add(lc[i]);
+    } else {
+      // rare: a bucket this large means a long run of nearly equal scores
+      for_rows(Wc, ldw, 0, n, rs, cv, [&](int r, float w) {
+        const uint32_t key = orderable(weight_score(w, fc));
+        if ((key >> kShift0) == bin)
+          add(((unsigned long long)(key & ((1u << kShift0) - 1u)) << idx_bits) |
+              (unsigned long long)((uint32_t)c * (uint32_t)n + (uint32_t)r));
+      });
     }
     __syncthreads();
-    if (lane == 63) wsum[threadIdx.x >> 6] = inc;
-    __syncthreads();
-    uint32_t bb = 0, tot = 0;
-    for (int w = 0; w < 4; ++w) {
-      if (w < (int)(threadIdx.x >> 6)) bb += wsum[w];
-      tot += wsum[w];
-    }
-    if (is && seen + bb + inc == need) st->tie_idx = idx;
-    seen += tot;
-    if (seen >= need) break;  // uniform
+    uint32_t d, rk2, ct2;
+    find_bucket<(1 << kDigit) / 256>(lh, rk, sh, d, rk2, ct2);
+    pref |= (unsigned long long)d << s;
+    rk = rk2;
   }
-  (void)found;
+  for (int i = tid; i < kBins0; i += 256) hist[i] = 0;
+  if (tid == 0) {
+    st->key = (bin << kShift0) | (uint32_t)(pref >> idx_bits);
+    st->tie = (uint32_t)(pref & ((1ull << idx_bits) - 1ull));
+    st->ncand = 0;
+  }
 }
 
 // ---------------------------------------------------------------------------
 // in-block sweep
 // ---------------------------------------------------------------------------
-constexpr int GS = 8;    // lanes per row
-constexpr int NPT = 16;  // columns per lane
-constexpr int RPB = 32;  // rows per workgroup
+constexpr int IB_Q = 16;                  // lanes per row (one DPP row)
+constexpr int IB_I = kMaxBlock / IB_Q;    // columns per lane: c = q + 16 i
+constexpr int IB_ROWS = 256 / IB_Q;       // rows per workgroup
+constexpr int IB_QS = IB_I + 1;           // LDS stride between lanes (odd: no bank conflicts)
+constexpr int IB_JS = IB_Q * IB_QS;       // LDS floats per column step
+
+// Lane O of every 16-lane row, broadcast to the row.
+template <int O>
+__device__ __forceinline__ float row_bcast(float v) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x150 + O, 0xF, 0xF, false));
+}
+
+struct IbRow {
+  float w[IB_I];     // current values of columns q + 16 i
+  float e[IB_I];     // E of the columns this lane owns
+  float w0[IB_I];    // values before pruning of the columns this lane owns
+  uint32_t kb[IB_I]; // keep bits of the row: bit o of kb[g] is column 16 g + o
+};
+
+// LDS operands of one column step: the staged L and D entries of this lane's
+// columns that are still live (i >= g) and 1 / L_JJ.
+struct IbBuf {
+  float l[IB_I], d[IB_I];
+  float il;
+};
+
+template <int J>
+__device__ __forceinline__ void ib_load(IbBuf& b, const float* __restrict__ lq, const float* __restrict__ dq,
+                                        const float* __restrict__ il, int q) {
+  if constexpr (J < kMaxBlock) {
+    constexpr int g = J / IB_Q;
+    const float* lr = lq + J * IB_JS + q * IB_QS;
+    const float* dr = dq + J * IB_JS + q * IB_QS;
+#pragma unroll
+    for (int i = g; i < IB_I; ++i) {
+      b.l[i] = lr[i];
+      b.d[i] = dr[i];
+    }
+    b.il = il[J];
+  }
+}
+
+// Column J = 16 g + o of the block (owner lane o, register g).  The staged L
+// column is already divided by L_JJ, so u = w0 - p feeds the update directly
+// and e = u / L_JJ is only needed for the owner's record.  Columns past the
+// ragged end of the block have zero L, D entries and values: their steps
+// change nothing.  Step J issues the LDS reads of step J + 2 (three-slot
+// ring); the scheduling barrier keeps the compiler from hoisting more.
+template <int J>
+__device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* __restrict__ lq,
+                                        const float* __restrict__ dq, const float* __restrict__ il, int q) {
+  constexpr int g = J / IB_Q, o = J % IB_Q;
+  ib_load<J + 2>(buf[(J + 2) % 3], lq, dq, il, q);
+  const IbBuf& b = buf[J % 3];
+  const float v = row_bcast<o>(s.w[g]);
+  const bool kj = (s.kb[g] >> o) & 1u;
+  const float u = kj ? 0.f : v;
+  if (q == o) {
+    s.w[g] = v - u;
+    s.e[g] = u * b.il;
+    s.w0[g] = v;
+  }
+  // columns c = q + 16 i > J; the LDS entries of columns <= J are zero
+#pragma unroll
+  for (int i = g; i < IB_I; ++i) s.w[i] = fmaf(-u, b.l[i], fmaf(v, b.d[i], s.w[i]));
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int... Js>
+__device__ __forceinline__ void ib_steps(IbRow& s, const float* lq, const float* dq, const float* il, int q,
+                                         std::integer_sequence<int, Js...>) {
+  IbBuf buf[3];
+  ib_load<0>(buf[0], lq, dq, il, q);
+  ib_load<1>(buf[1], lq, dq, il, q);
+  (ib_step<Js>(s, buf, lq, dq, il, q), ...);
+}
 
 __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int B,
                                                       const float* __restrict__ L, int64_t ldl,
@@ -174,61 +351,75 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
                                                       const uint32_t* __restrict__ mask_in, float* __restrict__ EW,
                                                       uint8_t* __restrict__ bmask) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
-  float* Lq = sm;                           // [128][8][16]: L[j0+q+8i][j0+j] for q+8i > j
-  float* Dq = sm + kMaxBlock * GS * NPT;    // [128][8][16]: D[j0+j][j0+q+8i] for q+8i > j
-  float* Ld = Dq + kMaxBlock * GS * NPT;    // [128]: L[j0+j][j0+j]
+  float* lq = sm;                       // [j][q][i]: L[j0+q+16i][j0+j] / L[j0+j][j0+j] where q+16i > j, else 0
+  float* dq = sm + kMaxBlock * IB_JS;   // [j][q][i]: D[j0+j][j0+q+16i] where q+16i > j, else 0
+  float* il = dq + kMaxBlock * IB_JS;   // [j]: 1 / L[j0+j][j0+j]
   const int tid = threadIdx.x;
-  for (int p = tid; p < kMaxBlock * GS; p += 256) {
-    {  // L: j fastest so that global reads are contiguous
-      const int j = p % kMaxBlock, q = p / kMaxBlock;
-      float v[NPT];
+  if (tid < kMaxBlock) il[tid] = tid < Bb ? 1.0f / L[(int64_t)(j0 + tid) * ldl + j0 + tid] : 1.f;
+  __syncthreads();
+  // stage L: one wave covers 8 consecutive j of the 8 rows q + 16 i (one q);
+  // all of a thread's loads are issued before its LDS stores
+  constexpr int SPT = kMaxBlock * IB_Q * IB_I / 256;  // 64 elements per thread
 #pragma unroll
-      for (int i = 0; i < NPT; ++i) {
-        const int c = q + GS * i;
-        v[i] = (c > j && c < Bb && j < Bb) ? L[(int64_t)(j0 + c) * ldl + j0 + j] : 0.f;
-      }
-      float4* dst = (float4*)&Lq[(j * GS + q) * NPT];
+  for (int h = 0; h < 2; ++h) {
+    float v[SPT / 2];
 #pragma unroll
-      for (int i = 0; i < NPT / 4; ++i) dst[i] = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+    for (int u = 0; u < SPT / 2; ++u) {
+      const int p = tid + 256 * (h * SPT / 2 + u);
+      const int jj = p & 7, i = (p >> 3) & 7, q = (p >> 6) & 15, j = ((p >> 10) << 3) + jj;
+      const int c = q + IB_Q * i;
+      v[u] = (c > j && c < Bb) ? L[(int64_t)(j0 + c) * ldl + j0 + j] : 0.f;
     }
-    {  // D: q fastest
-      const int q = p % GS, j = p / GS;
-      float v[NPT];
 #pragma unroll
-      for (int i = 0; i < NPT; ++i) {
-        const int c = q + GS * i;
-        v[i] = (c > j && c < Bb && j < Bb) ? D[(int64_t)(j0 + j) * ldd + j0 + c] : 0.f;
-      }
-      float4* dst = (float4*)&Dq[(j * GS + q) * NPT];
-#pragma unroll
-      for (int i = 0; i < NPT / 4; ++i) dst[i] = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+    for (int u = 0; u < SPT / 2; ++u) {
+      const int p = tid + 256 * (h * SPT / 2 + u);
+      const int jj = p & 7, i = (p >> 3) & 7, q = (p >> 6) & 15, j = ((p >> 10) << 3) + jj;
+      lq[j * IB_JS + q * IB_QS + i] = v[u] * il[j];
     }
   }
-  if (tid < kMaxBlock) Ld[tid] = tid < Bb ? L[(int64_t)(j0 + tid) * ldl + j0 + tid] : 1.f;
+  // stage D: one wave covers 64 consecutive columns of one row j
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    float v[SPT / 2];
+#pragma unroll
+    for (int u = 0; u < SPT / 2; ++u) {
+      const int p = tid + 256 * (h * SPT / 2 + u);
+      const int q = p & 15, i = (p >> 4) & 7, j = p >> 7;
+      const int c = q + IB_Q * i;
+      v[u] = (c > j && c < Bb && j < Bb) ? D[(int64_t)(j0 + j) * ldd + j0 + c] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < SPT / 2; ++u) {
+      const int p = tid + 256 * (h * SPT / 2 + u);
+      const int q = p & 15, i = (p >> 4) & 7, j = p >> 7;
+      dq[j * IB_JS + q * IB_QS + i] = v[u];
+    }
+  }
   __syncthreads();
 
-  const int row = blockIdx.x * RPB + (tid >> 3);
-  const int q = tid & 7;
+  const int lane = tid & 63;
+  const int q = tid & 15;
+  const int row = blockIdx.x * IB_ROWS + (tid >> 4);
   const bool rv = row < n;
-  float w[NPT];
-  uint32_t my = 0;  // bit i: column q + 8i kept
-  uint32_t T = 0;
-  long long tie = -1;
+  uint32_t T = 0, tie = 0;
   if (mode == MODE_SELECT) {
-    T = st->prefix;
-    tie = st->tie_idx;
+    T = st->key;
+    tie = st->tie;
   }
   const int words = (k + 31) / 32;
+  IbRow s;
 #pragma unroll
-  for (int i = 0; i < NPT; ++i) {
-    const int c = q + GS * i;
+  for (int i = 0; i < IB_I; ++i) {
+    const int c = q + IB_Q * i;
     const bool cv = rv && c < Bb;
-    w[i] = cv ? Wo[(int64_t)row * k + j0 + c] : 0.f;
+    s.w[i] = cv ? Wo[(int64_t)row * k + j0 + c] : 0.f;
+    s.e[i] = 0.f;
+    s.w0[i] = 0.f;
     bool keep = true;
     if (cv) {
       if (mode == MODE_SELECT) {
-        const uint32_t key = orderable(weight_score(w[i], fac[j0 + c]));
-        const long long idx = (long long)c * n + row;
+        const uint32_t key = orderable(weight_score(s.w[i], fac[j0 + c]));
+        const uint32_t idx = (uint32_t)c * (uint32_t)n + (uint32_t)row;
         keep = !(key < T || (key == T && idx <= tie));
       } else if (mode == MODE_FORCED) {
         const int gc = j0 + c;
@@ -237,51 +428,19 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
         keep = mode == MODE_KEEP_ALL;
       }
     }
-    my |= (keep ? 1u : 0u) << i;
+    const unsigned long long ball = __ballot(keep);
+    s.kb[i] = (uint32_t)(ball >> (IB_Q * (lane >> 4))) & 0xFFFFu;
   }
-  uint32_t m[GS];  // keep bits of the 8 lanes of this row (bit i: group g + i)
+  ib_steps(s, lq, dq, il, q, std::make_integer_sequence<int, kMaxBlock>{});
 #pragma unroll
-  for (int o = 0; o < GS; ++o) m[o] = __shfl(my, o, GS);
-  const int ngroups = (Bb + GS - 1) / GS;
-
-  // Group g holds columns 8g..8g+7 (column 8g+o belongs to lane o).  After each
-  // group the register arrays shift down by one so that the current group is
-  // always w[0] and every register index is a compile-time constant.
-  for (int g = 0; g < ngroups; ++g) {
-    float e_own = 0.f, w0_own = 0.f;
-#pragma unroll
-    for (int o = 0; o < GS; ++o) {
-      const int j = g * GS + o;
-      if (j < Bb) {  // uniform
-        const float wj = __shfl(w[0], o, GS);
-        const bool kj = m[o] & 1u;
-        const float p = kj ? wj : 0.f;
-        const float e = (wj - p) / Ld[j];
-        if (q == o) {
-          w[0] = p;
-          e_own = e;
-          w0_own = wj;
-        }
-        const float* lq = &Lq[(j * GS + q) * NPT + g];
-        const float* dq = &Dq[(j * GS + q) * NPT + g];
-#pragma unroll
-        for (int i = 0; i < NPT; ++i) {
-          if (i < NPT - g && (i > 0 || q > o)) w[i] -= fmaf(e, lq[i], -(wj * dq[i]));
-        }
-      }
-    }
-    const int c = q + GS * g;
+  for (int i = 0; i < IB_I; ++i) {
+    const int c = q + IB_Q * i;
     if (rv && c < Bb) {
-      Wo[(int64_t)row * k + j0 + c] = w[0];
-      EW[(int64_t)row * 2 * B + c] = e_own;
-      EW[(int64_t)row * 2 * B + B + c] = w0_own;
-      bmask[(int64_t)row * k + j0 + c] = (uint8_t)((my >> g) & 1u);
+      Wo[(int64_t)row * k + j0 + c] = s.w[i];
+      EW[(int64_t)row * 2 * B + c] = s.e[i];
+      EW[(int64_t)row * 2 * B + B + c] = s.w0[i];
+      bmask[(int64_t)row * k + j0 + c] = (uint8_t)((s.kb[i] >> q) & 1u);
     }
-#pragma unroll
-    for (int i = 0; i < NPT - 1; ++i) w[i] = w[i + 1];
-    w[NPT - 1] = 0.f;
-#pragma unroll
-    for (int o = 0; o < GS; ++o) m[o] >>= 1;
   }
 }
 
@@ -316,6 +475,7 @@ __global__ void finalize_kernel(const float* Wo, const uint8_t* bmask, int n, in
 struct SweepWs {
   SelState* st;
   uint32_t* hist;
+  unsigned long long* cand;
   float* EW;
   uint8_t* bmask;
   size_t bytes;
@@ -325,7 +485,8 @@ SweepWs carve(void* ws, int64_t n, int64_t k, int B) {
   Carver c(ws);
   SweepWs w;
   w.st = c.take<SelState>(1);
-  w.hist = c.take<uint32_t>(kBins);
+  w.hist = c.take<uint32_t>(kBins0);
+  w.cand = c.take<unsigned long long>(kSelCap);
   w.EW = c.take<float>((size_t)n * 2 * B);
   w.bmask = c.take<uint8_t>((size_t)n * k);
   w.bytes = c.off;
@@ -345,8 +506,14 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   hipLaunchKernelGGL(init_w_kernel, dim3((unsigned)cdiv(nk, 256)), dim3(256), 0, s, W, (int)w_dtype, ldw, (int)n,
                      (int)k, W_out);
   DUO_LAUNCH_CHECK();
-  const size_t lds = (size_t)(2 * kMaxBlock * GS * NPT + kMaxBlock) * sizeof(float);
-  DUO_HIP_TRY(hipFuncSetAttribute((const void*)inblock_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+  hipLaunchKernelGGL(sel_reset_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist);
+  DUO_LAUNCH_CHECK();
+  const size_t ib_lds = (size_t)(2 * kMaxBlock * IB_JS + kMaxBlock) * sizeof(float);
+  DUO_HIP_TRY(hipFuncSetAttribute((const void*)inblock_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ib_lds));
+  const size_t sel_lds = (size_t)(16 + (1 << kDigit)) * sizeof(uint32_t) + (size_t)kSelCap * sizeof(unsigned long long);
+  DUO_HIP_TRY(
+      hipFuncSetAttribute((const void*)sel_resolve_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sel_lds));
+  const int P = (int)(cdiv(n, 32) < kSelWG ? cdiv(n, 32) : kSelWG);
   int64_t prev = 0;
   for (int64_t j0 = 0; j0 < k; j0 += B) {
     const int Bb = (int)(k - j0 < B ? k - j0 : B);
@@ -362,27 +529,26 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
       mode = MODE_KEEP_ALL;
     else if (z >= total)
       mode = MODE_PRUNE_ALL;
-    // few workgroups: each pushes its local histogram to the global one with
-    // integer atomics, and hot bins serialise across workgroups
-    const int pgrid = (int)(cdiv(total, 8192) < 128 ? cdiv(total, 8192) : 128);
+    int idx_bits = 1;
+    while (idx_bits < 31 && ((int64_t)1 << idx_bits) < total) ++idx_bits;
     prof_begin(DUO_PROF_SELECT, s);
-    if (mode == MODE_SELECT) {
-      hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist, (uint32_t)z);
+    if (mode == MODE_SELECT || scores_out) {
+      hipLaunchKernelGGL(sel_hist_kernel, dim3(P), dim3(256), 0, s, (const float*)W_out, k, (int)n, Bb, (int)j0, fac,
+                         w.hist, scores_out, mode == MODE_SELECT ? 1 : 0);
       DUO_LAUNCH_CHECK();
-      for (int pass = 0; pass < 3; ++pass) {
-        hipLaunchKernelGGL(sel_pass_kernel, dim3(pgrid), dim3(256), 0, s, (const float*)W_out, k, (int)n, Bb, (int)j0,
-                           fac, w.st, w.hist, pass, 1, scores_out);
-        DUO_LAUNCH_CHECK();
-      }
-    } else if (scores_out) {
-      hipLaunchKernelGGL(sel_pass_kernel, dim3(pgrid), dim3(256), 0, s, (const float*)W_out, k, (int)n, Bb, (int)j0,
-                         fac, w.st, w.hist, 0, 0, scores_out);
+    }
+    if (mode == MODE_SELECT) {
+      hipLaunchKernelGGL(sel_gather_kernel, dim3(P), dim3(256), 0, s, (const float*)W_out, k, (int)n, Bb, (int)j0,
+                         fac, (uint32_t)z, idx_bits, (const uint32_t*)w.hist, w.st, w.cand);
+      DUO_LAUNCH_CHECK();
+      hipLaunchKernelGGL(sel_resolve_kernel, dim3(1), dim3(256), sel_lds, s, (const float*)W_out, k, (int)n, Bb,
+                         (int)j0, fac, (uint32_t)z, idx_bits, w.hist, w.st, (const unsigned long long*)w.cand);
       DUO_LAUNCH_CHECK();
     }
     prof_end(DUO_PROF_SELECT, s);
     prof_begin(DUO_PROF_INBLOCK, s);
-    hipLaunchKernelGGL(inblock_kernel, dim3((unsigned)cdiv(n, RPB)), dim3(256), lds, s, W_out, (int)n, (int)k, (int)j0,
-                       Bb, B, L, ldl, D, ldd, fac, (const SelState*)w.st, mode, mask_in, w.EW, w.bmask);
+    hipLaunchKernelGGL(inblock_kernel, dim3((unsigned)cdiv(n, IB_ROWS)), dim3(256), ib_lds, s, W_out, (int)n, (int)k,
+                       (int)j0, Bb, B, L, ldl, D, ldd, fac, (const SelState*)w.st, mode, mask_in, w.EW, w.bmask);
     DUO_LAUNCH_CHECK();
     prof_end(DUO_PROF_INBLOCK, s);
     if (j1 < k) {
