@@ -127,6 +127,47 @@ def cpu_baseline(W, X, c):
     }
 
 
+def bench_block(args):
+    """The LLaMA-2-7B decoder block pruned group by group (7 linears, 4 shared
+    Hessians) on 128 x 2048 tokens; the forward passes of the two activation
+    streams between groups are reported separately from the solver."""
+    import torch
+
+    from paper_2506_20194_amd import block
+    from workloads import synth
+
+    name = args.workload
+    c = synth.BLOCKS[name]
+    cfg = synth.block_cfg(name)
+    dev = torch.device("cuda:0")
+    h, w = synth.block_inputs(name, device=dev)
+    runs = []
+    for i in range(args.warmup + args.steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        out = block.prune_block(h, w, cfg, c["p_x"], c["p_w"], damp=c["damp"], block=c["block"], timing=True)
+        wall = time.perf_counter() - t0
+        if i >= args.warmup:
+            runs.append((out["ms"], wall))
+        del out
+    ms = {k: sum(r[0][k] for r in runs) / len(runs) for k in runs[0][0]}
+    solve_ms = sum(v for k, v in ms.items() if k.startswith("solve"))
+    line = {
+        "metric": "s/block for DuoGPT pruning of a LLaMA-2-7B-shaped decoder block (solver time; the two "
+                  "activation streams' forward passes reported separately)",
+        "value": solve_ms / 1e3, "unit": "s/block", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": solve_ms, "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16 MFMA (H, G) + fp32", "data": "synthetic",
+        "config": {"workload": name, "d": c["d"], "ffn": c["ffn"], "heads": c["heads"], "head_dim": c["head_dim"],
+                   "tokens": cfg["nseq"] * cfg["seq_len"], "p_x": c["p_x"], "p_w": c["p_w"], "block": c["block"],
+                   "damp": c["damp"], "parallelism": "single GPU"},
+        "group_solve_ms": {k: v for k, v in ms.items() if k.startswith("solve")},
+        "forward_ms_both_streams": ms["forward"],
+        "wall_s_per_block": sum(r[1] for r in runs) / len(runs),
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -135,6 +176,11 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    from workloads import synth as _synth
+
+    if args.workload in _synth.BLOCKS:
+        bench_block(args)
         return
     import torch
 

@@ -235,6 +235,69 @@ enum {
 duo_status duo_profile_enable(int32_t on);
 duo_status duo_profile_read(int32_t kernel, double* total_ms, int64_t* launches);
 
+/*
+ * Decoder-block harness.  When a whole decoder block is pruned group by group,
+ * each group's solver input comes from two streams (the multi-layer case of
+ * Sec. 4.2): the dense model's activations (X-tilde, dense weights, no
+ * activation sparsity) and the pruned model's own activations (pruned
+ * weights, every linear input sparsified per token with the rule above).
+ * These calls carry both streams through a LLaMA-style block (Sec. 5 models:
+ * RMSNorm, rotary attention, SiLU-gated MLP).  Activations are bf16,
+ * token-major (row t = token t), arithmetic fp32, device pointers, stream
+ * ordered; argument errors return before anything is enqueued.
+ */
+enum {
+  DUO_BOP_ACT_SPARSIFY = 0, /* duo_act_sparsify (uses m)                 */
+  DUO_BOP_LINEAR = 1,       /* duo_linear (fixed size)                   */
+  DUO_BOP_ATTENTION = 2     /* duo_attention (uses seq_len, heads)       */
+};
+/* Bytes of workspace a harness call needs (0 for a bad op or size). */
+size_t duo_block_workspace_size(int32_t op, int64_t m, int64_t seq_len, int64_t heads);
+
+/* duo_rmsnorm - Y[t] = X[t] / sqrt(mean_c X[t][c]^2 + eps) (unit gain).
+ *   X, Y: m x d bf16 with row strides ldx, ldy >= d (Y may equal X). */
+duo_status duo_rmsnorm(const void* X, int64_t m, int64_t d, int64_t ldx, double eps, void* Y, int64_t ldy,
+                       void* stream);
+
+/* duo_act_sparsify - Y = X-hat: X (m x k bf16, ldx) with the per-token rule
+ *   of duo_act_rule applied (z = floor(p*k + 0.5) smallest (|x|, channel)
+ *   entries of each token set to +0); Y is m x k bf16 (ldy), not aliasing X.
+ *   The kept set is the one duo_hessian_accum uses.
+ *   Workspace: DUO_BOP_ACT_SPARSIFY with the same m.  1 <= k <= 32768. */
+duo_status duo_act_sparsify(const void* X, int64_t m, int64_t k, int64_t ldx, duo_act_rule rule, void* Y,
+                            int64_t ldy, void* ws, size_t ws_bytes, void* stream);
+
+/* duo_linear - Y = X W^T (+ R): X m x k (ldx), W n x k (ldw, a Linear's
+ *   out x in weights), optional residual R m x n (ldr; NULL for none), Y m x n
+ *   (ldy; may equal R).  bf16 in and out, fp32 accumulation, one rounding.
+ *   Computed by rocBLAS (gemm_ex) on the caller's stream, with its scratch
+ *   memory taken from the workspace.  Workspace: DUO_BOP_LINEAR. */
+duo_status duo_linear(const void* X, int64_t m, int64_t k, int64_t ldx, const void* W, int64_t n, int64_t ldw,
+                      const void* R, int64_t ldr, void* Y, int64_t ldy, void* ws, size_t ws_bytes, void* stream);
+
+/* duo_rope - in place rotary position embedding of X (m x heads*head_dim bf16,
+ *   ldx): in every head the pair (i, i + head_dim/2) of token t is rotated by
+ *   the angle (t mod seq_len) * theta^(-2i/head_dim) (angles in fp64). */
+duo_status duo_rope(void* X, int64_t m, int64_t heads, int64_t head_dim, int64_t ldx, int64_t seq_len, double theta,
+                    void* stream);
+
+/* duo_attention - causal attention of nseq sequences of seq_len tokens:
+ *   for each sequence and head h, O_h = softmax(Q_h K_h^T / sqrt(head_dim)
+ *   with positions j > i masked) V_h, where Q_h is columns
+ *   [h*head_dim, (h+1)*head_dim) of the sequence's rows of Q.  Q, K, V share
+ *   the row stride ld; O has ldo.  Scores are fp32 (rocBLAS batched products),
+ *   the row softmax is fp32 and the probabilities are rounded to bf16 before
+ *   the product with V.  Workspace: DUO_BOP_ATTENTION with the same seq_len
+ *   and heads (fp32 and bf16 score planes of one sequence). */
+duo_status duo_attention(const void* Q, const void* K, const void* V, int64_t ld, int64_t nseq, int64_t seq_len,
+                         int64_t heads, int64_t head_dim, void* O, int64_t ldo, void* ws, size_t ws_bytes,
+                         void* stream);
+
+/* duo_silu_mul - Y = SiLU(G) * U elementwise, SiLU(g) = g / (1 + exp(-g));
+ *   G, U m x n bf16 with row stride ld, Y m x n (ldy). */
+duo_status duo_silu_mul(const void* G, const void* U, int64_t m, int64_t n, int64_t ld, void* Y, int64_t ldy,
+                        void* stream);
+
 #ifdef __cplusplus
 }
 #endif

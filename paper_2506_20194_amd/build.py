@@ -11,7 +11,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libduo.so")
-SOURCES = ["abi.hip", "hessian.hip", "gemm_f32.hip", "chol.hip", "score.hip", "sweep.hip", "profile.hip"]
+SOURCES = ["abi.hip", "hessian.hip", "gemm_f32.hip", "chol.hip", "score.hip", "sweep.hip", "profile.hip",
+           "block.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [
@@ -45,7 +46,8 @@ def build(verbose: bool = False) -> str:
             if o.strip():
                 print(o, file=sys.stderr)
     tmp = LIB + f".tmp{os.getpid()}"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp, "-L/opt/rocm/lib", "-lrocblas",
+          "-Wl,-rpath,/opt/rocm/lib"])
     os.replace(tmp, LIB)
     return LIB
 

@@ -33,23 +33,6 @@ bool ws_ok(const void* ws, size_t ws_bytes, size_t need) {
   return (reinterpret_cast<uintptr_t>(ws) % kAlign) == 0;
 }
 
-// 0 unknown, 1 gfx950, 2 something else
-std::atomic<int> g_arch[64];
-
-duo_status device_ok() {
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return DUO_ERR_NO_DEVICE;
-  if (dev >= 64) return DUO_ERR_UNSUPPORTED;
-  int v = g_arch[dev].load(std::memory_order_acquire);
-  if (v == 0) {
-    hipDeviceProp_t p;
-    if (hipGetDeviceProperties(&p, dev) != hipSuccess) return DUO_ERR_NO_DEVICE;
-    v = std::strncmp(p.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
-    g_arch[dev].store(v, std::memory_order_release);
-  }
-  return v == 1 ? DUO_OK : DUO_ERR_NO_DEVICE;
-}
-
 struct PruneWs {
   float* D;
   float* fac;
@@ -72,6 +55,27 @@ PruneWs carve_prune(void* ws, int64_t n, int64_t k, int B) {
 bool k_ok(int64_t k) { return k >= 1 && k <= kMaxK; }
 
 }  // namespace
+
+namespace duo {
+
+// 0 unknown, 1 gfx950, 2 something else
+static std::atomic<int> g_arch[64];
+
+duo_status device_ok() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return DUO_ERR_NO_DEVICE;
+  if (dev >= 64) return DUO_ERR_UNSUPPORTED;
+  int v = g_arch[dev].load(std::memory_order_acquire);
+  if (v == 0) {
+    hipDeviceProp_t p;
+    if (hipGetDeviceProperties(&p, dev) != hipSuccess) return DUO_ERR_NO_DEVICE;
+    v = std::strncmp(p.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+    g_arch[dev].store(v, std::memory_order_release);
+  }
+  return v == 1 ? DUO_OK : DUO_ERR_NO_DEVICE;
+}
+
+}  // namespace duo
 
 extern "C" {
 

@@ -157,6 +157,12 @@ static duo_status launch_act_select(const T* X, int64_t ldx, int m, int k, int z
   return DUO_OK;
 }
 
+duo_status act_threshold_run(const void* X, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z, int64_t* thr,
+                             hipStream_t s) {
+  if (dtype == DUO_BF16) return launch_act_select<uint16_t>((const uint16_t*)X, ldx, (int)m, (int)k, z, thr, s);
+  return launch_act_select<float>((const float*)X, ldx, (int)m, (int)k, z, thr, s);
+}
+
 // ---------------------------------------------------------------------------
 // mask export (test hook): bit c of token t = kept
 // ---------------------------------------------------------------------------

@@ -16,6 +16,14 @@ size_t hessian_ws_bytes(int64_t m, int64_t k);
 duo_status hessian_run(const void* Xs, const void* Xd, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z,
                        float* H, int64_t ldh, float* G, int64_t ldg, float* a, void* ws, bool want_h,
                        hipStream_t s);
+// DUO_OK when the current device is a gfx950 (cached per device), else
+// DUO_ERR_NO_DEVICE (or DUO_ERR_UNSUPPORTED for a device index >= 64).
+duo_status device_ok();
+
+// Per-token threshold keys of the (|x|, channel) rule: entry c of token t is
+// kept iff ((magnitude bits of x) << 32 | c) > thr[t]; z entries are zeroed.
+duo_status act_threshold_run(const void* X, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z, int64_t* thr,
+                             hipStream_t s);
 duo_status act_mask_run(const void* X, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z, uint32_t* mask,
                         void* ws, hipStream_t s);
 

@@ -26,9 +26,11 @@ DUO_OP_HESSIAN, DUO_OP_CHOL_INV, DUO_OP_SCORE_TERMS, DUO_OP_SWEEP, DUO_OP_PRUNE_
 EXPORTED = (
     "duo_workspace_size", "duo_status_string", "duo_version", "duo_act_sparsify_mask",
     "duo_hessian_accum", "duo_residual_term", "duo_chol_inv", "duo_score_terms", "duo_sweep",
-    "duo_prune_layer", "duo_profile_enable", "duo_profile_read",
+    "duo_prune_layer", "duo_profile_enable", "duo_profile_read", "duo_block_workspace_size", "duo_rmsnorm",
+    "duo_act_sparsify", "duo_linear", "duo_rope", "duo_attention", "duo_silu_mul",
 )
 PROF = dict(gram=0, hessian=1, chol=2, score=3, sweep=4, inblock=5, trail=6, select=7)
+DUO_BOP_ACT_SPARSIFY, DUO_BOP_LINEAR, DUO_BOP_ATTENTION = 0, 1, 2
 
 
 class DuoError(RuntimeError):
@@ -80,6 +82,20 @@ def lib():
         L.duo_sweep.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, P, P, P, P, P, P, SZ, P]
         L.duo_prune_layer.restype = I32
         L.duo_prune_layer.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, P, P, P, P, P, P, SZ, P]
+        L.duo_block_workspace_size.restype = SZ
+        L.duo_block_workspace_size.argtypes = [I32, I64, I64, I64]
+        L.duo_rmsnorm.restype = I32
+        L.duo_rmsnorm.argtypes = [P, I64, I64, I64, F64, P, I64, P]
+        L.duo_act_sparsify.restype = I32
+        L.duo_act_sparsify.argtypes = [P, I64, I64, I64, ActRule, P, I64, P, SZ, P]
+        L.duo_linear.restype = I32
+        L.duo_linear.argtypes = [P, I64, I64, I64, P, I64, I64, P, I64, P, I64, P, SZ, P]
+        L.duo_rope.restype = I32
+        L.duo_rope.argtypes = [P, I64, I64, I64, I64, I64, F64, P]
+        L.duo_attention.restype = I32
+        L.duo_attention.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, I64, P, SZ, P]
+        L.duo_silu_mul.restype = I32
+        L.duo_silu_mul.argtypes = [P, P, I64, I64, I64, P, I64, P]
         L.duo_profile_enable.restype = I32
         L.duo_profile_enable.argtypes = [I32]
         L.duo_profile_read.restype = I32
@@ -346,3 +362,99 @@ def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=N
     lam, _ = duo_chol_inv(H, damp)
     W_out, lowp, mask, _ = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp)
     return dict(W_out=W_out, W_lowp=lowp, mask=unpack_mask(mask, k), lam=lam)
+
+
+# ---------------------------------------------------------------------------
+# decoder-block harness (bf16 activations, token-major)
+# ---------------------------------------------------------------------------
+
+def _bf16_rows(t, name):
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"duo: {name} must be bfloat16")
+    return _ld(t)
+
+
+def block_workspace(op: int, m: int, seq_len: int, heads: int, device) -> torch.Tensor:
+    nbytes = int(lib().duo_block_workspace_size(op, m, seq_len, heads))
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+def duo_rmsnorm(X, eps=1e-5, out=None):
+    m, d = X.shape
+    Y = torch.empty_like(X) if out is None else out
+    _same_device(X, Y)
+    _shape(Y, (m, d), "Y")
+    _check(lib().duo_rmsnorm(_ptr(X), m, d, _bf16_rows(X, "X"), float(eps), _ptr(Y), _bf16_rows(Y, "Y"),
+                             _stream(X.device)), "duo_rmsnorm")
+    return Y
+
+
+def duo_act_sparsify(X, act_sparsity, out=None, ws=None):
+    m, k = X.shape
+    Y = torch.empty_like(X) if out is None else out
+    _same_device(X, Y, ws)
+    _shape(Y, (m, k), "Y")
+    if ws is None:
+        ws = block_workspace(DUO_BOP_ACT_SPARSIFY, m, 0, 0, X.device)
+    _check(lib().duo_act_sparsify(_ptr(X), m, k, _bf16_rows(X, "X"), act_rule(act_sparsity), _ptr(Y),
+                                  _bf16_rows(Y, "Y"), _ptr(ws), ws.numel(), _stream(X.device)), "duo_act_sparsify")
+    return Y
+
+
+def duo_linear(X, W, R=None, out=None, ws=None):
+    """Y = X W^T (+ R), bf16."""
+    m, k = X.shape
+    n = W.shape[0]
+    _shape(W, (n, k), "W")
+    _shape(R, (m, n), "R")
+    Y = torch.empty((m, n), dtype=torch.bfloat16, device=X.device) if out is None else out
+    _same_device(X, W, R, Y, ws)
+    _shape(Y, (m, n), "Y")
+    if ws is None:
+        ws = block_workspace(DUO_BOP_LINEAR, 0, 0, 0, X.device)
+    _check(lib().duo_linear(_ptr(X), m, k, _bf16_rows(X, "X"), _ptr(W), n, _bf16_rows(W, "W"), _ptr(R),
+                            _bf16_rows(R, "R") if R is not None else 0, _ptr(Y), _bf16_rows(Y, "Y"), _ptr(ws),
+                            ws.numel(), _stream(X.device)), "duo_linear")
+    return Y
+
+
+def duo_rope(X, heads, head_dim, seq_len, theta=1e4):
+    """In place."""
+    m = X.shape[0]
+    if X.shape[1] < heads * head_dim:
+        raise ValueError("duo: X is narrower than heads * head_dim")
+    _same_device(X)
+    _check(lib().duo_rope(_ptr(X), m, heads, head_dim, _bf16_rows(X, "X"), seq_len, float(theta),
+                          _stream(X.device)), "duo_rope")
+    return X
+
+
+def duo_attention(Q, K, V, nseq, seq_len, heads, head_dim, out=None, ws=None):
+    m = nseq * seq_len
+    for t, nm in ((Q, "Q"), (K, "K"), (V, "V")):
+        if t.shape[0] < m or t.shape[1] < heads * head_dim:
+            raise ValueError(f"duo: {nm} is smaller than nseq*seq_len x heads*head_dim")
+    if not (Q.stride(0) == K.stride(0) == V.stride(0)):
+        raise ValueError("duo: Q, K and V must share their row stride")
+    O = torch.empty((m, heads * head_dim), dtype=torch.bfloat16, device=Q.device) if out is None else out
+    _same_device(Q, K, V, O, ws)
+    if ws is None:
+        ws = block_workspace(DUO_BOP_ATTENTION, 0, seq_len, heads, Q.device)
+    _check(lib().duo_attention(_ptr(Q), _ptr(K), _ptr(V), _bf16_rows(Q, "Q"), nseq, seq_len, heads, head_dim,
+                               _ptr(O), _bf16_rows(O, "O"), _ptr(ws), ws.numel(), _stream(Q.device)),
+           "duo_attention")
+    return O
+
+
+def duo_silu_mul(G, U, out=None):
+    m, n = G.shape
+    _shape(U, (m, n), "U")
+    if G.stride(0) != U.stride(0):
+        raise ValueError("duo: G and U must share their row stride")
+    Y = torch.empty_like(G) if out is None else out
+    _same_device(G, U, Y)
+    _check(lib().duo_silu_mul(_ptr(G), _ptr(U), m, n, _bf16_rows(G, "G"), _ptr(Y), _bf16_rows(Y, "Y"),
+                              _stream(G.device)), "duo_silu_mul")
+    return Y

@@ -127,3 +127,36 @@ def test_binding_refuses_host_tensors(duo_lib):
         duo_lib.duo_chol_inv(H, 0.01, ws=torch.zeros(1 << 20, dtype=torch.uint8))
     with pytest.raises(ValueError):
         duo_lib.prune_linear(torch.zeros(4, 8), torch.zeros(16, 8), 0.5, 0.5)
+
+
+def test_block_harness_argument_errors(duo_lib):
+    """The decoder-block calls validate before touching the device."""
+    L = duo_lib.lib()
+    E, W_, NODEV = duo_lib.DUO_ERR_INVALID_ARG, duo_lib.DUO_ERR_WORKSPACE, duo_lib.DUO_ERR_NO_DEVICE
+    big = 10 ** 12
+    assert L.duo_rmsnorm(FAKE, 8, 64, 64, 1e-5, FAKE, 64, None) == NODEV
+    assert L.duo_rmsnorm(FAKE, 8, 64, 63, 1e-5, FAKE, 64, None) == E
+    assert L.duo_rmsnorm(None, 8, 64, 64, 1e-5, FAKE, 64, None) == E
+    assert L.duo_rmsnorm(FAKE, 8, 64, 64, -1.0, FAKE, 64, None) == E
+    assert L.duo_rmsnorm(None, 0, 64, 64, 1e-5, None, 64, None) == duo_lib.DUO_OK   # nothing to do
+    assert L.duo_act_sparsify(FAKE, 8, 64, 64, _rule(), FAKE, 64, WS, big, None) == NODEV
+    assert L.duo_act_sparsify(FAKE, 8, 64, 64, _rule(1.5), FAKE, 64, WS, big, None) == E
+    assert L.duo_act_sparsify(FAKE, 8, 64, 64, _rule(), FAKE, 64, WS, 4, None) == W_
+    assert L.duo_act_sparsify(FAKE, 8, 40000, 40000, _rule(), FAKE, 40000, WS, big, None) == E
+    assert L.duo_linear(FAKE, 8, 64, 64, FAKE, 32, 64, None, 0, FAKE, 32, WS, big, None) == NODEV
+    assert L.duo_linear(FAKE, 8, 64, 64, FAKE, 32, 63, None, 0, FAKE, 32, WS, big, None) == E
+    assert L.duo_linear(FAKE, 8, 64, 64, FAKE, 32, 64, FAKE, 31, FAKE, 32, WS, big, None) == E
+    assert L.duo_linear(FAKE, 8, 64, 64, FAKE, 32, 64, None, 0, FAKE, 32, WS, 1024, None) == W_
+    assert L.duo_rope(FAKE, 8, 2, 64, 128, 4, 1e4, None) == NODEV
+    assert L.duo_rope(FAKE, 8, 2, 63, 128, 4, 1e4, None) == E          # odd head_dim
+    assert L.duo_rope(FAKE, 8, 2, 64, 127, 4, 1e4, None) == E
+    assert L.duo_rope(FAKE, 8, 2, 64, 128, 4, 0.0, None) == E
+    need = L.duo_block_workspace_size(duo_lib.DUO_BOP_ATTENTION, 0, 16, 2)
+    assert need >= 2 * 16 * 16 * 6
+    assert L.duo_attention(FAKE, FAKE, FAKE, 128, 2, 16, 2, 64, FAKE, 128, WS, need, None) == NODEV
+    assert L.duo_attention(FAKE, FAKE, FAKE, 128, 2, 16, 2, 64, FAKE, 128, WS, need - 1, None) == W_
+    assert L.duo_attention(FAKE, FAKE, FAKE, 127, 2, 16, 2, 64, FAKE, 128, WS, need, None) == E
+    assert L.duo_silu_mul(FAKE, FAKE, 8, 64, 64, FAKE, 64, None) == NODEV
+    assert L.duo_silu_mul(FAKE, FAKE, 8, 64, 32, FAKE, 64, None) == E
+    assert L.duo_block_workspace_size(99, 1, 1, 1) == 0
+    assert L.duo_block_workspace_size(duo_lib.DUO_BOP_ACT_SPARSIFY, 100, 0, 0) >= 800

@@ -1,0 +1,271 @@
+"""Decoder-block harness on the GPU (through the C ABI) against the float64
+block reference.
+
+Outputs are bf16.  The kernels round an fp32 value once and the reference
+rounds its float64 value once, so an element may differ by one bf16 unit in
+the last place (2^-7 relative at most) plus the fp32 accumulation error of
+the op (at most K u relative to sum |terms| for a K-term dot product); the
+per-op bar is |gpu - ref| <= 2^-7 |ref| + 1e-5 rms(ref) (two units for
+attention, whose probabilities are also rounded to bf16 on both sides).
+Activation sparsification is integer work: bit-exact.  Attention has its
+own bar (ATT below).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import block_ref as BR
+from oracle import duo_ref as R
+from workloads import synth
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def duo(duo_lib):
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    return duo_lib
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+def f64(t):
+    return t.detach().cpu().double().numpy()
+
+
+def bf(x, seed, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn(x, generator=g) * scale).to(torch.bfloat16)
+
+
+def close(gpu, ref, ulps=1, atol_rel=1e-5):
+    tol = ulps * 2.0 ** -7 * np.abs(ref) + atol_rel * np.sqrt(np.mean(ref * ref)) + 1e-30
+    bad = np.abs(gpu - ref) > tol
+    return not bad.any(), float(np.max(np.abs(gpu - ref) / tol))
+
+
+# Attention: both sides round the probabilities to bf16, but an fp32 and a
+# float64 probability can round to neighbouring bf16 values; one such flip
+# moves an output by 2^-8 * P * |v|.  Bar: two units of the output plus 2^-8
+# of its rms, and 2^-8 in relative Frobenius norm over the whole tensor.
+ATT = dict(ulps=2, atol_rel=2.0 ** -8)
+
+
+def relfro(a, b):
+    return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+
+@pytest.mark.parametrize("m,d", [(5, 64), (300, 4096), (17, 11008)])
+def test_rmsnorm(duo, m, d):
+    say("rmsnorm", m, d)
+    x = bf((m, d), d + m, 3.0)
+    ok, r = close(f64(duo.duo_rmsnorm(x.to(DEV))), BR.rmsnorm(x.double().numpy()))
+    assert ok, r
+
+
+@pytest.mark.parametrize("m,k,p", [(64, 4096, 0.5), (33, 352, 0.6), (9, 100, 0.0), (8, 96, 1.0)])
+def test_act_sparsify_bit_exact(duo, m, k, p):
+    say("act_sparsify", m, k, p)
+    x = bf((m, k), k, 2.0)
+    x[:, ::3] = x[:, ::3].sign() * 0.25        # magnitude ties
+    y = duo.duo_act_sparsify(x.to(DEV), p).cpu()
+    ref = R.sparsify_tokens(x.double().numpy(), p)[0]
+    assert np.array_equal(y.double().numpy(), ref)
+
+
+@pytest.mark.parametrize("m,k,n,res", [(200, 128, 352, False), (257, 4096, 640, True), (64, 11008, 4096, True)])
+def test_linear(duo, m, k, n, res):
+    say("linear", m, k, n, res)
+    x, w = bf((m, k), 1), bf((n, k), 2, 0.02)
+    r = bf((m, n), 3) if res else None
+    y = duo.duo_linear(x.to(DEV), w.to(DEV), R=None if r is None else r.to(DEV))
+    ref = BR.linear(x.double().numpy(), w.double().numpy(), None if r is None else r.double().numpy())
+    ok, e = close(f64(y), ref)
+    assert ok, e
+
+
+def test_rope(duo):
+    say("rope")
+    heads, hd, L, nseq = 4, 128, 300, 2
+    x = bf((nseq * L, heads * hd), 4)
+    y = x.to(DEV)
+    duo.duo_rope(y, heads, hd, L, 1e4)
+    ok, e = close(f64(y), BR.rope(x.double().numpy(), heads, hd, L, 1e4))
+    assert ok, e
+
+
+@pytest.mark.parametrize("nseq,L,heads,hd", [(2, 96, 2, 64), (1, 520, 4, 128)])
+def test_attention(duo, nseq, L, heads, hd):
+    say("attention", nseq, L, heads, hd)
+    q, k, v = (bf((nseq * L, heads * hd), s) for s in (5, 6, 7))
+    o = duo.duo_attention(q.to(DEV), k.to(DEV), v.to(DEV), nseq, L, heads, hd)
+    ref = BR.attention(*(t.double().numpy() for t in (q, k, v)), nseq, L, heads, hd)
+    ok, e = close(f64(o), ref, **ATT)
+    say(f"attention worst error / bound {e:.3f}, relative Frobenius {relfro(f64(o), ref):.2e}")
+    assert ok, e
+    assert relfro(f64(o), ref) < 2.0 ** -8
+
+
+def test_silu_mul(duo):
+    say("silu_mul")
+    g, u = bf((70, 352), 8, 3.0), bf((70, 352), 9)
+    ok, e = close(f64(duo.duo_silu_mul(g.to(DEV), u.to(DEV))), BR.silu_mul(g.double().numpy(), u.double().numpy()))
+    assert ok, e
+
+
+def _tiny_run(duo, p_x, p_w):
+    from paper_2506_20194_amd import block
+
+    c = synth.BLOCKS["tiny_block"]
+    cfg = synth.block_cfg("tiny_block")
+    h, w = synth.block_inputs("tiny_block")
+    out = block.prune_block(h.to(DEV), {k: v.to(DEV) for k, v in w.items()}, cfg, p_x, p_w, damp=c["damp"],
+                            block=c["block"], keep_inputs=True)
+    W = {k: v.double().numpy() for k, v in w.items()}
+    ref = BR.prune_block(h.double().numpy(), W, cfg, p_x, p_w, damp=c["damp"], B=c["block"])
+    return c, W, out, ref
+
+
+def _group_checks(duo, c, W, out, ref, p_x, p_w, strict_first=True):
+    """Per linear: exact counts; the reference run on its own streams, forced
+    to the GPU mask, must show every disagreement to be a near-tie of its
+    scores and must match the GPU weights.  The first group's inputs are the
+    same on both sides: the layer solver's bars apply (gap 1e-5, W 1e-3).
+    Later groups' inputs differ by delta (relative Frobenius) from single-unit
+    bf16 differences upstream; without activation sparsity the scores, being
+    quadratic in the inputs, move by a small multiple of that: gap and weight
+    difference are allowed 20 * delta more.  With activation sparsity a
+    single-unit difference between two equal-magnitude entries at a token's
+    selection threshold swaps which one is kept, which moves that channel's
+    Hessian entries by a whole token's contribution; those groups are held to
+    a sensitivity bar instead (agreement >= 98 %, W within 5e-2 of the forced
+    run; the measured worst case is about 1e-2)."""
+    first = True
+    for names, (xs, xd) in ref["inputs"].items():
+        gs, gd = (f64(t) for t in out["inputs"][names])
+        delta = max(relfro(gs, xs), relfro(gd, xd))
+        for nm in names:
+            n, k = W[nm].shape
+            keep = duo.unpack_mask(out["mask"][nm], k).cpu().numpy()
+            Wg = f64(out["W_out"][nm])
+            assert (~keep).sum() == sum(R.block_prune_counts(n, k, p_w, c["block"]))
+            agree = float(np.mean(keep == ref["keep"][nm]))
+            scores = []
+            forced = R.prune_layer(W[nm], xs, p_x, p_w, damp=c["damp"], B=c["block"], X_dense=xd, mask_in=keep,
+                                   scores_out=scores)
+            counts = R.block_prune_counts(n, k, p_w, c["block"])
+            gap = 0.0
+            for bi, j0 in enumerate(range(0, k, c["block"])):
+                S = scores[bi]
+                kb = keep[:, j0:j0 + c["block"]]
+                if kb.all() or (~kb).all():
+                    continue
+                T = np.sort(S.T.reshape(-1), kind="stable")[counts[bi] - 1]
+                gap = max(gap, (S[~kb].max() - T) / T, (T - S[kb].min()) / T)
+            err = relfro(Wg, forced["W_hat"])
+            say(f"{nm}: input delta {delta:.1e}, mask agreement {agree:.5f}, near-tie gap {gap:.1e}, "
+                f"W rel err (forced) {err:.1e}")
+            if first and strict_first:
+                assert delta == 0.0
+                assert agree >= 0.999 and gap < 1e-5 and err < 1e-3, nm
+            elif p_x == 0.0:
+                assert gap < 1e-5 + 20 * delta, nm
+                assert err < 1e-3 + 20 * delta, nm
+            else:
+                assert agree >= 0.98 and err < 5e-2, nm
+        first = False
+
+
+def test_tiny_block_without_sparsity(duo):
+    """p_x = p_w = 0: nothing is pruned, both streams stay equal and equal to
+    the reference's, and every weight comes back bit-unchanged."""
+    say("tiny block, no sparsity")
+    c, W, out, ref = _tiny_run(duo, 0.0, 0.0)
+    for nm in synth.BLOCK_LINEARS:
+        assert torch.equal(out["W_out"][nm].cpu(), torch.tensor(W[nm], dtype=torch.float32))
+    s, d = out["h3"]
+    assert torch.equal(s, d)
+    ok, e = close(f64(d), ref["h3"][1], **ATT)
+    assert ok, e
+
+
+def test_tiny_block_weight_sparsity(duo):
+    """p_x = 0, p_w = 0.5: the streams differ only through the pruned
+    weights; every group passes the layer solver's bar (agreement >= 99.9 %)
+    with near-tie gaps and weights within 20 delta."""
+    say("tiny block, weight sparsity only")
+    c, W, out, ref = _tiny_run(duo, 0.0, 0.5)
+    _group_checks(duo, c, W, out, ref, 0.0, 0.5)
+    for nm in synth.BLOCK_LINEARS:
+        k = W[nm].shape[1]
+        keep = duo.unpack_mask(out["mask"][nm], k).cpu().numpy()
+        assert np.mean(keep == ref["keep"][nm]) >= 0.999, nm
+
+
+def test_tiny_block_duogpt(duo):
+    """The block's own setting (p_x = p_w = 0.5).  The first group sees
+    identical inputs on both sides and must match exactly as a single layer
+    does; later groups inherit near-tie swaps of the per-token activation
+    selection (bf16 values one unit apart) and are held to the sensitivity
+    bar of _group_checks."""
+    say("tiny block, activation and weight sparsity")
+    c, W, out, ref = _tiny_run(duo, c_px := synth.BLOCKS["tiny_block"]["p_x"], synth.BLOCKS["tiny_block"]["p_w"])
+    _group_checks(duo, c, W, out, ref, c_px, c["p_w"])
+
+
+def test_llama2_7b_block_full_size(duo):
+    """LLaMA-2-7B block shape on 128 x 2048 tokens.  The dense stream of the
+    first sequence is recomputed by the reference for sampled tokens (it
+    depends only on the block input and the dense weights); each later stage
+    inherits the differences of the earlier ones, so its bar grows (1, 2, 4, 8
+    units, with attention's 2^-8 rms term from the first attention output on).  Every pruned linear is checked for its exact count, zeros
+    where pruned and the bf16 copy."""
+    from paper_2506_20194_amd import block
+
+    name = "llama2_7b_block"
+    c = synth.BLOCKS[name]
+    cfg = synth.block_cfg(name)
+    say("full-size block", name)
+    h, w = synth.block_inputs(name, device=DEV)
+    out = block.prune_block(h, w, cfg, c["p_x"], c["p_w"], damp=c["damp"], block=c["block"], keep_inputs=True,
+                            timing=True)
+    say("phase ms", {k: round(v, 1) for k, v in out["ms"].items()})
+    for nm in synth.BLOCK_LINEARS:
+        n, k = w[nm].shape
+        keep = duo.unpack_mask(out["mask"][nm], k)
+        assert int((~keep).sum()) == sum(R.block_prune_counts(n, k, c["p_w"], c["block"])), nm
+        assert not bool(out["W_out"][nm][~keep].any()), nm
+        assert torch.equal(out["W_lowp"][nm], out["W_out"][nm].to(torch.bfloat16)), nm
+    # dense stream of sequence 0 for sampled tokens, from the block input alone
+    L, heads, hd = cfg["seq_len"], cfg["heads"], cfg["head_dim"]
+    toks = np.array([0, 1, 77, 1000, L - 1])
+    h0 = h[:L].double().cpu().numpy()
+    W = {k: v.double().cpu().numpy() for k, v in w.items()}
+    x1 = BR.rmsnorm(h0, cfg["eps"])
+    qf = BR.rope(BR.linear(x1, W["q"]), heads, hd, L, cfg["theta"])
+    kf = BR.rope(BR.linear(x1, W["k"]), heads, hd, L, cfg["theta"])
+    vf = BR.linear(x1, W["v"])
+    att = np.zeros((len(toks), heads * hd))
+    for i, t in enumerate(toks):
+        for hh in range(heads):
+            cs = slice(hh * hd, (hh + 1) * hd)
+            s = kf[:t + 1, cs] @ qf[t, cs] / np.sqrt(hd)
+            p = np.exp(s - s.max())
+            p = BR.bf16(p / p.sum())
+            att[i, cs] = p @ vf[:t + 1, cs]
+    att = BR.bf16(att)
+    h2 = BR.linear(att, W["o"], h0[toks])
+    x2 = BR.rmsnorm(h2, cfg["eps"])
+    md = BR.silu_mul(BR.linear(x2, W["gate"]), BR.linear(x2, W["up"]))
+    gx1 = f64(out["inputs"][("q", "k", "v")][1][:L])[toks]
+    gatt = f64(out["inputs"][("o",)][1][:L])[toks]
+    gx2 = f64(out["inputs"][("gate", "up")][1][:L])[toks]
+    gmd = f64(out["inputs"][("down",)][1][:L])[toks]
+    for nm, g, r, u in (("x1", gx1, x1[toks], 1), ("attn", gatt, att, 2), ("x2", gx2, x2, 4), ("m", gmd, md, 8)):
+        ok, e = close(g, r, ulps=u, atol_rel=1e-5 if nm == "x1" else 2.0 ** -8)
+        say(f"dense stream {nm}: worst error / bound {e:.3f}")
+        assert ok, (nm, e)

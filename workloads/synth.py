@@ -102,3 +102,41 @@ def config_inputs(name: str, device="cpu", m: int | None = None):
     c = CONFIGS[name]
     return layer_inputs(c["n"], c["k"], c["m"] if m is None else m, c["x_dtype"], c["w_dtype"], seed=c["seed"],
                         device=device, kind=c["kind"], sigma=c["sigma"], outliers=c["outliers"])
+
+
+# LLaMA-style decoder blocks for the block harness: hidden size d, MLP width
+# ffn, heads x head_dim attention, nseq sequences of seq_len tokens.  The
+# block input has the lognormal channel structure (8 outlier channels x20 at
+# full size); every weight is N(0, 0.02^2) in bf16.
+BLOCKS = {
+    # LLaMA-2-7B block shape on 128 x 2048 tokens
+    "llama2_7b_block": dict(d=4096, ffn=11008, heads=32, head_dim=128, seq_len=2048, nseq=128, sigma=1.0,
+                            outliers=8, p_x=0.5, p_w=0.5, block=128, damp=0.01, theta=1e4, eps=1e-5, seed=4000),
+    # the same structure at a size the float64 oracle runs end to end
+    "tiny_block": dict(d=128, ffn=352, heads=2, head_dim=64, seq_len=256, nseq=4, sigma=1.0, outliers=2,
+                       p_x=0.5, p_w=0.5, block=32, damp=0.01, theta=1e4, eps=1e-5, seed=4100),
+}
+
+BLOCK_LINEARS = ("q", "k", "v", "o", "gate", "up", "down")
+
+
+def block_shapes(c):
+    d, f = c["d"], c["ffn"]
+    return dict(q=(d, d), k=(d, d), v=(d, d), o=(d, d), gate=(f, d), up=(f, d), down=(d, f))
+
+
+def block_inputs(name: str, device="cpu", nseq: int | None = None):
+    """(h, weights) of a block workload; h is (nseq*seq_len) x d bf16."""
+    c = BLOCKS[name]
+    nseq = c["nseq"] if nseq is None else nseq
+    h = make_activations(nseq * c["seq_len"], c["d"], torch.bfloat16, seed=c["seed"], device=device,
+                         kind="lognormal", sigma=c["sigma"], outliers=c["outliers"])
+    weights = {nm: make_weight(n, k, torch.bfloat16, seed=c["seed"] + 10 * (i + 1), device=device)
+               for i, (nm, (n, k)) in enumerate(block_shapes(c).items())}
+    return h, weights
+
+
+def block_cfg(name: str, nseq: int | None = None):
+    c = BLOCKS[name]
+    return dict(heads=c["heads"], head_dim=c["head_dim"], seq_len=c["seq_len"],
+                nseq=c["nseq"] if nseq is None else nseq, theta=c["theta"], eps=c["eps"])
