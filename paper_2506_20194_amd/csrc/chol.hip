@@ -52,125 +52,210 @@ __global__ __launch_bounds__(256) void damp_kernel(float* H, int64_t ldh, int k,
 }
 
 // Factor the s x s diagonal block at (r0, r0), s <= 128, read from its upper
-// triangle: A = V V^T with V upper, eliminating the last column first, and
+// triangle: A = V V^T with V upper, eliminating from the last column, and
 // return N = V^-1 (upper; zeros below the diagonal) in `vinv` (128 x 128,
 // row-major).  V itself is not needed by the callers and is not stored.
 //
-// 192 threads; thread (h, q) keeps rows 64h..64h+63 of column q in registers
-// (h = 0 for q < 64; h = 0, 1 for q >= 64: the lower-left quadrant is never
-// needed).  Step c (c = s-1 .. 0) broadcasts column c of the working matrix
-// and row c of N through LDS (one barrier per step):
-//   columns q < c:  A[r][q] -= A[r][c] A[q][c] / A[c][c]       (factorisation)
-//   column  q = c:  N[r][c]  = -A[r][c] / A[c][c], N[c][c] = 1 / sqrt(A[c][c])
-//   columns q > c:  N[c][q] /= V[c][c]; N[r][q] -= V[r][c] N[c][q]  (r < c)
-// The last two are back substitution of V N = I, driven by the same column c.
+// The block is split into four 32-column leaves J = 3..0 (bottom-up, like the
+// whole factorisation):
+//   leaf     one wave factors A_JJ = V_JJ V_JJ^T and inverts it in the same
+//            sweep (column c of the working matrix drives both the rank-1
+//            update of the columns before it and the back substitution
+//            V N = I of the columns after it); the column and row of step c
+//            reach the wave's lanes through LDS, so the 32 steps need no
+//            workgroup barrier;
+//   panel    V_IJ = A_IJ N_JJ^T for the leaves I < J;
+//   update   A_II' -= V_IJ V_I'J^T for I, I' < J;
+// and finally the off-diagonal blocks of N by block back substitution,
+//   N_IJ = -N_II sum_{K=I+1..J} V_IK N_KJ, in order of J - I.
+// The small products run on all four waves with fp32 MFMA, one 32 x 32
+// block per wave.
 // Padding rows/columns beyond s are an identity block.
-struct DiagCtx {
-  float* colbuf;  // [2][128]
-  float* rowbuf;  // [2][128]
-  float* pivbuf;  // [2]
-  int tid, h, q, hh, buf;
-  int fail;  // first column (from the bottom) with a non-positive pivot, or -1
+constexpr int DS = kTile + 2;  // LDS row stride of the working matrices (rows 2 banks apart)
+constexpr int LF = 32;         // leaf width
+
+// acc(32x32) += A(32x32) * op(B)(32x32) for one wave on fp32 MFMA
+// (16x16x4): lane l supplies A[16a + l%16][k + l/16] and op(B)[k + l/16][16b +
+// l%16]; acc[a][b][r] is out[16a + 4(l/16) + r][16b + l%16].
+template <bool BT>
+__device__ inline void wave_gemm32(const float* A, const float* B, f4 (&acc)[2][2], int lane) {
+  const int l16 = lane & 15, kq = lane >> 4;
+  {
+#pragma unroll
+    for (int k0 = 0; k0 < LF; k0 += 4) {
+      const int k = k0 + kq;
+      float av[2], bv[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        av[i] = A[(16 * i + l16) * DS + k];
+        bv[i] = BT ? B[(16 * i + l16) * DS + k] : B[k * DS + 16 * i + l16];
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
+__device__ inline void store32(float* C, const f4 (&acc)[2][2], int lane, float scale, bool add) {
+  const int l16 = lane & 15, rq = 4 * (lane >> 4);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float* p = &C[(16 * i + rq + r) * DS + 16 * j + l16];
+        *p = add ? *p + scale * acc[i][j][r] : scale * acc[i][j][r];
+      }
+}
+
+struct LeafCtx {
+  float* col;  // [LF]: column c of the working leaf (rows >= c zeroed)
+  float* row;  // [LF]: row c of the working leaf
+  int q, h;    // lane: column q, rows 16h .. 16h+15
+  int fail;    // first column (from the bottom) with a non-positive pivot
 };
 
-// One elimination step for column c = 64*hh + I0 (I0 a compile-time constant so
-// that every register index below is static).
-template <int I0>
-__device__ __forceinline__ void diag_step(float (&x)[64], DiagCtx& d) {
-  const int hh = d.hh, h = d.h, q = d.q;
-  const int c = 64 * hh + I0;
-  float* colbuf = d.colbuf + d.buf * kTile;
-  float* rowbuf = d.rowbuf + d.buf * kTile;
-  if (q == c) {
-    float4* cb = (float4*)&colbuf[64 * h];
-    if (h < hh) {
+// Step c of the leaf sweep; x[i] is row 16h+i of column q.  The lane
+// coordinates are made opaque per step so that the compiler evaluates the
+// lane tests where they are used instead of hoisting (and spilling) the
+// masks of every step.
+template <int C>
+__device__ __forceinline__ void leaf_step(float (&x)[16], LeafCtx& d) {
+  constexpr int CH = C / 16, CI = C % 16;
+  int q = d.q, h = d.h;
+  asm volatile("" : "+v"(q), "+v"(h));
+  const bool hi = h != 0;
+  if (q == C) {
 #pragma unroll
-      for (int i = 0; i < 64; i += 4) cb[i / 4] = make_float4(x[i], x[i + 1], x[i + 2], x[i + 3]);
-    } else if (h > hh) {
-#pragma unroll
-      for (int i = 0; i < 64; i += 4) cb[i / 4] = make_float4(0.f, 0.f, 0.f, 0.f);
-    } else {
-#pragma unroll
-      for (int i = 0; i < 64; ++i) colbuf[64 * h + i] = i < I0 ? x[i] : 0.f;
-      d.pivbuf[d.buf] = x[I0];
+    for (int i = 0; i < 16; ++i) {
+      const float lo_v = i < C ? x[i] : 0.f, hi_v = 16 + i < C ? x[i] : 0.f;
+      d.col[16 * h + i] = hi ? hi_v : lo_v;
     }
   }
-  if (h == hh && q > c) rowbuf[q] = x[I0];
-  __syncthreads();
-  const float piv = d.pivbuf[d.buf];
-  if (!(piv > 0.f) && d.fail < 0) d.fail = c;  // uniform: every thread sees the same pivot
-  const float inv = 1.0f / sqrtf(piv);
+  if (h == CH) d.row[q] = x[CI];
+  __builtin_amdgcn_wave_barrier();
+  float cv[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) cv[i] = d.col[16 * h + i];
+  const float piv = d.row[C];
+  const float cq = d.col[q], rq = d.row[q];
+  __builtin_amdgcn_wave_barrier();
+  if (!(piv > 0.f) && d.fail < 0) d.fail = C;  // every lane sees the same pivot
+  const float inv = __builtin_amdgcn_rsqf(piv);
   const float inv2 = inv * inv;
-  if (q == c) {
-    // column c of N: N[r][c] = -A[r][c] / A[c][c] for r < c (x[i] holds A[r][c])
-    if (h < hh) {
+  if (q == C) {
+    // rows below the diagonal of a finished column are never read again
 #pragma unroll
-      for (int i = 0; i < 64; ++i) x[i] = -x[i] * inv2;
-    } else if (h == hh) {
+    for (int i = 0; i < 16; ++i) x[i] = -x[i] * inv2;
+    if (h == CH) x[CI] = inv;
+  } else {
+    const float coef = q < C ? inv2 * cq : inv2 * rq;
 #pragma unroll
-      for (int i = 0; i < I0; ++i) x[i] = -x[i] * inv2;
-    }
-  } else if (64 * h < c) {
-    // columns q < c (factorisation) and q > c (back substitution) share one
-    // FMA stream; colbuf rows >= c are zero
-    const float coef = q < c ? inv2 * colbuf[q] : inv2 * rowbuf[q];
-    const float4* cb = (const float4*)&colbuf[64 * h];
-#pragma unroll
-    for (int i = 0; i < 64; i += 4) {
-      const float4 v = cb[i / 4];
-      x[i] = fmaf(-v.x, coef, x[i]);
-      x[i + 1] = fmaf(-v.y, coef, x[i + 1]);
-      x[i + 2] = fmaf(-v.z, coef, x[i + 2]);
-      x[i + 3] = fmaf(-v.w, coef, x[i + 3]);
-    }
+    for (int i = 0; i < 16; ++i) x[i] = fmaf(-cv[i], coef, x[i]);  // cv is zero for rows >= C
+    if (q > C && h == CH) x[CI] *= inv;
   }
-  if (h == hh) {
-    if (q > c) x[I0] = x[I0] * inv;
-    if (q == c) x[I0] = inv;
-  }
-  d.buf ^= 1;
 }
 
-template <int... Is>
-__device__ __forceinline__ void diag_steps(float (&x)[64], DiagCtx& d, std::integer_sequence<int, Is...>) {
-  (diag_step<63 - Is>(x, d), ...);  // columns 64*hh + 63 down to 64*hh
+template <int... Cs>
+__device__ __forceinline__ void leaf_steps(float (&x)[16], LeafCtx& d, std::integer_sequence<int, Cs...>) {
+  (leaf_step<LF - 1 - Cs>(x, d), ...);
 }
 
-__global__ __launch_bounds__(192) void diag_factor_kernel(const float* H, int64_t ldh, int r0, int s, float* vinv,
+__global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_t ldh, int r0, int s, float* vinv,
                                                           CholStatus* st) {
-  __shared__ __attribute__((aligned(16))) float colbuf[2][kTile];
-  __shared__ float rowbuf[2][kTile];
-  __shared__ float pivbuf[2];
-  const int tid = threadIdx.x;
-  const int w = tid >> 6, lane = tid & 63;
-  const int h = w == 2 ? 1 : 0;
-  const int q = w == 0 ? lane : 64 + lane;
-  float x[64];
+  extern __shared__ __attribute__((aligned(16))) float dsm[];
+  float* A = dsm;                  // [128][DS] working matrix (both triangles); then V's upper off-diagonal
+                                   // blocks, and the back substitution's products in blocks (1..3, 0)
+  float* N = A + kTile * DS;       // [128][DS] the inverse
+  float* col = N + kTile * DS;     // [LF]
+  float* row = col + LF;           // [LF]
+  int* fail_sh = (int*)(row + LF); // [1]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // load the upper triangle, mirror it; identity outside the s x s block
+  for (int e0 = 0; e0 < kTile * kTile; e0 += 256 * 16) {
+    float v[16];
 #pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    const int r = 64 * h + i;
-    float v = 0.f;
-    if (r < s && q < s)
-      v = r <= q ? H[(int64_t)(r0 + r) * ldh + r0 + q] : H[(int64_t)(r0 + q) * ldh + r0 + r];
-    else if (r == q)
-      v = 1.f;
-    x[i] = v;
+    for (int u = 0; u < 16; ++u) {
+      const int e = e0 + 256 * u + tid, r = e / kTile, c = e % kTile;
+      v[u] = (r <= c && c < s) ? H[(int64_t)(r0 + r) * ldh + r0 + c] : (r == c ? 1.f : 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int e = e0 + 256 * u + tid, r = e / kTile, c = e % kTile;
+      if (r <= c) {
+        A[r * DS + c] = v[u];
+        A[c * DS + r] = v[u];
+      }
+      N[r * DS + c] = 0.f;
+    }
   }
-  DiagCtx d{&colbuf[0][0], &rowbuf[0][0], pivbuf, tid, h, q, 1, 0, -1};
-  diag_steps(x, d, std::make_integer_sequence<int, 64>{});
-  d.hh = 0;
-  diag_steps(x, d, std::make_integer_sequence<int, 64>{});
-  if (tid == 0 && d.fail >= 0 && d.fail < s && st->status == DUO_OK) {
+  if (tid == 0) *fail_sh = -1;
+  __syncthreads();
+  for (int J = kTile / LF - 1; J >= 0; --J) {
+    const int j0 = J * LF;
+    if (wave == 0) {
+      LeafCtx d{col, row, lane & 31, lane >> 5, -1};
+      float x[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) x[i] = A[(j0 + 16 * d.h + i) * DS + j0 + d.q];
+      leaf_steps(x, d, std::make_integer_sequence<int, LF>{});
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = 16 * d.h + i;
+        N[(j0 + r) * DS + j0 + d.q] = r <= d.q ? x[i] : 0.f;
+      }
+      if (lane == 0 && d.fail >= 0 && *fail_sh < 0) *fail_sh = j0 + d.fail;
+    }
+    __syncthreads();
+    if (J == 0) break;
+    // panel: V_IJ = A_IJ N_JJ^T for I < J (one wave per block), kept in registers
+    // until every wave has read A_IJ
+    f4 acc[2][2] = {};
+    if (wave < J) {
+      wave_gemm32<true>(&A[wave * LF * DS + j0], &N[j0 * DS + j0], acc, lane);
+    }
+    __syncthreads();
+    if (wave < J) store32(&A[wave * LF * DS + j0], acc, lane, 1.f, false);
+    __syncthreads();
+    // update: A_II' -= V_IJ V_I'J^T for I, I' < J (both triangles)
+    for (int blk = wave; blk < J * J; blk += 4) {
+      const int I = blk / J, I2 = blk % J;
+      f4 u[2][2] = {};
+      wave_gemm32<true>(&A[I * LF * DS + j0], &A[I2 * LF * DS + j0], u, lane);
+      store32(&A[I * LF * DS + I2 * LF], u, lane, -1.f, true);
+    }
+    __syncthreads();
+  }
+  // off-diagonal blocks of N, by distance D = J - I
+  constexpr int NB = kTile / LF;
+  for (int D = 1; D < NB; ++D) {
+    const int nblk = NB - D;
+    f4 acc[2][2] = {};
+    if (wave < nblk) {  // T_I = sum_{K=I+1..I+D} V_IK N_{K,I+D}
+      const int I = wave, J = wave + D;
+      for (int K = I + 1; K <= J; ++K) wave_gemm32<false>(&A[I * LF * DS + K * LF], &N[K * LF * DS + J * LF], acc, lane);
+      store32(&A[(wave + 1) * LF * DS], acc, lane, 1.f, false);  // A's lower blocks are free by now
+    }
+    __syncthreads();
+    if (wave < nblk) {  // N_IJ = -N_II T_I
+      const int I = wave, J = wave + D;
+      f4 n2[2][2] = {};
+      wave_gemm32<false>(&N[I * LF * DS + I * LF], &A[(wave + 1) * LF * DS], n2, lane);
+      store32(&N[I * LF * DS + J * LF], n2, lane, -1.f, false);
+    }
+    __syncthreads();
+  }
+  if (tid == 0 && *fail_sh >= 0 && *fail_sh < s && st->status == DUO_OK) {
     st->status = DUO_ERR_NOT_PD;
-    st->fail = r0 + d.fail;
+    st->fail = r0 + *fail_sh;
   }
-  // N (upper, rows <= q) to vinv; everything else 0
-#pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    const int r = 64 * h + i;
-    vinv[r * kTile + q] = (r <= q && r < s && q < s) ? x[i] : 0.f;
+  for (int e = tid; e < kTile * kTile; e += 256) {
+    const int r = e / kTile, c = e % kTile;
+    vinv[e] = (r <= c && r < s && c < s) ? N[r * DS + c] : 0.f;
   }
-  for (int e = tid; e < 64 * 64; e += 192) vinv[(64 + e / 64) * kTile + (e % 64)] = 0.f;  // lower-left quadrant
 }
 
 // Copy the inverted diagonal blocks into place (full 128 x 128 incl. zeros).
@@ -297,8 +382,12 @@ duo_status trinv(float* H, int64_t ldh, int64_t k, int T, float* X, hipStream_t 
 
 size_t chol_ws_bytes(int64_t k) { return carve(nullptr, k).bytes; }
 
+constexpr size_t kDiagLds = (size_t)(2 * kTile * DS + 2 * LF + 4) * sizeof(float);
+
 duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hipStream_t s, CholStatus** status_dev) {
   const CholWs w = carve(ws, k);
+  DUO_HIP_TRY(hipFuncSetAttribute((const void*)diag_factor_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)kDiagLds));
   *status_dev = w.st;
   const int T = (int)cdiv(k, kTile);
   hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, H, ldh, (int)k, damp, w.st);
@@ -306,7 +395,7 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
   for (int b = T - 1; b >= 0; --b) {
     const int r0 = b * kTile;
     const int sz = (int)((int64_t)r0 + kTile <= k ? kTile : k - r0);
-    hipLaunchKernelGGL(diag_factor_kernel, dim3(1), dim3(192), 0, s, (const float*)H, ldh, r0, sz,
+    hipLaunchKernelGGL(diag_factor_kernel, dim3(1), dim3(256), kDiagLds, s, (const float*)H, ldh, r0, sz,
                        w.vinv + (int64_t)b * kTile * kTile, w.st);
     DUO_LAUNCH_CHECK();
     if (r0 == 0) break;
