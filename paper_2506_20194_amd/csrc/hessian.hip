@@ -129,10 +129,116 @@ __global__ __launch_bounds__(256) void act_select_kernel(const T* __restrict__ X
   }
 }
 
+// One wave per token (bf16, 16-byte aligned rows, k % 8 == 0, k <= 512 V):
+// lane l holds channels 512u + 8l + j (u < V, j < 8) in registers, so the
+// bisection and the tie scan reduce with cross-lane operations only.  Same
+// threshold key as act_select_kernel.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ inline int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ inline int wave_incl_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(v, o);
+    if (lane >= o) v += y;
+  }
+  return v;
+}
+
+template <int V>
+__global__ __launch_bounds__(256) void act_select_wave_kernel(const uint16_t* __restrict__ X, int64_t ldx, int m,
+                                                              int k, int z, int64_t* __restrict__ thr) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= m) return;  // uniform per wave
+  if (z <= 0 || z >= k) {
+    if (lane == 0) thr[t] = z <= 0 ? (int64_t)-1 : INT64_MAX;
+    return;
+  }
+  const uint16_t* row = X + (int64_t)t * ldx;
+  uint32_t mag[8 * V];
+#pragma unroll
+  for (int u = 0; u < V; ++u) {
+    const int c = 512 * u + 8 * lane;
+    const bool ok = c < k;
+    const u32x4 w = *(const u32x4*)(row + (ok ? c : 0));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mag[8 * u + j] = ok ? (w[j >> 1] >> (16 * (j & 1))) & 0x7fffu : 0xffffffffu;
+  }
+  // smallest v with count(mag <= v) >= z
+  uint32_t lo = 0, hi = 0x7fffu;
+  while (lo < hi) {
+    const uint32_t mid = lo + ((hi - lo) >> 1);
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < 8 * V; ++e) cnt += mag[e] <= mid;
+    if (wave_sum_i(cnt) >= z)
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  const uint32_t v = lo;
+  int lt = 0;
+#pragma unroll
+  for (int e = 0; e < 8 * V; ++e) lt += mag[e] < v;
+  int need = z - wave_sum_i(lt);  // 1 <= need <= number of ties
+  // the need-th tie in channel order (u, lane, j)
+#pragma unroll
+  for (int u = 0; u < V; ++u) {
+    int eq = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) eq += mag[8 * u + j] == v;
+    const int incl = wave_incl_scan(eq);
+    const int tot = __shfl(incl, 63);
+    if (need <= tot) {  // uniform
+      int cnt = incl - eq;
+      if (cnt < need && need <= incl) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (mag[8 * u + j] == v && ++cnt == need) thr[t] = ((int64_t)v << 32) | (int64_t)(512 * u + 8 * lane + j);
+      }
+      break;
+    }
+    need -= tot;
+  }
+}
+
+// Whether the bf16 fast paths apply: 16-byte aligned rows of whole 8-channel
+// vectors.
+__host__ inline bool bf16_vec_ok(const void* X, int64_t ldx, int64_t k) {
+  return X && (reinterpret_cast<uintptr_t>(X) % 16) == 0 && ldx % 8 == 0 && k % 8 == 0;
+}
+
 template <typename T>
 static duo_status launch_act_select(const T* X, int64_t ldx, int m, int k, int z, int64_t* thr,
                                     hipStream_t s) {
   if (m <= 0) return DUO_OK;
+  if constexpr (sizeof(T) == 2) {
+    if (bf16_vec_ok(X, ldx, k) && k <= 8192) {
+      const int v = (int)cdiv(k, 512);
+      dim3 g((unsigned)cdiv(m, 4)), b(256);
+#define DUO_WSEL(VV) hipLaunchKernelGGL((act_select_wave_kernel<VV>), g, b, 0, s, (const uint16_t*)X, ldx, m, k, z, thr)
+      if (v <= 1)
+        DUO_WSEL(1);
+      else if (v <= 2)
+        DUO_WSEL(2);
+      else if (v <= 4)
+        DUO_WSEL(4);
+      else if (v <= 8)
+        DUO_WSEL(8);
+      else
+        DUO_WSEL(16);
+#undef DUO_WSEL
+      DUO_LAUNCH_CHECK();
+      return DUO_OK;
+    }
+  }
   const int per = (int)cdiv(k, 256);
   dim3 g(m), b(256);
 #define DUO_SEL(CC) hipLaunchKernelGGL((act_select_kernel<T, CC>), g, b, 0, s, X, ldx, m, k, z, thr)
@@ -272,6 +378,107 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* __restrict__ Xs, con
     for (int r = 0; r < 32; ++r) s += sa[r * 257 + threadIdx.x];
     apart[(int64_t)blockIdx.y * kp + c] = s;
   }
+}
+
+// bf16 pack without LDS (16-byte aligned rows, k % 8 == 0).  Workgroup
+// (x, y) covers channels [512x, 512x + 512) of tokens [256y, 256y + 256): wave
+// w handles tokens 8w..8w+7 of every 32-token block, lane l channels
+// 512x + 8l .. +7.  Each lane loads its 8 x 8 tile with 16-byte reads,
+// applies the threshold in registers, transposes it (tokens become the
+// contiguous dimension) and stores one 16-byte vector per channel: exactly
+// the packed layout above.
+__device__ inline uint32_t lo_pair(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
+__device__ inline uint32_t hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
+
+template <bool TWO>
+__global__ __launch_bounds__(256) void pack16_kernel(const uint16_t* __restrict__ Xs, const uint16_t* __restrict__ Xd,
+                                                     int64_t ldx, int mc, int k, int kp,
+                                                     const int64_t* __restrict__ thr, uint16_t* __restrict__ Ph,
+                                                     uint16_t* __restrict__ Pz, uint16_t* __restrict__ Pl,
+                                                     float* __restrict__ apart) {
+  __shared__ float red[4][512];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c0 = blockIdx.x * 512 + 8 * lane;
+  const bool cv = c0 < k;   // all 8 channels valid (k % 8 == 0) or none
+  const bool cw = c0 < kp;  // inside the packed width
+  float acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+  for (int tt = 0; tt < 8; ++tt) {
+    const int tb = blockIdx.y * 8 + tt;
+    if (tb * kTokBlk >= mc) break;  // uniform
+    const int tbase = tb * kTokBlk + 8 * wave;
+    u32x4 xs[8], xd[8];
+    int64_t th[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int t = tbase + e;
+      const bool ok = cv && t < mc;
+      const int64_t off = ok ? (int64_t)t * ldx + c0 : 0;
+      xs[e] = *(const u32x4*)(Xs + off);
+      if (TWO) xd[e] = *(const u32x4*)(Xd + off);
+      if (!ok) xs[e] = u32x4{0u, 0u, 0u, 0u};
+      if (TWO && !ok) xd[e] = u32x4{0u, 0u, 0u, 0u};
+      th[e] = t < mc ? thr[t] : INT64_MAX;
+    }
+    u32x4 oh[8], oz[8], ol[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+#pragma unroll
+      for (int w2 = 0; w2 < 4; ++w2) {
+        uint32_t hv[2], zv[2], lv[2];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const uint32_t x = (xs[e][w2] >> (16 * hf)) & 0xffffu;
+          const int64_t key = ((int64_t)(x & 0x7fffu) << 32) | (int64_t)(c0 + 2 * w2 + hf);
+          const bool keep = key > th[e];
+          const uint32_t vh = keep ? x : 0u;
+          float d;
+          if (TWO) {
+            d = bf16_bits_to_f32((uint16_t)((xd[e][w2] >> (16 * hf)) & 0xffffu)) - bf16_bits_to_f32((uint16_t)vh);
+            const uint16_t vz = f32_to_bf16_bits(d);
+            zv[hf] = vz;
+            lv[hf] = f32_to_bf16_bits(d - bf16_bits_to_f32(vz));
+          } else {
+            zv[hf] = keep ? 0u : x;
+            d = bf16_bits_to_f32((uint16_t)zv[hf]);
+            lv[hf] = 0u;
+          }
+          hv[hf] = vh;
+          acc[2 * w2 + hf] = fmaf(d, d, acc[2 * w2 + hf]);
+        }
+        oh[e][w2] = hv[0] | (hv[1] << 16);
+        oz[e][w2] = zv[0] | (zv[1] << 16);
+        ol[e][w2] = lv[0] | (lv[1] << 16);
+      }
+    }
+    if (cw) {
+      const int64_t base = ((int64_t)(tb * (kTokBlk / 8) + wave) * kp + c0) * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int w2 = j >> 1;
+        u32x4 vh, vz, vl;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          vh[p] = (j & 1) ? hi_pair(oh[2 * p][w2], oh[2 * p + 1][w2]) : lo_pair(oh[2 * p][w2], oh[2 * p + 1][w2]);
+          vz[p] = (j & 1) ? hi_pair(oz[2 * p][w2], oz[2 * p + 1][w2]) : lo_pair(oz[2 * p][w2], oz[2 * p + 1][w2]);
+          vl[p] = (j & 1) ? hi_pair(ol[2 * p][w2], ol[2 * p + 1][w2]) : lo_pair(ol[2 * p][w2], ol[2 * p + 1][w2]);
+        }
+        *(u32x4*)(Ph + base + 8 * j) = vh;
+        *(u32x4*)(Pz + base + 8 * j) = vz;
+        if (TWO) *(u32x4*)(Pl + base + 8 * j) = vl;
+      }
+    }
+  }
+  // per-channel sum of dX^2 over this workgroup's tokens, fixed order
+#pragma unroll
+  for (int j = 0; j < 8; ++j) red[wave][8 * lane + j] = acc[j];
+  __syncthreads();
+  if (apart)
+    for (int i = threadIdx.x; i < 512; i += 256) {
+      const int c = blockIdx.x * 512 + i;
+      if (c < kp) apart[(int64_t)blockIdx.y * kp + c] = (red[0][i] + red[1][i]) + (red[2][i] + red[3][i]);
+    }
 }
 
 __global__ void a_reduce_kernel(const float* __restrict__ apart, int nblk, int kp, int k,
@@ -640,12 +847,27 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
     duo_status st = launch_act_select<T>(xs, ldx, mc, (int)k, z, w.thr, s);
     if (st != DUO_OK) return st;
     dim3 pg((unsigned)(kp / 256), (unsigned)cdiv(mc, 256));
+    if constexpr (sizeof(T) == 2) {
+      if (bf16_vec_ok(xs, ldx, k) && (!two || bf16_vec_ok(xd, ldx, k))) {
+        dim3 pg16((unsigned)cdiv(kp, 512), (unsigned)cdiv(mc, 256));
+        if (two)
+          hipLaunchKernelGGL(pack16_kernel<true>, pg16, dim3(256), 0, s, (const uint16_t*)xs, (const uint16_t*)xd,
+                             ldx, mc, (int)k, (int)kp, w.thr, (uint16_t*)w.Ph, (uint16_t*)w.Pz, (uint16_t*)w.Pl,
+                             want_g ? w.apart : nullptr);
+        else
+          hipLaunchKernelGGL(pack16_kernel<false>, pg16, dim3(256), 0, s, (const uint16_t*)xs, (const uint16_t*)xs,
+                             ldx, mc, (int)k, (int)kp, w.thr, (uint16_t*)w.Ph, (uint16_t*)w.Pz, (uint16_t*)w.Pl,
+                             want_g ? w.apart : nullptr);
+        goto packed;
+      }
+    }
     if (two)
       hipLaunchKernelGGL((pack_kernel<T, true>), pg, dim3(256), 0, s, xs, xd, ldx, mc, (int)k, (int)kp, w.thr,
                          (T*)w.Ph, (T*)w.Pz, (T*)w.Pl, want_g ? w.apart : nullptr);
     else
       hipLaunchKernelGGL((pack_kernel<T, false>), pg, dim3(256), 0, s, xs, xs, ldx, mc, (int)k, (int)kp, w.thr,
                          (T*)w.Ph, (T*)w.Pz, (T*)w.Pl, want_g ? w.apart : nullptr);
+  packed:
     DUO_LAUNCH_CHECK();
     if (want_g) {
       hipLaunchKernelGGL(a_reduce_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.apart, (int)cdiv(mc, 256),
