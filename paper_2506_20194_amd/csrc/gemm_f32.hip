@@ -16,7 +16,9 @@ namespace duo {
 namespace {
 
 constexpr int KT = 32;          // K per stage
-constexpr int LS = kTile + 16;  // LDS row stride (floats): conflict-free fragment reads
+constexpr int LS = kTile + 16;  // stride of the k-major LDS layout [k][LS] (operand loaded along rows/columns)
+constexpr int KS = KT + 2;      // stride of the k-contiguous LDS layout [row][KS] (operand loaded along k)
+constexpr int SLOT = kTile * KS > KT * LS ? kTile * KS : KT * LS;  // floats per operand per stage
 constexpr int PQ = KT / 8;      // float4 loads per thread per operand per stage
 
 struct Stage {
@@ -86,7 +88,12 @@ __device__ inline void load_stage(const GemmTerm& t, int M, int N, int i0, int j
   }
 }
 
-// LDS layout of both operands: [k][128 + 16] (k-major), alpha folded into A.
+// LDS layout per operand: an operand loaded 4 consecutive rows/columns at a
+// time is stored k-major, [k][LS] (float4 stores); one loaded 4 consecutive k
+// at a time is stored k-contiguous, [row][KS] (float2 stores), so that neither
+// the stores nor the fragment reads meet bank conflicts (KS = 34: the 32
+// lanes of a half-wave read rows 2 banks apart, at k and k+1).  alpha is
+// folded into A.
 template <bool AR, bool BR>
 __device__ inline void store_stage(float* sA, float* sB, const Stage& st, float alpha) {
   const int tid = threadIdx.x;
@@ -95,10 +102,8 @@ __device__ inline void store_stage(float* sA, float* sB, const Stage& st, float 
     const float4 a = st.a[q];
     if (AR) {
       const int row = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
-      sA[(l4 + 0) * LS + row] = alpha * a.x;
-      sA[(l4 + 1) * LS + row] = alpha * a.y;
-      sA[(l4 + 2) * LS + row] = alpha * a.z;
-      sA[(l4 + 3) * LS + row] = alpha * a.w;
+      *(float2*)&sA[row * KS + l4] = make_float2(alpha * a.x, alpha * a.y);
+      *(float2*)&sA[row * KS + l4 + 2] = make_float2(alpha * a.z, alpha * a.w);
     } else {
       const int lr = (tid >> 5) + 8 * q, i4 = (tid & 31) * 4;
       *(float4*)&sA[lr * LS + i4] = make_float4(alpha * a.x, alpha * a.y, alpha * a.z, alpha * a.w);
@@ -109,14 +114,13 @@ __device__ inline void store_stage(float* sA, float* sB, const Stage& st, float 
       *(float4*)&sB[lr * LS + j4] = b;
     } else {
       const int col = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
-      sB[(l4 + 0) * LS + col] = b.x;
-      sB[(l4 + 1) * LS + col] = b.y;
-      sB[(l4 + 2) * LS + col] = b.z;
-      sB[(l4 + 3) * LS + col] = b.w;
+      *(float2*)&sB[col * KS + l4] = make_float2(b.x, b.y);
+      *(float2*)&sB[col * KS + l4 + 2] = make_float2(b.z, b.w);
     }
   }
 }
 
+template <bool AR, bool BR>
 __device__ inline void compute_stage(const float* sA, const float* sB, f4 (&acc)[4][4]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wi = wave >> 1, wj = wave & 1;
@@ -126,8 +130,9 @@ __device__ inline void compute_stage(const float* sA, const float* sB, f4 (&acc)
     float av[4], bv[4];
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
-      av[a] = sA[kr * LS + wi * 64 + a * 16 + (lane & 15)];
-      bv[a] = sB[kr * LS + wj * 64 + a * 16 + (lane & 15)];
+      const int r = wi * 64 + a * 16 + (lane & 15), c = wj * 64 + a * 16 + (lane & 15);
+      av[a] = AR ? sA[r * KS + kr] : sA[kr * LS + r];
+      bv[a] = BR ? sB[kr * LS + c] : sB[c * KS + kr];
     }
 #pragma unroll
     for (int a = 0; a < 4; ++a)
@@ -145,8 +150,8 @@ __device__ inline void run_term(const GemmTerm& t, int M, int N, int i0, int j0,
   const int64_t khi = hi_of(t.khi, i0, j0, t.K);
   if (klo >= khi) return;
   const int nst = (int)((khi - klo + KT - 1) / KT);
-  float* sa[2] = {smem, smem + 2 * KT * LS};
-  float* sb[2] = {smem + KT * LS, smem + 3 * KT * LS};
+  float* sa[2] = {smem, smem + 2 * SLOT};
+  float* sb[2] = {smem + SLOT, smem + 3 * SLOT};
   Stage st0, st1;
   load_stage<AR, BR>(t, M, N, i0, j0, klo, klo, khi, st0);
   if (nst > 1) load_stage<AR, BR>(t, M, N, i0, j0, klo + KT, klo, khi, st1);
@@ -155,12 +160,12 @@ __device__ inline void run_term(const GemmTerm& t, int M, int N, int i0, int j0,
   lds_barrier();
   for (int s = 0; s < nst; s += 2) {
     if (s + 2 < nst) load_stage<AR, BR>(t, M, N, i0, j0, klo + (int64_t)(s + 2) * KT, klo, khi, st0);
-    compute_stage(sa[0], sb[0], acc);
+    compute_stage<AR, BR>(sa[0], sb[0], acc);
     if (s + 1 < nst) store_stage<AR, BR>(sa[1], sb[1], st1, t.alpha);
     lds_barrier();
     if (s + 1 >= nst) break;
     if (s + 3 < nst) load_stage<AR, BR>(t, M, N, i0, j0, klo + (int64_t)(s + 3) * KT, klo, khi, st1);
-    compute_stage(sa[1], sb[1], acc);
+    compute_stage<AR, BR>(sa[1], sb[1], acc);
     if (s + 2 < nst) store_stage<AR, BR>(sa[0], sb[0], st0, t.alpha);
     lds_barrier();
   }
@@ -173,7 +178,7 @@ __device__ inline int xcd_remap_g(int b, int nblocks) {
 
 template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmDesc d, int ntiles) {
-  __shared__ __attribute__((aligned(16))) float smem[4 * KT * LS];  // 2 buffers x (A, B)
+  __shared__ __attribute__((aligned(16))) float smem[4 * SLOT];  // 2 buffers x (A, B)
   const int id = xcd_remap_g(blockIdx.x, gridDim.x);
   if (id >= ntiles) return;
   if (blockIdx.y) {
