@@ -340,6 +340,7 @@ duo_status merge_nodes(float* H, int64_t ldh, int64_t k, int64_t span, int64_t h
   a.nterms = 1;
   a.t[0] = GemmTerm{H + r_lo * ldh + r_mid, ldh, 1, H + r_mid * ldh + r_mid, ldh, 1, m2, 1.f, KLO_ZERO, KHI_COL};
   a.batch = nodes;
+  a.order = ORDER_PLAIN;  // K ranges grow with the column: deal the tiles round-robin
   a.sC = (int64_t)m1 * m2;
   a.sA[0] = diag_step;
   a.sB[0] = diag_step;
@@ -356,6 +357,7 @@ duo_status merge_nodes(float* H, int64_t ldh, int64_t k, int64_t span, int64_t h
   b.nterms = 1;
   b.t[0] = GemmTerm{H + r_lo * ldh + r_lo, ldh, 1, X, m2, 1, m1, -1.f, KLO_ROW, KHI_FULL};
   b.batch = nodes;
+  b.order = ORDER_PLAIN;  // K ranges shrink with the row: deal the tiles round-robin
   b.sC = diag_step;
   b.sA[0] = diag_step;
   b.sB[0] = (int64_t)m1 * m2;

@@ -179,7 +179,7 @@ __device__ inline int xcd_remap_g(int b, int nblocks) {
 template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmDesc d, int ntiles) {
   __shared__ __attribute__((aligned(16))) float smem[4 * SLOT];  // 2 buffers x (A, B)
-  const int id = xcd_remap_g(blockIdx.x, gridDim.x);
+  const int id = d.order == ORDER_XCD ? xcd_remap_g(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   if (id >= ntiles) return;
   if (blockIdx.y) {
     const int64_t z = blockIdx.y;
@@ -196,6 +196,13 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmDesc d, int ntiles) {
     tj = id % tn;
   } else if (d.tri == TRI_LOWER) {
     tri_pair(id, &ti, &tj);
+  } else if (d.order == ORDER_DIAG) {
+    // group s holds the s + 1 tiles at distance T - 1 - s from the diagonal
+    const int T = (int)cdiv(d.N, kTile);
+    int sgrp, off;
+    tri_pair(id, &sgrp, &off);
+    ti = off;
+    tj = off + (T - 1 - sgrp);
   } else {
     tri_pair(id, &tj, &ti);
   }

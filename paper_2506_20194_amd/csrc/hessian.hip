@@ -615,7 +615,8 @@ __device__ __forceinline__ void lds_barrier() {
 // of the tile (8 x 4 accumulator blocks of 16 x 16).  Operand tiles stream
 // through a ring of NS LDS stages (one 32-token block each) filled by direct
 // global->LDS loads (global_load_lds_dwordx4: each lane moves 16 bytes, a wave
-// 1 KB), issued NS - 1 stages ahead.  LDS layout of one operand tile:
+// 1 KB), issued NS - 1 stages ahead (NS = 5 stages of 32 KB, or 3 of 48 KB
+// for the two-stream form, fill the 160 KB of LDS).  LDS layout of one operand tile:
 // [group][256 rows][16 bytes], identical to the packed global layout.
 template <typename T, bool HAS_LO>
 __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
@@ -626,8 +627,8 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
   constexpr int STAGE_B = NOP * TILE_B;
   constexpr int CHUNKS = TILE_B / 16;           // 16-byte chunks per operand tile
   constexpr int DPW = NOP * CHUNKS / 64 / 8;    // wave-wide loads per wave per stage
-  constexpr int NS = STAGE_B * 3 <= 160 * 1024 ? 3 : 2;
-  static_assert(CHUNKS % 64 == 0 && (NOP * CHUNKS / 64) % 8 == 0, "load split");
+  constexpr int NS = (160 * 1024) / STAGE_B < 5 ? (160 * 1024) / STAGE_B : 5;  // ring depth
+  static_assert(NS >= 2 && CHUNKS % 64 == 0 && (NOP * CHUNKS / 64) % 8 == 0, "load split");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const int u = xcd_remap(blockIdx.x, gridDim.x);
@@ -672,11 +673,14 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
 
   for (int t = tb0; t < min(tb1, tb0 + NS - 1); ++t) issue(t);
   for (int t = tb0; t < tb1; ++t) {
-    // stage t complete (younger stages may still be in flight)
-    if (t + NS - 2 < tb1 && NS == 3)
-      wait_vmem<DPW>();
-    else
-      wait_vmem<0>();
+    // stage t complete; the stages issued after it (up to NS - 2) may still be
+    // in flight
+    switch (min(NS - 2, tb1 - 1 - t)) {
+      case 3: wait_vmem<3 * DPW>(); break;
+      case 2: wait_vmem<2 * DPW>(); break;
+      case 1: wait_vmem<DPW>(); break;
+      default: wait_vmem<0>(); break;
+    }
     lds_barrier();  // every wave's part of stage t has landed; stage t-1 is free
     if (t + NS - 1 < tb1) issue(t + NS - 1);
     const v4u* l_ = (const v4u*)(smem + ((t - tb0) % NS) * STAGE_B);
@@ -819,7 +823,8 @@ template <typename T, bool LO>
 static duo_status launch_gram(const GramArgs<T>& A, hipStream_t s) {
   constexpr int NOP = LO ? 3 : 2;
   const size_t stage = NOP * (size_t)GT * kTokBlk * sizeof(T);
-  const size_t lds = (stage * 3 <= 160 * 1024 ? 3 : 2) * stage;
+  const size_t ns = (160 * 1024) / stage < 5 ? (160 * 1024) / stage : 5;
+  const size_t lds = ns * stage;
   auto kern = gram_kernel<T, LO>;
   DUO_HIP_TRY(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   const int grid = (int)rup((int64_t)A.ntiles * A.nseg, 8);

@@ -57,7 +57,15 @@ struct GemmDesc {
   // batched launches: problem z (blockIdx.y) uses C + z*sC, A_i + z*sA[i], B_i + z*sB[i]
   int batch;  // 0 or 1: a single problem
   int64_t sC, sA[2], sB[2];
+  // tile order: ORDER_XCD gives each XCD a contiguous range of tiles (operand
+  // reuse in its L2; for tiles of equal cost); ORDER_PLAIN deals tiles to the
+  // XCDs round-robin in enumeration order (for upper tiles: by column, i.e.
+  // the longest first when the K range shrinks with the column); ORDER_DIAG
+  // (upper tiles only) deals them by decreasing distance from the diagonal
+  // (the longest first when the K range grows with that distance)
+  int order;
 };
+enum { ORDER_XCD = 0, ORDER_PLAIN = 1, ORDER_DIAG = 2 };
 
 duo_status gemm_f32(const GemmDesc& d, hipStream_t s);
 

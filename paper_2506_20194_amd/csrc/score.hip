@@ -70,6 +70,7 @@ duo_status score_run(const float* L, int64_t ldl, const float* G, int64_t ldg, c
   q.ldc = k;
   q.beta = 0.f;
   q.tri = TRI_UPPER;
+  q.order = ORDER_PLAIN;  // K range [j0, k): the first columns are the longest
   q.nterms = 1;
   q.t[0] = GemmTerm{G, ldg, 1, L, ldl, 1, (int)k, 1.f, KLO_COL, KHI_FULL};
   duo_status st = gemm_f32(q, s);
@@ -84,6 +85,7 @@ duo_status score_run(const float* L, int64_t ldl, const float* G, int64_t ldg, c
   d.ldc = ldd;
   d.beta = 0.f;
   d.tri = TRI_UPPER;
+  d.order = ORDER_DIAG;  // K range [i0, j0 + 128): grows with the distance from the diagonal
   d.nterms = 1;
   d.t[0] = GemmTerm{w.Q, k, 1, L, ldl, 0, (int)k, 1.f, KLO_ROW, KHI_COL};
   return gemm_f32(d, s);
