@@ -1,7 +1,8 @@
 // fp32 MFMA GEMM for gfx950 used by the dense k^3 stages (inverse Cholesky,
 // Q = G L, D = U L^T) and by the lazy trailing update of the column sweep.
 //
-// 128 x 128 output tile per 256-thread workgroup, 2 x 2 waves of 64 x 64,
+// 128 x 128 output tile per 256-thread workgroup, 2 x 2 waves of 64 x 64
+// (64 x 64 tiles for launches too small to fill the chip),
 // v_mfma_f32_16x16x4_f32; K staged 32 at a time through LDS, with the global
 // loads of the stage after next in flight during each multiply (fence-free
 // barriers, so the prefetch is not drained at every stage).  Triangular operands are handled by restricting each
@@ -15,31 +16,41 @@ namespace duo {
 
 namespace {
 
-constexpr int KT = 32;          // K per stage
-constexpr int LS = kTile + 16;  // stride of the k-major LDS layout [k][LS] (operand loaded along rows/columns)
-constexpr int KS = KT + 2;      // stride of the k-contiguous LDS layout [row][KS] (operand loaded along k)
-constexpr int SLOT = kTile * KS > KT * LS ? kTile * KS : KT * LS;  // floats per operand per stage
-constexpr int PQ = KT / 8;      // float4 loads per thread per operand per stage
+constexpr int KT = 32;      // K per stage
+constexpr int KS = KT + 2;  // stride of the k-contiguous LDS layout [row][KS] (operand loaded along k)
 
-struct Stage {
-  float4 a[PQ];
-  float4 b[PQ];
+// Per tile edge TE (128, or 64 for launches too small to fill the chip):
+// 2 x 2 waves of (TE/2)^2 outputs, NA x NA MFMA blocks of 16 x 16 per wave.
+template <int TE>
+struct Geo {
+  static constexpr int LS = TE + 16;                            // stride of the k-major layout [k][LS]
+  static constexpr int SLOT = TE * KS > KT * LS ? TE * KS : KT * LS;  // floats per operand per stage
+  static constexpr int PQ = TE * KT / 1024;                    // float4 loads per thread per operand per stage
+  static constexpr int TPR = TE / 4;                           // threads per k line in the k-major loads
+  static constexpr int NA = TE / 32;                           // 16 x 16 blocks per wave and dimension
 };
 
+template <int TE>
+struct Stage {
+  float4 a[Geo<TE>::PQ];
+  float4 b[Geo<TE>::PQ];
+};
+
+template <int TE>
 __device__ inline int64_t lo_of(int mode, int i0, int j0) {
   return mode == KLO_ROW ? i0 : mode == KLO_COL ? j0 : 0;
 }
+template <int TE>
 __device__ inline int64_t hi_of(int mode, int i0, int j0, int K) {
-  const int64_t v = mode == KHI_ROW ? (int64_t)i0 + kTile : mode == KHI_COL ? (int64_t)j0 + kTile : K;
+  const int64_t v = mode == KHI_ROW ? (int64_t)i0 + TE : mode == KHI_COL ? (int64_t)j0 + TE : K;
   return v < K ? v : K;
 }
 
 // Load 4 consecutive elements p[0..3] of a line whose valid index range is
-// [lo, hi), starting at index `idx`; vector load when fully inside and aligned.
+// [lo, hi), starting at index `idx` (edge tiles and ragged stages only).
 __device__ inline float4 load4(const float* p, int64_t idx, int64_t lo, int64_t hi, bool line_ok) {
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
   if (!line_ok) return v;
-  if (idx >= lo && idx + 3 < hi && ((reinterpret_cast<uintptr_t>(p) & 15) == 0)) return *(const float4*)p;
   if (idx + 0 >= lo && idx + 0 < hi) v.x = p[0];
   if (idx + 1 >= lo && idx + 1 < hi) v.y = p[1];
   if (idx + 2 >= lo && idx + 2 < hi) v.z = p[2];
@@ -57,61 +68,74 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// One stage = KT values of K for 128 rows of A and 128 columns of B; each of
-// the 256 threads moves PQ float4 of each operand.
-template <bool AR, bool BR>
+// One stage = KT values of K for TE rows of A and TE columns of B; each of
+// the 256 threads moves PQ float4 of each operand.  FAST (uniform over the
+// workgroup): the tile lies inside M x N, the stage inside [klo, khi) and
+// both operands are 16-byte aligned, so every load is a plain 16-byte one.
+template <int TE, bool AR, bool BR, bool FAST>
 __device__ inline void load_stage(const GemmTerm& t, int M, int N, int i0, int j0, int64_t k0, int64_t klo,
-                                  int64_t khi, Stage& st) {
+                                  int64_t khi, Stage<TE>& st) {
+  using G = Geo<TE>;
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < PQ; ++q) {
+  for (int q = 0; q < G::PQ; ++q) {
     if (AR) {  // A(i,l) = A[i*lda + l]: 4 consecutive l of one row
       const int row = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
       const int64_t i = i0 + row, l = k0 + l4;
-      st.a[q] = load4(t.A + i * t.lda + l, l, klo, khi, i < M);
+      st.a[q] = FAST ? *(const float4*)(t.A + i * t.lda + l) : load4(t.A + i * t.lda + l, l, klo, khi, i < M);
     } else {  // A(i,l) = A[l*lda + i]: 4 consecutive i of one l
-      const int lr = (tid >> 5) + 8 * q, i4 = (tid & 31) * 4;
+      const int lr = tid / G::TPR + (256 / G::TPR) * q, i4 = (tid % G::TPR) * 4;
       const int64_t i = i0 + i4, l = k0 + lr;
-      const bool ok = l >= klo && l < khi;
-      st.a[q] = load4(t.A + l * t.lda + i, i, 0, M, ok);
+      st.a[q] = FAST ? *(const float4*)(t.A + l * t.lda + i)
+                     : load4(t.A + l * t.lda + i, i, 0, M, l >= klo && l < khi);
     }
     if (BR) {  // B(l,j) = B[l*ldb + j]: 4 consecutive j of one l
-      const int lr = (tid >> 5) + 8 * q, j4 = (tid & 31) * 4;
+      const int lr = tid / G::TPR + (256 / G::TPR) * q, j4 = (tid % G::TPR) * 4;
       const int64_t j = j0 + j4, l = k0 + lr;
-      const bool ok = l >= klo && l < khi;
-      st.b[q] = load4(t.B + l * t.ldb + j, j, 0, N, ok);
+      st.b[q] = FAST ? *(const float4*)(t.B + l * t.ldb + j)
+                     : load4(t.B + l * t.ldb + j, j, 0, N, l >= klo && l < khi);
     } else {  // B(l,j) = B[j*ldb + l]: 4 consecutive l of one column
       const int col = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
       const int64_t j = j0 + col, l = k0 + l4;
-      st.b[q] = load4(t.B + j * t.ldb + l, l, klo, khi, j < N);
+      st.b[q] = FAST ? *(const float4*)(t.B + j * t.ldb + l) : load4(t.B + j * t.ldb + l, l, klo, khi, j < N);
     }
   }
+}
+
+template <int TE, bool AR, bool BR>
+__device__ inline void load_stage_any(const GemmTerm& t, int M, int N, int i0, int j0, int64_t k0, int64_t klo,
+                                      int64_t khi, bool fast_tile, Stage<TE>& st) {
+  if (fast_tile && k0 + KT <= khi)
+    load_stage<TE, AR, BR, true>(t, M, N, i0, j0, k0, klo, khi, st);
+  else
+    load_stage<TE, AR, BR, false>(t, M, N, i0, j0, k0, klo, khi, st);
 }
 
 // LDS layout per operand: an operand loaded 4 consecutive rows/columns at a
 // time is stored k-major, [k][LS] (float4 stores); one loaded 4 consecutive k
 // at a time is stored k-contiguous, [row][KS] (float2 stores), so that neither
 // the stores nor the fragment reads meet bank conflicts (KS = 34: the 32
-// lanes of a half-wave read rows 2 banks apart, at k and k+1).  alpha is
-// folded into A.
-template <bool AR, bool BR>
-__device__ inline void store_stage(float* sA, float* sB, const Stage& st, float alpha) {
+// lanes of a half-wave read rows 2 banks apart, at k and k+1; LS = TE + 16:
+// the two k lines of a half-wave sit 16 banks apart).  alpha is folded into A.
+template <int TE, bool AR, bool BR>
+__device__ inline void store_stage(float* sA, float* sB, const Stage<TE>& st, float alpha) {
+  using G = Geo<TE>;
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < PQ; ++q) {
+  for (int q = 0; q < G::PQ; ++q) {
     const float4 a = st.a[q];
     if (AR) {
       const int row = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
       *(float2*)&sA[row * KS + l4] = make_float2(alpha * a.x, alpha * a.y);
       *(float2*)&sA[row * KS + l4 + 2] = make_float2(alpha * a.z, alpha * a.w);
     } else {
-      const int lr = (tid >> 5) + 8 * q, i4 = (tid & 31) * 4;
-      *(float4*)&sA[lr * LS + i4] = make_float4(alpha * a.x, alpha * a.y, alpha * a.z, alpha * a.w);
+      const int lr = tid / G::TPR + (256 / G::TPR) * q, i4 = (tid % G::TPR) * 4;
+      *(float4*)&sA[lr * G::LS + i4] = make_float4(alpha * a.x, alpha * a.y, alpha * a.z, alpha * a.w);
     }
     const float4 b = st.b[q];
     if (BR) {
-      const int lr = (tid >> 5) + 8 * q, j4 = (tid & 31) * 4;
-      *(float4*)&sB[lr * LS + j4] = b;
+      const int lr = tid / G::TPR + (256 / G::TPR) * q, j4 = (tid % G::TPR) * 4;
+      *(float4*)&sB[lr * G::LS + j4] = b;
     } else {
       const int col = (tid >> 3) + 32 * q, l4 = (tid & 7) * 4;
       *(float2*)&sB[col * KS + l4] = make_float2(b.x, b.y);
@@ -120,53 +144,61 @@ __device__ inline void store_stage(float* sA, float* sB, const Stage& st, float 
   }
 }
 
-template <bool AR, bool BR>
-__device__ inline void compute_stage(const float* sA, const float* sB, f4 (&acc)[4][4]) {
+template <int TE, bool AR, bool BR>
+__device__ inline void compute_stage(const float* sA, const float* sB, f4 (&acc)[Geo<TE>::NA][Geo<TE>::NA]) {
+  using G = Geo<TE>;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wi = wave >> 1, wj = wave & 1;
 #pragma unroll
   for (int ks = 0; ks < KT / 4; ++ks) {
     const int kr = ks * 4 + (lane >> 4);
-    float av[4], bv[4];
+    float av[G::NA], bv[G::NA];
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const int r = wi * 64 + a * 16 + (lane & 15), c = wj * 64 + a * 16 + (lane & 15);
-      av[a] = AR ? sA[r * KS + kr] : sA[kr * LS + r];
-      bv[a] = BR ? sB[kr * LS + c] : sB[c * KS + kr];
+    for (int a = 0; a < G::NA; ++a) {
+      const int r = wi * (TE / 2) + a * 16 + (lane & 15), c = wj * (TE / 2) + a * 16 + (lane & 15);
+      av[a] = AR ? sA[r * KS + kr] : sA[kr * G::LS + r];
+      bv[a] = BR ? sB[kr * G::LS + c] : sB[c * KS + kr];
     }
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < G::NA; ++a)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
+      for (int b = 0; b < G::NA; ++b)
+        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
   }
 }
 
 // K loop of one term: stage s sits in LDS buffer s & 1; the global loads of
 // stage s + 2 are in flight while stage s is multiplied (two register slots,
 // the loop unrolled by two so that every slot index is static).
-template <bool AR, bool BR>
-__device__ inline void run_term(const GemmTerm& t, int M, int N, int i0, int j0, float* smem, f4 (&acc)[4][4]) {
-  const int64_t klo = lo_of(t.klo, i0, j0);
-  const int64_t khi = hi_of(t.khi, i0, j0, t.K);
+template <int TE, bool AR, bool BR>
+__device__ inline void run_term(const GemmTerm& t, int M, int N, int i0, int j0, float* smem,
+                                f4 (&acc)[Geo<TE>::NA][Geo<TE>::NA]) {
+  constexpr int SLOT = Geo<TE>::SLOT;
+  const int64_t klo = lo_of<TE>(t.klo, i0, j0);
+  const int64_t khi = hi_of<TE>(t.khi, i0, j0, t.K);
   if (klo >= khi) return;
   const int nst = (int)((khi - klo + KT - 1) / KT);
+  // klo is 0 or a tile start, so every stage start is a multiple of 4
+  const bool fast_tile = i0 + TE <= M && j0 + TE <= N && ((reinterpret_cast<uintptr_t>(t.A) & 15) == 0) &&
+                         ((reinterpret_cast<uintptr_t>(t.B) & 15) == 0) && (t.lda & 3) == 0 && (t.ldb & 3) == 0;
   float* sa[2] = {smem, smem + 2 * SLOT};
   float* sb[2] = {smem + SLOT, smem + 3 * SLOT};
-  Stage st0, st1;
-  load_stage<AR, BR>(t, M, N, i0, j0, klo, klo, khi, st0);
-  if (nst > 1) load_stage<AR, BR>(t, M, N, i0, j0, klo + KT, klo, khi, st1);
+  Stage<TE> st0, st1;
+  load_stage_any<TE, AR, BR>(t, M, N, i0, j0, klo, klo, khi, fast_tile, st0);
+  if (nst > 1) load_stage_any<TE, AR, BR>(t, M, N, i0, j0, klo + KT, klo, khi, fast_tile, st1);
   lds_barrier();  // earlier users of the LDS buffers are done
-  store_stage<AR, BR>(sa[0], sb[0], st0, t.alpha);
+  store_stage<TE, AR, BR>(sa[0], sb[0], st0, t.alpha);
   lds_barrier();
+#pragma nounroll
   for (int s = 0; s < nst; s += 2) {
-    if (s + 2 < nst) load_stage<AR, BR>(t, M, N, i0, j0, klo + (int64_t)(s + 2) * KT, klo, khi, st0);
-    compute_stage<AR, BR>(sa[0], sb[0], acc);
-    if (s + 1 < nst) store_stage<AR, BR>(sa[1], sb[1], st1, t.alpha);
+    if (s + 2 < nst) load_stage_any<TE, AR, BR>(t, M, N, i0, j0, klo + (int64_t)(s + 2) * KT, klo, khi, fast_tile, st0);
+    compute_stage<TE, AR, BR>(sa[0], sb[0], acc);
+    if (s + 1 < nst) store_stage<TE, AR, BR>(sa[1], sb[1], st1, t.alpha);
     lds_barrier();
     if (s + 1 >= nst) break;
-    if (s + 3 < nst) load_stage<AR, BR>(t, M, N, i0, j0, klo + (int64_t)(s + 3) * KT, klo, khi, st1);
-    compute_stage<AR, BR>(sa[1], sb[1], acc);
-    if (s + 2 < nst) store_stage<AR, BR>(sa[0], sb[0], st0, t.alpha);
+    if (s + 3 < nst) load_stage_any<TE, AR, BR>(t, M, N, i0, j0, klo + (int64_t)(s + 3) * KT, klo, khi, fast_tile, st1);
+    compute_stage<TE, AR, BR>(sa[1], sb[1], acc);
+    if (s + 2 < nst) store_stage<TE, AR, BR>(sa[0], sb[0], st0, t.alpha);
     lds_barrier();
   }
 }
@@ -176,9 +208,14 @@ __device__ inline int xcd_remap_g(int b, int nblocks) {
   return (b % 8) * per + b / 8;
 }
 
-template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmDesc d, int ntiles) {
-  __shared__ __attribute__((aligned(16))) float smem[4 * SLOT];  // 2 buffers x (A, B)
+// Tiles are enumerated on the 128 grid (the triangular filters and the tile
+// orders are defined there); with TE = 64 each 128 tile is split into its
+// four quarters, which are consecutive ids.
+template <int TE, bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
+__global__ __launch_bounds__(256, 2) void gemm_kernel(GemmDesc d, int ntiles) {
+  using G = Geo<TE>;
+  constexpr int SUB = kTile / TE;  // tiles per 128 edge
+  __shared__ __attribute__((aligned(16))) float smem[4 * G::SLOT];  // 2 buffers x (A, B)
   const int id = d.order == ORDER_XCD ? xcd_remap_g(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   if (id >= ntiles) return;
   if (blockIdx.y) {
@@ -189,42 +226,44 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmDesc d, int ntiles) {
     d.t[1].A += z * d.sA[1];
     d.t[1].B += z * d.sB[1];
   }
-  int ti, tj;
+  const int pid = id / (SUB * SUB), sub = id % (SUB * SUB);
+  int ti, tj;  // on the 128 grid
   if (d.tri == TRI_ALL) {
     const int tn = (int)cdiv(d.N, kTile);
-    ti = id / tn;
-    tj = id % tn;
+    ti = pid / tn;
+    tj = pid % tn;
   } else if (d.tri == TRI_LOWER) {
-    tri_pair(id, &ti, &tj);
+    tri_pair(pid, &ti, &tj);
   } else if (d.order == ORDER_DIAG) {
     // group s holds the s + 1 tiles at distance T - 1 - s from the diagonal
     const int T = (int)cdiv(d.N, kTile);
     int sgrp, off;
-    tri_pair(id, &sgrp, &off);
+    tri_pair(pid, &sgrp, &off);
     ti = off;
     tj = off + (T - 1 - sgrp);
   } else {
-    tri_pair(id, &tj, &ti);
+    tri_pair(pid, &tj, &ti);
   }
-  const int i0 = ti * kTile, j0 = tj * kTile;
-  f4 acc[4][4];
+  const int i0 = ti * kTile + (sub / SUB) * TE, j0 = tj * kTile + (sub % SUB) * TE;
+  if (i0 >= d.M || j0 >= d.N) return;
+  f4 acc[G::NA][G::NA];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < G::NA; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
-  run_term<A1R, B1R>(d.t[0], d.M, d.N, i0, j0, smem, acc);
-  if (TWO) run_term<A2R, B2R>(d.t[1], d.M, d.N, i0, j0, smem, acc);
+    for (int b = 0; b < G::NA; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
+  run_term<TE, A1R, B1R>(d.t[0], d.M, d.N, i0, j0, smem, acc);
+  if (TWO) run_term<TE, A2R, B2R>(d.t[1], d.M, d.N, i0, j0, smem, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wi = wave >> 1, wj = wave & 1;
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < G::NA; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+    for (int b = 0; b < G::NA; ++b)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t i = i0 + wi * 64 + a * 16 + (lane >> 4) * 4 + r;
-        const int64_t j = j0 + wj * 64 + b * 16 + (lane & 15);
+        const int64_t i = i0 + wi * (TE / 2) + a * 16 + (lane >> 4) * 4 + r;
+        const int64_t j = j0 + wj * (TE / 2) + b * 16 + (lane & 15);
         if (i < d.M && j < d.N) {
           float* c = d.C + i * d.ldc + j;
           *c = d.beta != 0.f ? d.beta * *c + acc[a][b][r] : acc[a][b][r];
@@ -232,14 +271,23 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmDesc d, int ntiles) {
       }
 }
 
+// A launch with fewer 128 tiles than kSmallTiles runs on 64 tiles: four
+// times the workgroups, so that short products still cover the 256 CUs.
+constexpr int kSmallTiles = 512;
+
 template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
 duo_status launch(const GemmDesc& d, hipStream_t s) {
   const int tm = (int)cdiv(d.M, kTile), tn = (int)cdiv(d.N, kTile);
-  int ntiles = d.tri == TRI_ALL ? tm * tn : tm * (tm + 1) / 2;
+  const int ntiles = d.tri == TRI_ALL ? tm * tn : tm * (tm + 1) / 2;
   if (ntiles <= 0) return DUO_OK;
-  const int grid = (int)rup(ntiles, 8);
   const int nb = d.batch > 1 ? d.batch : 1;
-  hipLaunchKernelGGL((gemm_kernel<A1R, B1R, A2R, B2R, TWO>), dim3(grid, nb), dim3(256), 0, s, d, ntiles);
+  if ((int64_t)ntiles * nb < kSmallTiles) {
+    const int grid = (int)rup(4 * ntiles, 8);
+    hipLaunchKernelGGL((gemm_kernel<64, A1R, B1R, A2R, B2R, TWO>), dim3(grid, nb), dim3(256), 0, s, d, 4 * ntiles);
+  } else {
+    const int grid = (int)rup(ntiles, 8);
+    hipLaunchKernelGGL((gemm_kernel<kTile, A1R, B1R, A2R, B2R, TWO>), dim3(grid, nb), dim3(256), 0, s, d, ntiles);
+  }
   DUO_LAUNCH_CHECK();
   return DUO_OK;
 }
@@ -251,11 +299,18 @@ duo_status gemm_f32(const GemmDesc& d, hipStream_t s) {
   if (d.tri != TRI_ALL && d.M != d.N) return DUO_ERR_UNSUPPORTED;
   const int c1 = d.t[0].a_row * 2 + d.t[0].b_row;
   if (d.nterms == 1) {
+    // one-term products run the two-term kernel with an empty second term
+    // (K = 0: it returns before any access).  Compiled on its own, the
+    // one-term kernel needs more than 256 VGPRs (one wave per SIMD, or
+    // spills at two); in the two-term form it stays near 210.
+    GemmDesc e = d;
+    e.t[1] = GemmTerm{nullptr, 0, d.t[0].a_row, nullptr, 0, d.t[0].b_row, 0, 0.f, KLO_ZERO, KHI_FULL};
+    e.sA[1] = e.sB[1] = 0;
     switch (c1) {
-      case 0: return launch<false, false, false, false, false>(d, s);
-      case 1: return launch<false, true, false, false, false>(d, s);
-      case 2: return launch<true, false, false, false, false>(d, s);
-      default: return launch<true, true, false, false, false>(d, s);
+      case 0: return launch<false, false, false, false, true>(e, s);
+      case 1: return launch<false, true, false, true, true>(e, s);
+      case 2: return launch<true, false, true, false, true>(e, s);
+      default: return launch<true, true, true, true, true>(e, s);
     }
   }
   const int c2 = d.t[1].a_row * 2 + d.t[1].b_row;

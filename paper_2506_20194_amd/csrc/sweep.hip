@@ -344,7 +344,7 @@ __device__ __forceinline__ void ib_steps(IbRow& s, const float* lq, const float*
   (ib_step<Js>(s, buf, lq, dq, il, q), ...);
 }
 
-__global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int B,
+__global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int64_t ew_ld,
                                                       const float* __restrict__ L, int64_t ldl,
                                                       const float* __restrict__ D, int64_t ldd,
                                                       const float* __restrict__ fac, const SelState* st, int mode,
@@ -437,8 +437,8 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
     const int c = q + IB_Q * i;
     if (rv && c < Bb) {
       Wo[(int64_t)row * k + j0 + c] = s.w[i];
-      EW[(int64_t)row * 2 * B + c] = s.e[i];
-      EW[(int64_t)row * 2 * B + B + c] = s.w0[i];
+      EW[(int64_t)row * ew_ld + c] = s.e[i];
+      EW[(int64_t)row * ew_ld + (ew_ld >> 1) + c] = s.w0[i];
       bmask[(int64_t)row * k + j0 + c] = (uint8_t)((s.kb[i] >> q) & 1u);
     }
   }
@@ -472,6 +472,18 @@ __global__ void finalize_kernel(const float* Wo, const uint8_t* bmask, int n, in
   }
 }
 
+// Two-level lazy update.  The weight update that a processed block owes the
+// columns to its right is linear in that block's (E, W0) pair, so it may be
+// applied in pieces: right after block [j0, j1) only the columns up to the
+// end of its super-block of kSuper columns are updated (K = block width);
+// when a super-block is complete, one product with K = super-block width
+// brings every column beyond it up to date.  Each block still sees, before
+// its selection, every update owed to it.  EW holds the super-block's pairs,
+// row-major with stride 2 S: E of column sb0 + c at c, W0 at S + c.
+constexpr int kSuper = 512;
+
+int super_width(int B) { return B * (kSuper / B > 1 ? kSuper / B : 1); }
+
 struct SweepWs {
   SelState* st;
   uint32_t* hist;
@@ -487,7 +499,7 @@ SweepWs carve(void* ws, int64_t n, int64_t k, int B) {
   w.st = c.take<SelState>(1);
   w.hist = c.take<uint32_t>(kBins0);
   w.cand = c.take<unsigned long long>(kSelCap);
-  w.EW = c.take<float>((size_t)n * 2 * B);
+  w.EW = c.take<float>((size_t)n * 2 * super_width(B));
   w.bmask = c.take<uint8_t>((size_t)n * k);
   w.bytes = c.off;
   return w;
@@ -503,6 +515,7 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
                      hipStream_t s) {
   const SweepWs w = carve(ws, n, k, B);
   const int64_t nk = n * k;
+  const int64_t S = super_width(B);
   hipLaunchKernelGGL(init_w_kernel, dim3((unsigned)cdiv(nk, 256)), dim3(256), 0, s, W, (int)w_dtype, ldw, (int)n,
                      (int)k, W_out);
   DUO_LAUNCH_CHECK();
@@ -547,21 +560,27 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     }
     prof_end(DUO_PROF_SELECT, s);
     prof_begin(DUO_PROF_INBLOCK, s);
+    const int64_t sb0 = j0 / S * S, sb1 = sb0 + S < k ? sb0 + S : k;
     hipLaunchKernelGGL(inblock_kernel, dim3((unsigned)cdiv(n, IB_ROWS)), dim3(256), ib_lds, s, W_out, (int)n, (int)k,
-                       (int)j0, Bb, B, L, ldl, D, ldd, fac, (const SelState*)w.st, mode, mask_in, w.EW, w.bmask);
+                       (int)j0, Bb, (int64_t)2 * S, L, ldl, D, ldd, fac, (const SelState*)w.st, mode, mask_in,
+                       w.EW + (j0 - sb0), w.bmask);
     DUO_LAUNCH_CHECK();
     prof_end(DUO_PROF_INBLOCK, s);
-    if (j1 < k) {
+    // inside the super-block: columns [j1, sb1) from this block (K = Bb);
+    // at its end: columns [sb1, k) from the whole super-block (K = sb1 - sb0)
+    const int64_t u0 = j1 < sb1 ? j0 : sb0, c0 = j1, c1 = j1 < sb1 ? sb1 : k;
+    if (c0 < c1) {
+      const int K = (int)(j1 - u0);
       GemmDesc g{};
       g.M = (int)n;
-      g.N = (int)(k - j1);
-      g.C = W_out + j1;
+      g.N = (int)(c1 - c0);
+      g.C = W_out + c0;
       g.ldc = k;
       g.beta = 1.f;
       g.tri = TRI_ALL;
       g.nterms = 2;
-      g.t[0] = GemmTerm{w.EW, 2 * B, 1, L + j1 * ldl + j0, ldl, 0, Bb, -1.f, KLO_ZERO, KHI_FULL};
-      g.t[1] = GemmTerm{w.EW + B, 2 * B, 1, D + j0 * ldd + j1, ldd, 1, Bb, 1.f, KLO_ZERO, KHI_FULL};
+      g.t[0] = GemmTerm{w.EW + (u0 - sb0), 2 * S, 1, L + c0 * ldl + u0, ldl, 0, K, -1.f, KLO_ZERO, KHI_FULL};
+      g.t[1] = GemmTerm{w.EW + S + (u0 - sb0), 2 * S, 1, D + u0 * ldd + c0, ldd, 1, K, 1.f, KLO_ZERO, KHI_FULL};
       prof_begin(DUO_PROF_TRAIL, s);
       duo_status st = gemm_f32(g, s);
       prof_end(DUO_PROF_TRAIL, s);
