@@ -629,6 +629,9 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
   constexpr int DPW = NOP * CHUNKS / 64 / 8;    // wave-wide loads per wave per stage
   constexpr int NS = (160 * 1024) / STAGE_B < 5 ? (160 * 1024) / STAGE_B : 5;  // ring depth
   static_assert(NS >= 2 && CHUNKS % 64 == 0 && (NOP * CHUNKS / 64) % 8 == 0, "load split");
+  // fragment reads pipelined half a stage ahead: bf16, one stream (the
+  // register budget of the extra fragments is not there for the two-stream form)
+  constexpr bool PIPE = MfmaOp<T>::kFrags == 1 && !HAS_LO && NS >= 4;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const int u = xcd_remap(blockIdx.x, gridDim.x);
@@ -672,40 +675,109 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
     for (int b = 0; b < 4; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
 
   for (int t = tb0; t < min(tb1, tb0 + NS - 1); ++t) issue(t);
-  for (int t = tb0; t < tb1; ++t) {
-    // stage t complete; the stages issued after it (up to NS - 2) may still be
-    // in flight
-    switch (min(NS - 2, tb1 - 1 - t)) {
+  if (tb1 <= tb0) {
+    // empty segment: the partial tile stays zero
+  } else if constexpr (PIPE) {
+    // Half-stage pipeline: the second half of stage t's A fragments is read
+    // during the MFMAs of the first half, and the B and first-half A fragments
+    // of stage t + 1 during those of the second half, so the LDS reads of all
+    // eight waves overlap the matrix work instead of following each barrier.
+    const int fo = (lane >> 4) * GT + (lane & 15);
+    auto slot = [&](int t) { return (const v4u*)(smem + ((t - tb0) % NS) * STAGE_B); };
+    auto read_b = [&](int t, v4u (&F)[4]) {
+      const v4u* l_ = slot(t);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) F[b] = l_[fo + wj * 64 + b * 16];
+    };
+    auto read_a = [&](int t, int h2, v4u (&F)[4]) {
+      const v4u* l_ = slot(t);
+#pragma unroll
+      for (int a = 0; a < 4; ++a) F[a] = l_[CHUNKS + fo + wi * 128 + (4 * h2 + a) * 16];
+    };
+    auto mma_half = [&](int h2, const v4u (&Fa)[4], const v4u (&Fb)[4]) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[4 * h2 + a][b] = MfmaOp<T>::mma(Fa[a], Fb[b], acc[4 * h2 + a][b]);
+    };
+    // stage t + 1 complete and readable by every wave; stage t + NS - 1 issued
+    // into the slot of stage t - 1, which every wave has finished reading
+    auto advance = [&](int t) {
+      switch (min(NS - 3, tb1 - 2 - t)) {
+        case 2: wait_vmem<2 * DPW>(); break;
+        case 1: wait_vmem<DPW>(); break;
+        default: wait_vmem<0>(); break;
+      }
+      lds_barrier();
+      if (t + NS - 1 < tb1) issue(t + NS - 1);
+    };
+    v4u fb[4], fa0[4];
+    switch (min(NS - 2, tb1 - 1 - tb0)) {  // stage tb0 complete
       case 3: wait_vmem<3 * DPW>(); break;
       case 2: wait_vmem<2 * DPW>(); break;
       case 1: wait_vmem<DPW>(); break;
       default: wait_vmem<0>(); break;
     }
-    lds_barrier();  // every wave's part of stage t has landed; stage t-1 is free
-    if (t + NS - 1 < tb1) issue(t + NS - 1);
-    const v4u* l_ = (const v4u*)(smem + ((t - tb0) % NS) * STAGE_B);
+    lds_barrier();
+    read_b(tb0, fb);
+    read_a(tb0, 0, fa0);
+    // (fb, fa0) hold stage t's B and first A half on entry to each stage
+    for (int t = tb0; t < tb1 - 1; ++t) {
+      v4u fa1[4], nb[4], na0[4];
+      read_a(t, 1, fa1);
+      mma_half(0, fa0, fb);
+      advance(t);
+      read_b(t + 1, nb);
+      read_a(t + 1, 0, na0);
+      mma_half(1, fa1, fb);
 #pragma unroll
-    for (int f = 0; f < MfmaOp<T>::kFrags; ++f) {
-      const int fo = (f * 4 + (lane >> 4)) * GT + (lane & 15);
-      v4u bf[4];
+      for (int i = 0; i < 4; ++i) {
+        fb[i] = nb[i];
+        fa0[i] = na0[i];
+      }
+    }
+    {
+      v4u fa1[4];
+      read_a(tb1 - 1, 1, fa1);
+      mma_half(0, fa0, fb);
+      mma_half(1, fa1, fb);
+    }
+  } else {
+    for (int t = tb0; t < tb1; ++t) {
+      // stage t complete; the stages issued after it (up to NS - 2) may still be
+      // in flight
+      switch (min(NS - 2, tb1 - 1 - t)) {
+        case 3: wait_vmem<3 * DPW>(); break;
+        case 2: wait_vmem<2 * DPW>(); break;
+        case 1: wait_vmem<DPW>(); break;
+        default: wait_vmem<0>(); break;
+      }
+      lds_barrier();  // every wave's part of stage t has landed; stage t-1 is free
+      if (t + NS - 1 < tb1) issue(t + NS - 1);
+      const v4u* l_ = (const v4u*)(smem + ((t - tb0) % NS) * STAGE_B);
 #pragma unroll
-      for (int b = 0; b < 4; ++b) bf[b] = l_[fo + wj * 64 + b * 16];
+      for (int f = 0; f < MfmaOp<T>::kFrags; ++f) {
+        const int fo = (f * 4 + (lane >> 4)) * GT + (lane & 15);
+        v4u bf[4];
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        v4u af[4];
+        for (int b = 0; b < 4; ++b) bf[b] = l_[fo + wj * 64 + b * 16];
 #pragma unroll
-        for (int a = 0; a < 4; ++a) af[a] = l_[CHUNKS + fo + wi * 128 + (4 * h2 + a) * 16];
+        for (int h2 = 0; h2 < 2; ++h2) {
+          v4u af[4];
 #pragma unroll
-        for (int a = 0; a < 4; ++a)
-#pragma unroll
-          for (int b = 0; b < 4; ++b) acc[4 * h2 + a][b] = MfmaOp<T>::mma(af[a], bf[b], acc[4 * h2 + a][b]);
-        if (HAS_LO && isg) {
-#pragma unroll
-          for (int a = 0; a < 4; ++a) af[a] = l_[2 * CHUNKS + fo + wi * 128 + (4 * h2 + a) * 16];
+          for (int a = 0; a < 4; ++a) af[a] = l_[CHUNKS + fo + wi * 128 + (4 * h2 + a) * 16];
 #pragma unroll
           for (int a = 0; a < 4; ++a)
 #pragma unroll
             for (int b = 0; b < 4; ++b) acc[4 * h2 + a][b] = MfmaOp<T>::mma(af[a], bf[b], acc[4 * h2 + a][b]);
+          if (HAS_LO && isg) {
+#pragma unroll
+            for (int a = 0; a < 4; ++a) af[a] = l_[2 * CHUNKS + fo + wi * 128 + (4 * h2 + a) * 16];
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+              for (int b = 0; b < 4; ++b) acc[4 * h2 + a][b] = MfmaOp<T>::mma(af[a], bf[b], acc[4 * h2 + a][b]);
+          }
         }
       }
     }
