@@ -38,6 +38,9 @@ R-lazy  the residual-correction term of the lazy batch update uses the value
         column (eager) sweep.
 R-sign  the residual is R = W (X_dense - Xh); Eq. 4 prints the opposite sign,
         which contradicts Eq. 3 and the update rule of Algorithm 1.
+R-order act_order (App. B) processes the channels by decreasing diag(H) of the
+        sparse stream, equal values in channel order; off unless asked for
+        (Algorithm 1 does not include it).
 """
 
 from __future__ import annotations
@@ -56,6 +59,7 @@ __all__ = [
     "select_block_mask",
     "sweep_eager",
     "sweep_blocked",
+    "act_order_perm",
     "prune_layer",
     "objective",
     "sparsegpt_layer",
@@ -355,15 +359,45 @@ def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=Non
 # Whole layer, objective and comparators
 # ---------------------------------------------------------------------------
 
+def act_order_perm(H):
+    """act_order (App. B, calibration settings): the columns are processed in
+    the order of decreasing Hessian diagonal, H = Xh^T Xh of the sparse stream
+    (reading R-order: largest first, as in the SparseGPT option the paper
+    names; equal diagonals keep their channel order).  Returns perm with
+    perm[i] = the channel processed i-th."""
+    d = np.diag(_f64(H))
+    k = d.shape[0]
+    return np.lexsort((np.arange(k), -d))
+
+
 def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 128,
-                X_dense=None, mask_in=None, blocked: bool = True, scores_out=None):
-    """DuoGPT on one linear layer: Alg. 1 end to end.  Returns a dict."""
+                X_dense=None, mask_in=None, blocked: bool = True, scores_out=None,
+                act_order: bool = False):
+    """DuoGPT on one linear layer: Alg. 1 end to end.  Returns a dict.
+
+    act_order=True permutes the channels by act_order_perm(H) before the
+    inverse Cholesky: W's columns, H's and G's rows and columns, a and a
+    forced mask all follow the permutation; blocks are formed in that order.
+    W_hat and keep come back in the original channel order; the returned H,
+    G, a are the unpermuted ones, while L, D, fac, b, c and the block scores
+    appended to scores_out belong to the permuted problem (perm alongside)."""
     H, G, a = hessian_terms(X_src, p_x, X_dense)
-    L, lam = inverse_cholesky(H, damp)
-    fac, D, (_, b, c) = score_terms(G, L, a)
+    W = _f64(W)
+    perm = None
+    Hs, Gs, As, Ws, Ms = H, G, a, W, _check_mask_in(mask_in, W.shape[0], W.shape[1])
+    if act_order:
+        perm = act_order_perm(H)
+        Hs, Gs, As, Ws = H[np.ix_(perm, perm)], G[np.ix_(perm, perm)], a[perm], W[:, perm]
+        if Ms is not None:
+            Ms = Ms[:, perm]
+    L, lam = inverse_cholesky(Hs, damp)
+    fac, D, (_, b, c) = score_terms(Gs, L, As)
     sweep = sweep_blocked if blocked else sweep_eager
-    W_hat, keep = sweep(W, L, D, fac, p_w, B, mask_in=mask_in, scores_out=scores_out)
-    return dict(W_hat=W_hat, keep=keep, H=H, G=G, a=a, b=b, c=c, L=L, lam=lam, fac=fac, D=D)
+    W_hat, keep = sweep(Ws, L, D, fac, p_w, B, mask_in=Ms, scores_out=scores_out)
+    if act_order:
+        inv = np.argsort(perm)
+        W_hat, keep = W_hat[:, inv], keep[:, inv]
+    return dict(W_hat=W_hat, keep=keep, H=H, G=G, a=a, b=b, c=c, L=L, lam=lam, fac=fac, D=D, perm=perm)
 
 
 def objective(W, W_hat, X_src, p_x: float, X_dense=None):

@@ -459,3 +459,77 @@ def test_window_terms_trailing_block(t):
     for i, p in enumerate(range(k - t, k)):
         _, val = _ridge(Xh[:, p + 1:], Xd[:, p], lam)
         assert abs(facw[i] - (lam + val)) <= 1e-8 * facw[i]
+
+
+# ---------------------------------------------------------------------------
+# act_order (App. B, calibration settings): channels by decreasing diag(H)
+# ---------------------------------------------------------------------------
+
+def test_act_order_perm_direction_and_ties():
+    """Closed form: largest diagonal first, equal diagonals in channel order."""
+    H = np.diag([1.0, 3.0, 3.0, 0.0, 2.0, 3.0])
+    H[0, 1] = H[1, 0] = 0.5  # off-diagonal entries play no part
+    assert R.act_order_perm(H).tolist() == [1, 2, 5, 4, 0, 3]
+
+
+def test_act_order_is_identity_for_sorted_diagonal():
+    """When diag(H) already decreases, act_order changes nothing (bitwise)."""
+    rng = np.random.default_rng(70)
+    k, n, m = 40, 12, 256
+    X = rng.standard_normal((m, k))
+    X *= np.sqrt((k - np.arange(k)) / np.sum(X * X, axis=0))  # column c: |x_c|^2 = k - c
+    W = 0.02 * rng.standard_normal((n, k))
+    H, _, _ = R.hessian_terms(X, 0.0)
+    assert np.all(np.diff(np.diag(H)) < 0)  # precondition of the pin
+    a = R.prune_layer(W, X, 0.0, 0.5, B=8)
+    b = R.prune_layer(W, X, 0.0, 0.5, B=8, act_order=True)
+    assert b["perm"].tolist() == list(range(k))
+    assert np.array_equal(a["keep"], b["keep"])
+    assert np.array_equal(a["W_hat"], b["W_hat"])
+
+
+@pytest.mark.parametrize("seed", [71, 72])
+def test_act_order_channel_permutation_invariance(seed):
+    """With act_order the result no longer depends on how the input channels
+    are numbered (no ties): relabelling the channels of W and X relabels the
+    output the same way.  Without act_order the result does depend on it."""
+    W, X = _layer(seed, 10, 48, 200, scale_sigma=1.0)
+    pi = np.random.default_rng(seed + 100).permutation(48)
+    a = R.prune_layer(W, X, 0.5, 0.5, B=16, act_order=True)
+    b = R.prune_layer(W[:, pi], X[:, pi], 0.5, 0.5, B=16, act_order=True)
+    assert np.array_equal(a["keep"][:, pi], b["keep"])
+    np.testing.assert_allclose(b["W_hat"], a["W_hat"][:, pi], rtol=1e-9, atol=1e-12)
+    c = R.prune_layer(W, X, 0.5, 0.5, B=16)
+    d = R.prune_layer(W[:, pi], X[:, pi], 0.5, 0.5, B=16)
+    assert not np.allclose(d["W_hat"], c["W_hat"][:, pi], rtol=1e-6, atol=1e-9)
+
+
+def test_act_order_lazy_equals_eager():
+    W, X = _layer(73, 9, 40, 180, scale_sigma=1.0)
+    a = R.prune_layer(W, X, 0.5, 0.5, B=8, act_order=True)
+    b = R.prune_layer(W, X, 0.5, 0.5, B=8, act_order=True, blocked=False)
+    assert np.array_equal(a["keep"], b["keep"])
+    np.testing.assert_allclose(a["W_hat"], b["W_hat"], rtol=1e-9, atol=1e-13)
+
+
+def test_act_order_forced_mask_follows_channels():
+    """A forced mask is given in the original channel order."""
+    W, X = _layer(74, 8, 32, 160, scale_sigma=1.0)
+    a = R.prune_layer(W, X, 0.5, 0.5, B=8, act_order=True)
+    b = R.prune_layer(W, X, 0.5, 0.5, B=8, act_order=True, mask_in=a["keep"])
+    assert np.array_equal(a["keep"], b["keep"])
+    np.testing.assert_allclose(a["W_hat"], b["W_hat"], rtol=1e-12, atol=1e-15)
+
+
+def test_act_order_equals_plain_method_on_reordered_channels():
+    """act_order = the plain method (pinned above) run on the channels listed
+    in act_order_perm order, relabelled back."""
+    W, X = _layer(75, 10, 48, 200, scale_sigma=1.0)
+    a = R.prune_layer(W, X, 0.5, 0.5, B=16, act_order=True)
+    H, _, _ = R.hessian_terms(X, 0.5)
+    perm = R.act_order_perm(H)
+    assert np.array_equal(a["perm"], perm)
+    b = R.prune_layer(W[:, perm], X[:, perm], 0.5, 0.5, B=16)
+    inv = np.argsort(perm)
+    assert np.array_equal(a["keep"], b["keep"][:, inv])
+    np.testing.assert_allclose(a["W_hat"], b["W_hat"][:, inv], rtol=1e-9, atol=1e-12)
