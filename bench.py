@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama2_7b_q_proj")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--act-order", action="store_true",
+                    help="process channels by decreasing Hessian diagonal (App. B); adds the gathers to the step")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a device-to-device copy of MIB MiB (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -201,13 +203,33 @@ def main():
     lowp = torch.empty((n, k), dtype=W.dtype, device=dev)
     mask = torch.empty((n, (k + 31) // 32), dtype=torch.int32, device=dev)
 
+    if args.act_order:
+        hdiag = torch.zeros(k, dtype=torch.float64, device=dev)
+        Hp, Gp = torch.empty_like(H), torch.empty_like(G)
+        ap_, Wp = torch.empty((1, k), dtype=torch.float32, device=dev), torch.empty_like(W)
+        W_out_p, lowp_p, mask_p = torch.empty_like(W_out), torch.empty_like(lowp), torch.empty_like(mask)
+
     def step(check=False):
         H.zero_()
         G.zero_()
         a.zero_()
-        duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h)
-        info = duo.duo_chol_inv(H, c["damp"], ws=ws_c, sync=check)
-        duo.duo_prune_layer(W, H, G, a, c["p_w"], B, ws=ws_p, out=(W_out, lowp, mask, None))
+        if not args.act_order:
+            duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h)
+            info = duo.duo_chol_inv(H, c["damp"], ws=ws_c, sync=check)
+            duo.duo_prune_layer(W, H, G, a, c["p_w"], B, ws=ws_p, out=(W_out, lowp, mask, None))
+            return info
+        hdiag.zero_()
+        duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h, hdiag=hdiag)
+        perm, inv = duo.duo_act_order(hdiag)
+        duo.duo_permute(H, perm, perm, out=Hp)
+        duo.duo_permute(G, perm, perm, out=Gp)
+        duo.duo_permute(a.view(1, k), None, perm, out=ap_)
+        duo.duo_permute(W, None, perm, out=Wp)
+        info = duo.duo_chol_inv(Hp, c["damp"], ws=ws_c, sync=check)
+        duo.duo_prune_layer(Wp, Hp, Gp, ap_.view(k), c["p_w"], B, ws=ws_p, out=(W_out_p, lowp_p, mask_p, None))
+        duo.duo_permute(W_out_p, None, inv, out=W_out)
+        duo.duo_permute(lowp_p, None, inv, out=lowp)
+        duo.duo_permute_mask(mask_p, k, inv, out=mask)
         return info
 
     lam, fail = step(check=True)  # also checks that the damped Hessian factors
@@ -265,7 +287,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "n": n, "k": k, "m": m, "p_x": c["p_x"], "p_w": c["p_w"],
                    "block": B, "damp": c["damp"], "x_dtype": str(c["x_dtype"]).replace("torch.", ""),
-                   "inputs": c["kind"], "parallelism": "single GPU"},
+                   "inputs": c["kind"], "act_order": bool(args.act_order), "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "gram_kernel (H, G)", "achieved": gram_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": gram_tflops / PEAK_BF16_TFLOPS,
                      "traffic": gram_traffic(args.workload), "ms_per_launch": per("gram"), "flop_per_launch": gram_flop_step / gram_launches},

@@ -123,8 +123,11 @@ duo_status duo_act_sparsify_mask(const void* X, int32_t x_dtype, int64_t m, int6
  *   H        k x k fp32, ldh: H += Xh^T Xh over the m tokens (both triangles).
  *   G, a     optional (both NULL or both set): G += dX^T Xh with dX = X_dense - Xh,
  *            a[p] += sum_t dX[t][p]^2.  G is k x k fp32 with row stride ldg.
- *   The caller zeroes H, G and a before the first token chunk; further calls
- *   add more tokens (raw sums, no 1/m scaling).  For X_src != X_dense, dX is
+ *   hdiag    NULL or k doubles: hdiag[p] += sum_t Xh[t][p]^2 summed in fp64
+ *            (each square exact), the diagonal of H at the precision that
+ *            decides the act_order channel order (duo_act_order).
+ *   The caller zeroes H, G, a and hdiag before the first token chunk; further
+ *   calls add more tokens (raw sums, no 1/m scaling).  For X_src != X_dense, dX is
  *   represented to ~16 significant bits inside the product (exact when the
  *   two streams' values are within a factor of 2^7 of each other or the entry
  *   is dropped); a is accumulated from exact fp32 differences.
@@ -132,8 +135,8 @@ duo_status duo_act_sparsify_mask(const void* X, int32_t x_dtype, int64_t m, int6
  */
 duo_status duo_hessian_accum(const void* X_src, const void* X_dense, int32_t x_dtype, int64_t m,
                              int64_t k, int64_t ldx, duo_act_rule rule, float* H, int64_t ldh,
-                             float* G, int64_t ldg, float* a, void* ws, size_t ws_bytes,
-                             void* stream);
+                             float* G, int64_t ldg, float* a, double* hdiag, void* ws,
+                             size_t ws_bytes, void* stream);
 
 /*
  * duo_residual_term - stage 1, residual part only (Sec. 4.3: G = dX Xh^T,
@@ -202,6 +205,43 @@ duo_status duo_sweep(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
                      double w_sparsity, int32_t block, const uint32_t* mask_in, float* W_out,
                      void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws,
                      size_t ws_bytes, void* stream);
+
+/*
+ * act_order (App. B, calibration settings: the weight columns are processed
+ * in the order of decreasing Hessian diagonal; off in Algorithm 1 as printed).
+ * A layer is pruned with act_order by running the stages on its channels in
+ * that order: H and G permuted on both sides, a, the columns of W and of a
+ * forced mask permuted, then W_out, W_out_lowp and mask_out permuted back.
+ *
+ * duo_act_order - the order.
+ *   hdiag    k doubles from duo_hessian_accum.
+ *   perm     k int32: perm[i] = the channel processed i-th (decreasing
+ *            hdiag, equal values in channel order; NaN and +inf first).
+ *   inv_perm NULL or k int32: inv_perm[perm[i]] = i.
+ */
+duo_status duo_act_order(const double* hdiag, int64_t k, int32_t* perm, int32_t* inv_perm, void* stream);
+
+/*
+ * duo_permute - gather: dst[i][j] = src[r][c], r = row_idx ? row_idx[i] : i,
+ *   c = col_idx ? col_idx[j] : j, for i < rows, j < cols.
+ *   src      src_rows x src_cols, row stride lds, dtype DUO_F32 or DUO_BF16.
+ *   row_idx  NULL or rows int32; col_idx NULL or cols int32.  An index
+ *            outside the source writes 0 (no access outside src is made).
+ *   dst      rows x cols, row stride ldd, same dtype; must not alias src.
+ *   rows <= 65535.
+ */
+duo_status duo_permute(const void* src, int32_t dtype, int64_t src_rows, int64_t src_cols, int64_t lds,
+                       const int32_t* row_idx, const int32_t* col_idx, int64_t rows, int64_t cols, void* dst,
+                       int64_t ldd, void* stream);
+
+/*
+ * duo_permute_mask - column gather of a bit-packed mask (n x ceil(k/32)
+ *   uint32 words, bit c of word c/32 = column c): bit j of dst row r = bit
+ *   col_idx[j] of src row r (0 for an index outside [0, k)).  col_idx holds
+ *   k int32; dst must not alias src.
+ */
+duo_status duo_permute_mask(const uint32_t* src, int64_t n, int64_t k, const int32_t* col_idx, uint32_t* dst,
+                            void* stream);
 
 /*
  * duo_prune_layer - stage 3 in one call: duo_score_terms then duo_sweep, with

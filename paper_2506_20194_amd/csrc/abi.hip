@@ -127,7 +127,7 @@ duo_status duo_act_sparsify_mask(const void* X, int32_t x_dtype, int64_t m, int6
 
 static duo_status hessian_common(const void* X_src, const void* X_dense, int32_t x_dtype, int64_t m, int64_t k,
                                  int64_t ldx, duo_act_rule rule, float* H, int64_t ldh, float* G, int64_t ldg,
-                                 float* a, void* ws, size_t ws_bytes, void* stream, bool want_h) {
+                                 float* a, double* hdiag, void* ws, size_t ws_bytes, void* stream, bool want_h) {
   if (!dtype_ok(x_dtype) || m < 0 || !rule_ok(rule)) return DUO_ERR_INVALID_ARG;
   if (!k_ok(k)) return k < 1 ? DUO_ERR_INVALID_ARG : DUO_ERR_UNSUPPORTED;
   if (ldx < k) return DUO_ERR_INVALID_ARG;
@@ -142,16 +142,17 @@ static duo_status hessian_common(const void* X_src, const void* X_dense, int32_t
   duo_status d = device_ok();
   if (d != DUO_OK) return d;
   prof_begin(DUO_PROF_HESSIAN, (hipStream_t)stream);
-  duo_status r = hessian_run(X_src, X_dense, x_dtype, m, k, ldx, zero_count(rule, k), H, ldh, G, ldg, a, ws,
-                             want_h, (hipStream_t)stream);
+  duo_status r = hessian_run(X_src, X_dense, x_dtype, m, k, ldx, zero_count(rule, k), H, ldh, G, ldg, a, hdiag,
+                             ws, want_h, (hipStream_t)stream);
   prof_end(DUO_PROF_HESSIAN, (hipStream_t)stream);
   return r;
 }
 
 duo_status duo_hessian_accum(const void* X_src, const void* X_dense, int32_t x_dtype, int64_t m, int64_t k,
                              int64_t ldx, duo_act_rule rule, float* H, int64_t ldh, float* G, int64_t ldg, float* a,
-                             void* ws, size_t ws_bytes, void* stream) {
-  return hessian_common(X_src, X_dense, x_dtype, m, k, ldx, rule, H, ldh, G, ldg, a, ws, ws_bytes, stream, true);
+                             double* hdiag, void* ws, size_t ws_bytes, void* stream) {
+  return hessian_common(X_src, X_dense, x_dtype, m, k, ldx, rule, H, ldh, G, ldg, a, hdiag, ws, ws_bytes, stream,
+                        true);
 }
 
 duo_status duo_residual_term(const void* X_dense, const void* X_src, int32_t x_dtype, int64_t m, int64_t k,
@@ -160,7 +161,8 @@ duo_status duo_residual_term(const void* X_dense, const void* X_src, int32_t x_d
   if (!G || !a) return DUO_ERR_INVALID_ARG;
   if (m > 0 && !X_dense) return DUO_ERR_INVALID_ARG;
   const void* src = X_src ? X_src : X_dense;
-  return hessian_common(src, X_dense, x_dtype, m, k, ldx, rule, nullptr, k, G, ldg, a, ws, ws_bytes, stream, false);
+  return hessian_common(src, X_dense, x_dtype, m, k, ldx, rule, nullptr, k, G, ldg, a, nullptr, ws, ws_bytes, stream,
+                        false);
 }
 
 duo_status duo_chol_inv(float* H_inout, int64_t k, int64_t ldh, double damp_ratio, duo_chol_info* info, void* ws,

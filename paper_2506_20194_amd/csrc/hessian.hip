@@ -860,6 +860,44 @@ int gram_split(int64_t ntiles) {
   return best;
 }
 
+// Diagonal of H in fp64 for act_order: hdiag[c] += sum_t Xh[t][c]^2, read
+// from the packed operand.  Each square is exact in fp64; the sum runs in a
+// fixed order (token slices in sequence), so the result is deterministic and
+// within a few fp64 ulps of the exact value, which lets the channel order be
+// decided identically on any implementation that sums in fp64.
+template <typename T>
+__global__ __launch_bounds__(256) void hdiag_part_kernel(const T* __restrict__ Ph, int kp, int ntb, int slice_len,
+                                                         double* __restrict__ dpart) {
+  constexpr int EPG = 16 / (int)sizeof(T);
+  constexpr int NG = kTokBlk / EPG;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int tb0 = blockIdx.y * slice_len;
+  const int tb1 = min(ntb, tb0 + slice_len);
+  if (c >= kp) return;
+  double s = 0.0;
+  for (int tb = tb0; tb < tb1; ++tb)
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const uint4 v = *(const uint4*)(Ph + (((int64_t)tb * NG + g) * kp + c) * EPG);
+      const T* e = (const T*)&v;
+#pragma unroll
+      for (int i = 0; i < EPG; ++i) {
+        const double x = (double)Elem<T>::to_f32(e[i]);
+        s = fma(x, x, s);
+      }
+    }
+  dpart[(int64_t)blockIdx.y * kp + c] = s;
+}
+
+__global__ void hdiag_reduce_kernel(const double* __restrict__ dpart, int nsl, int kp, int k,
+                                    double* __restrict__ hdiag) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= k) return;
+  double s = 0.0;
+  for (int i = 0; i < nsl; ++i) s += dpart[(int64_t)i * kp + c];
+  hdiag[c] += s;
+}
+
 struct HessWs {
   int64_t* thr;
   uint8_t* Ph;
@@ -867,8 +905,19 @@ struct HessWs {
   uint8_t* Pl;
   float* apart;
   float* part;
+  double* dpart;
   size_t bytes;
 };
+
+// token slices of the fp64 diagonal (act_order): at most kDiagSlices, and at
+// most 2^21 partial sums in all
+constexpr int kDiagSlices = 64;
+static int diag_slices(int64_t kp, int ntb) {
+  int64_t n = (int64_t(1) << 21) / kp;
+  if (n > kDiagSlices) n = kDiagSlices;
+  if (n > ntb) n = ntb;
+  return n < 1 ? 1 : (int)n;
+}
 
 static HessWs carve_hessian(void* ws, int64_t m, int64_t k) {
   const int64_t ch = hessian_chunk_tokens(m, k);
@@ -885,6 +934,7 @@ static HessWs carve_hessian(void* ws, int64_t m, int64_t k) {
   h.Pl = c.take<uint8_t>((size_t)tokp * kp * 2);  // low part exists for bf16 only
   h.apart = c.take<float>((size_t)(tokp / 256) * kp);
   h.part = c.take<float>(nseg > 1 ? (size_t)nseg * ntiles * GT * GT : 1);
+  h.dpart = c.take<double>((size_t)diag_slices(kp, kDiagSlices) * kp);
   h.bytes = c.off;
   return h;
 }
@@ -907,7 +957,8 @@ static duo_status launch_gram(const GramArgs<T>& A, hipStream_t s) {
 
 template <typename T>
 static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, int64_t ldx, int z, float* H,
-                                int64_t ldh, float* G, int64_t ldg, float* a, void* ws, bool want_h, hipStream_t s) {
+                                int64_t ldh, float* G, int64_t ldg, float* a, double* hdiag, void* ws, bool want_h,
+                                hipStream_t s) {
   const bool want_g = G != nullptr;
   const bool two = Xd != nullptr && Xd != Xs;
   const bool lo = two && sizeof(T) == 2;
@@ -946,6 +997,17 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
                          (T*)w.Ph, (T*)w.Pz, (T*)w.Pl, want_g ? w.apart : nullptr);
   packed:
     DUO_LAUNCH_CHECK();
+    if (hdiag) {
+      const int ntb = (int)cdiv(mc, kTokBlk);
+      const int nsl = diag_slices(kp, ntb);
+      const int slen = (int)cdiv(ntb, nsl);
+      hipLaunchKernelGGL(hdiag_part_kernel<T>, dim3((unsigned)(kp / 256), (unsigned)nsl), dim3(256), 0, s,
+                         (const T*)w.Ph, (int)kp, ntb, slen, w.dpart);
+      DUO_LAUNCH_CHECK();
+      hipLaunchKernelGGL(hdiag_reduce_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, (const double*)w.dpart,
+                         nsl, (int)kp, (int)k, hdiag);
+      DUO_LAUNCH_CHECK();
+    }
     if (want_g) {
       hipLaunchKernelGGL(a_reduce_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.apart, (int)cdiv(mc, 256),
                          (int)kp, (int)k, a);
@@ -984,13 +1046,13 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
 }
 
 duo_status hessian_run(const void* Xs, const void* Xd, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z,
-                       float* H, int64_t ldh, float* G, int64_t ldg, float* a, void* ws, bool want_h,
+                       float* H, int64_t ldh, float* G, int64_t ldg, float* a, double* hdiag, void* ws, bool want_h,
                        hipStream_t s) {
   if (dtype == DUO_BF16)
     return hessian_typed<uint16_t>((const uint16_t*)Xs, (const uint16_t*)Xd, m, k, ldx, z, H, ldh, G, ldg, a,
-                                   ws, want_h, s);
-  return hessian_typed<float>((const float*)Xs, (const float*)Xd, m, k, ldx, z, H, ldh, G, ldg, a, ws, want_h,
-                              s);
+                                   hdiag, ws, want_h, s);
+  return hessian_typed<float>((const float*)Xs, (const float*)Xd, m, k, ldx, z, H, ldh, G, ldg, a, hdiag, ws,
+                              want_h, s);
 }
 
 duo_status act_mask_run(const void* X, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z, uint32_t* mask,

@@ -14,7 +14,7 @@ int64_t hessian_chunk_tokens(int64_t m, int64_t k);
 int gram_split(int64_t npairs);
 size_t hessian_ws_bytes(int64_t m, int64_t k);
 duo_status hessian_run(const void* Xs, const void* Xd, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z,
-                       float* H, int64_t ldh, float* G, int64_t ldg, float* a, void* ws, bool want_h,
+                       float* H, int64_t ldh, float* G, int64_t ldg, float* a, double* hdiag, void* ws, bool want_h,
                        hipStream_t s);
 // DUO_OK when the current device is a gfx950 (cached per device), else
 // DUO_ERR_NO_DEVICE (or DUO_ERR_UNSUPPORTED for a device index >= 64).

@@ -27,7 +27,8 @@ EXPORTED = (
     "duo_workspace_size", "duo_status_string", "duo_version", "duo_act_sparsify_mask",
     "duo_hessian_accum", "duo_residual_term", "duo_chol_inv", "duo_score_terms", "duo_sweep",
     "duo_prune_layer", "duo_profile_enable", "duo_profile_read", "duo_block_workspace_size", "duo_rmsnorm",
-    "duo_act_sparsify", "duo_linear", "duo_rope", "duo_attention", "duo_silu_mul",
+    "duo_act_sparsify", "duo_linear", "duo_rope", "duo_attention", "duo_silu_mul", "duo_act_order",
+    "duo_permute", "duo_permute_mask",
 )
 PROF = dict(gram=0, hessian=1, chol=2, score=3, sweep=4, inblock=5, trail=6, select=7)
 DUO_BOP_ACT_SPARSIFY, DUO_BOP_LINEAR, DUO_BOP_ATTENTION = 0, 1, 2
@@ -71,7 +72,7 @@ def lib():
         L.duo_act_sparsify_mask.restype = I32
         L.duo_act_sparsify_mask.argtypes = [P, I32, I64, I64, I64, ActRule, P, P, SZ, P]
         L.duo_hessian_accum.restype = I32
-        L.duo_hessian_accum.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, I64, P, P, SZ, P]
+        L.duo_hessian_accum.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, I64, P, P, P, SZ, P]
         L.duo_residual_term.restype = I32
         L.duo_residual_term.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, P, SZ, P]
         L.duo_chol_inv.restype = I32
@@ -96,6 +97,12 @@ def lib():
         L.duo_attention.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, I64, P, SZ, P]
         L.duo_silu_mul.restype = I32
         L.duo_silu_mul.argtypes = [P, P, I64, I64, I64, P, I64, P]
+        L.duo_act_order.restype = I32
+        L.duo_act_order.argtypes = [P, I64, P, P, P]
+        L.duo_permute.restype = I32
+        L.duo_permute.argtypes = [P, I32, I64, I64, I64, P, P, I64, I64, P, I64, P]
+        L.duo_permute_mask.restype = I32
+        L.duo_permute_mask.argtypes = [P, I64, I64, P, P, P]
         L.duo_profile_enable.restype = I32
         L.duo_profile_enable.argtypes = [I32]
         L.duo_profile_read.restype = I32
@@ -190,20 +197,24 @@ def duo_act_sparsify_mask(X, act_sparsity, mask_out=None, ws=None):
     return mask_out
 
 
-def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=None):
+def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=None, hdiag=None):
     m, k = X_src.shape
-    _same_device(X_src, X_dense, H, G, a, ws)
+    _same_device(X_src, X_dense, H, G, a, ws, hdiag)
     _shape(H, (k, k), "H")
     _shape(G, (k, k), "G")
     _shape(a, (k,), "a")
     _contig(a, "a")
+    _shape(hdiag, (k,), "hdiag")
+    _contig(hdiag, "hdiag")
+    if hdiag is not None and hdiag.dtype != torch.float64:
+        raise TypeError("hdiag must be float64")
     if ws is None:
         ws = workspace(DUO_OP_HESSIAN, 0, k, m, 0, X_src.device)
     if X_dense is not None and (X_dense.shape != X_src.shape or X_dense.stride() != X_src.stride()):
         raise ValueError("X_dense must have the shape and strides of X_src")
     st = lib().duo_hessian_accum(_ptr(X_src), _ptr(X_dense), _dtype(X_src), m, k, _ld(X_src), act_rule(act_sparsity),
-                                 _ptr(H), _ld(H), _ptr(G), _ld(G) if G is not None else k, _ptr(a), _ptr(ws),
-                                 ws.numel(), _stream(X_src.device))
+                                 _ptr(H), _ld(H), _ptr(G), _ld(G) if G is not None else k, _ptr(a), _ptr(hdiag),
+                                 _ptr(ws), ws.numel(), _stream(X_src.device))
     _check(st, "duo_hessian_accum")
 
 
@@ -346,22 +357,92 @@ def unpack_mask(words: torch.Tensor, k: int) -> torch.Tensor:
     return bits.reshape(words.shape[0], -1)[:, :k].bool()
 
 
-def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=None, want_lowp=True):
+def duo_act_order(hdiag):
+    """act_order channel order from duo_hessian_accum's fp64 diagonal:
+    returns (perm, inv_perm), int32 on hdiag's device."""
+    k = hdiag.shape[0]
+    if hdiag.dtype != torch.float64 or hdiag.dim() != 1:
+        raise TypeError("hdiag must be a 1-D float64 tensor")
+    _contig(hdiag, "hdiag")
+    perm = torch.empty(k, dtype=torch.int32, device=hdiag.device)
+    inv = torch.empty(k, dtype=torch.int32, device=hdiag.device)
+    _check(lib().duo_act_order(_ptr(hdiag), k, _ptr(perm), _ptr(inv), _stream(hdiag.device)), "duo_act_order")
+    return perm, inv
+
+
+def _idx(t, n, name):
+    if t is None:
+        return None
+    if t.dtype != torch.int32 or t.dim() != 1 or t.shape[0] != n:
+        raise ValueError(f"{name} must be int32 of length {n}")
+    _contig(t, name)
+    return t
+
+
+def duo_permute(src, row_idx=None, col_idx=None, out=None):
+    """out[i][j] = src[row_idx[i]][col_idx[j]] (either index may be None =
+    identity) for a 2-D fp32 or bf16 tensor with unit column stride."""
+    if src.dim() != 2 or src.stride(1) != 1:
+        raise ValueError("src must be 2-D with unit column stride")
+    rows = row_idx.shape[0] if row_idx is not None else src.shape[0]
+    cols = col_idx.shape[0] if col_idx is not None else src.shape[1]
+    _idx(row_idx, rows, "row_idx")
+    _idx(col_idx, cols, "col_idx")
+    if out is None:
+        out = torch.empty((rows, cols), dtype=src.dtype, device=src.device)
+    _shape(out, (rows, cols), "out")
+    _same_device(src, row_idx, col_idx, out)
+    st = lib().duo_permute(_ptr(src), _dtype(src), src.shape[0], src.shape[1], _ld(src), _ptr(row_idx),
+                           _ptr(col_idx), rows, cols, _ptr(out), _ld(out), _stream(src.device))
+    _check(st, "duo_permute")
+    return out
+
+
+def duo_permute_mask(words, k, col_idx, out=None):
+    """Column gather of a bit-packed n x ceil(k/32) mask (int32 words)."""
+    n = words.shape[0]
+    _idx(col_idx, k, "col_idx")
+    _contig(words, "mask")
+    if out is None:
+        out = torch.empty_like(words)
+    _same_device(words, col_idx, out)
+    _check(lib().duo_permute_mask(_ptr(words), n, k, _ptr(col_idx), _ptr(out), _stream(words.device)),
+           "duo_permute_mask")
+    return out
+
+
+def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=None, want_lowp=True,
+                 act_order=False):
     """DuoGPT on one linear layer (stages 1-3 on the device).
 
     W: n x k (out x in), X: m x k token-major calibration input of the pruned
     stream (sparsified per token), X_dense: the dense stream (defaults to X).
-    Returns dict(W_out fp32, W_lowp in W's dtype, mask (bool n x k), lam).
+    act_order: process the channels by decreasing Hessian diagonal (App. B);
+    the outputs are returned in the original channel order.
+    Returns dict(W_out fp32, W_lowp in W's dtype, mask (bool n x k), lam, and
+    perm when act_order).
     """
     n, k = W.shape
     dev = W.device
     H = torch.zeros((k, k), dtype=torch.float32, device=dev)
     G = torch.zeros((k, k), dtype=torch.float32, device=dev)
     a = torch.zeros(k, dtype=torch.float32, device=dev)
-    duo_hessian_accum(X, H, act_sparsity, X_dense=X_dense, G=G, a=a)
+    hdiag = torch.zeros(k, dtype=torch.float64, device=dev) if act_order else None
+    duo_hessian_accum(X, H, act_sparsity, X_dense=X_dense, G=G, a=a, hdiag=hdiag)
+    perm = None
+    if act_order:
+        perm, inv = duo_act_order(hdiag)
+        H = duo_permute(H, perm, perm)
+        G = duo_permute(G, perm, perm)
+        a = duo_permute(a.view(1, k), None, perm).view(k)
+        W = duo_permute(W, None, perm)
     lam, _ = duo_chol_inv(H, damp)
     W_out, lowp, mask, _ = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp)
-    return dict(W_out=W_out, W_lowp=lowp, mask=unpack_mask(mask, k), lam=lam)
+    if act_order:
+        W_out = duo_permute(W_out, None, inv)
+        lowp = duo_permute(lowp, None, inv) if lowp is not None else None
+        mask = duo_permute_mask(mask, k, inv)
+    return dict(W_out=W_out, W_lowp=lowp, mask=unpack_mask(mask, k), lam=lam, perm=perm)
 
 
 # ---------------------------------------------------------------------------

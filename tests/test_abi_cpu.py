@@ -65,8 +65,8 @@ def test_hessian_argument_errors(duo_lib):
     big = 10 ** 10
 
     def call(X=FAKE, Xd=None, dt=1, m=64, k=32, ldx=32, rule=None, H=FAKE, ldh=32, G=None, ldg=32, a=None, ws=WS,
-             wsb=big):
-        return L.duo_hessian_accum(X, Xd, dt, m, k, ldx, rule or _rule(), H, ldh, G, ldg, a, ws, wsb, None)
+             wsb=big, hdiag=None):
+        return L.duo_hessian_accum(X, Xd, dt, m, k, ldx, rule or _rule(), H, ldh, G, ldg, a, hdiag, ws, wsb, None)
 
     assert call() == NODEV
     assert call(X=None) == E
@@ -86,6 +86,7 @@ def test_hessian_argument_errors(duo_lib):
     assert call(wsb=16) == duo_lib.DUO_ERR_WORKSPACE
     assert call(ws=ctypes.c_void_p((256 << 20) + 8)) == duo_lib.DUO_ERR_WORKSPACE
     assert call(m=0) == duo_lib.DUO_OK           # nothing to do, nothing enqueued
+    assert call(hdiag=FAKE) == NODEV
     assert L.duo_residual_term(None, None, 1, 64, 32, 32, _rule(), FAKE, 32, FAKE, WS, big, None) == E
     assert L.duo_residual_term(FAKE, None, 1, 64, 32, 32, _rule(), FAKE, 32, FAKE, WS, big, None) == NODEV
 
@@ -160,3 +161,34 @@ def test_block_harness_argument_errors(duo_lib):
     assert L.duo_silu_mul(FAKE, FAKE, 8, 64, 32, FAKE, 64, None) == E
     assert L.duo_block_workspace_size(99, 1, 1, 1) == 0
     assert L.duo_block_workspace_size(duo_lib.DUO_BOP_ACT_SPARSIFY, 100, 0, 0) >= 800
+
+
+def test_act_order_argument_errors(duo_lib):
+    L = duo_lib.lib()
+    E, NODEV = duo_lib.DUO_ERR_INVALID_ARG, duo_lib.DUO_ERR_NO_DEVICE
+    assert L.duo_act_order(FAKE, 64, FAKE, None, None) == NODEV
+    assert L.duo_act_order(None, 64, FAKE, None, None) == E
+    assert L.duo_act_order(FAKE, 64, None, None, None) == E
+    assert L.duo_act_order(FAKE, 0, FAKE, None, None) == E
+    assert L.duo_act_order(FAKE, 40000, FAKE, None, None) == duo_lib.DUO_ERR_UNSUPPORTED
+    OTHER = ctypes.c_void_p(FAKE.value + (1 << 20))
+
+    def perm(src=FAKE, dt=0, sr=8, sc=16, lds=16, ri=None, ci=None, r=8, c=16, dst=OTHER, ldd=16):
+        return L.duo_permute(src, dt, sr, sc, lds, ri, ci, r, c, dst, ldd, None)
+
+    assert perm() == NODEV
+    assert perm(ri=FAKE, ci=FAKE, r=100, c=100, ldd=100) == NODEV  # gathers may change the shape
+    assert perm(dt=5) == E
+    assert perm(lds=15) == E
+    assert perm(ldd=15) == E
+    assert perm(r=9) == E                      # more rows than the source without an index
+    assert perm(c=17, ldd=17) == E
+    assert perm(dst=FAKE) == E                 # in place
+    assert perm(src=None) == E
+    assert perm(r=0) == duo_lib.DUO_OK
+    assert perm(ri=FAKE, r=70000) == duo_lib.DUO_ERR_UNSUPPORTED
+    assert L.duo_permute_mask(FAKE, 8, 64, FAKE, OTHER, None) == NODEV
+    assert L.duo_permute_mask(FAKE, 8, 64, None, OTHER, None) == E
+    assert L.duo_permute_mask(FAKE, 8, 64, FAKE, FAKE, None) == E
+    assert L.duo_permute_mask(FAKE, -1, 64, FAKE, OTHER, None) == E
+    assert L.duo_permute_mask(FAKE, 0, 64, FAKE, OTHER, None) == duo_lib.DUO_OK
