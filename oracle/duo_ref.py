@@ -276,6 +276,24 @@ def select_block_mask(S, z: int):
     return keep.reshape(Bb, n).T
 
 
+def select_nm_mask(S, N: int):
+    """Keep-mask of an n x M score group with the N lowest scores of every row
+    removed, equal scores in column order (the N:M variant of App. B)."""
+    S = _f64(S)
+    order = np.argsort(S, axis=1, kind="stable")
+    keep = np.ones(S.shape, dtype=bool)
+    keep[np.arange(S.shape[0])[:, None], order[:, :N]] = False
+    return keep
+
+
+def _check_nm(nm, k: int, B: int):
+    if nm is None:
+        return None
+    N, M = nm
+    assert 0 <= N <= M and k % M == 0 and B % M == 0, "N:M needs M | k and M | B"
+    return N, M
+
+
 # ---------------------------------------------------------------------------
 # Column sweep: definition (eager) and Algorithm 1 (blocked, lazy batches)
 # ---------------------------------------------------------------------------
@@ -288,41 +306,15 @@ def _check_mask_in(mask_in, n, k):
     return mask_in
 
 
-def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None):
+def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None):
     """Column sweep with every column's update applied to all later columns at once.
 
     Processing column j: w0 = W[:, j]; p = w0 * m_j; e = (w0 - p) / L_jj and
     every later column j' gets  W[:, j'] -= e * L[j', j] - w0 * D[j, j'].
     The mask of each block is chosen when the sweep reaches the block, from
-    S = W[:, blk]^2 * fac[blk].  Returns (W_hat, keep).
-    """
-    W = _f64(W).copy()
-    L = _f64(L)
-    D = _f64(D)
-    fac = _f64(fac)
-    n, k = W.shape
-    mask_in = _check_mask_in(mask_in, n, k)
-    keep = np.ones((n, k), dtype=bool)
-    counts = block_prune_counts(n, k, p_w, B)
-    for bi, j0 in enumerate(range(0, k, B)):
-        j1 = min(k, j0 + B)
-        S = W[:, j0:j1] ** 2 * fac[j0:j1]
-        if scores_out is not None:
-            scores_out.append(S.copy())
-        keep[:, j0:j1] = select_block_mask(S, counts[bi]) if mask_in is None else mask_in[:, j0:j1]
-        for j in range(j0, j1):
-            w0 = W[:, j].copy()
-            p = w0 * keep[:, j]
-            e = (w0 - p) / L[j, j]
-            W[:, j] = p
-            W[:, j + 1:] -= np.outer(e, L[j + 1:, j]) - np.outer(w0, D[j, j + 1:])
-    return W * keep, keep
-
-
-def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None):
-    """Algorithm 1: in-block sequential updates, then one lazy batch update
-    W[:, rest] -= E L[rest, blk]^T - W0 D[blk, rest] per block (reading R-lazy:
-    W0 holds each column's value at the time it was processed).
+    S = W[:, blk]^2 * fac[blk].  With nm = (N, M) the mask is instead chosen
+    per row for each group of M columns when the sweep reaches the group, from
+    the group's current S (select_nm_mask); p_w is then not used.
     Returns (W_hat, keep).
     """
     W = _f64(W).copy()
@@ -331,18 +323,62 @@ def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=Non
     fac = _f64(fac)
     n, k = W.shape
     mask_in = _check_mask_in(mask_in, n, k)
+    nm = _check_nm(nm, k, B)
+    keep = np.ones((n, k), dtype=bool)
+    counts = block_prune_counts(n, k, p_w, B)
+    for bi, j0 in enumerate(range(0, k, B)):
+        j1 = min(k, j0 + B)
+        S = W[:, j0:j1] ** 2 * fac[j0:j1]
+        if nm is None:
+            keep[:, j0:j1] = select_block_mask(S, counts[bi]) if mask_in is None else mask_in[:, j0:j1]
+        elif mask_in is not None:
+            keep[:, j0:j1] = mask_in[:, j0:j1]
+        for j in range(j0, j1):
+            if nm is not None and j % nm[1] == 0:
+                S[:, j - j0:j - j0 + nm[1]] = W[:, j:j + nm[1]] ** 2 * fac[j:j + nm[1]]
+                if mask_in is None:
+                    keep[:, j:j + nm[1]] = select_nm_mask(S[:, j - j0:j - j0 + nm[1]], nm[0])
+            w0 = W[:, j].copy()
+            p = w0 * keep[:, j]
+            e = (w0 - p) / L[j, j]
+            W[:, j] = p
+            W[:, j + 1:] -= np.outer(e, L[j + 1:, j]) - np.outer(w0, D[j, j + 1:])
+        if scores_out is not None:
+            scores_out.append(S.copy())
+    return W * keep, keep
+
+
+def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None):
+    """Algorithm 1: in-block sequential updates, then one lazy batch update
+    W[:, rest] -= E L[rest, blk]^T - W0 D[blk, rest] per block (reading R-lazy:
+    W0 holds each column's value at the time it was processed).  nm as in
+    sweep_eager.  scores_out receives, per block, the scores each weight's
+    selection used.  Returns (W_hat, keep).
+    """
+    W = _f64(W).copy()
+    L = _f64(L)
+    D = _f64(D)
+    fac = _f64(fac)
+    n, k = W.shape
+    mask_in = _check_mask_in(mask_in, n, k)
+    nm = _check_nm(nm, k, B)
     keep = np.ones((n, k), dtype=bool)
     counts = block_prune_counts(n, k, p_w, B)
     for bi, j0 in enumerate(range(0, k, B)):
         j1 = min(k, j0 + B)
         Bb = j1 - j0
         S = W[:, j0:j1] ** 2 * fac[j0:j1]
-        if scores_out is not None:
-            scores_out.append(S.copy())
-        keep[:, j0:j1] = select_block_mask(S, counts[bi]) if mask_in is None else mask_in[:, j0:j1]
+        if nm is None:
+            keep[:, j0:j1] = select_block_mask(S, counts[bi]) if mask_in is None else mask_in[:, j0:j1]
+        elif mask_in is not None:
+            keep[:, j0:j1] = mask_in[:, j0:j1]
         E = np.zeros((n, Bb))
         W0 = np.zeros((n, Bb))
         for j in range(j0, j1):
+            if nm is not None and j % nm[1] == 0:
+                S[:, j - j0:j - j0 + nm[1]] = W[:, j:j + nm[1]] ** 2 * fac[j:j + nm[1]]
+                if mask_in is None:
+                    keep[:, j:j + nm[1]] = select_nm_mask(S[:, j - j0:j - j0 + nm[1]], nm[0])
             w0 = W[:, j].copy()
             p = w0 * keep[:, j]
             e = (w0 - p) / L[j, j]
@@ -352,6 +388,8 @@ def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=Non
             W[:, j + 1:j1] -= np.outer(e, L[j + 1:j1, j]) - np.outer(w0, D[j, j + 1:j1])
         if j1 < k:
             W[:, j1:] -= E @ L[j1:, j0:j1].T - W0 @ D[j0:j1, j1:]
+        if scores_out is not None:
+            scores_out.append(S.copy())
     return W * keep, keep
 
 
@@ -372,7 +410,7 @@ def act_order_perm(H):
 
 def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 128,
                 X_dense=None, mask_in=None, blocked: bool = True, scores_out=None,
-                act_order: bool = False):
+                act_order: bool = False, nm=None):
     """DuoGPT on one linear layer: Alg. 1 end to end.  Returns a dict.
 
     act_order=True permutes the channels by act_order_perm(H) before the
@@ -380,7 +418,14 @@ def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 1
     forced mask all follow the permutation; blocks are formed in that order.
     W_hat and keep come back in the original channel order; the returned H,
     G, a are the unpermuted ones, while L, D, fac, b, c and the block scores
-    appended to scores_out belong to the permuted problem (perm alongside)."""
+    appended to scores_out belong to the permuted problem (perm alongside).
+
+    nm = (N, M): the N:M semi-structured variant (App. B: mask selection and
+    pruning over every group of M consecutive columns); p_w is then unused.
+    It is not combined with act_order, whose permuted groups would not be
+    groups of the layer's own consecutive columns."""
+    if act_order and nm is not None:
+        raise ValueError("act_order and N:M groups are not combined")
     H, G, a = hessian_terms(X_src, p_x, X_dense)
     W = _f64(W)
     perm = None
@@ -393,7 +438,7 @@ def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 1
     L, lam = inverse_cholesky(Hs, damp)
     fac, D, (_, b, c) = score_terms(Gs, L, As)
     sweep = sweep_blocked if blocked else sweep_eager
-    W_hat, keep = sweep(Ws, L, D, fac, p_w, B, mask_in=Ms, scores_out=scores_out)
+    W_hat, keep = sweep(Ws, L, D, fac, p_w, B, mask_in=Ms, scores_out=scores_out, nm=nm)
     if act_order:
         inv = np.argsort(perm)
         W_hat, keep = W_hat[:, inv], keep[:, inv]

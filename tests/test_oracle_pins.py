@@ -533,3 +533,78 @@ def test_act_order_equals_plain_method_on_reordered_channels():
     inv = np.argsort(perm)
     assert np.array_equal(a["keep"], b["keep"][:, inv])
     np.testing.assert_allclose(a["W_hat"], b["W_hat"][:, inv], rtol=1e-9, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# N:M semi-structured variant (App. B: mask selection and pruning over every
+# group of 4 consecutive columns)
+# ---------------------------------------------------------------------------
+
+def test_nm_selection_closed_form():
+    S = np.array([[3.0, 1.0, 2.0, 1.0], [0.0, 0.0, 0.0, 0.0], [4.0, 3.0, 2.0, 1.0]])
+    keep = R.select_nm_mask(S, 2)
+    assert keep.tolist() == [[True, False, True, False], [False, False, True, True], [True, True, False, False]]
+    assert R.select_nm_mask(S, 0).all() and not R.select_nm_mask(S, 4).any()
+
+
+def test_nm_orthogonal_inputs_closed_form():
+    """Orthogonal input channels and no activation sparsity: H is diagonal, so
+    L is diagonal, G = 0, D = 0 and nothing is compensated; the 2:4 result is
+    W with the two lowest w^2 (|x_j|^2 + lambda) of every row and group of 4
+    removed."""
+    rng = np.random.default_rng(80)
+    n, k, m, damp = 6, 24, 64, 0.01
+    Q, _ = np.linalg.qr(rng.standard_normal((m, k)))
+    s = np.exp(rng.standard_normal(k))
+    X = Q * s
+    W = rng.standard_normal((n, k))
+    out = R.prune_layer(W, X, 0.0, 0.5, damp=damp, B=8, nm=(2, 4))
+    lam = damp * np.mean(s * s)
+    S = W * W * (s * s + lam)
+    keep = np.concatenate([R.select_nm_mask(S[:, g:g + 4], 2) for g in range(0, k, 4)], axis=1)
+    assert np.array_equal(out["keep"], keep)
+    np.testing.assert_allclose(out["W_hat"], W * keep, rtol=1e-9, atol=1e-12)
+
+
+@pytest.mark.parametrize("nm", [(2, 4), (1, 4), (3, 4)])
+def test_nm_counts_and_lowest_scores(nm):
+    W, X = _layer(81, 12, 64, 256, scale_sigma=1.0)
+    scores = []
+    out = R.prune_layer(W, X, 0.5, 0.5, B=16, nm=nm, scores_out=scores)
+    keep = out["keep"]
+    N, M = nm
+    assert np.all((~keep).reshape(12, -1, M).sum(axis=2) == N)
+    S = np.concatenate(scores, axis=1)
+    for g in range(0, 64, M):
+        assert np.array_equal(keep[:, g:g + M], R.select_nm_mask(S[:, g:g + M], N))
+    assert np.all(out["W_hat"][~keep] == 0)
+
+
+def test_nm_lazy_equals_eager():
+    W, X = _layer(82, 10, 48, 200, scale_sigma=1.0)
+    a = R.prune_layer(W, X, 0.5, 0.5, B=16, nm=(2, 4))
+    b = R.prune_layer(W, X, 0.5, 0.5, B=16, nm=(2, 4), blocked=False)
+    assert np.array_equal(a["keep"], b["keep"])
+    np.testing.assert_allclose(a["W_hat"], b["W_hat"], rtol=1e-9, atol=1e-13)
+
+
+def test_nm_uses_current_values_and_compensates():
+    """The group mask is chosen from the values the sweep has updated so far,
+    not from the dense weights, and the kept weights are compensated: the
+    result has a lower objective than pruning the dense 2:4 magnitude mask."""
+    W, X = _layer(83, 16, 64, 400, scale_sigma=1.0)
+    out = R.prune_layer(W, X, 0.5, 0.5, B=16, nm=(2, 4))
+    H, G, a = R.hessian_terms(X, 0.5)
+    L, _ = R.inverse_cholesky(H, 0.01)
+    fac, _, _ = R.score_terms(G, L, a)
+    S0 = W * W * fac
+    keep0 = np.concatenate([R.select_nm_mask(S0[:, g:g + 4], 2) for g in range(0, 64, 4)], axis=1)
+    assert not np.array_equal(out["keep"], keep0)  # later groups see compensated values
+    J = R.objective(W, out["W_hat"], X, 0.5)
+    assert J < R.objective(W, W * keep0, X, 0.5)
+
+
+def test_nm_with_act_order_is_refused():
+    W, X = _layer(84, 4, 16, 64)
+    with pytest.raises(ValueError):
+        R.prune_layer(W, X, 0.5, 0.5, B=8, nm=(2, 4), act_order=True)
