@@ -188,6 +188,13 @@ duo_status duo_score_terms(const float* L, int64_t ldl, const float* G, int64_t 
  *            min(block, k - j0); blocks 0..b hold floor(p^w*n*(j0+B_b) + 0.5)
  *            zeros in total.  Within a block the weights with the smallest key
  *            (S, column, row) are pruned.
+ *   nm_n     0: the unstructured mask above.  1..4: the N:4 variant (App. B:
+ *            mask selection and pruning over every group of 4 consecutive
+ *            columns): in each row, nm_n of every group of 4 columns are
+ *            pruned, those with the smallest (S, column) when the sweep reaches
+ *            the group's first column (S from the values at that moment);
+ *            w_sparsity is then not used (still range-checked).  Needs
+ *            k % 4 == 0 and block % 4 == 0.
  *   The correction term of the lazy batch update uses each column's value at
  *   the moment it is processed (before pruning), so the blocked sweep equals
  *   the column-by-column sweep.
@@ -197,12 +204,12 @@ duo_status duo_score_terms(const float* L, int64_t ldl, const float* G, int64_t 
  *   W_out_lowp  NULL or n x k (row stride k) in w_dtype (round to nearest even).
  *   mask_out NULL or n x ceil(k/32) uint32 words, 1 = kept.
  *   block_scores_out  NULL or n x k fp32: each weight's score S at the time
- *            its block was selected.
+ *            its block (N:4: its group) was selected.
  *   Workspace: DUO_OP_SWEEP with the same n, k, block.
  */
 duo_status duo_sweep(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw,
                      const float* L, int64_t ldl, const float* D, int64_t ldd, const float* fac,
-                     double w_sparsity, int32_t block, const uint32_t* mask_in, float* W_out,
+                     double w_sparsity, int32_t nm_n, int32_t block, const uint32_t* mask_in, float* W_out,
                      void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws,
                      size_t ws_bytes, void* stream);
 
@@ -250,7 +257,7 @@ duo_status duo_permute_mask(const uint32_t* src, int64_t n, int64_t k, const int
  */
 duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw,
                            const float* L, int64_t ldl, const float* G, int64_t ldg, const float* a,
-                           double w_sparsity, int32_t block, const uint32_t* mask_in, float* W_out,
+                           double w_sparsity, int32_t nm_n, int32_t block, const uint32_t* mask_in, float* W_out,
                            void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws,
                            size_t ws_bytes, void* stream);
 

@@ -86,8 +86,10 @@ duo_status score_run(const float* L, int64_t ldl, const float* G, int64_t ldg, c
                      float* D, int64_t ldd, float* fac, void* ws, hipStream_t s);
 
 size_t sweep_ws_bytes(int64_t n, int64_t k, int B);
+// nm_n > 0: the N:4 variant (nm_n of every 4 consecutive columns of a row
+// pruned, chosen when the sweep reaches the group); p_w is then unused.
 duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L,
-                     int64_t ldl, const float* D, int64_t ldd, const float* fac, double p_w, int B,
+                     int64_t ldl, const float* D, int64_t ldd, const float* fac, double p_w, int nm_n, int B,
                      const uint32_t* mask_in, float* W_out, void* W_out_lowp, uint32_t* mask_out,
                      float* scores_out, void* ws, hipStream_t s);
 

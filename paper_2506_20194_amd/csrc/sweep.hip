@@ -30,7 +30,7 @@ namespace duo {
 
 namespace {
 
-enum { MODE_SELECT = 0, MODE_FORCED = 1, MODE_KEEP_ALL = 2, MODE_PRUNE_ALL = 3 };
+enum { MODE_SELECT = 0, MODE_FORCED = 1, MODE_KEEP_ALL = 2, MODE_PRUNE_ALL = 3, MODE_NM = 4 };
 constexpr int kShift0 = 19;                 // launch 0 histograms key bits 31..19
 constexpr int kBins0 = 1 << (32 - kShift0); // 8192 bins
 constexpr int kDigit = 8;                   // radix digit of the final select
@@ -284,6 +284,8 @@ struct IbRow {
   float e[IB_I];     // E of the columns this lane owns
   float w0[IB_I];    // values before pruning of the columns this lane owns
   uint32_t kb[IB_I]; // keep bits of the row: bit o of kb[g] is column 16 g + o
+  float f[IB_I];     // N:M only: score factors of this lane's columns
+  float sc[IB_I];    // N:M only: the scores the group selections used
 };
 
 // LDS operands of one column step: the staged L and D entries of this lane's
@@ -315,11 +317,38 @@ __device__ __forceinline__ void ib_load(IbBuf& b, const float* __restrict__ lq, 
 // ragged end of the block have zero L, D entries and values: their steps
 // change nothing.  Step J issues the LDS reads of step J + 2 (three-slot
 // ring); the scheduling barrier keeps the compiler from hoisting more.
-template <int J>
+template <int O>
+__device__ __forceinline__ uint32_t row_bcast_u(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x150 + O, 0xF, 0xF, false);
+}
+
+// N:M groups of 4 columns: at the first column of a group every lane of the
+// row receives the four columns' current score keys from their owner lanes
+// and derives the same keep bits: the nm_n lowest (equal keys in column
+// order) are pruned.
+template <int G, int O>
+__device__ __forceinline__ void nm_select(IbRow& s, int nm_n) {
+  const float S = weight_score(s.w[G], s.f[G]);
+  s.sc[G] = S;
+  const uint32_t key = orderable(S);
+  const uint32_t k0 = row_bcast_u<O>(key), k1 = row_bcast_u<O + 1>(key);
+  const uint32_t k2 = row_bcast_u<O + 2>(key), k3 = row_bcast_u<O + 3>(key);
+  const int r0 = (k1 < k0) + (k2 < k0) + (k3 < k0);
+  const int r1 = (k0 <= k1) + (k2 < k1) + (k3 < k1);
+  const int r2 = (k0 <= k2) + (k1 <= k2) + (k3 < k2);
+  const int r3 = (k0 <= k3) + (k1 <= k3) + (k2 <= k3);
+  const uint32_t keep = (r0 >= nm_n ? 1u : 0u) | (r1 >= nm_n ? 2u : 0u) | (r2 >= nm_n ? 4u : 0u) |
+                        (r3 >= nm_n ? 8u : 0u);
+  s.kb[G] = (s.kb[G] & ~(0xFu << O)) | (keep << O);
+}
+
+template <int J, bool NM>
 __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* __restrict__ lq,
-                                        const float* __restrict__ dq, const float* __restrict__ il, int q) {
+                                        const float* __restrict__ dq, const float* __restrict__ il, int q,
+                                        int nm_n) {
   constexpr int g = J / IB_Q, o = J % IB_Q;
   ib_load<J + 2>(buf[(J + 2) % 3], lq, dq, il, q);
+  if constexpr (NM && o % 4 == 0) nm_select<g, o>(s, nm_n);
   const IbBuf& b = buf[J % 3];
   const float v = row_bcast<o>(s.w[g]);
   const bool kj = (s.kb[g] >> o) & 1u;
@@ -335,21 +364,25 @@ __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* 
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int... Js>
+template <bool NM, int... Js>
 __device__ __forceinline__ void ib_steps(IbRow& s, const float* lq, const float* dq, const float* il, int q,
-                                         std::integer_sequence<int, Js...>) {
+                                         int nm_n, std::integer_sequence<int, Js...>) {
   IbBuf buf[3];
   ib_load<0>(buf[0], lq, dq, il, q);
   ib_load<1>(buf[1], lq, dq, il, q);
-  (ib_step<Js>(s, buf, lq, dq, il, q), ...);
+  (ib_step<Js, NM>(s, buf, lq, dq, il, q, nm_n), ...);
 }
 
+// NM: the N:M variant (mode MODE_NM): the keep bits are chosen inside the
+// column loop, and the scores they used go to scores_out when it is set.
+template <bool NM>
 __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int64_t ew_ld,
                                                       const float* __restrict__ L, int64_t ldl,
                                                       const float* __restrict__ D, int64_t ldd,
                                                       const float* __restrict__ fac, const SelState* st, int mode,
                                                       const uint32_t* __restrict__ mask_in, float* __restrict__ EW,
-                                                      uint8_t* __restrict__ bmask) {
+                                                      uint8_t* __restrict__ bmask, int nm_n,
+                                                      float* __restrict__ scores_out) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
   float* lq = sm;                       // [j][q][i]: L[j0+q+16i][j0+j] / L[j0+j][j0+j] where q+16i > j, else 0
   float* dq = sm + kMaxBlock * IB_JS;   // [j][q][i]: D[j0+j][j0+q+16i] where q+16i > j, else 0
@@ -415,6 +448,10 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
     s.w[i] = cv ? Wo[(int64_t)row * k + j0 + c] : 0.f;
     s.e[i] = 0.f;
     s.w0[i] = 0.f;
+    if constexpr (NM) {
+      s.f[i] = c < Bb ? fac[j0 + c] : 0.f;
+      s.sc[i] = 0.f;
+    }
     bool keep = true;
     if (cv) {
       if (mode == MODE_SELECT) {
@@ -425,13 +462,13 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
         const int gc = j0 + c;
         keep = (mask_in[(int64_t)row * words + gc / 32] >> (gc % 32)) & 1u;
       } else {
-        keep = mode == MODE_KEEP_ALL;
+        keep = mode == MODE_KEEP_ALL || mode == MODE_NM;  // N:M bits are chosen in the column loop
       }
     }
     const unsigned long long ball = __ballot(keep);
     s.kb[i] = (uint32_t)(ball >> (IB_Q * (lane >> 4))) & 0xFFFFu;
   }
-  ib_steps(s, lq, dq, il, q, std::make_integer_sequence<int, kMaxBlock>{});
+  ib_steps<NM>(s, lq, dq, il, q, nm_n, std::make_integer_sequence<int, kMaxBlock>{});
 #pragma unroll
   for (int i = 0; i < IB_I; ++i) {
     const int c = q + IB_Q * i;
@@ -440,6 +477,7 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
       EW[(int64_t)row * ew_ld + c] = s.e[i];
       EW[(int64_t)row * ew_ld + (ew_ld >> 1) + c] = s.w0[i];
       bmask[(int64_t)row * k + j0 + c] = (uint8_t)((s.kb[i] >> q) & 1u);
+      if (NM && scores_out) scores_out[(int64_t)row * k + j0 + c] = s.sc[i];
     }
   }
 }
@@ -510,9 +548,9 @@ SweepWs carve(void* ws, int64_t n, int64_t k, int B) {
 size_t sweep_ws_bytes(int64_t n, int64_t k, int B) { return carve(nullptr, n, k, B).bytes; }
 
 duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L, int64_t ldl,
-                     const float* D, int64_t ldd, const float* fac, double p_w, int B, const uint32_t* mask_in,
-                     float* W_out, void* W_out_lowp, uint32_t* mask_out, float* scores_out, void* ws,
-                     hipStream_t s) {
+                     const float* D, int64_t ldd, const float* fac, double p_w, int nm_n, int B,
+                     const uint32_t* mask_in, float* W_out, void* W_out_lowp, uint32_t* mask_out, float* scores_out,
+                     void* ws, hipStream_t s) {
   const SweepWs w = carve(ws, n, k, B);
   const int64_t nk = n * k;
   const int64_t S = super_width(B);
@@ -522,7 +560,9 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   hipLaunchKernelGGL(sel_reset_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist);
   DUO_LAUNCH_CHECK();
   const size_t ib_lds = (size_t)(2 * kMaxBlock * IB_JS + kMaxBlock) * sizeof(float);
-  DUO_HIP_TRY(hipFuncSetAttribute((const void*)inblock_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ib_lds));
+  const bool nm = nm_n > 0 && !mask_in;
+  auto ib_kern = nm ? inblock_kernel<true> : inblock_kernel<false>;
+  DUO_HIP_TRY(hipFuncSetAttribute((const void*)ib_kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ib_lds));
   const size_t sel_lds = (size_t)(16 + (1 << kDigit)) * sizeof(uint32_t) + (size_t)kSelCap * sizeof(unsigned long long);
   DUO_HIP_TRY(
       hipFuncSetAttribute((const void*)sel_resolve_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sel_lds));
@@ -538,6 +578,8 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     int mode = MODE_SELECT;
     if (mask_in)
       mode = MODE_FORCED;
+    else if (nm)
+      mode = MODE_NM;
     else if (z <= 0)
       mode = MODE_KEEP_ALL;
     else if (z >= total)
@@ -545,7 +587,7 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     int idx_bits = 1;
     while (idx_bits < 31 && ((int64_t)1 << idx_bits) < total) ++idx_bits;
     prof_begin(DUO_PROF_SELECT, s);
-    if (mode == MODE_SELECT || scores_out) {
+    if (mode == MODE_SELECT || (scores_out && mode != MODE_NM)) {
       hipLaunchKernelGGL(sel_hist_kernel, dim3(P), dim3(256), 0, s, (const float*)W_out, k, (int)n, Bb, (int)j0, fac,
                          w.hist, scores_out, mode == MODE_SELECT ? 1 : 0);
       DUO_LAUNCH_CHECK();
@@ -561,9 +603,9 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     prof_end(DUO_PROF_SELECT, s);
     prof_begin(DUO_PROF_INBLOCK, s);
     const int64_t sb0 = j0 / S * S, sb1 = sb0 + S < k ? sb0 + S : k;
-    hipLaunchKernelGGL(inblock_kernel, dim3((unsigned)cdiv(n, IB_ROWS)), dim3(256), ib_lds, s, W_out, (int)n, (int)k,
+    hipLaunchKernelGGL(ib_kern, dim3((unsigned)cdiv(n, IB_ROWS)), dim3(256), ib_lds, s, W_out, (int)n, (int)k,
                        (int)j0, Bb, (int64_t)2 * S, L, ldl, D, ldd, fac, (const SelState*)w.st, mode, mask_in,
-                       w.EW + (j0 - sb0), w.bmask);
+                       w.EW + (j0 - sb0), w.bmask, nm_n, scores_out);
     DUO_LAUNCH_CHECK();
     prof_end(DUO_PROF_INBLOCK, s);
     // inside the super-block: columns [j1, sb1) from this block (K = Bb);

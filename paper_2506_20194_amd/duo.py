@@ -80,9 +80,10 @@ def lib():
         L.duo_score_terms.restype = I32
         L.duo_score_terms.argtypes = [P, I64, P, I64, P, I64, P, I64, P, P, SZ, P]
         L.duo_sweep.restype = I32
-        L.duo_sweep.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, P, P, P, P, P, P, SZ, P]
+        L.duo_sweep.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, I32, P, P, P, P, P, P, SZ, P]
         L.duo_prune_layer.restype = I32
-        L.duo_prune_layer.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, P, P, P, P, P, P, SZ, P]
+        L.duo_prune_layer.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, I32, P, P, P, P, P, P, SZ,
+                                      P]
         L.duo_block_workspace_size.restype = SZ
         L.duo_block_workspace_size.argtypes = [I32, I64, I64, I64]
         L.duo_rmsnorm.restype = I32
@@ -297,7 +298,7 @@ def _sweep_outputs(W, want_lowp, want_mask, want_scores):
 
 
 def duo_sweep(W, L, D, fac, w_sparsity, block=128, mask_in=None, want_lowp=False, want_mask=True,
-              want_scores=False, ws=None, out=None):
+              want_scores=False, ws=None, out=None, nm_n=0):
     n, k = W.shape
     _same_device(W, L, D, fac, mask_in, ws)
     _shape(L, (k, k), "L")
@@ -311,14 +312,14 @@ def duo_sweep(W, L, D, fac, w_sparsity, block=128, mask_in=None, want_lowp=False
     W_out, lowp, mask, scores = out if out is not None else _sweep_outputs(W, want_lowp, want_mask, want_scores)
     _check_outputs((W_out, lowp, mask, scores), W)
     st = lib().duo_sweep(_ptr(W), _dtype(W), n, k, _ld(W), _ptr(L), _ld(L), _ptr(D), _ld(D), _ptr(fac),
-                         float(w_sparsity), int(block), _ptr(mask_in), _ptr(W_out), _ptr(lowp), _ptr(mask),
-                         _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
+                         float(w_sparsity), int(nm_n), int(block), _ptr(mask_in), _ptr(W_out), _ptr(lowp),
+                         _ptr(mask), _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
     _check(st, "duo_sweep")
     return W_out, lowp, mask, scores
 
 
 def duo_prune_layer(W, L, G, a, w_sparsity, block=128, mask_in=None, want_lowp=False, want_mask=True,
-                    want_scores=False, ws=None, out=None):
+                    want_scores=False, ws=None, out=None, nm_n=0):
     n, k = W.shape
     _same_device(W, L, G, a, mask_in, ws)
     _shape(L, (k, k), "L")
@@ -332,8 +333,8 @@ def duo_prune_layer(W, L, G, a, w_sparsity, block=128, mask_in=None, want_lowp=F
     W_out, lowp, mask, scores = out if out is not None else _sweep_outputs(W, want_lowp, want_mask, want_scores)
     _check_outputs((W_out, lowp, mask, scores), W)
     st = lib().duo_prune_layer(_ptr(W), _dtype(W), n, k, _ld(W), _ptr(L), _ld(L), _ptr(G), _ld(G), _ptr(a),
-                               float(w_sparsity), int(block), _ptr(mask_in), _ptr(W_out), _ptr(lowp), _ptr(mask),
-                               _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
+                               float(w_sparsity), int(nm_n), int(block), _ptr(mask_in), _ptr(W_out), _ptr(lowp),
+                               _ptr(mask), _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
     _check(st, "duo_prune_layer")
     return W_out, lowp, mask, scores
 
@@ -412,18 +413,25 @@ def duo_permute_mask(words, k, col_idx, out=None):
 
 
 def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=None, want_lowp=True,
-                 act_order=False):
+                 act_order=False, nm=None):
     """DuoGPT on one linear layer (stages 1-3 on the device).
 
     W: n x k (out x in), X: m x k token-major calibration input of the pruned
     stream (sparsified per token), X_dense: the dense stream (defaults to X).
     act_order: process the channels by decreasing Hessian diagonal (App. B);
     the outputs are returned in the original channel order.
+    nm: None, or (N, 4) for the N:4 semi-structured variant (App. B), in which
+    w_sparsity is not used; not combined with act_order.
     Returns dict(W_out fp32, W_lowp in W's dtype, mask (bool n x k), lam, and
     perm when act_order).
     """
     n, k = W.shape
     dev = W.device
+    nm_n = 0
+    if nm is not None:
+        if tuple(nm)[1] != 4 or act_order:
+            raise ValueError("nm must be (N, 4) and is not combined with act_order")
+        nm_n = int(nm[0])
     H = torch.zeros((k, k), dtype=torch.float32, device=dev)
     G = torch.zeros((k, k), dtype=torch.float32, device=dev)
     a = torch.zeros(k, dtype=torch.float32, device=dev)
@@ -437,7 +445,7 @@ def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=N
         a = duo_permute(a.view(1, k), None, perm).view(k)
         W = duo_permute(W, None, perm)
     lam, _ = duo_chol_inv(H, damp)
-    W_out, lowp, mask, _ = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp)
+    W_out, lowp, mask, _ = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp, nm_n=nm_n)
     if act_order:
         W_out = duo_permute(W_out, None, inv)
         lowp = duo_permute(lowp, None, inv) if lowp is not None else None

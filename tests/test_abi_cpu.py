@@ -104,8 +104,8 @@ def test_chol_and_sweep_argument_errors(duo_lib):
     assert L.duo_score_terms(FAKE, 64, FAKE, 64, FAKE, 64, FAKE, 64, FAKE, WS, big, None) == NODEV
     assert L.duo_score_terms(FAKE, 64, None, 64, FAKE, 64, FAKE, 64, FAKE, WS, big, None) == E
 
-    def sweep(W=FAKE, dt=1, n=32, k=64, ldw=64, p=0.5, B=16, Wo=FAKE, fn=L.duo_sweep):
-        return fn(W, dt, n, k, ldw, FAKE, 64, FAKE, 64, FAKE, p, B, None, Wo, None, None, None, WS, big, None)
+    def sweep(W=FAKE, dt=1, n=32, k=64, ldw=64, p=0.5, B=16, Wo=FAKE, fn=L.duo_sweep, nm=0):
+        return fn(W, dt, n, k, ldw, FAKE, 64, FAKE, 64, FAKE, p, nm, B, None, Wo, None, None, None, WS, big, None)
 
     for fn in (L.duo_sweep, L.duo_prune_layer):
         assert sweep(fn=fn) == NODEV
@@ -118,6 +118,11 @@ def test_chol_and_sweep_argument_errors(duo_lib):
         assert sweep(B=0, fn=fn) == E
         assert sweep(B=129, fn=fn) == E
         assert sweep(dt=3, fn=fn) == E
+        assert sweep(nm=2, fn=fn) == NODEV         # N:4 with k, B multiples of 4
+        assert sweep(nm=5, fn=fn) == E
+        assert sweep(nm=-1, fn=fn) == E
+        assert sweep(nm=2, B=18, fn=fn) == E       # B not a multiple of 4
+        assert sweep(nm=2, k=62, ldw=64, fn=fn) == E
 
 
 def test_binding_refuses_host_tensors(duo_lib):
