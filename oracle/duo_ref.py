@@ -57,6 +57,9 @@ __all__ = [
     "window_terms",
     "block_prune_counts",
     "select_block_mask",
+    "select_nm_mask",
+    "quant_grid",
+    "quantize",
     "sweep_eager",
     "sweep_blocked",
     "act_order_perm",
@@ -286,6 +289,35 @@ def select_nm_mask(S, N: int):
     return keep
 
 
+def quant_grid(w, bits: int):
+    """Round-to-nearest grid of one row group (Table 4: b-bit uniform integer,
+    channel-wise, asymmetric): the range [min(0, min w), max(0, max w)] (or
+    [-1, 1] when it is empty) split into 2^b - 1 steps; zero is the integer
+    code of 0.  Returns (scale, zero)."""
+    w = _f64(w)
+    maxq = 2 ** bits - 1
+    lo, hi = min(0.0, float(np.min(w))), max(0.0, float(np.max(w)))
+    if lo == hi:
+        lo, hi = -1.0, 1.0
+    scale = (hi - lo) / maxq
+    return scale, float(np.round(-lo / scale))
+
+
+def quantize(x, scale: float, zero: float, bits: int):
+    """Value of x on the grid: scale * (clamp(round(x / scale) + zero, 0,
+    2^b - 1) - zero), round half to even."""
+    q = np.clip(np.round(_f64(x) / scale) + zero, 0, 2 ** bits - 1)
+    return scale * (q - zero)
+
+
+def _check_quant(quant, B: int):
+    if quant is None:
+        return None
+    bits, group = quant
+    assert 2 <= bits <= 8 and group >= 1 and B % group == 0, "quantisation groups must divide the block"
+    return bits, group
+
+
 def _check_nm(nm, k: int, B: int):
     if nm is None:
         return None
@@ -298,6 +330,23 @@ def _check_nm(nm, k: int, B: int):
 # Column sweep: definition (eager) and Algorithm 1 (blocked, lazy batches)
 # ---------------------------------------------------------------------------
 
+def _group_grids(Wg, bits: int, qparams_out):
+    n = Wg.shape[0]
+    qs, qz = np.empty(n), np.empty(n)
+    for r in range(n):
+        qs[r], qz[r] = quant_grid(Wg[r], bits)
+    if qparams_out is not None:
+        qparams_out.append((qs.copy(), qz.copy()))
+    return qs, qz
+
+
+def _kept_value(w0, keep_j, quant, qs, qz):
+    """The value a processed column keeps: w0 (or its grid value) where kept, 0 where pruned."""
+    if quant is None:
+        return w0 * keep_j
+    q = np.clip(np.round(w0 / qs) + qz, 0, 2 ** quant[0] - 1)
+    return np.where(keep_j, qs * (q - qz), 0.0)
+
 def _check_mask_in(mask_in, n, k):
     if mask_in is None:
         return None
@@ -306,7 +355,8 @@ def _check_mask_in(mask_in, n, k):
     return mask_in
 
 
-def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None):
+def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
+                qparams_out=None):
     """Column sweep with every column's update applied to all later columns at once.
 
     Processing column j: w0 = W[:, j]; p = w0 * m_j; e = (w0 - p) / L_jj and
@@ -315,6 +365,11 @@ def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None,
     S = W[:, blk]^2 * fac[blk].  With nm = (N, M) the mask is instead chosen
     per row for each group of M columns when the sweep reaches the group, from
     the group's current S (select_nm_mask); p_w is then not used.
+    quant = (bits, group): joint pruning and quantisation (Table 4): when the
+    sweep reaches a group of `group` columns, every row's grid is fixed from
+    the group's current values (quant_grid); a kept weight becomes its grid
+    value and a pruned one 0, and the compensation carries both errors.
+    qparams_out (a list) receives (scale, zero) arrays of shape (n,) per group.
     Returns (W_hat, keep).
     """
     W = _f64(W).copy()
@@ -324,8 +379,10 @@ def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None,
     n, k = W.shape
     mask_in = _check_mask_in(mask_in, n, k)
     nm = _check_nm(nm, k, B)
+    quant = _check_quant(quant, B)
     keep = np.ones((n, k), dtype=bool)
     counts = block_prune_counts(n, k, p_w, B)
+    qs = qz = None
     for bi, j0 in enumerate(range(0, k, B)):
         j1 = min(k, j0 + B)
         S = W[:, j0:j1] ** 2 * fac[j0:j1]
@@ -338,8 +395,10 @@ def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None,
                 S[:, j - j0:j - j0 + nm[1]] = W[:, j:j + nm[1]] ** 2 * fac[j:j + nm[1]]
                 if mask_in is None:
                     keep[:, j:j + nm[1]] = select_nm_mask(S[:, j - j0:j - j0 + nm[1]], nm[0])
+            if quant is not None and j % quant[1] == 0:
+                qs, qz = _group_grids(W[:, j:j + quant[1]], quant[0], qparams_out)
             w0 = W[:, j].copy()
-            p = w0 * keep[:, j]
+            p = _kept_value(w0, keep[:, j], quant, qs, qz)
             e = (w0 - p) / L[j, j]
             W[:, j] = p
             W[:, j + 1:] -= np.outer(e, L[j + 1:, j]) - np.outer(w0, D[j, j + 1:])
@@ -348,11 +407,12 @@ def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None,
     return W * keep, keep
 
 
-def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None):
+def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
+                  qparams_out=None):
     """Algorithm 1: in-block sequential updates, then one lazy batch update
     W[:, rest] -= E L[rest, blk]^T - W0 D[blk, rest] per block (reading R-lazy:
-    W0 holds each column's value at the time it was processed).  nm as in
-    sweep_eager.  scores_out receives, per block, the scores each weight's
+    W0 holds each column's value at the time it was processed).  nm, quant and
+    qparams_out as in sweep_eager.  scores_out receives, per block, the scores each weight's
     selection used.  Returns (W_hat, keep).
     """
     W = _f64(W).copy()
@@ -362,8 +422,10 @@ def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=Non
     n, k = W.shape
     mask_in = _check_mask_in(mask_in, n, k)
     nm = _check_nm(nm, k, B)
+    quant = _check_quant(quant, B)
     keep = np.ones((n, k), dtype=bool)
     counts = block_prune_counts(n, k, p_w, B)
+    qs = qz = None
     for bi, j0 in enumerate(range(0, k, B)):
         j1 = min(k, j0 + B)
         Bb = j1 - j0
@@ -379,8 +441,10 @@ def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=Non
                 S[:, j - j0:j - j0 + nm[1]] = W[:, j:j + nm[1]] ** 2 * fac[j:j + nm[1]]
                 if mask_in is None:
                     keep[:, j:j + nm[1]] = select_nm_mask(S[:, j - j0:j - j0 + nm[1]], nm[0])
+            if quant is not None and j % quant[1] == 0:
+                qs, qz = _group_grids(W[:, j:min(j + quant[1], j1)], quant[0], qparams_out)
             w0 = W[:, j].copy()
-            p = w0 * keep[:, j]
+            p = _kept_value(w0, keep[:, j], quant, qs, qz)
             e = (w0 - p) / L[j, j]
             E[:, j - j0] = e
             W0[:, j - j0] = w0
@@ -410,7 +474,7 @@ def act_order_perm(H):
 
 def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 128,
                 X_dense=None, mask_in=None, blocked: bool = True, scores_out=None,
-                act_order: bool = False, nm=None):
+                act_order: bool = False, nm=None, quant=None, qparams_out=None):
     """DuoGPT on one linear layer: Alg. 1 end to end.  Returns a dict.
 
     act_order=True permutes the channels by act_order_perm(H) before the
@@ -423,7 +487,10 @@ def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 1
     nm = (N, M): the N:M semi-structured variant (App. B: mask selection and
     pruning over every group of M consecutive columns); p_w is then unused.
     It is not combined with act_order, whose permuted groups would not be
-    groups of the layer's own consecutive columns."""
+    groups of the layer's own consecutive columns.
+
+    quant = (bits, group): joint pruning and RTN quantisation (Table 4), see
+    sweep_eager; with act_order the groups are formed in the permuted order."""
     if act_order and nm is not None:
         raise ValueError("act_order and N:M groups are not combined")
     H, G, a = hessian_terms(X_src, p_x, X_dense)
@@ -438,7 +505,8 @@ def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 1
     L, lam = inverse_cholesky(Hs, damp)
     fac, D, (_, b, c) = score_terms(Gs, L, As)
     sweep = sweep_blocked if blocked else sweep_eager
-    W_hat, keep = sweep(Ws, L, D, fac, p_w, B, mask_in=Ms, scores_out=scores_out, nm=nm)
+    W_hat, keep = sweep(Ws, L, D, fac, p_w, B, mask_in=Ms, scores_out=scores_out, nm=nm, quant=quant,
+                        qparams_out=qparams_out)
     if act_order:
         inv = np.argsort(perm)
         W_hat, keep = W_hat[:, inv], keep[:, inv]

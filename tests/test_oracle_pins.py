@@ -608,3 +608,92 @@ def test_nm_with_act_order_is_refused():
     W, X = _layer(84, 4, 16, 64)
     with pytest.raises(ValueError):
         R.prune_layer(W, X, 0.5, 0.5, B=8, nm=(2, 4), act_order=True)
+
+
+# ---------------------------------------------------------------------------
+# Joint pruning and RTN quantisation (Table 4: channel-wise uniform integer,
+# group size 128, inside the sweep)
+# ---------------------------------------------------------------------------
+
+def test_quant_grid_closed_form():
+    # range [-1, 2] in 3 steps of 1.0 (2 bits); zero code 1
+    assert R.quant_grid(np.array([-1.0, 0.5, 2.0]), 2) == (1.0, 1.0)
+    # positive values: the range still includes 0; 4 bits: 15 steps of 0.2
+    s, z = R.quant_grid(np.array([1.0, 3.0]), 4)
+    assert abs(s - 0.2) < 1e-15 and z == 0.0
+    # empty range -> [-1, 1]
+    assert R.quant_grid(np.zeros(4), 8) == (2.0 / 255, 128.0)
+    x = np.array([-1.2, -0.5, 0.49, 0.51, 1.5, 2.6])
+    np.testing.assert_array_equal(R.quantize(x, 1.0, 1.0, 2), [-1.0, -0.0, 0.0, 1.0, 2.0, 2.0])
+    assert R.quantize(np.array([0.0]), 0.3, 5.0, 4)[0] == 0.0  # 0 is on every grid
+
+
+def test_quant_orthogonal_inputs_is_plain_rtn():
+    """Orthogonal channels, no activation sparsity, no pruning: nothing is
+    compensated, so the result is plain round-to-nearest of W with one grid
+    per row and group of the dense weights."""
+    rng = np.random.default_rng(90)
+    n, k, m = 5, 32, 64
+    Q, _ = np.linalg.qr(rng.standard_normal((m, k)))
+    X = Q * np.exp(rng.standard_normal(k))
+    W = rng.standard_normal((n, k))
+    for bits, group in ((4, 8), (8, 16), (3, 4)):
+        out = R.prune_layer(W, X, 0.0, 0.0, B=16, quant=(bits, group))
+        want = np.empty_like(W)
+        for r in range(n):
+            for g in range(0, k, group):
+                s, z = R.quant_grid(W[r, g:g + group], bits)
+                want[r, g:g + group] = R.quantize(W[r, g:g + group], s, z, bits)
+        assert out["keep"].all()
+        np.testing.assert_allclose(out["W_hat"], want, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("bits,group", [(4, 16), (8, 32), (4, 8)])
+def test_quant_values_on_grids_fixed_at_group_start(bits, group):
+    W, X = _layer(91, 8, 64, 256, scale_sigma=1.0)
+    qp = []
+    out = R.prune_layer(W, X, 0.5, 0.5, B=32, quant=(bits, group), qparams_out=qp)
+    assert len(qp) == 64 // group
+    Wh, keep = out["W_hat"], out["keep"]
+    assert np.all(Wh[~keep] == 0)
+    for gi, (s, z) in enumerate(qp):
+        cols = slice(gi * group, (gi + 1) * group)
+        codes = Wh[:, cols] / s[:, None] + z[:, None]
+        assert np.allclose(codes, np.round(codes), atol=1e-9)          # on the grid
+        assert np.all(np.round(codes) >= -1e-9) and np.all(np.round(codes) <= 2 ** bits - 1 + 1e-9)
+    # grids come from the values the sweep has compensated so far, not the dense W
+    s0, _ = R.quant_grid(W[0, group:2 * group], bits)
+    assert abs(qp[1][0][0] - s0) > 1e-12
+
+
+def test_quant_lazy_equals_eager():
+    W, X = _layer(92, 9, 48, 200, scale_sigma=1.0)
+    a = R.prune_layer(W, X, 0.5, 0.5, B=16, quant=(4, 8))
+    b = R.prune_layer(W, X, 0.5, 0.5, B=16, quant=(4, 8), blocked=False)
+    assert np.array_equal(a["keep"], b["keep"])
+    np.testing.assert_allclose(a["W_hat"], b["W_hat"], rtol=1e-9, atol=1e-12)
+
+
+@pytest.mark.parametrize("quant", [None, (4, 4), (8, 8), (3, 2)])
+def test_quant_last_column_is_ridge_optimum_given_frozen_prefix(quant):
+    """Without activation sparsity the sweep leaves the last column at the
+    damped least-squares optimum given every earlier column's final (pruned
+    or quantised) value, v* = (r.x + lambda w) / (x.x + lambda) with r the
+    target minus the prefix's contribution; the column then keeps the grid
+    value of v* (or 0 where pruned).  This pins the compensation of the
+    quantisation error, which the pruning pins do not see."""
+    rng = np.random.default_rng(94)
+    n, k, m, damp = 6, 24, 200, 0.01
+    X = rng.standard_normal((m, k)) * np.exp(rng.standard_normal(k))
+    W = 0.02 * rng.standard_normal((n, k))
+    qp = []
+    out = R.prune_layer(W, X, 0.0, 0.5, damp=damp, B=8, quant=quant, qparams_out=qp)
+    Wh, keep = out["W_hat"], out["keep"][:, k - 1]
+    lam = damp * np.mean(np.sum(X * X, axis=0))
+    r = W @ X.T - Wh[:, :k - 1] @ X[:, :k - 1].T
+    x = X[:, k - 1]
+    v = (r @ x + lam * W[:, k - 1]) / (x @ x + lam)
+    if quant is not None:
+        sc, z = qp[-1]
+        v = sc * (np.clip(np.round(v / sc) + z, 0, 2 ** quant[0] - 1) - z)
+    np.testing.assert_allclose(Wh[:, k - 1], np.where(keep, v, 0.0), rtol=0, atol=1e-12)
