@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--nm", type=int, default=0, metavar="N",
                     help="N:4 semi-structured mask (App. B 2:4 variant) instead of the unstructured p_w mask")
+    ap.add_argument("--quant", type=int, default=0, metavar="BITS",
+                    help="joint RTN quantisation of the kept weights (Table 4), one grid per row and 128 columns")
     ap.add_argument("--act-order", action="store_true",
                     help="process channels by decreasing Hessian diagonal (App. B); adds the gathers to the step")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -176,6 +178,8 @@ def main():
     args = parse()
     if args.nm and (args.act_order or not 0 < args.nm <= 4):
         sys.exit("bench.py: --nm takes N in 1..4 and is not combined with --act-order")
+    if args.quant and (args.act_order or not 2 <= args.quant <= 8):
+        sys.exit("bench.py: --quant takes 2..8 bits and is timed without --act-order")
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the multi-GPU path is a design note, not implemented", file=sys.stderr)
@@ -220,7 +224,8 @@ def main():
         if not args.act_order:
             duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h)
             info = duo.duo_chol_inv(H, c["damp"], ws=ws_c, sync=check)
-            duo.duo_prune_layer(W, H, G, a, c["p_w"], B, ws=ws_p, out=(W_out, lowp, mask, None), nm_n=args.nm)
+            duo.duo_prune_layer(W, H, G, a, c["p_w"], B, ws=ws_p, out=(W_out, lowp, mask, None), nm_n=args.nm,
+                                quant=(args.quant, 128) if args.quant else None)
             return info
         hdiag.zero_()
         duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h, hdiag=hdiag)
@@ -292,7 +297,8 @@ def main():
         "config": {"workload": args.workload, "n": n, "k": k, "m": m, "p_x": c["p_x"], "p_w": c["p_w"],
                    "block": B, "damp": c["damp"], "x_dtype": str(c["x_dtype"]).replace("torch.", ""),
                    "inputs": c["kind"], "act_order": bool(args.act_order),
-                   "mask": f"{args.nm}:4" if args.nm else "unstructured", "parallelism": "single GPU"},
+                   "mask": f"{args.nm}:4" if args.nm else "unstructured",
+                   "quant": f"int{args.quant} g128" if args.quant else None, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "gram_kernel (H, G)", "achieved": gram_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": gram_tflops / PEAK_BF16_TFLOPS,
                      "traffic": gram_traffic(args.workload), "ms_per_launch": per("gram"), "flop_per_launch": gram_flop_step / gram_launches},

@@ -181,6 +181,38 @@ duo_status duo_score_terms(const float* L, int64_t ldl, const float* G, int64_t 
                            void* stream);
 
 /*
+ * Options of the sweep (duo_sweep, duo_prune_layer).  A NULL pointer means
+ * all fields 0.
+ *   nm_n     0: the unstructured block mask (w_sparsity).  1..4: the N:4
+ *            variant (App. B: mask selection and pruning over every group of 4
+ *            consecutive columns): in each row, nm_n of every group of 4
+ *            columns are pruned, those with the smallest (S, column) when the
+ *            sweep reaches the group's first column (S from the values at that
+ *            moment); w_sparsity is then not used (still range-checked).
+ *            Needs k % 4 == 0 and block % 4 == 0.
+ *   q_bits   0: no quantisation.  2..8: joint pruning and round-to-nearest
+ *            quantisation (Table 4: uniform integer, channel-wise, in groups):
+ *            when the sweep reaches a group of q_group columns, every row's
+ *            grid is fixed from the group's current values: range
+ *            [min(0, min w), max(0, max w)] ([-1, 1] if empty), step
+ *            s = range / (2^q_bits - 1), zero code z = rint(-min / s).  A kept
+ *            weight becomes s * (clamp(rint(w / s) + z, 0, 2^q_bits - 1) - z)
+ *            (its value is exactly that fp32 product), a pruned one 0, and the
+ *            later columns compensate both errors.
+ *   q_group  16, 32, 64 or 128 columns per grid, dividing block.
+ *   q_scale_out, q_zero_out  NULL or n x ceil(k / q_group) fp32 each: s and z
+ *            per row and group (row-major), so that the integer code of a kept
+ *            weight is rint(W_out / s) + z.
+ */
+typedef struct {
+  int32_t nm_n;
+  int32_t q_bits;
+  int32_t q_group;
+  float* q_scale_out;
+  float* q_zero_out;
+} duo_sweep_opts;
+
+/*
  * duo_sweep - stage 3 sweep (Algorithm 1 outer/inner loops, lazy updates).
  *   W        n x k, ldw, w_dtype: dense weights (not modified).
  *   L, D     from duo_chol_inv / duo_score_terms; fac from duo_score_terms.
@@ -188,13 +220,8 @@ duo_status duo_score_terms(const float* L, int64_t ldl, const float* G, int64_t 
  *            min(block, k - j0); blocks 0..b hold floor(p^w*n*(j0+B_b) + 0.5)
  *            zeros in total.  Within a block the weights with the smallest key
  *            (S, column, row) are pruned.
- *   nm_n     0: the unstructured mask above.  1..4: the N:4 variant (App. B:
- *            mask selection and pruning over every group of 4 consecutive
- *            columns): in each row, nm_n of every group of 4 columns are
- *            pruned, those with the smallest (S, column) when the sweep reaches
- *            the group's first column (S from the values at that moment);
- *            w_sparsity is then not used (still range-checked).  Needs
- *            k % 4 == 0 and block % 4 == 0.
+ *   opts     NULL (defaults: unstructured mask, no quantisation) or the
+ *            options of duo_sweep_opts below.
  *   The correction term of the lazy batch update uses each column's value at
  *   the moment it is processed (before pruning), so the blocked sweep equals
  *   the column-by-column sweep.
@@ -209,7 +236,8 @@ duo_status duo_score_terms(const float* L, int64_t ldl, const float* G, int64_t 
  */
 duo_status duo_sweep(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw,
                      const float* L, int64_t ldl, const float* D, int64_t ldd, const float* fac,
-                     double w_sparsity, int32_t nm_n, int32_t block, const uint32_t* mask_in, float* W_out,
+                     double w_sparsity, const duo_sweep_opts* opts, int32_t block, const uint32_t* mask_in,
+                     float* W_out,
                      void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws,
                      size_t ws_bytes, void* stream);
 
@@ -257,7 +285,8 @@ duo_status duo_permute_mask(const uint32_t* src, int64_t n, int64_t k, const int
  */
 duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw,
                            const float* L, int64_t ldl, const float* G, int64_t ldg, const float* a,
-                           double w_sparsity, int32_t nm_n, int32_t block, const uint32_t* mask_in, float* W_out,
+                           double w_sparsity, const duo_sweep_opts* opts, int32_t block, const uint32_t* mask_in,
+                           float* W_out,
                            void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws,
                            size_t ws_bytes, void* stream);
 

@@ -356,7 +356,7 @@ def _check_mask_in(mask_in, n, k):
 
 
 def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
-                qparams_out=None):
+                qparams_out=None, values_in=None, w0_out=None):
     """Column sweep with every column's update applied to all later columns at once.
 
     Processing column j: w0 = W[:, j]; p = w0 * m_j; e = (w0 - p) / L_jj and
@@ -370,7 +370,9 @@ def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None,
     the group's current values (quant_grid); a kept weight becomes its grid
     value and a pruned one 0, and the compensation carries both errors.
     qparams_out (a list) receives (scale, zero) arrays of shape (n,) per group.
-    Returns (W_hat, keep).
+    Test hooks: values_in (n x k) replaces the value every kept weight takes
+    (as mask_in replaces the mask); w0_out (n x k) receives each column's value
+    when it was processed.  Returns (W_hat, keep).
     """
     W = _f64(W).copy()
     L = _f64(L)
@@ -399,6 +401,10 @@ def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None,
                 qs, qz = _group_grids(W[:, j:j + quant[1]], quant[0], qparams_out)
             w0 = W[:, j].copy()
             p = _kept_value(w0, keep[:, j], quant, qs, qz)
+            if values_in is not None:
+                p = np.where(keep[:, j], _f64(values_in[:, j]), 0.0)
+            if w0_out is not None:
+                w0_out[:, j] = w0
             e = (w0 - p) / L[j, j]
             W[:, j] = p
             W[:, j + 1:] -= np.outer(e, L[j + 1:, j]) - np.outer(w0, D[j, j + 1:])
@@ -408,11 +414,11 @@ def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None,
 
 
 def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
-                  qparams_out=None):
+                  qparams_out=None, values_in=None, w0_out=None):
     """Algorithm 1: in-block sequential updates, then one lazy batch update
     W[:, rest] -= E L[rest, blk]^T - W0 D[blk, rest] per block (reading R-lazy:
-    W0 holds each column's value at the time it was processed).  nm, quant and
-    qparams_out as in sweep_eager.  scores_out receives, per block, the scores each weight's
+    W0 holds each column's value at the time it was processed).  nm, quant,
+    qparams_out, values_in and w0_out as in sweep_eager.  scores_out receives, per block, the scores each weight's
     selection used.  Returns (W_hat, keep).
     """
     W = _f64(W).copy()
@@ -445,6 +451,10 @@ def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=Non
                 qs, qz = _group_grids(W[:, j:min(j + quant[1], j1)], quant[0], qparams_out)
             w0 = W[:, j].copy()
             p = _kept_value(w0, keep[:, j], quant, qs, qz)
+            if values_in is not None:
+                p = np.where(keep[:, j], _f64(values_in[:, j]), 0.0)
+            if w0_out is not None:
+                w0_out[:, j] = w0
             e = (w0 - p) / L[j, j]
             E[:, j - j0] = e
             W0[:, j - j0] = w0

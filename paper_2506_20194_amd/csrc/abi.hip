@@ -203,38 +203,48 @@ duo_status duo_score_terms(const float* L, int64_t ldl, const float* G, int64_t 
 }
 
 static duo_status sweep_args(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, double w_sparsity,
-                             int32_t nm_n, int32_t block, float* W_out) {
+                             const duo_sweep_opts* opts, int32_t block, float* W_out, SweepOpts* o) {
   if (!W || !W_out || !dtype_ok(w_dtype)) return DUO_ERR_INVALID_ARG;
   if (n < 1 || ldw < k || !finite_in(w_sparsity, 0.0, 1.0)) return DUO_ERR_INVALID_ARG;
   if (block < 1 || block > kMaxBlock) return DUO_ERR_INVALID_ARG;
-  if (nm_n < 0 || nm_n > 4 || (nm_n > 0 && (k % 4 != 0 || block % 4 != 0))) return DUO_ERR_INVALID_ARG;
+  *o = SweepOpts{};
+  if (opts) {
+    const int nm = opts->nm_n, qb = opts->q_bits, qg = opts->q_group;
+    if (nm < 0 || nm > 4 || (nm > 0 && (k % 4 != 0 || block % 4 != 0))) return DUO_ERR_INVALID_ARG;
+    if (qb != 0 && (qb < 2 || qb > 8)) return DUO_ERR_INVALID_ARG;
+    if (qb > 0 && !((qg == 16 || qg == 32 || qg == 64 || qg == 128) && block % qg == 0)) return DUO_ERR_INVALID_ARG;
+    *o = SweepOpts{nm, qb, qb > 0 ? qg : 0, qb > 0 ? opts->q_scale_out : nullptr, qb > 0 ? opts->q_zero_out : nullptr};
+  }
   if (!k_ok(k)) return k < 1 ? DUO_ERR_INVALID_ARG : DUO_ERR_UNSUPPORTED;
   if (n > INT32_MAX / 2 || n * k > ((int64_t)1 << 40)) return DUO_ERR_UNSUPPORTED;
   return DUO_OK;
 }
 
 duo_status duo_sweep(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L, int64_t ldl,
-                     const float* D, int64_t ldd, const float* fac, double w_sparsity, int32_t nm_n,
+                     const float* D, int64_t ldd, const float* fac, double w_sparsity, const duo_sweep_opts* opts,
                      int32_t block, const uint32_t* mask_in, float* W_out, void* W_out_lowp, uint32_t* mask_out,
                      float* block_scores_out, void* ws, size_t ws_bytes, void* stream) {
-  duo_status a = sweep_args(W, w_dtype, n, k, ldw, w_sparsity, nm_n, block, W_out);
+  SweepOpts o;
+  duo_status a = sweep_args(W, w_dtype, n, k, ldw, w_sparsity, opts, block, W_out, &o);
   if (a != DUO_OK) return a;
   if (!L || !D || !fac || ldl < k || ldd < k) return DUO_ERR_INVALID_ARG;
   if (!ws_ok(ws, ws_bytes, sweep_ws_bytes(n, k, block))) return DUO_ERR_WORKSPACE;
   duo_status d = device_ok();
   if (d != DUO_OK) return d;
   prof_begin(DUO_PROF_SWEEP, (hipStream_t)stream);
-  duo_status r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, D, ldd, fac, w_sparsity, nm_n, block, mask_in, W_out,
+  duo_status r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, D, ldd, fac, w_sparsity, o, block, mask_in, W_out,
                            W_out_lowp, mask_out, block_scores_out, ws, (hipStream_t)stream);
   prof_end(DUO_PROF_SWEEP, (hipStream_t)stream);
   return r;
 }
 
 duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L,
-                           int64_t ldl, const float* G, int64_t ldg, const float* a, double w_sparsity, int32_t nm_n,
-                           int32_t block, const uint32_t* mask_in, float* W_out, void* W_out_lowp,
-                           uint32_t* mask_out, float* block_scores_out, void* ws, size_t ws_bytes, void* stream) {
-  duo_status e = sweep_args(W, w_dtype, n, k, ldw, w_sparsity, nm_n, block, W_out);
+                           int64_t ldl, const float* G, int64_t ldg, const float* a, double w_sparsity,
+                           const duo_sweep_opts* opts, int32_t block, const uint32_t* mask_in, float* W_out,
+                           void* W_out_lowp, uint32_t* mask_out, float* block_scores_out, void* ws, size_t ws_bytes,
+                           void* stream) {
+  SweepOpts o;
+  duo_status e = sweep_args(W, w_dtype, n, k, ldw, w_sparsity, opts, block, W_out, &o);
   if (e != DUO_OK) return e;
   if (!L || !G || !a || ldl < k || ldg < k) return DUO_ERR_INVALID_ARG;
   const PruneWs pw = carve_prune(nullptr, n, k, block);
@@ -248,7 +258,7 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   prof_end(DUO_PROF_SCORE, s);
   if (r != DUO_OK) return r;
   prof_begin(DUO_PROF_SWEEP, s);
-  r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, w.D, k, w.fac, w_sparsity, nm_n, block, mask_in, W_out, W_out_lowp,
+  r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, w.D, k, w.fac, w_sparsity, o, block, mask_in, W_out, W_out_lowp,
                 mask_out, block_scores_out, w.sweep, s);
   prof_end(DUO_PROF_SWEEP, s);
   return r;

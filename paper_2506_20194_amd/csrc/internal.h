@@ -86,10 +86,20 @@ duo_status score_run(const float* L, int64_t ldl, const float* G, int64_t ldg, c
                      float* D, int64_t ldd, float* fac, void* ws, hipStream_t s);
 
 size_t sweep_ws_bytes(int64_t n, int64_t k, int B);
-// nm_n > 0: the N:4 variant (nm_n of every 4 consecutive columns of a row
-// pruned, chosen when the sweep reaches the group); p_w is then unused.
+// Sweep options (validated by the caller).  nm_n > 0: the N:4 variant (nm_n
+// of every 4 consecutive columns of a row pruned, chosen when the sweep reaches
+// the group; p_w unused).  q_bits > 0: joint RTN quantisation with one grid per
+// row and group of q_group columns (q_group in {16, 32, 64, 128}, dividing B);
+// q_scale / q_zero (NULL or n x ceil(k / q_group)) receive the grids.
+struct SweepOpts {
+  int nm_n = 0;
+  int q_bits = 0;
+  int q_group = 0;
+  float* q_scale = nullptr;
+  float* q_zero = nullptr;
+};
 duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L,
-                     int64_t ldl, const float* D, int64_t ldd, const float* fac, double p_w, int nm_n, int B,
+                     int64_t ldl, const float* D, int64_t ldd, const float* fac, double p_w, const SweepOpts& o, int B,
                      const uint32_t* mask_in, float* W_out, void* W_out_lowp, uint32_t* mask_out,
                      float* scores_out, void* ws, hipStream_t s);
 

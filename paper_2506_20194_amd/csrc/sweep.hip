@@ -286,6 +286,16 @@ struct IbRow {
   uint32_t kb[IB_I]; // keep bits of the row: bit o of kb[g] is column 16 g + o
   float f[IB_I];     // N:M only: score factors of this lane's columns
   float sc[IB_I];    // N:M only: the scores the group selections used
+  float qs, qz;      // quantisation only: the row's current grid (step, code of 0)
+};
+
+// Options of the sweep that the in-block kernel applies.
+struct IbOpts {
+  int nm_n;      // N of N:4 (MODE_NM)
+  int q_bits;    // quantisation: bits of the grid (QUANT)
+  int q_group;   // columns per grid: 16, 32, 64 or 128
+  float* q_scale;  // NULL or n x ceil(k / q_group)
+  float* q_zero;
 };
 
 // LDS operands of one column step: the staged L and D entries of this lane's
@@ -342,19 +352,63 @@ __device__ __forceinline__ void nm_select(IbRow& s, int nm_n) {
   s.kb[G] = (s.kb[G] & ~(0xFu << O)) | (keep << O);
 }
 
-template <int J, bool NM>
+// Joint quantisation: at the first column of a group of q_group columns the
+// row's grid is fixed from the group's current values (min and max over the
+// row's 16 lanes, 0 always inside the range, [-1, 1] for an empty range).
+template <int G>
+__device__ __forceinline__ void quant_grid(IbRow& s, const IbOpts& opt, int64_t row, bool rv, int q, int gcol,
+                                           int ngroups) {
+  const int i1 = G + opt.q_group / IB_Q;  // slots G .. i1-1 hold the group's columns
+  float mn = 0.f, mx = 0.f;
+#pragma unroll
+  for (int i = G; i < IB_I; ++i)
+    if (i < i1) {
+      mn = fminf(mn, s.w[i]);
+      mx = fmaxf(mx, s.w[i]);
+    }
+#pragma unroll
+  for (int d = 8; d > 0; d >>= 1) {
+    mn = fminf(mn, __shfl_xor(mn, d));
+    mx = fmaxf(mx, __shfl_xor(mx, d));
+  }
+  if (mn == mx) {
+    mn = -1.f;
+    mx = 1.f;
+  }
+  s.qs = (mx - mn) / (float)((1 << opt.q_bits) - 1);
+  s.qz = rintf(-mn / s.qs);
+  if (q == 0 && rv) {
+    if (opt.q_scale) opt.q_scale[row * ngroups + gcol] = s.qs;
+    if (opt.q_zero) opt.q_zero[row * ngroups + gcol] = s.qz;
+  }
+}
+
+template <int J, bool NM, bool QUANT>
 __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* __restrict__ lq,
                                         const float* __restrict__ dq, const float* __restrict__ il, int q,
-                                        int nm_n) {
+                                        const IbOpts& opt, int64_t row, bool rv, int j0, int Bb, int ngroups) {
   constexpr int g = J / IB_Q, o = J % IB_Q;
   ib_load<J + 2>(buf[(J + 2) % 3], lq, dq, il, q);
-  if constexpr (NM && o % 4 == 0) nm_select<g, o>(s, nm_n);
+  if constexpr (NM && o % 4 == 0) nm_select<g, o>(s, opt.nm_n);
+  if constexpr (QUANT && o == 0) {
+    // groups start inside the block only (a short last block has no more)
+    if (J < Bb && J % opt.q_group == 0) quant_grid<g>(s, opt, row, rv, q, (j0 + J) / opt.q_group, ngroups);
+  }
   const IbBuf& b = buf[J % 3];
   const float v = row_bcast<o>(s.w[g]);
   const bool kj = (s.kb[g] >> o) & 1u;
-  const float u = kj ? 0.f : v;
+  // p: the value the column keeps (its grid value with QUANT), u = v - p the
+  // error the later columns compensate
+  float p;
+  if constexpr (QUANT) {
+    const float code = fminf(fmaxf(rintf(v / s.qs) + s.qz, 0.f), (float)((1 << opt.q_bits) - 1));
+    p = kj ? s.qs * (code - s.qz) : 0.f;
+  } else {
+    p = kj ? v : 0.f;
+  }
+  const float u = v - p;
   if (q == o) {
-    s.w[g] = v - u;
+    s.w[g] = p;
     s.e[g] = u * b.il;
     s.w0[g] = v;
   }
@@ -364,24 +418,26 @@ __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* 
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <bool NM, int... Js>
+template <bool NM, bool QUANT, int... Js>
 __device__ __forceinline__ void ib_steps(IbRow& s, const float* lq, const float* dq, const float* il, int q,
-                                         int nm_n, std::integer_sequence<int, Js...>) {
+                                         const IbOpts& opt, int64_t row, bool rv, int j0, int Bb, int ngroups,
+                                         std::integer_sequence<int, Js...>) {
   IbBuf buf[3];
   ib_load<0>(buf[0], lq, dq, il, q);
   ib_load<1>(buf[1], lq, dq, il, q);
-  (ib_step<Js, NM>(s, buf, lq, dq, il, q, nm_n), ...);
+  (ib_step<Js, NM, QUANT>(s, buf, lq, dq, il, q, opt, row, rv, j0, Bb, ngroups), ...);
 }
 
 // NM: the N:M variant (mode MODE_NM): the keep bits are chosen inside the
 // column loop, and the scores they used go to scores_out when it is set.
-template <bool NM>
+// QUANT: joint RTN quantisation of the kept weights (grids per row and group).
+template <bool NM, bool QUANT>
 __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int64_t ew_ld,
                                                       const float* __restrict__ L, int64_t ldl,
                                                       const float* __restrict__ D, int64_t ldd,
                                                       const float* __restrict__ fac, const SelState* st, int mode,
                                                       const uint32_t* __restrict__ mask_in, float* __restrict__ EW,
-                                                      uint8_t* __restrict__ bmask, int nm_n,
+                                                      uint8_t* __restrict__ bmask, IbOpts opt,
                                                       float* __restrict__ scores_out) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
   float* lq = sm;                       // [j][q][i]: L[j0+q+16i][j0+j] / L[j0+j][j0+j] where q+16i > j, else 0
@@ -468,7 +524,10 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
     const unsigned long long ball = __ballot(keep);
     s.kb[i] = (uint32_t)(ball >> (IB_Q * (lane >> 4))) & 0xFFFFu;
   }
-  ib_steps<NM>(s, lq, dq, il, q, nm_n, std::make_integer_sequence<int, kMaxBlock>{});
+  const int ngroups = QUANT ? (k + opt.q_group - 1) / opt.q_group : 0;
+  s.qs = 1.f;
+  s.qz = 0.f;
+  ib_steps<NM, QUANT>(s, lq, dq, il, q, opt, row, rv, j0, Bb, ngroups, std::make_integer_sequence<int, kMaxBlock>{});
 #pragma unroll
   for (int i = 0; i < IB_I; ++i) {
     const int c = q + IB_Q * i;
@@ -548,7 +607,7 @@ SweepWs carve(void* ws, int64_t n, int64_t k, int B) {
 size_t sweep_ws_bytes(int64_t n, int64_t k, int B) { return carve(nullptr, n, k, B).bytes; }
 
 duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L, int64_t ldl,
-                     const float* D, int64_t ldd, const float* fac, double p_w, int nm_n, int B,
+                     const float* D, int64_t ldd, const float* fac, double p_w, const SweepOpts& o, int B,
                      const uint32_t* mask_in, float* W_out, void* W_out_lowp, uint32_t* mask_out, float* scores_out,
                      void* ws, hipStream_t s) {
   const SweepWs w = carve(ws, n, k, B);
@@ -560,8 +619,11 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   hipLaunchKernelGGL(sel_reset_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist);
   DUO_LAUNCH_CHECK();
   const size_t ib_lds = (size_t)(2 * kMaxBlock * IB_JS + kMaxBlock) * sizeof(float);
-  const bool nm = nm_n > 0 && !mask_in;
-  auto ib_kern = nm ? inblock_kernel<true> : inblock_kernel<false>;
+  const bool nm = o.nm_n > 0 && !mask_in;
+  const bool qt = o.q_bits > 0;
+  auto ib_kern = nm ? (qt ? inblock_kernel<true, true> : inblock_kernel<true, false>)
+                    : (qt ? inblock_kernel<false, true> : inblock_kernel<false, false>);
+  const IbOpts ibo{o.nm_n, o.q_bits, qt ? o.q_group : kMaxBlock, o.q_scale, o.q_zero};
   DUO_HIP_TRY(hipFuncSetAttribute((const void*)ib_kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ib_lds));
   const size_t sel_lds = (size_t)(16 + (1 << kDigit)) * sizeof(uint32_t) + (size_t)kSelCap * sizeof(unsigned long long);
   DUO_HIP_TRY(
@@ -605,7 +667,7 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     const int64_t sb0 = j0 / S * S, sb1 = sb0 + S < k ? sb0 + S : k;
     hipLaunchKernelGGL(ib_kern, dim3((unsigned)cdiv(n, IB_ROWS)), dim3(256), ib_lds, s, W_out, (int)n, (int)k,
                        (int)j0, Bb, (int64_t)2 * S, L, ldl, D, ldd, fac, (const SelState*)w.st, mode, mask_in,
-                       w.EW + (j0 - sb0), w.bmask, nm_n, scores_out);
+                       w.EW + (j0 - sb0), w.bmask, ibo, scores_out);
     DUO_LAUNCH_CHECK();
     prof_end(DUO_PROF_INBLOCK, s);
     // inside the super-block: columns [j1, sb1) from this block (K = Bb);

@@ -44,6 +44,11 @@ class ActRule(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("sparsity", ctypes.c_double)]
 
 
+class SweepOpts(ctypes.Structure):
+    _fields_ = [("nm_n", ctypes.c_int32), ("q_bits", ctypes.c_int32), ("q_group", ctypes.c_int32),
+                ("q_scale_out", ctypes.c_void_p), ("q_zero_out", ctypes.c_void_p)]
+
+
 class CholInfo(ctypes.Structure):
     _fields_ = [("lam", ctypes.c_double), ("fail_index", ctypes.c_int64), ("status", ctypes.c_int32)]
 
@@ -80,10 +85,11 @@ def lib():
         L.duo_score_terms.restype = I32
         L.duo_score_terms.argtypes = [P, I64, P, I64, P, I64, P, I64, P, P, SZ, P]
         L.duo_sweep.restype = I32
-        L.duo_sweep.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, I32, P, P, P, P, P, P, SZ, P]
+        L.duo_sweep.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, ctypes.POINTER(SweepOpts), I32, P, P,
+                                P, P, P, P, SZ, P]
         L.duo_prune_layer.restype = I32
-        L.duo_prune_layer.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, I32, I32, P, P, P, P, P, P, SZ,
-                                      P]
+        L.duo_prune_layer.argtypes = [P, I32, I64, I64, I64, P, I64, P, I64, P, F64, ctypes.POINTER(SweepOpts), I32,
+                                      P, P, P, P, P, P, SZ, P]
         L.duo_block_workspace_size.restype = SZ
         L.duo_block_workspace_size.argtypes = [I32, I64, I64, I64]
         L.duo_rmsnorm.restype = I32
@@ -297,8 +303,26 @@ def _sweep_outputs(W, want_lowp, want_mask, want_scores):
     return W_out, lowp, mask, scores
 
 
+def _opts(W, nm_n, quant):
+    """(SweepOpts or None, q_scale, q_zero) for the sweep; quant = (bits, group)."""
+    if not nm_n and quant is None:
+        return None, None, None
+    n, k = W.shape
+    qs = qz = None
+    bits, group = (0, 0) if quant is None else (int(quant[0]), int(quant[1]))
+    if bits:
+        ng = (k + group - 1) // group
+        qs = torch.empty((n, ng), dtype=torch.float32, device=W.device)
+        qz = torch.empty((n, ng), dtype=torch.float32, device=W.device)
+    o = SweepOpts(int(nm_n), bits, group, qs.data_ptr() if qs is not None else None,
+                  qz.data_ptr() if qz is not None else None)
+    return o, qs, qz
+
+
 def duo_sweep(W, L, D, fac, w_sparsity, block=128, mask_in=None, want_lowp=False, want_mask=True,
-              want_scores=False, ws=None, out=None, nm_n=0):
+              want_scores=False, ws=None, out=None, nm_n=0, quant=None):
+    """Returns (W_out, W_lowp, mask, scores), plus (q_scale, q_zero) when
+    quant = (bits, group) is given."""
     n, k = W.shape
     _same_device(W, L, D, fac, mask_in, ws)
     _shape(L, (k, k), "L")
@@ -311,15 +335,21 @@ def duo_sweep(W, L, D, fac, w_sparsity, block=128, mask_in=None, want_lowp=False
         ws = workspace(DUO_OP_SWEEP, n, k, 0, block, W.device)
     W_out, lowp, mask, scores = out if out is not None else _sweep_outputs(W, want_lowp, want_mask, want_scores)
     _check_outputs((W_out, lowp, mask, scores), W)
+    o, qs, qz = _opts(W, nm_n, quant)
     st = lib().duo_sweep(_ptr(W), _dtype(W), n, k, _ld(W), _ptr(L), _ld(L), _ptr(D), _ld(D), _ptr(fac),
-                         float(w_sparsity), int(nm_n), int(block), _ptr(mask_in), _ptr(W_out), _ptr(lowp),
-                         _ptr(mask), _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
+                         float(w_sparsity), ctypes.byref(o) if o is not None else None, int(block), _ptr(mask_in),
+                         _ptr(W_out), _ptr(lowp), _ptr(mask), _ptr(scores), _ptr(ws), ws.numel(),
+                         _stream(W.device))
     _check(st, "duo_sweep")
+    if quant is not None:
+        return W_out, lowp, mask, scores, qs, qz
     return W_out, lowp, mask, scores
 
 
 def duo_prune_layer(W, L, G, a, w_sparsity, block=128, mask_in=None, want_lowp=False, want_mask=True,
-                    want_scores=False, ws=None, out=None, nm_n=0):
+                    want_scores=False, ws=None, out=None, nm_n=0, quant=None):
+    """Returns (W_out, W_lowp, mask, scores), plus (q_scale, q_zero) when
+    quant = (bits, group) is given."""
     n, k = W.shape
     _same_device(W, L, G, a, mask_in, ws)
     _shape(L, (k, k), "L")
@@ -332,10 +362,14 @@ def duo_prune_layer(W, L, G, a, w_sparsity, block=128, mask_in=None, want_lowp=F
         ws = workspace(DUO_OP_PRUNE_LAYER, n, k, 0, block, W.device)
     W_out, lowp, mask, scores = out if out is not None else _sweep_outputs(W, want_lowp, want_mask, want_scores)
     _check_outputs((W_out, lowp, mask, scores), W)
+    o, qs, qz = _opts(W, nm_n, quant)
     st = lib().duo_prune_layer(_ptr(W), _dtype(W), n, k, _ld(W), _ptr(L), _ld(L), _ptr(G), _ld(G), _ptr(a),
-                               float(w_sparsity), int(nm_n), int(block), _ptr(mask_in), _ptr(W_out), _ptr(lowp),
-                               _ptr(mask), _ptr(scores), _ptr(ws), ws.numel(), _stream(W.device))
+                               float(w_sparsity), ctypes.byref(o) if o is not None else None, int(block),
+                               _ptr(mask_in), _ptr(W_out), _ptr(lowp), _ptr(mask), _ptr(scores), _ptr(ws),
+                               ws.numel(), _stream(W.device))
     _check(st, "duo_prune_layer")
+    if quant is not None:
+        return W_out, lowp, mask, scores, qs, qz
     return W_out, lowp, mask, scores
 
 
@@ -413,7 +447,7 @@ def duo_permute_mask(words, k, col_idx, out=None):
 
 
 def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=None, want_lowp=True,
-                 act_order=False, nm=None):
+                 act_order=False, nm=None, quant=None):
     """DuoGPT on one linear layer (stages 1-3 on the device).
 
     W: n x k (out x in), X: m x k token-major calibration input of the pruned
@@ -422,6 +456,9 @@ def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=N
     the outputs are returned in the original channel order.
     nm: None, or (N, 4) for the N:4 semi-structured variant (App. B), in which
     w_sparsity is not used; not combined with act_order.
+    quant: None, or (bits, group) for joint RTN quantisation (Table 4); the
+    grids (q_scale, q_zero: n x ceil(k / group)) are returned too (in the
+    permuted channel order when act_order is set, as their groups are).
     Returns dict(W_out fp32, W_lowp in W's dtype, mask (bool n x k), lam, and
     perm when act_order).
     """
@@ -445,12 +482,16 @@ def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=N
         a = duo_permute(a.view(1, k), None, perm).view(k)
         W = duo_permute(W, None, perm)
     lam, _ = duo_chol_inv(H, damp)
-    W_out, lowp, mask, _ = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp, nm_n=nm_n)
+    res = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp, nm_n=nm_n, quant=quant)
+    W_out, lowp, mask = res[0], res[1], res[2]
     if act_order:
         W_out = duo_permute(W_out, None, inv)
         lowp = duo_permute(lowp, None, inv) if lowp is not None else None
         mask = duo_permute_mask(mask, k, inv)
-    return dict(W_out=W_out, W_lowp=lowp, mask=unpack_mask(mask, k), lam=lam, perm=perm)
+    out = dict(W_out=W_out, W_lowp=lowp, mask=unpack_mask(mask, k), lam=lam, perm=perm)
+    if quant is not None:
+        out["q_scale"], out["q_zero"] = res[4], res[5]
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -104,8 +104,11 @@ def test_chol_and_sweep_argument_errors(duo_lib):
     assert L.duo_score_terms(FAKE, 64, FAKE, 64, FAKE, 64, FAKE, 64, FAKE, WS, big, None) == NODEV
     assert L.duo_score_terms(FAKE, 64, None, 64, FAKE, 64, FAKE, 64, FAKE, WS, big, None) == E
 
-    def sweep(W=FAKE, dt=1, n=32, k=64, ldw=64, p=0.5, B=16, Wo=FAKE, fn=L.duo_sweep, nm=0):
-        return fn(W, dt, n, k, ldw, FAKE, 64, FAKE, 64, FAKE, p, nm, B, None, Wo, None, None, None, WS, big, None)
+    from paper_2506_20194_amd.duo import SweepOpts
+
+    def sweep(W=FAKE, dt=1, n=32, k=64, ldw=64, p=0.5, B=16, Wo=FAKE, fn=L.duo_sweep, nm=0, qb=0, qg=0):
+        o = ctypes.byref(SweepOpts(nm, qb, qg, None, None)) if (nm or qb or qg) else None
+        return fn(W, dt, n, k, ldw, FAKE, 64, FAKE, 64, FAKE, p, o, B, None, Wo, None, None, None, WS, big, None)
 
     for fn in (L.duo_sweep, L.duo_prune_layer):
         assert sweep(fn=fn) == NODEV
@@ -123,6 +126,13 @@ def test_chol_and_sweep_argument_errors(duo_lib):
         assert sweep(nm=-1, fn=fn) == E
         assert sweep(nm=2, B=18, fn=fn) == E       # B not a multiple of 4
         assert sweep(nm=2, k=62, ldw=64, fn=fn) == E
+        assert sweep(qb=4, qg=16, fn=fn) == NODEV  # quantisation grids of 16 columns in blocks of 16
+        assert sweep(qb=4, qg=16, B=32, nm=2, fn=fn) == NODEV
+        assert sweep(qb=1, qg=16, fn=fn) == E      # bits outside 2..8
+        assert sweep(qb=9, qg=16, fn=fn) == E
+        assert sweep(qb=4, qg=24, B=48, fn=fn) == E   # group not 16/32/64/128
+        assert sweep(qb=4, qg=32, B=16, fn=fn) == E   # group does not divide the block
+        assert sweep(qg=7, fn=fn) == NODEV         # the group is ignored without bits
 
 
 def test_binding_refuses_host_tensors(duo_lib):

@@ -697,3 +697,20 @@ def test_quant_last_column_is_ridge_optimum_given_frozen_prefix(quant):
         sc, z = qp[-1]
         v = sc * (np.clip(np.round(v / sc) + z, 0, 2 ** quant[0] - 1) - z)
     np.testing.assert_allclose(Wh[:, k - 1], np.where(keep, v, 0.0), rtol=0, atol=1e-12)
+
+
+def test_forced_values_hook_reproduces_the_run():
+    """values_in (a test hook, like mask_in) fed with a run's own output
+    reproduces that run, and w0_out holds the values the grids rounded."""
+    W, X = _layer(95, 8, 64, 256, scale_sigma=1.0)
+    H, G, a = R.hessian_terms(X, 0.5)
+    L, _ = R.inverse_cholesky(H, 0.01)
+    fac, D, _ = R.score_terms(G, L, a)
+    qp, w0 = [], np.zeros((8, 64))
+    Wh, keep = R.sweep_blocked(W, L, D, fac, 0.5, 32, quant=(4, 16), qparams_out=qp, w0_out=w0)
+    Wf, _ = R.sweep_blocked(W, L, D, fac, 0.5, 32, mask_in=keep, quant=(4, 16), values_in=Wh)
+    np.testing.assert_array_equal(Wf, Wh)
+    for gi, (sc, z) in enumerate(qp):
+        cols = slice(16 * gi, 16 * gi + 16)
+        want = sc[:, None] * (np.clip(np.round(w0[:, cols] / sc[:, None]) + z[:, None], 0, 15) - z[:, None])
+        np.testing.assert_array_equal(np.where(keep[:, cols], want, 0.0), Wh[:, cols])
