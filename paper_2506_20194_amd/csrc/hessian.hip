@@ -380,13 +380,15 @@ __global__ __launch_bounds__(256) void pack_kernel(const T* __restrict__ Xs, con
   }
 }
 
-// bf16 pack without LDS (16-byte aligned rows, k % 8 == 0).  Workgroup
-// (x, y) covers channels [512x, 512x + 512) of tokens [256y, 256y + 256): wave
-// w handles tokens 8w..8w+7 of every 32-token block, lane l channels
-// 512x + 8l .. +7.  Each lane loads its 8 x 8 tile with 16-byte reads,
-// applies the threshold in registers, transposes it (tokens become the
-// contiguous dimension) and stores one 16-byte vector per channel: exactly
-// the packed layout above.
+// bf16 pack (16-byte aligned rows, k % 8 == 0).  Workgroup (x, y) covers
+// channels [512x, 512x + 512) of tokens [256y, 256y + 256): wave w handles
+// tokens 8w..8w+7 of every 32-token block, lane l channels 512x + 8l .. +7.
+// Each lane loads its 8 x 8 tile with 16-byte reads, applies the threshold in
+// registers and transposes it (tokens become the contiguous dimension): one
+// 16-byte vector per channel, exactly the packed layout above.  A wave's
+// vectors for one token block are 8 KB of contiguous output per operand;
+// they pass through LDS so that every global store writes 1 KB contiguously
+// (stored straight from registers, each store touched 64 cache lines).
 __device__ inline uint32_t lo_pair(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
 __device__ inline uint32_t hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
 
@@ -397,10 +399,10 @@ __global__ __launch_bounds__(256) void pack16_kernel(const uint16_t* __restrict_
                                                      uint16_t* __restrict__ Pz, uint16_t* __restrict__ Pl,
                                                      float* __restrict__ apart) {
   __shared__ float red[4][512];
+  __shared__ u32x4 stg[4][576];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c0 = blockIdx.x * 512 + 8 * lane;
   const bool cv = c0 < k;   // all 8 channels valid (k % 8 == 0) or none
-  const bool cw = c0 < kp;  // inside the packed width
   float acc[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) acc[j] = 0.f;
@@ -452,22 +454,32 @@ __global__ __launch_bounds__(256) void pack16_kernel(const uint16_t* __restrict_
         ol[e][w2] = lv[0] | (lv[1] << 16);
       }
     }
-    if (cw) {
-      const int64_t base = ((int64_t)(tb * (kTokBlk / 8) + wave) * kp + c0) * 8;
+    {
+      // the wave's output for this token block is 512 contiguous 16-byte
+      // chunks per operand (chunk 8 lane + j); staged through LDS (skewed by
+      // one chunk per lane) so that each global store writes 1 KB contiguously
+      u32x4* sw = stg[wave];
+      const int64_t wbase = ((int64_t)(tb * (kTokBlk / 8) + wave) * kp + blockIdx.x * 512) * 8;
+      auto put = [&](uint16_t* P, const u32x4 (&o)[8]) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int w2 = j >> 1;
-        u32x4 vh, vz, vl;
+        for (int j = 0; j < 8; ++j) {
+          const int w2 = j >> 1;
+          u32x4 v;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          vh[p] = (j & 1) ? hi_pair(oh[2 * p][w2], oh[2 * p + 1][w2]) : lo_pair(oh[2 * p][w2], oh[2 * p + 1][w2]);
-          vz[p] = (j & 1) ? hi_pair(oz[2 * p][w2], oz[2 * p + 1][w2]) : lo_pair(oz[2 * p][w2], oz[2 * p + 1][w2]);
-          vl[p] = (j & 1) ? hi_pair(ol[2 * p][w2], ol[2 * p + 1][w2]) : lo_pair(ol[2 * p][w2], ol[2 * p + 1][w2]);
+          for (int p = 0; p < 4; ++p)
+            v[p] = (j & 1) ? hi_pair(o[2 * p][w2], o[2 * p + 1][w2]) : lo_pair(o[2 * p][w2], o[2 * p + 1][w2]);
+          sw[9 * lane + j] = v;
         }
-        *(u32x4*)(Ph + base + 8 * j) = vh;
-        *(u32x4*)(Pz + base + 8 * j) = vz;
-        if (TWO) *(u32x4*)(Pl + base + 8 * j) = vl;
-      }
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const int q = 64 * jj + lane;
+          const u32x4 v = sw[q + (q >> 3)];
+          if (blockIdx.x * 512 + 8 * (q >> 3) < kp) *(u32x4*)(P + wbase + 8 * q) = v;
+        }
+      };
+      put(Ph, oh);
+      put(Pz, oz);
+      if (TWO) put(Pl, ol);
     }
   }
   // per-channel sum of dX^2 over this workgroup's tokens, fixed order
