@@ -306,10 +306,48 @@ enum {
   DUO_PROF_INBLOCK = 5,  /* stage 3: in-block kernel, one launch per block     */
   DUO_PROF_TRAIL = 6,    /* stage 3: lazy trailing-update GEMM, one per block  */
   DUO_PROF_SELECT = 7,   /* stage 3: mask selection passes of one block        */
-  DUO_PROF_COUNT = 8
+  DUO_PROF_DECODE = 8,   /* decode: the dual-sparse GEMV kernel                */
+  DUO_PROF_COUNT = 9
 };
 duo_status duo_profile_enable(int32_t on);
 duo_status duo_profile_read(int32_t kernel, double* total_ms, int64_t* launches);
+
+/*
+ * Dual-sparse decode (Preliminaries "Activation Sparsity", Sec. 4.1): at
+ * decoding time a pruned linear layer computes y = W (x * m^x), the sum over
+ * the input channels i whose activation survives of W[:, i] x_i, so only
+ * those weight columns are read, each stored compressed (the paper leaves this
+ * kernel to future work; the storage is this library's own):
+ *   col_ptr    k + 1 int64: channel i's kept values are values[col_ptr[i] ..
+ *              col_ptr[i + 1]);
+ *   maskT      k x ceil(n/32) uint32, channel-major: bit r % 32 of word r / 32
+ *              of channel i set when W[r][i] is kept;
+ *   chunk_off  k x ceil(n/256) uint16: kept weights of channel i in rows
+ *              [0, 256 c);
+ *   values     col_ptr[k] bf16 (bit patterns): each channel's kept weights in
+ *              row order; the allocation holds col_ptr[k] + 8 elements and is
+ *              16-byte aligned (the GEMV reads aligned 16-byte windows).
+ * Limits: n <= 65535 (duo_dsc_gemv: n <= 32768), k <= 32768.  Workspace:
+ * duo_dsc_workspace_size(n, k).
+ *
+ * duo_dsc_layout - col_ptr, maskT and chunk_off from a pruned layer's mask
+ *   (n x ceil(k/32) words as duo_sweep writes it).  The caller then reads
+ *   col_ptr[k] (the number of kept weights) to size values.
+ * duo_dsc_pack - values from the pruned weights W (n x k, ldw, fp32 rounded to
+ *   nearest even bf16, or bf16 copied) and the layout.
+ * duo_dsc_gemv - one decode step: x (k, x_dtype) is sparsified with `rule`
+ *   (the calibration rule: the smallest (|x|, channel) entries zeroed), then
+ *   y (n fp32) = sum over kept channels of W[:, i] x_i, products of bf16
+ *   weights and activations in fp32, summed in a fixed order (deterministic).
+ */
+size_t duo_dsc_workspace_size(int64_t n, int64_t k);
+duo_status duo_dsc_layout(const uint32_t* mask, int64_t n, int64_t k, int64_t* col_ptr, uint32_t* maskT,
+                          uint16_t* chunk_off, void* ws, size_t ws_bytes, void* stream);
+duo_status duo_dsc_pack(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const int64_t* col_ptr,
+                        const uint32_t* maskT, const uint16_t* chunk_off, uint16_t* values, void* stream);
+duo_status duo_dsc_gemv(const void* x, int32_t x_dtype, int64_t n, int64_t k, duo_act_rule rule,
+                        const int64_t* col_ptr, const uint32_t* maskT, const uint16_t* chunk_off,
+                        const uint16_t* values, float* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Decoder-block harness.  When a whole decoder block is pruned group by group,

@@ -12,7 +12,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libduo.so")
 SOURCES = ["abi.hip", "hessian.hip", "gemm_f32.hip", "chol.hip", "score.hip", "sweep.hip", "profile.hip",
-           "block.hip", "permute.hip"]
+           "block.hip", "permute.hip", "decode.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

@@ -9,7 +9,10 @@
 #define DUO_HIP_TRY(expr)                         \
   do {                                            \
     hipError_t duo_e_ = (expr);                   \
-    if (duo_e_ != hipSuccess) return DUO_ERR_HIP; \
+    if (duo_e_ != hipSuccess) {                   \
+      (void)hipGetLastError(); /* not sticky */   \
+      return DUO_ERR_HIP;                         \
+    }                                             \
   } while (0)
 
 #define DUO_LAUNCH_CHECK() DUO_HIP_TRY(hipGetLastError())
@@ -25,6 +28,7 @@ constexpr size_t kAlign = 256;
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ inline int64_t rup(int64_t a, int64_t b) { return cdiv(a, b) * b; }

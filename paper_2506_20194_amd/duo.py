@@ -28,9 +28,10 @@ EXPORTED = (
     "duo_hessian_accum", "duo_residual_term", "duo_chol_inv", "duo_score_terms", "duo_sweep",
     "duo_prune_layer", "duo_profile_enable", "duo_profile_read", "duo_block_workspace_size", "duo_rmsnorm",
     "duo_act_sparsify", "duo_linear", "duo_rope", "duo_attention", "duo_silu_mul", "duo_act_order",
-    "duo_permute", "duo_permute_mask",
+    "duo_permute", "duo_permute_mask", "duo_dsc_workspace_size", "duo_dsc_layout", "duo_dsc_pack",
+    "duo_dsc_gemv",
 )
-PROF = dict(gram=0, hessian=1, chol=2, score=3, sweep=4, inblock=5, trail=6, select=7)
+PROF = dict(gram=0, hessian=1, chol=2, score=3, sweep=4, inblock=5, trail=6, select=7, decode=8)
 DUO_BOP_ACT_SPARSIFY, DUO_BOP_LINEAR, DUO_BOP_ATTENTION = 0, 1, 2
 
 
@@ -110,6 +111,14 @@ def lib():
         L.duo_permute.argtypes = [P, I32, I64, I64, I64, P, P, I64, I64, P, I64, P]
         L.duo_permute_mask.restype = I32
         L.duo_permute_mask.argtypes = [P, I64, I64, P, P, P]
+        L.duo_dsc_workspace_size.restype = SZ
+        L.duo_dsc_workspace_size.argtypes = [I64, I64]
+        L.duo_dsc_layout.restype = I32
+        L.duo_dsc_layout.argtypes = [P, I64, I64, P, P, P, P, SZ, P]
+        L.duo_dsc_pack.restype = I32
+        L.duo_dsc_pack.argtypes = [P, I32, I64, I64, I64, P, P, P, P, P]
+        L.duo_dsc_gemv.restype = I32
+        L.duo_dsc_gemv.argtypes = [P, I32, I64, I64, ActRule, P, P, P, P, P, P, SZ, P]
         L.duo_profile_enable.restype = I32
         L.duo_profile_enable.argtypes = [I32]
         L.duo_profile_read.restype = I32
@@ -492,6 +501,61 @@ def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=N
     if quant is not None:
         out["q_scale"], out["q_zero"] = res[4], res[5]
     return out
+
+
+# ---------------------------------------------------------------------------
+# dual-sparse decode (compressed columns, activation-sparse GEMV)
+# ---------------------------------------------------------------------------
+
+def dsc_workspace(n: int, k: int, device) -> torch.Tensor:
+    nbytes = int(lib().duo_dsc_workspace_size(n, k))
+    if nbytes == 0:
+        raise DuoError(DUO_ERR_UNSUPPORTED, "duo_dsc_workspace_size")
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def dsc_compress(W, mask, ws=None):
+    """Compressed decode storage of a pruned layer: W (n x k fp32 or bf16, the
+    pruned weights) and its bit mask (n x ceil(k/32) words as the sweep writes
+    it).  Returns dict(col_ptr, maskT, chunk_off, values, n, k)."""
+    n, k = W.shape
+    _shape(mask, (n, (k + 31) // 32), "mask")
+    _contig(mask, "mask")
+    dev = W.device
+    _same_device(W, mask, ws)
+    if ws is None:
+        ws = dsc_workspace(n, k, dev)
+    col_ptr = torch.empty(k + 1, dtype=torch.int64, device=dev)
+    maskT = torch.empty((k, (n + 31) // 32), dtype=torch.int32, device=dev)
+    chunk_off = torch.empty((k, (n + 255) // 256), dtype=torch.int16, device=dev)
+    st = lib().duo_dsc_layout(_ptr(mask), n, k, _ptr(col_ptr), _ptr(maskT), _ptr(chunk_off), _ptr(ws), ws.numel(),
+                              _stream(dev))
+    _check(st, "duo_dsc_layout")
+    nnz = int(col_ptr[k].item())
+    values = torch.zeros(nnz + 8, dtype=torch.int16, device=dev)  # + 8: the GEMV reads aligned 16-byte windows
+    st = lib().duo_dsc_pack(_ptr(W), _dtype(W), n, k, _ld(W), _ptr(col_ptr), _ptr(maskT), _ptr(chunk_off),
+                            _ptr(values), _stream(dev))
+    _check(st, "duo_dsc_pack")
+    return dict(col_ptr=col_ptr, maskT=maskT, chunk_off=chunk_off, values=values, n=n, k=k)
+
+
+def dsc_gemv(comp, x, act_sparsity, ws=None, out=None):
+    """One decode step y = W (x * m^x) over the compressed columns: x (k,)
+    fp32 or bf16, sparsified with the calibration rule; y (n,) fp32."""
+    n, k = comp["n"], comp["k"]
+    if x.dim() != 1 or x.shape[0] != k:
+        raise ValueError(f"x must have shape ({k},)")
+    _contig(x, "x")
+    dev = x.device
+    if ws is None:
+        ws = dsc_workspace(n, k, dev)
+    y = out if out is not None else torch.empty(n, dtype=torch.float32, device=dev)
+    _same_device(x, y, ws, comp["values"])
+    st = lib().duo_dsc_gemv(_ptr(x), _dtype(x), n, k, act_rule(act_sparsity), _ptr(comp["col_ptr"]),
+                            _ptr(comp["maskT"]), _ptr(comp["chunk_off"]), _ptr(comp["values"]), _ptr(y), _ptr(ws),
+                            ws.numel(), _stream(dev))
+    _check(st, "duo_dsc_gemv")
+    return y
 
 
 # ---------------------------------------------------------------------------

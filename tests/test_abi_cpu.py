@@ -207,3 +207,24 @@ def test_act_order_argument_errors(duo_lib):
     assert L.duo_permute_mask(FAKE, 8, 64, FAKE, FAKE, None) == E
     assert L.duo_permute_mask(FAKE, -1, 64, FAKE, OTHER, None) == E
     assert L.duo_permute_mask(FAKE, 0, 64, FAKE, OTHER, None) == duo_lib.DUO_OK
+
+
+def test_decode_argument_errors(duo_lib):
+    L = duo_lib.lib()
+    E, NODEV = duo_lib.DUO_ERR_INVALID_ARG, duo_lib.DUO_ERR_NO_DEVICE
+    ws = L.duo_dsc_workspace_size(4096, 4096)
+    assert ws >= 4096 * 8 and L.duo_dsc_workspace_size(70000, 16) == 0 and L.duo_dsc_workspace_size(0, 16) == 0
+    big = 10 ** 10
+    assert L.duo_dsc_layout(FAKE, 64, 32, FAKE, FAKE, FAKE, WS, big, None) == NODEV
+    assert L.duo_dsc_layout(None, 64, 32, FAKE, FAKE, FAKE, WS, big, None) == E
+    assert L.duo_dsc_layout(FAKE, 0, 32, FAKE, FAKE, FAKE, WS, big, None) == E
+    assert L.duo_dsc_layout(FAKE, 70000, 32, FAKE, FAKE, FAKE, WS, big, None) == duo_lib.DUO_ERR_UNSUPPORTED
+    assert L.duo_dsc_layout(FAKE, 64, 32, FAKE, FAKE, FAKE, WS, 8, None) == duo_lib.DUO_ERR_WORKSPACE
+    assert L.duo_dsc_pack(FAKE, 1, 64, 32, 32, FAKE, FAKE, FAKE, FAKE, None) == NODEV
+    assert L.duo_dsc_pack(FAKE, 1, 64, 32, 31, FAKE, FAKE, FAKE, FAKE, None) == E
+    assert L.duo_dsc_pack(FAKE, 4, 64, 32, 32, FAKE, FAKE, FAKE, FAKE, None) == E
+    assert L.duo_dsc_gemv(FAKE, 1, 64, 32, _rule(), FAKE, FAKE, FAKE, FAKE, FAKE, WS, big, None) == NODEV
+    assert L.duo_dsc_gemv(FAKE, 1, 64, 32, _rule(1.5), FAKE, FAKE, FAKE, FAKE, FAKE, WS, big, None) == E
+    assert L.duo_dsc_gemv(FAKE, 1, 64, 32, _rule(), FAKE, FAKE, FAKE, None, FAKE, WS, big, None) == E
+    assert L.duo_dsc_gemv(FAKE, 1, 64, 32, _rule(), FAKE, FAKE, FAKE, FAKE, FAKE, WS, 16, None) == \
+        duo_lib.DUO_ERR_WORKSPACE
