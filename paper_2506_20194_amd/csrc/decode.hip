@@ -146,39 +146,19 @@ constexpr int kQV = (kWindowQ + 63) / 64;     // 16-byte value loads per lane: a
 constexpr int kSlotQ = 64 * kQV;              // a wave's value slot: every lane stores all of its loads
 constexpr int kTargetGroups = 256;            // one 1024-thread workgroup per CU
 
-__device__ inline int wave_sum(int v) {
-#pragma unroll
-  for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d);
-  return v;
-}
-
-// Block-wide sum with one barrier: two alternating slot sets, so a step's
-// writes never meet the previous step's reads.
-__device__ inline int block_count(int v, int (*sh)[kGemvWaves], int& par) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  v = wave_sum(v);
-  if (lane == 0) sh[par][wave] = v;
-  __syncthreads();
-  int t = 0;
-#pragma unroll
-  for (int w = 0; w < kGemvWaves; ++w) t += sh[par][w];
-  par ^= 1;
-  return t;
-}
-
 // Exclusive scan over the block's threads in thread order (two barriers).
-__device__ inline int block_excl_scan(int v, int* sh, int& total) {
+__device__ inline uint32_t block_excl_scan(uint32_t v, uint32_t* sh, uint32_t& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int incl = v;
+  uint32_t incl = v;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    const int o = __shfl_up(incl, d);
+    const uint32_t o = __shfl_up(incl, d);
     if (lane >= d) incl += o;
   }
   __syncthreads();
   if (lane == 63) sh[wave] = incl;
   __syncthreads();
-  int before = 0;
+  uint32_t before = 0;
   total = 0;
 #pragma unroll
   for (int w = 0; w < kGemvWaves; ++w) {
@@ -220,6 +200,105 @@ __device__ inline void load_mags(const T* __restrict__ x, int k, int c0, uint32_
   }
 }
 
+// bf16 magnitudes (15 bits): Tm = the z-th smallest (1 <= z < the number of
+// valid entries) and the number below it, from one LDS histogram of all 32768
+// magnitudes (one atomic per entry; bin b at word b + b / 32, so that thread
+// t's 32 bins [32 t, 32 t + 32) sit 33 words from its neighbours' and the
+// scan's reads are free of bank conflicts) and a block scan of the bins.
+constexpr int kHistWords = 32768 + 32768 / 32;
+
+template <int KPT>
+__device__ inline void hist_select(const uint32_t (&mag)[KPT], int z, uint32_t* hist, int* found, uint32_t* sh,
+                                   uint32_t& Tm, int& nbelow) {
+  const int t = threadIdx.x;
+  for (int q = t; q < kHistWords / 4; q += kGemvThreads) ((u32x4*)hist)[q] = u32x4{0u, 0u, 0u, 0u};
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < KPT; ++e)
+    if (mag[e] < 32768u) atomicAdd(&hist[mag[e] + (mag[e] >> 5)], 1u);
+  __syncthreads();
+  uint32_t sum = 0;
+#pragma unroll
+  for (int b = 0; b < 32; ++b) sum += hist[33 * t + b];
+  uint32_t tot;
+  const uint32_t before = block_excl_scan(sum, sh, tot);
+  if ((int)before < z && z <= (int)(before + sum)) {  // one thread: its bins again, all read at once
+    uint32_t h[32];
+#pragma unroll
+    for (int b = 0; b < 32; ++b) h[b] = hist[33 * t + b];
+    uint32_t run = before;
+    int fb = 0, fr = 0;
+#pragma unroll
+    for (int b = 0; b < 32; ++b) {
+      if ((int)run < z && z <= (int)(run + h[b])) {
+        fb = b;
+        fr = (int)run;
+      }
+      run += h[b];
+    }
+    found[0] = 32 * t + fb;
+    found[1] = fr;
+  }
+  __syncthreads();
+  Tm = (uint32_t)found[0];
+  nbelow = found[1];
+}
+
+// Tm = the z-th smallest magnitude (1 <= z < the number of valid entries) and
+// the number of magnitudes below it: a radix select over digits of up to 8
+// bits from the top, each digit found from an LDS histogram of the entries
+// that match the digits found so far.  Entries past k hold all ones, which
+// never match (magnitudes have MB bits).
+template <int MB, int KPT>
+__device__ inline void radix_select(const uint32_t (&mag)[KPT], int z, uint32_t* hist, int* found, uint32_t& Tm,
+                                    int& nbelow) {
+  const int t = threadIdx.x;
+  uint32_t prefix = 0;
+  int need = z, below = 0, top = MB;
+  while (top > 0) {
+    const int shift = top > 8 ? top - 8 : 0;
+    const uint32_t dmask = (1u << (top - shift)) - 1u;
+    if (t < 256) hist[t] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < KPT; ++e)
+      if ((mag[e] >> top) == prefix) atomicAdd(&hist[(mag[e] >> shift) & dmask], 1u);
+    __syncthreads();
+    if (t < 64) {  // one wave: the digit whose bin holds the need-th entry
+      uint32_t h[4], local = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        h[q] = hist[4 * t + q];
+        local += h[q];
+      }
+      uint32_t incl = local;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t o = __shfl_up(incl, d);
+        if (t >= d) incl += o;
+      }
+      int run = (int)(incl - local);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (run < need && need <= run + (int)h[q]) {
+          found[0] = 4 * t + q;
+          found[1] = run;
+        }
+        run += (int)h[q];
+      }
+    }
+    __syncthreads();
+    prefix = (prefix << (top - shift)) | (uint32_t)found[0];
+    below += found[1];
+    need -= found[1];
+    top = shift;
+  }
+  Tm = prefix;
+  nbelow = below;
+}
+
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
 struct DscSlab {
   uint32_t m;   // the lane's mask word
   uint32_t co;  // kept values of the channel before the word's 256-row chunk
@@ -234,78 +313,61 @@ __global__ __launch_bounds__(kGemvThreads) void dsc_gemv_kernel(const T* __restr
                                                                 const uint16_t* __restrict__ values, int S, int cap,
                                                                 float* __restrict__ ypart) {
   constexpr int KPT = kMaxK / kGemvThreads;  // channels per thread in the selection: 32
-  constexpr uint32_t MAXMAG = sizeof(T) == 2 ? 0x7fffu : 0x7fffffffu;
+  constexpr int MB = sizeof(T) == 2 ? 15 : 31;  // magnitude bits
   extern __shared__ __attribute__((aligned(16))) uint8_t dyn[];
-  __shared__ int cnt_sh[2][kGemvWaves];
-  __shared__ int scan_sh[kGemvWaves];
+  __shared__ uint32_t hist[256];
+  __shared__ int found[2];
+  __shared__ uint32_t scan_sh[kGemvWaves];
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // uniform: keeps the wave's loop scalar
   const int s = blockIdx.x % S, sl = blockIdx.x / S;
   const int64_t wn = (n + 31) / 32, nc = (n + kChunk - 1) / kChunk;
   int4* lmeta = (int4*)dyn;                         // [cap]: the share's channels
-  u32x4* slots = (u32x4*)(dyn + 16 * (size_t)cap);  // [kGemvWaves][kSlotQ]
+  u32x4* slots = (u32x4*)(dyn + 16 * (size_t)cap);  // [kGemvWaves][1 + kSlotQ]: a guard entry, then the slot
 
-  // 1. selection: the z smallest (|x|, channel) keys are dropped
+  // 1. selection: the z smallest (|x|, channel) keys are dropped; the
+  // workgroup's share is the active channels of rank [lo, hi) in channel order
   const int c0 = t * KPT;
   uint32_t mag[KPT];
   load_mags<T, KPT>(x, k, c0, mag);
-  int par = 0;
-  uint32_t Tm = 0;
+  uint32_t Tm = z >= k ? 0xffffffffu : 0u;  // z = 0: everything kept; z >= k: nothing
   int nbelow = 0;
   if (z > 0 && z < k) {
-    // Tm: the smallest magnitude with at least z entries at or below it
-    uint32_t lo = 0, hi = MAXMAG;
-    while (lo < hi) {
-      const uint32_t mid = lo + (hi - lo) / 2;
-      int c = 0;
-#pragma unroll
-      for (int e = 0; e < KPT; ++e) c += mag[e] <= mid ? 1 : 0;
-      if (block_count(c, cnt_sh, par) >= z)
-        hi = mid;
-      else
-        lo = mid + 1;
-    }
-    Tm = lo;
-    int c = 0;
-#pragma unroll
-    for (int e = 0; e < KPT; ++e) c += mag[e] < Tm ? 1 : 0;
-    nbelow = block_count(c, cnt_sh, par);
+    if constexpr (MB == 15)
+      hist_select<KPT>(mag, z, (uint32_t*)dyn, found, scan_sh, Tm, nbelow);
+    else
+      radix_select<MB, KPT>(mag, z, hist, found, Tm, nbelow);
   }
-  int eq = 0;
-#pragma unroll
-  for (int e = 0; e < KPT; ++e) eq += (c0 + e < k && mag[e] == Tm) ? 1 : 0;
-  int tot;
-  int eq_before = block_excl_scan(eq, scan_sh, tot);
-  const int drop_eq = z - nbelow;  // entries equal to Tm dropped, in channel order
-  uint32_t kept = 0;
+  const int drop_eq = z > 0 && z < k ? z - nbelow : 0;  // entries equal to Tm dropped, in channel order
+  const int nv = min(KPT, max(0, k - c0));                // the thread's valid entries
+  uint32_t gt = 0, eq = 0;
 #pragma unroll
   for (int e = 0; e < KPT; ++e) {
-    bool kp = c0 + e < k;
-    if (kp && z > 0) {
-      if (z >= k || mag[e] < Tm) {
-        kp = false;
-      } else if (mag[e] == Tm) {
-        kp = eq_before >= drop_eq;
-        ++eq_before;
-      }
-    }
-    kept |= (kp ? 1u : 0u) << e;
+    gt += e < nv && mag[e] > Tm ? 1u : 0u;
+    eq += e < nv && mag[e] == Tm ? 1u : 0u;
   }
-  int na;
-  const int j = block_excl_scan(__popc(kept), scan_sh, na);  // rank of the thread's first kept channel
-  int jq = j / S, jr = j - jq * S;                             // rank j = S jq + jr
-#pragma unroll
-  for (int e = 0; e < KPT; ++e)
-    if ((kept >> e) & 1u) {
-      if (jr == s) lmeta[jq] = int4{c0 + e, 0, 0, 0};
-      if (++jr == S) {
-        jr = 0;
-        ++jq;
-      }
-    }
-  __syncthreads();
+  uint32_t tot;  // both counts in one scan: each total is at most 32768
+  const uint32_t before = block_excl_scan((gt << 16) | eq, scan_sh, tot);
+  const int gt_b = (int)(before >> 16), eq_b = (int)(before & 0xffffu);
+  int na = (int)(tot >> 16) + max(0, (int)(tot & 0xffffu) - drop_eq);
   na = __builtin_amdgcn_readfirstlane(na);
-  const int mine = na > s ? (na - s + S - 1) / S : 0;
+  const int j0 = gt_b + max(0, eq_b - drop_eq);  // rank of the thread's first kept channel
+  const int kc = (int)gt + max(0, eq_b + (int)eq - max(eq_b, drop_eq));
+  const int lo = s * cap, hi = min(na, lo + cap);
+  if (kc > 0 && j0 < hi && j0 + kc > lo) {  // the few threads holding the share
+    uint32_t gm = 0, em = 0;
+#pragma unroll
+    for (int e = 0; e < KPT; ++e) {
+      gm |= (e < nv && mag[e] > Tm ? 1u : 0u) << e;
+      em |= (e < nv && mag[e] == Tm ? 1u : 0u) << e;
+    }
+    for (int r = drop_eq - eq_b; r > 0 && em; --r) em &= em - 1u;  // the first ties in channel order are dropped
+    uint32_t km = gm | em;
+    for (int j = j0; km; ++j, km &= km - 1u)
+      if (j >= lo && j < hi) lmeta[j - lo] = int4{c0 + (int)__builtin_ctz(km), 0, 0, 0};
+  }
+  __syncthreads();
+  const int mine = max(0, hi - lo);
 
   // 2. each channel's slab window: values[base + st, base + st + len)
   for (int q = t; q < mine; q += kGemvThreads) {
@@ -323,8 +385,11 @@ __global__ __launch_bounds__(kGemvThreads) void dsc_gemv_kernel(const T* __restr
   for (int b = 0; b < 32; ++b) acc[b] = 0.f;
   const int nw = mine > wave ? (mine - wave + kGemvWaves - 1) / kGemvWaves : 0;
   const int64_t w = 64 * (int64_t)sl + lane, wc = w < wn ? w : wn - 1;
-  u32x4* slot = slots + wave * kSlotQ;
+  u32x4* slot = slots + wave * (kSlotQ + 1) + 1;
   const uint16_t* slot16 = (const uint16_t*)slot;
+  // bf16 activations: each row is one v_dot2 of {w, 0} and {x, 0} (exact
+  // bf16 products, fp32 sums); fp32 activations: an fma
+  constexpr bool DOT = sizeof(T) == 2;
   auto entry = [&](int q) {  // the wave-uniform entry q
     const int4 e = lmeta[q];
     return int4{__builtin_amdgcn_readfirstlane(e.x), __builtin_amdgcn_readfirstlane(e.y),
@@ -357,6 +422,7 @@ __global__ __launch_bounds__(kGemvThreads) void dsc_gemv_kernel(const T* __restr
     int nq;
     window(e, a0, nq);
     const float xv = __int_as_float(e.y);
+    const bf16x2_t xb = __builtin_bit_cast(bf16x2_t, (uint32_t)e.y >> 16);  // {x, 0}: exact for bf16 x
 #pragma unroll
     for (int qv = 0; qv < kQV; ++qv) slot[lane + 64 * qv] = c.v[qv];  // past the window: unread
     __builtin_amdgcn_wave_barrier();
@@ -368,21 +434,27 @@ __global__ __launch_bounds__(kGemvThreads) void dsc_gemv_kernel(const T* __restr
       const int r = __shfl_up(incl, d, 8);
       if ((lane & 7) >= d) incl += r;
     }
-    // branch-free: every row reads the value at the running index (the next
-    // kept row's where this one is pruned, inside the slot) and masks it
-    int idx = (int)((int64_t)(uint32_t)e.z + c.co + incl - p - a0);
+    // branch-free, rows from the top: the pointer sits on the value of the
+    // highest kept row not yet passed and steps down past each kept row; a
+    // pruned row reads that value (or the guard entry) and masks it to zero
+    const uint16_t* ptr = slot16 + ((int)((int64_t)(uint32_t)e.z + c.co + incl - a0) - 1);
 #pragma unroll
-    for (int g = 0; g < 32; g += 8) {
+    for (int g = 24; g >= 0; g -= 8) {
       uint32_t raw[8];
+      int mk[8];
 #pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        raw[b] = slot16[idx];
-        idx += (m >> (g + b)) & 1u;
+      for (int b = 7; b >= 0; --b) {
+        mk[b] = (int)(m << (31 - g - b)) >> 31;  // all ones where the row is kept
+        raw[b] = *ptr;
+        ptr += mk[b];
       }
 #pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        const uint32_t mk = (uint32_t)((int)(m << (31 - g - b)) >> 31);  // all ones where the row is kept
-        acc[g + b] = fmaf(__uint_as_float((raw[b] << 16) & mk), xv, acc[g + b]);
+      for (int b = 7; b >= 0; --b) {
+        if constexpr (DOT)
+          acc[g + b] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, raw[b] & (uint32_t)mk[b]), xb,
+                                                       acc[g + b], false);
+        else
+          acc[g + b] = fmaf(__uint_as_float((raw[b] << 16) & (uint32_t)mk[b]), xv, acc[g + b]);
       }
     }
     __builtin_amdgcn_wave_barrier();
@@ -458,8 +530,9 @@ GemvPlan gemv_plan(int64_t n, int na) {
   const int per = kTargetGroups / p.ns > 0 ? kTargetGroups / p.ns : 1;
   p.S = na < per ? (na > 0 ? na : 1) : per;
   p.cap = (na + p.S - 1) / p.S;
-  const size_t a = 16 * (size_t)p.cap + (size_t)kGemvWaves * kSlotQ * 16;
+  const size_t a = 16 * (size_t)p.cap + (size_t)kGemvWaves * (kSlotQ + 1) * 16;
   p.lds = a > kRedBytes ? a : kRedBytes;
+  if (p.lds < kHistWords * sizeof(uint32_t)) p.lds = kHistWords * sizeof(uint32_t);  // the bf16 selection's histogram
   return p;
 }
 
