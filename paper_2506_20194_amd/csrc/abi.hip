@@ -6,6 +6,7 @@
 #include <atomic>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "internal.h"
 
@@ -60,6 +61,34 @@ namespace duo {
 
 // 0 unknown, 1 gfx950, 2 something else
 static std::atomic<int> g_arch[64];
+
+// The dynamic LDS limit of a kernel is raised once per device (and again only
+// when a launch needs more): the attribute call is host work that need not
+// sit in front of every launch.
+namespace {
+struct LdsLimit {
+  const void* fn;
+  int dev;
+  int bytes;
+};
+std::mutex g_lds_mu;
+LdsLimit g_lds[128];
+int g_lds_n = 0;
+}  // namespace
+
+duo_status set_max_lds(const void* fn, size_t bytes) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return DUO_ERR_NO_DEVICE;
+  std::lock_guard<std::mutex> lk(g_lds_mu);
+  int slot = -1;
+  for (int i = 0; i < g_lds_n; ++i)
+    if (g_lds[i].fn == fn && g_lds[i].dev == dev) slot = i;
+  if (slot >= 0 && g_lds[slot].bytes >= (int)bytes) return DUO_OK;
+  DUO_HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes));
+  if (slot < 0 && g_lds_n < 128) slot = g_lds_n++;
+  if (slot >= 0) g_lds[slot] = LdsLimit{fn, dev, (int)bytes};
+  return DUO_OK;
+}
 
 duo_status device_ok() {
   int dev = -1;

@@ -388,8 +388,7 @@ constexpr size_t kDiagLds = (size_t)(2 * kTile * DS + 2 * LF + 4) * sizeof(float
 
 duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hipStream_t s, CholStatus** status_dev) {
   const CholWs w = carve(ws, k);
-  DUO_HIP_TRY(hipFuncSetAttribute((const void*)diag_factor_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  (int)kDiagLds));
+  if (duo_status d = set_max_lds((const void*)diag_factor_kernel, kDiagLds); d != DUO_OK) return d;
   *status_dev = w.st;
   const int T = (int)cdiv(k, kTile);
   hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, H, ldh, (int)k, damp, w.st);

@@ -303,6 +303,10 @@ struct DscSlab {
   uint32_t m;   // the lane's mask word
   uint32_t co;  // kept values of the channel before the word's 256-row chunk
   u32x4 v[kQV];
+  // wave-uniform: the channel's first value, its activation (fp32 bits) and
+  // the window's aligned start (element offsets into values; the layout has
+  // fewer than 2^31 values at the GEMV's size limits)
+  uint32_t base, xbits, a0;
 };
 
 template <typename T>
@@ -395,49 +399,45 @@ __global__ __launch_bounds__(kGemvThreads) void dsc_gemv_kernel(const T* __restr
     return int4{__builtin_amdgcn_readfirstlane(e.x), __builtin_amdgcn_readfirstlane(e.y),
                 __builtin_amdgcn_readfirstlane(e.z), __builtin_amdgcn_readfirstlane(e.w)};
   };
-  auto window = [&](const int4& e, int64_t& a0, int& nq) {
-    const int64_t st = (int64_t)(uint32_t)e.z + (e.w & 0xffff), len = (uint32_t)e.w >> 16;
-    a0 = st & ~(int64_t)7;
-    nq = (int)((st + len - a0 + 7) >> 3);
-  };
+  const uint32_t wcu = (uint32_t)wc, wnu = (uint32_t)wn, ncu = (uint32_t)nc;
   auto fetch = [&](int jj, DscSlab& c) {
     const int4 e = entry(wave + kGemvWaves * (jj < nw ? jj : nw - 1));
-    const int64_t i = e.x;
-    int64_t a0;
-    int nq;
-    window(e, a0, nq);
+    const uint32_t i = (uint32_t)e.x, st = (uint32_t)e.z + ((uint32_t)e.w & 0xffffu), len = (uint32_t)e.w >> 16;
+    const uint32_t a0 = st & ~7u;
+    const int nq = (int)((st + len - a0 + 7u) >> 3);
     const int last = nq > 0 ? nq - 1 : 0;
-    c.m = maskT[i * wn + wc];
-    c.co = chunk_off[i * nc + wc / 8];
+    c.base = (uint32_t)e.z;
+    c.xbits = (uint32_t)e.y;
+    c.a0 = a0;
+    c.m = maskT[i * wnu + wcu];
+    c.co = chunk_off[i * ncu + wcu / 8u];
 #pragma unroll
     for (int qv = 0; qv < kQV; ++qv) {
       const int idx = lane + 64 * qv < last ? lane + 64 * qv : last;
-      c.v[qv] = *(const u32x4*)(values + a0 + 8 * (int64_t)idx);
+      c.v[qv] = *(const u32x4*)(values + (a0 + 8u * (uint32_t)idx));
     }
     __builtin_amdgcn_sched_barrier(0);  // issue the loads here, ahead of the consume that follows
   };
-  auto consume = [&](int jj, const DscSlab& c) {
-    const int4 e = entry(wave + kGemvWaves * jj);
-    int64_t a0;
-    int nq;
-    window(e, a0, nq);
-    const float xv = __int_as_float(e.y);
-    const bf16x2_t xb = __builtin_bit_cast(bf16x2_t, (uint32_t)e.y >> 16);  // {x, 0}: exact for bf16 x
+  auto consume = [&](const DscSlab& c) {
+    const float xv = __uint_as_float(c.xbits);
+    const bf16x2_t xb = __builtin_bit_cast(bf16x2_t, c.xbits >> 16);  // {x, 0}: exact for bf16 x
 #pragma unroll
     for (int qv = 0; qv < kQV; ++qv) slot[lane + 64 * qv] = c.v[qv];  // past the window: unread
     __builtin_amdgcn_wave_barrier();
     const uint32_t m = w < wn ? c.m : 0u;
     const int p = __popc(m);
+    // exclusive prefix of the popcounts over the 8 words of the lane's 256-row chunk (DPP row shifts)
     int incl = p;
-#pragma unroll
-    for (int d = 1; d < 8; d <<= 1) {
-      const int r = __shfl_up(incl, d, 8);
-      if ((lane & 7) >= d) incl += r;
-    }
+    int r = __builtin_amdgcn_update_dpp(0, incl, 0x111, 0xf, 0xf, true);  // row_shr:1
+    incl += (lane & 7) >= 1 ? r : 0;
+    r = __builtin_amdgcn_update_dpp(0, incl, 0x112, 0xf, 0xf, true);  // row_shr:2
+    incl += (lane & 7) >= 2 ? r : 0;
+    r = __builtin_amdgcn_update_dpp(0, incl, 0x114, 0xf, 0xf, true);  // row_shr:4
+    incl += (lane & 7) >= 4 ? r : 0;
     // branch-free, rows from the top: the pointer sits on the value of the
     // highest kept row not yet passed and steps down past each kept row; a
     // pruned row reads that value (or the guard entry) and masks it to zero
-    const uint16_t* ptr = slot16 + ((int)((int64_t)(uint32_t)e.z + c.co + incl - a0) - 1);
+    const uint16_t* ptr = slot16 + ((int)(c.base + c.co + (uint32_t)incl - c.a0) - 1);
 #pragma unroll
     for (int g = 24; g >= 0; g -= 8) {
       uint32_t raw[8];
@@ -469,14 +469,14 @@ __global__ __launch_bounds__(kGemvThreads) void dsc_gemv_kernel(const T* __restr
     int jj = 0;
     for (; jj + 3 <= nw; jj += 3) {
       fetch(jj + 2, cc);
-      consume(jj, ca);
+      consume(ca);
       fetch(jj + 3, ca);
-      consume(jj + 1, cb);
+      consume(cb);
       fetch(jj + 4, cb);
-      consume(jj + 2, cc);
+      consume(cc);
     }
-    if (jj < nw) consume(jj, ca);
-    if (jj + 1 < nw) consume(jj + 1, cb);
+    if (jj < nw) consume(ca);
+    if (jj + 1 < nw) consume(cb);
   }
 
   // 4. the waves' sums in a fixed order: (v + v + 8) for v < 8, then in v order
@@ -502,21 +502,27 @@ __global__ __launch_bounds__(kGemvThreads) void dsc_gemv_kernel(const T* __restr
 
 constexpr size_t kRedBytes = 8 * 32 * 65 * sizeof(float);
 
-// y[r] = sum of the S partial rows in a fixed order: four strided running sums
-// (partials g, g + 4, ...), then the four in order.
-__global__ __launch_bounds__(256) void dsc_reduce_kernel(const float* __restrict__ ypart, int64_t n, int S,
-                                                         float* __restrict__ y) {
-  __shared__ float part[4][64];
+// y[r] = sum of the S partial rows in a fixed order: 16 strided running sums
+// (partials g, g + 16, ...), then the 16 in order; a workgroup of 1024
+// threads takes 64 rows, so each thread issues only S / 16 loads at once.
+__global__ __launch_bounds__(1024) void dsc_reduce_kernel(const float* __restrict__ ypart, int64_t n, int S,
+                                                          float* __restrict__ y) {
+  __shared__ float part[16][65];
   const int g = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int64_t r = (int64_t)blockIdx.x * 64 + l;
   float a = 0.f;
   if (r < n) {
-#pragma unroll 8
-    for (int p = g; p < S; p += 4) a += ypart[(int64_t)p * n + r];
+#pragma unroll 16
+    for (int p = g; p < S; p += 16) a += ypart[(int64_t)p * n + r];
   }
   part[g][l] = a;
   __syncthreads();
-  if (g == 0 && r < n) y[r] = ((part[0][l] + part[1][l]) + part[2][l]) + part[3][l];
+  if (g == 0 && r < n) {
+    float v = 0.f;
+#pragma unroll
+    for (int h = 0; h < 16; ++h) v += part[h][l];
+    y[r] = v;
+  }
 }
 
 struct GemvPlan {
@@ -599,7 +605,7 @@ duo_status duo_dsc_gemv(const void* x, int32_t x_dtype, int64_t n, int64_t k, du
   const GemvPlan p = gemv_plan(n, (int)(k - z));  // the rule keeps exactly k - z channels
   float* ypart = (float*)ws;
   const void* kern = x_dtype == DUO_BF16 ? (const void*)dsc_gemv_kernel<uint16_t> : (const void*)dsc_gemv_kernel<float>;
-  DUO_HIP_TRY(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds));
+  if (duo_status d = set_max_lds(kern, p.lds); d != DUO_OK) return d;
   prof_begin(DUO_PROF_DECODE, s);
   if (x_dtype == DUO_BF16)
     hipLaunchKernelGGL(dsc_gemv_kernel<uint16_t>, dim3((unsigned)(p.ns * p.S)), dim3(kGemvThreads), p.lds, s,
@@ -609,7 +615,7 @@ duo_status duo_dsc_gemv(const void* x, int32_t x_dtype, int64_t n, int64_t k, du
                        (const float*)x, (int)k, z, n, col_ptr, maskT, chunk_off, values, p.S, p.cap, ypart);
   DUO_LAUNCH_CHECK();
   prof_end(DUO_PROF_DECODE, s);
-  hipLaunchKernelGGL(dsc_reduce_kernel, dim3((unsigned)cdiv(n, 64)), dim3(256), 0, s, (const float*)ypart, n, p.S, y);
+  hipLaunchKernelGGL(dsc_reduce_kernel, dim3((unsigned)cdiv(n, 64)), dim3(1024), 0, s, (const float*)ypart, n, p.S, y);
   DUO_LAUNCH_CHECK();
   return DUO_OK;
 }

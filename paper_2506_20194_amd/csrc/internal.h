@@ -19,6 +19,8 @@ duo_status hessian_run(const void* Xs, const void* Xd, int32_t dtype, int64_t m,
 // DUO_OK when the current device is a gfx950 (cached per device), else
 // DUO_ERR_NO_DEVICE (or DUO_ERR_UNSUPPORTED for a device index >= 64).
 duo_status device_ok();
+// raise a kernel's dynamic LDS limit on the current device (cached)
+duo_status set_max_lds(const void* fn, size_t bytes);
 
 // Per-token threshold keys of the (|x|, channel) rule: entry c of token t is
 // kept iff ((magnitude bits of x) << 32 | c) > thr[t]; z entries are zeroed.

@@ -624,10 +624,9 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   auto ib_kern = nm ? (qt ? inblock_kernel<true, true> : inblock_kernel<true, false>)
                     : (qt ? inblock_kernel<false, true> : inblock_kernel<false, false>);
   const IbOpts ibo{o.nm_n, o.q_bits, qt ? o.q_group : kMaxBlock, o.q_scale, o.q_zero};
-  DUO_HIP_TRY(hipFuncSetAttribute((const void*)ib_kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ib_lds));
+  if (duo_status d = set_max_lds((const void*)ib_kern, ib_lds); d != DUO_OK) return d;
   const size_t sel_lds = (size_t)(16 + (1 << kDigit)) * sizeof(uint32_t) + (size_t)kSelCap * sizeof(unsigned long long);
-  DUO_HIP_TRY(
-      hipFuncSetAttribute((const void*)sel_resolve_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sel_lds));
+  if (duo_status d = set_max_lds((const void*)sel_resolve_kernel, sel_lds); d != DUO_OK) return d;
   const int P = (int)(cdiv(n, 32) < kSelWG ? cdiv(n, 32) : kSelWG);
   int64_t prev = 0;
   for (int64_t j0 = 0; j0 < k; j0 += B) {
