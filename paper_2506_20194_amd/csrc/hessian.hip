@@ -493,13 +493,28 @@ __global__ __launch_bounds__(256) void pack16_kernel(const uint16_t* __restrict_
     }
 }
 
-__global__ void a_reduce_kernel(const float* __restrict__ apart, int nblk, int kp, int k,
-                                float* __restrict__ a) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= k) return;
+// a[c] += the sum of the per-block partials of channel c, in a fixed order:
+// eight strided running sums (partials g, g + 8, ...), then the eight in
+// order.  A workgroup takes 32 channels, so every thread has only nblk / 8
+// independent loads in flight instead of nblk sequential ones.
+__global__ __launch_bounds__(256) void a_reduce_kernel(const float* __restrict__ apart, int nblk, int kp, int k,
+                                                       float* __restrict__ a) {
+  __shared__ float part[8][33];
+  const int l = threadIdx.x & 31, g = threadIdx.x >> 5;
+  const int c = blockIdx.x * 32 + l;
   float s = 0.f;
-  for (int b = 0; b < nblk; ++b) s += apart[(int64_t)b * kp + c];
-  a[c] += s;
+  if (c < k) {
+#pragma unroll 8
+    for (int b = g; b < nblk; b += 8) s += apart[(int64_t)b * kp + c];
+  }
+  part[g][l] = s;
+  __syncthreads();
+  if (g == 0 && c < k) {
+    float v = 0.f;
+#pragma unroll
+    for (int h = 0; h < 8; ++h) v += part[h][l];
+    a[c] += v;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -825,24 +840,35 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
       }
 }
 
-// Fixed-order sum of the per-segment partial tiles into H and G.
+// Fixed-order sum of the per-segment partial tiles into H and G.  Block
+// (tile, q) takes the 64 x 64 sub-block q: its rows are added with coalesced
+// accesses, and for an off-diagonal H tile the mirrored entries H[col][row]
+// pass through an LDS transpose so that those writes are coalesced too.
 template <typename T>
 __global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A) {
+  __shared__ float tr[64][65];
   const int tile = blockIdx.x;
   int isg, I, J;
   gram_tile(tile, A.nh, A.nt, &isg, &I, &J);
+  const int sr = (blockIdx.y >> 2) * 64, sc = (blockIdx.y & 3) * 64;
   const int64_t stride = (int64_t)A.ntiles * GT * GT;
   const float* p0 = A.part + (int64_t)tile * GT * GT;
   float* C = isg ? A.G : A.H;
   const int64_t ldc = isg ? A.ldg : A.ldh;
-  const int e0 = blockIdx.y * 4096;
-  for (int e = e0 + threadIdx.x; e < e0 + 4096; e += 256) {
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int rr = ty; rr < 64; rr += 4) {
+    const int e = (sr + rr) * GT + sc + tx;
     float s = 0.f;
     for (int sg = 0; sg < A.nseg; ++sg) s += p0[sg * stride + e];
-    const int row = I * GT + e / GT, col = J * GT + e % GT;
-    if (row < A.k && col < A.k) {
-      C[(int64_t)row * ldc + col] += s;
-      if (!isg && I != J) A.H[(int64_t)col * A.ldh + row] += s;
+    const int row = I * GT + sr + rr, col = J * GT + sc + tx;
+    if (row < A.k && col < A.k) C[(int64_t)row * ldc + col] += s;
+    tr[rr][tx] = s;
+  }
+  if (!isg && I != J) {
+    __syncthreads();
+    for (int cc = ty; cc < 64; cc += 4) {
+      const int hrow = J * GT + sc + cc, hcol = I * GT + sr + tx;
+      if (hrow < A.k && hcol < A.k) A.H[(int64_t)hrow * A.ldh + hcol] += tr[tx][cc];
     }
   }
 }
@@ -1021,7 +1047,7 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
       DUO_LAUNCH_CHECK();
     }
     if (want_g) {
-      hipLaunchKernelGGL(a_reduce_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.apart, (int)cdiv(mc, 256),
+      hipLaunchKernelGGL(a_reduce_kernel, dim3((unsigned)cdiv(k, 32)), dim3(256), 0, s, w.apart, (int)cdiv(mc, 256),
                          (int)kp, (int)k, a);
       DUO_LAUNCH_CHECK();
     }
@@ -1050,7 +1076,7 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
     prof_end(DUO_PROF_GRAM, s);
     if (st != DUO_OK) return st;
     if (nseg > 1) {
-      hipLaunchKernelGGL(gram_reduce_kernel<T>, dim3(A.ntiles, (GT * GT) / 4096), dim3(256), 0, s, A);
+      hipLaunchKernelGGL(gram_reduce_kernel<T>, dim3(A.ntiles, (GT / 64) * (GT / 64)), dim3(256), 0, s, A);
       DUO_LAUNCH_CHECK();
     }
   }
