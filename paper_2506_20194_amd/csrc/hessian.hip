@@ -171,23 +171,56 @@ __global__ __launch_bounds__(256) void act_select_wave_kernel(const uint16_t* __
 #pragma unroll
     for (int j = 0; j < 8; ++j) mag[8 * u + j] = ok ? (w[j >> 1] >> (16 * (j & 1))) & 0x7fffu : 0xffffffffu;
   }
-  // smallest v with count(mag <= v) >= z
-  uint32_t lo = 0, hi = 0x7fffu;
-  while (lo < hi) {
-    const uint32_t mid = lo + ((hi - lo) >> 1);
-    int cnt = 0;
+  // v = the smallest magnitude with count(mag <= v) >= z, from two LDS
+  // histograms of the wave's own: the top 8 of the 15 magnitude bits (lane l
+  // scans bins 4l .. 4l+3), then the low 7 bits of the entries in the bin of
+  // the z-th entry (lane l: bins 2l, 2l+1).  Within a wave the LDS operations
+  // run in order, so no barrier is needed.
+  __shared__ uint32_t hist_w[4][256 + 128];
+  uint32_t* hc = hist_w[threadIdx.x >> 6];
+  uint32_t* hf = hc + 256;
+  for (int i = lane; i < 256 + 128; i += 64) hc[i] = 0u;
+  __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int e = 0; e < 8 * V; ++e) cnt += mag[e] <= mid;
-    if (wave_sum_i(cnt) >= z)
-      hi = mid;
-    else
-      lo = mid + 1;
+  for (int e = 0; e < 8 * V; ++e)
+    if (mag[e] < 0x8000u) atomicAdd(&hc[mag[e] >> 7], 1u);
+  __builtin_amdgcn_wave_barrier();
+  int h[4], loc = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h[i] = (int)hc[4 * lane + i];
+    loc += h[i];
   }
-  const uint32_t v = lo;
-  int lt = 0;
+  int incl = wave_incl_scan(loc), run = incl - loc, cb = -1, below = 0;
 #pragma unroll
-  for (int e = 0; e < 8 * V; ++e) lt += mag[e] < v;
-  int need = z - wave_sum_i(lt);  // 1 <= need <= number of ties
+  for (int i = 0; i < 4; ++i) {
+    if (run < z && z <= run + h[i]) {
+      cb = 4 * lane + i;
+      below = run;
+    }
+    run += h[i];
+  }
+  const int src = __builtin_ctzll(__ballot(cb >= 0));  // the one lane holding the z-th entry's bin
+  cb = __shfl(cb, src);
+  below = __shfl(below, src);
+#pragma unroll
+  for (int e = 0; e < 8 * V; ++e)
+    if ((int)(mag[e] >> 7) == cb) atomicAdd(&hf[mag[e] & 127u], 1u);
+  __builtin_amdgcn_wave_barrier();
+  const int f0 = (int)hf[2 * lane], f1 = (int)hf[2 * lane + 1];
+  incl = wave_incl_scan(f0 + f1);
+  run = below + incl - f0 - f1;
+  int fb = -1, lt = 0;
+  if (run < z && z <= run + f0) {
+    fb = 2 * lane;
+    lt = run;
+  } else if (run + f0 < z && z <= run + f0 + f1) {
+    fb = 2 * lane + 1;
+    lt = run + f0;
+  }
+  const int src2 = __builtin_ctzll(__ballot(fb >= 0));
+  const uint32_t v = ((uint32_t)cb << 7) | (uint32_t)__shfl(fb, src2);
+  int need = z - __shfl(lt, src2);  // 1 <= need <= number of ties
   // the need-th tie in channel order (u, lane, j)
 #pragma unroll
   for (int u = 0; u < V; ++u) {
