@@ -111,57 +111,42 @@ __device__ inline void store32(float* C, const f4 (&acc)[2][2], int lane, float 
       }
 }
 
-struct LeafCtx {
-  float* col;  // [LF]: column c of the working leaf (rows >= c zeroed)
-  float* row;  // [LF]: row c of the working leaf
-  int q, h;    // lane: column q, rows 16h .. 16h+15
-  int fail;    // first column (from the bottom) with a non-positive pivot
-};
-
-// Step c of the leaf sweep; x[i] is row 16h+i of column q.  The lane
-// coordinates are made opaque per step so that the compiler evaluates the
-// lane tests where they are used instead of hoisting (and spilling) the
-// masks of every step.
+// Step c of the leaf sweep.  Lane q (and its twin q + 32, which repeats the
+// same work) holds column q of the 32 x 32 working matrix in x[0..31].  Column
+// c reaches every lane as scalars read from lane c, so a step needs no LDS
+// round trip and no barrier.  The leading c x c block stays symmetric (every
+// update to it is a symmetric rank-1 term), so the coefficient W[q][c] of a
+// column q < c is the lane's own W[c][q]; for q > c (the columns that become
+// the inverse) it is W[c][q] by definition.
 template <int C>
-__device__ __forceinline__ void leaf_step(float (&x)[16], LeafCtx& d) {
-  constexpr int CH = C / 16, CI = C % 16;
-  int q = d.q, h = d.h;
-  asm volatile("" : "+v"(q), "+v"(h));
-  const bool hi = h != 0;
-  if (q == C) {
+__device__ __forceinline__ void leaf_step(float (&x)[LF], int q, int& fail) {
+  // the lane's column made opaque per step, so that the compiler evaluates
+  // the lane tests where they are used instead of hoisting (and spilling)
+  // the masks of every step out of the leaf loop
+  asm volatile("" : "+v"(q));
+  float cv[C > 0 ? C : 1];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float lo_v = i < C ? x[i] : 0.f, hi_v = 16 + i < C ? x[i] : 0.f;
-      d.col[16 * h + i] = hi ? hi_v : lo_v;
-    }
-  }
-  if (h == CH) d.row[q] = x[CI];
-  __builtin_amdgcn_wave_barrier();
-  float cv[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) cv[i] = d.col[16 * h + i];
-  const float piv = d.row[C];
-  const float cq = d.col[q], rq = d.row[q];
-  __builtin_amdgcn_wave_barrier();
-  if (!(piv > 0.f) && d.fail < 0) d.fail = C;  // every lane sees the same pivot
+  for (int i = 0; i < C; ++i)
+    cv[i] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x[i]), C));
+  const float piv = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x[C]), C));
+  if (!(piv > 0.f) && fail < 0) fail = C;  // uniform
   const float inv = __builtin_amdgcn_rsqf(piv);
   const float inv2 = inv * inv;
+  const float xc = x[C];
+  const float coef = xc * inv2;
+#pragma unroll
+  for (int i = 0; i < C; ++i) x[i] = fmaf(-cv[i], coef, x[i]);
   if (q == C) {
-    // rows below the diagonal of a finished column are never read again
+    // the pivot column: rows below the diagonal are never read again
 #pragma unroll
-    for (int i = 0; i < 16; ++i) x[i] = -x[i] * inv2;
-    if (h == CH) x[CI] = inv;
-  } else {
-    const float coef = q < C ? inv2 * cq : inv2 * rq;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) x[i] = fmaf(-cv[i], coef, x[i]);  // cv is zero for rows >= C
-    if (q > C && h == CH) x[CI] *= inv;
+    for (int i = 0; i < C; ++i) x[i] = -cv[i] * inv2;
   }
+  x[C] = q == C ? inv : (q > C ? xc * inv : xc);
 }
 
 template <int... Cs>
-__device__ __forceinline__ void leaf_steps(float (&x)[16], LeafCtx& d, std::integer_sequence<int, Cs...>) {
-  (leaf_step<LF - 1 - Cs>(x, d), ...);
+__device__ __forceinline__ void leaf_steps(float (&x)[LF], int q, int& fail, std::integer_sequence<int, Cs...>) {
+  (leaf_step<LF - 1 - Cs>(x, q, fail), ...);
 }
 
 __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_t ldh, int r0, int s, float* vinv,
@@ -170,24 +155,32 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
   float* A = dsm;                  // [128][DS] working matrix (both triangles); then V's upper off-diagonal
                                    // blocks, and the back substitution's products in blocks (1..3, 0)
   float* N = A + kTile * DS;       // [128][DS] the inverse
-  float* col = N + kTile * DS;     // [LF]
-  float* row = col + LF;           // [LF]
-  int* fail_sh = (int*)(row + LF); // [1]
+  int* fail_sh = (int*)(N + kTile * DS);  // [1]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // load the upper triangle, mirror it; identity outside the s x s block
-  for (int e0 = 0; e0 < kTile * kTile; e0 += 256 * 16) {
-    float v[16];
+  // load the upper triangle, mirror it; identity outside the s x s block.
+  // Every load is issued before the first is used (addresses clamped into
+  // the block, so none is conditional): one memory latency, not one per row
+  // group.
+  {
+    constexpr int NU = kTile * kTile / 256;
+    const int c = tid % kTile, cc = min(c, s - 1);
+    const float* Hb = H + (int64_t)r0 * ldh + r0;
+    float v[NU];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int e = e0 + 256 * u + tid, r = e / kTile, c = e % kTile;
-      v[u] = (r <= c && c < s) ? H[(int64_t)(r0 + r) * ldh + r0 + c] : (r == c ? 1.f : 0.f);
+    for (int u = 0; u < NU; ++u) {
+      // 32-bit lane offsets within the block (128 rows of at most 2^24
+      // columns); kept in vector registers rather than 64 scalar pairs
+      int off = min(2 * u + tid / kTile, s - 1) * (int)ldh + cc;
+      asm volatile("" : "+v"(off));
+      v[u] = Hb[off];
     }
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int e = e0 + 256 * u + tid, r = e / kTile, c = e % kTile;
+    for (int u = 0; u < NU; ++u) {
+      const int r = 2 * u + tid / kTile;
+      const float w = (c < s) ? v[u] : (r == c ? 1.f : 0.f);
       if (r <= c) {
-        A[r * DS + c] = v[u];
-        A[c * DS + r] = v[u];
+        A[r * DS + c] = w;
+        A[c * DS + r] = w;
       }
       N[r * DS + c] = 0.f;
     }
@@ -197,17 +190,19 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
   for (int J = kTile / LF - 1; J >= 0; --J) {
     const int j0 = J * LF;
     if (wave == 0) {
-      LeafCtx d{col, row, lane & 31, lane >> 5, -1};
-      float x[16];
+      const int q = lane & (LF - 1);
+      int fail = -1;
+      float x[LF];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) x[i] = A[(j0 + 16 * d.h + i) * DS + j0 + d.q];
-      leaf_steps(x, d, std::make_integer_sequence<int, LF>{});
+      for (int i = 0; i < LF; ++i) x[i] = A[(j0 + i) * DS + j0 + q];
+      leaf_steps(x, q, fail, std::make_integer_sequence<int, LF>{});
+      if (lane < LF) {
+        int qs = q;
+        asm volatile("" : "+v"(qs));  // no hoisted per-row masks
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int r = 16 * d.h + i;
-        N[(j0 + r) * DS + j0 + d.q] = r <= d.q ? x[i] : 0.f;
+        for (int i = 0; i < LF; ++i) N[(j0 + i) * DS + j0 + qs] = i <= qs ? x[i] : 0.f;
       }
-      if (lane == 0 && d.fail >= 0 && *fail_sh < 0) *fail_sh = j0 + d.fail;
+      if (lane == 0 && fail >= 0 && *fail_sh < 0) *fail_sh = j0 + fail;
     }
     __syncthreads();
     if (J == 0) break;
@@ -252,9 +247,16 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
     st->status = DUO_ERR_NOT_PD;
     st->fail = r0 + *fail_sh;
   }
-  for (int e = tid; e < kTile * kTile; e += 256) {
-    const int r = e / kTile, c = e % kTile;
-    vinv[e] = (r <= c && r < s && c < s) ? N[r * DS + c] : 0.f;
+#pragma unroll 4
+  for (int e4 = tid; e4 < kTile * kTile / 4; e4 += 256) {
+    const int r = e4 / (kTile / 4), c0 = 4 * (e4 % (kTile / 4));
+    float o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = c0 + i;
+      o[i] = (r <= c && r < s && c < s) ? N[r * DS + c] : 0.f;
+    }
+    ((float4*)vinv)[e4] = make_float4(o[0], o[1], o[2], o[3]);
   }
 }
 
@@ -384,7 +386,7 @@ duo_status trinv(float* H, int64_t ldh, int64_t k, int T, float* X, hipStream_t 
 
 size_t chol_ws_bytes(int64_t k) { return carve(nullptr, k).bytes; }
 
-constexpr size_t kDiagLds = (size_t)(2 * kTile * DS + 2 * LF + 4) * sizeof(float);
+constexpr size_t kDiagLds = (size_t)(2 * kTile * DS + 4) * sizeof(float);
 
 duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hipStream_t s, CholStatus** status_dev) {
   const CholWs w = carve(ws, k);
