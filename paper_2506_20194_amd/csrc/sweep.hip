@@ -6,11 +6,11 @@
 //            pruned.  Every element has the unique key (bits of S,
 //            column*n + row).  One launch histograms the top 13 key bits over
 //            the block; the next gathers the elements of the bucket that
-//            holds the z-th key (normally a few thousand) and its last
-//            workgroup finds the exact threshold among them by a radix select
-//            in LDS (a bucket larger than kSelCap is read from the block
-//            itself).  Counting uses integer atomics only, so the result is
-//            deterministic.
+//            holds the z-th key (normally a few thousand), and a third, one
+//            workgroup, finds the exact threshold among them (radix passes
+//            in registers down to at most 256, then direct ranking; a bucket
+//            larger than kSelCap is read from the block itself).  Counting
+//            uses integer atomics only, so the result is deterministic.
 //   in-block one row per 16 lanes (one DPP row), each lane owning the 8 columns
 //            c = lane%16 + 16i; L[blk, blk] and D[blk, blk] sit in LDS.  For
 //            column j the owner's current value w0 reaches the other 15 lanes
@@ -193,67 +193,101 @@ __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict
   });
 }
 
-// 3. one workgroup: radix select of the rank-th composite of the bucket, from
-//    the gathered candidates in LDS (or, for a bucket larger than kSelCap,
-//    straight from the block); then clears the histogram for the next block
+// 3. one workgroup: the rank-th composite of the bucket, then the histogram is
+//    cleared for the next block.  Gathered candidates (at most kSelCap) stay
+//    in registers, 32 per thread: radix passes of up to kDigitR bits narrow
+//    them to the prefix that holds the rank-th composite until at most 256
+//    remain, and those are ranked against each other directly (composites
+//    are unique, so exactly one has the wanted rank).  A bucket larger than
+//    kSelCap is resolved by 8-bit passes straight over the block.
+constexpr int kDigitR = 11;
+constexpr int kRankMax = 256;
 __global__ __launch_bounds__(256) void sel_resolve_kernel(const float* __restrict__ W, int64_t ldw, int n, int Bb,
                                                           int j0, const float* __restrict__ fac, uint32_t z,
                                                           int idx_bits, uint32_t* hist, SelState* st,
                                                           const unsigned long long* cand) {
   extern __shared__ __attribute__((aligned(16))) uint32_t sel_sm[];
-  uint32_t* sh = sel_sm;                                          // [16]
-  uint32_t* lh = sel_sm + 16;                                     // [1 << kDigit]
-  unsigned long long* lc = (unsigned long long*)(lh + (1 << kDigit));  // [kSelCap]
+  uint32_t* sh = sel_sm;                                                   // [16]
+  uint32_t* lh = sel_sm + 16;                                              // [1 << kDigitR]
+  unsigned long long* lr = (unsigned long long*)(lh + (1 << kDigitR));     // [kRankMax]
   const int tid = threadIdx.x;
+  if (tid == 0) sh[12] = 0;  // compaction counter (published by find_bucket's barriers)
+  // every one of the kSelCap candidate slots exists: they are loaded before
+  // the bucket is known, so both loads are in flight together
+  constexpr int NU = kSelCap / 256;
+  unsigned long long v[NU];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) v[u] = cand[256 * u + tid];
   uint32_t bin, rank, cnt;
   find_bucket<kBins0 / 256>(hist, z, sh, bin, rank, cnt);
-  const bool gather = cnt <= (uint32_t)kSelCap;
-  if (gather)
-    for (uint32_t i0 = 0; i0 < cnt; i0 += 256 * 8) {
-      unsigned long long v[8];
+  const int tb = kShift0 + idx_bits;  // composite bits
+  unsigned long long pref = 0;
+  if (cnt <= (uint32_t)kSelCap) {
+    // slots past cnt become all-ones, which matches no prefix (composites
+    // are below 2^50)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const uint32_t i = i0 + 256 * u + tid;
-        v[u] = cand[i < cnt ? i : 0];
-      }
+    for (int u = 0; u < NU; ++u) v[u] = (uint32_t)(256 * u + tid) < cnt ? v[u] : ~0ull;
+    int s = tb;         // bits [s, tb) of the wanted composite are known (in pref)
+    uint32_t rk = rank, cur = cnt;
+    while (cur > (uint32_t)kRankMax) {
+      const int d = s < kDigitR ? s : kDigitR;
+      const int hs = s;
+      s -= d;
+      for (int i = tid; i < (1 << kDigitR); i += 256) lh[i] = 0;
+      __syncthreads();
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const uint32_t i = i0 + 256 * u + tid;
-        if (i < cnt) lc[i] = v[u];
+      for (int u = 0; u < NU; ++u)
+        if ((v[u] >> hs) == (pref >> hs))
+          atomicAdd(&lh[(uint32_t)(v[u] >> s) & ((1u << d) - 1u)], 1u);
+      __syncthreads();
+      uint32_t dg, rk2, c2;
+      find_bucket<(1 << kDigitR) / 256>(lh, rk, sh, dg, rk2, c2);
+      pref |= (unsigned long long)dg << s;
+      rk = rk2;
+      cur = c2;
+    }
+    // the cur <= kRankMax composites with the known prefix, ranked directly
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+      if ((v[u] >> s) == (pref >> s)) lr[atomicAdd(&sh[12], 1u)] = v[u];
+    __syncthreads();
+    if ((uint32_t)tid < cur) {
+      const unsigned long long my = lr[tid];
+      uint32_t r = 1;
+      for (uint32_t j = 0; j < cur; ++j) r += lr[j] < my;
+      if (r == rk) {
+        sh[13] = (uint32_t)my;
+        sh[14] = (uint32_t)(my >> 32);
       }
     }
-  const int c = min(tid & 127, Bb - 1), rs = tid >> 7;
-  const bool cv = (tid & 127) < Bb;
-  const float fc = fac[j0 + c];
-  const float* Wc = W + j0 + c;
-  const int tb = kShift0 + idx_bits;
-  const int start = (tb + kDigit - 1) / kDigit * kDigit;
-  unsigned long long pref = 0;
-  uint32_t rk = rank;
-  for (int s = start - kDigit; s >= 0; s -= kDigit) {
-    for (int i = tid; i < (1 << kDigit); i += 256) lh[i] = 0;
     __syncthreads();
-    const int hs = s + kDigit;
-    auto add = [&](unsigned long long v) {
-      if ((v >> hs) == (pref >> hs)) atomicAdd(&lh[(uint32_t)(v >> s) & ((1u << kDigit) - 1u)], 1u);
-    };
-    if (gather) {
-#pragma unroll 8
-      for (uint32_t i = tid; i < cnt; i += 256) add(lc[i]);
-    } else {
-      // rare: a bucket this large means a long run of nearly equal scores
+    pref = (unsigned long long)sh[13] | ((unsigned long long)sh[14] << 32);
+  } else {
+    // rare: a bucket this large means a long run of nearly equal scores
+    const int c = min(tid & 127, Bb - 1), rs = tid >> 7;
+    const bool cv = (tid & 127) < Bb;
+    const float fc = fac[j0 + c];
+    const float* Wc = W + j0 + c;
+    const int start = (tb + kDigit - 1) / kDigit * kDigit;
+    uint32_t rk = rank;
+    for (int s = start - kDigit; s >= 0; s -= kDigit) {
+      for (int i = tid; i < (1 << kDigit); i += 256) lh[i] = 0;
+      __syncthreads();
+      const int hs = s + kDigit;
       for_rows(Wc, ldw, 0, n, rs, cv, [&](int r, float w) {
         const uint32_t key = orderable(weight_score(w, fc));
-        if ((key >> kShift0) == bin)
-          add(((unsigned long long)(key & ((1u << kShift0) - 1u)) << idx_bits) |
-              (unsigned long long)((uint32_t)c * (uint32_t)n + (uint32_t)r));
+        if ((key >> kShift0) == bin) {
+          const unsigned long long v = ((unsigned long long)(key & ((1u << kShift0) - 1u)) << idx_bits) |
+                                       (unsigned long long)((uint32_t)c * (uint32_t)n + (uint32_t)r);
+          if ((v >> hs) == (pref >> hs)) atomicAdd(&lh[(uint32_t)(v >> s) & ((1u << kDigit) - 1u)], 1u);
+        }
       });
+      __syncthreads();
+      uint32_t d, rk2, ct2;
+      find_bucket<(1 << kDigit) / 256>(lh, rk, sh, d, rk2, ct2);
+      pref |= (unsigned long long)d << s;
+      rk = rk2;
     }
-    __syncthreads();
-    uint32_t d, rk2, ct2;
-    find_bucket<(1 << kDigit) / 256>(lh, rk, sh, d, rk2, ct2);
-    pref |= (unsigned long long)d << s;
-    rk = rk2;
   }
   for (int i = tid; i < kBins0; i += 256) hist[i] = 0;
   if (tid == 0) {
@@ -625,7 +659,7 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
                     : (qt ? inblock_kernel<false, true> : inblock_kernel<false, false>);
   const IbOpts ibo{o.nm_n, o.q_bits, qt ? o.q_group : kMaxBlock, o.q_scale, o.q_zero};
   if (duo_status d = set_max_lds((const void*)ib_kern, ib_lds); d != DUO_OK) return d;
-  const size_t sel_lds = (size_t)(16 + (1 << kDigit)) * sizeof(uint32_t) + (size_t)kSelCap * sizeof(unsigned long long);
+  const size_t sel_lds = (size_t)(16 + (1 << kDigitR)) * sizeof(uint32_t) + (size_t)kRankMax * sizeof(unsigned long long);
   if (duo_status d = set_max_lds((const void*)sel_resolve_kernel, sel_lds); d != DUO_OK) return d;
   const int P = (int)(cdiv(n, 32) < kSelWG ? cdiv(n, 32) : kSelWG);
   int64_t prev = 0;
