@@ -125,6 +125,21 @@ __device__ __forceinline__ void for_rows(const float* Wc, int64_t ldw, int r0, i
   }
 }
 
+// Minimum and maximum over a wave: DPP steps inside each 16-lane row (quad
+// swaps, half-row and row mirrors leave the row's result in every lane), then
+// the four rows' results read as scalars.
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_extreme(uint32_t v) {
+  auto pick = [](uint32_t a, uint32_t b) { return MAX ? (a > b ? a : b) : (a < b ? a : b); };
+  v = pick(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  v = pick(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  v = pick(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  v = pick(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x140, 0xF, 0xF, false));  // row_mirror
+  const uint32_t a = pick((uint32_t)__builtin_amdgcn_readlane((int)v, 0), (uint32_t)__builtin_amdgcn_readlane((int)v, 16));
+  const uint32_t b = pick((uint32_t)__builtin_amdgcn_readlane((int)v, 32), (uint32_t)__builtin_amdgcn_readlane((int)v, 48));
+  return pick(a, b);
+}
+
 // Selection of one block in three launches (see the file comment); kernel
 // boundaries are the only synchronisation, so no cache-wide fences are needed.
 //
@@ -143,14 +158,64 @@ __global__ __launch_bounds__(256) void sel_hist_kernel(const float* __restrict__
   const bool cv = (tid & 127) < Bb;
   const float fc = fac[j0 + c];
   const float* Wc = W + j0 + c;
+  // usual case: the thread's rows fit one batch, loaded before the histogram
+  // is cleared so that the two overlap
+  const bool one = r1 - r0 <= 2 * kRowU && !scores_out;  // uniform
+  float v[kRowU];
+  if (one) {
+#pragma unroll
+    for (int u = 0; u < kRowU; ++u) {
+      const int r = r0 + rs + 2 * u;
+      v[u] = Wc[(int64_t)(r < r1 ? r : min(r0, n - 1)) * ldw];
+    }
+  }
+  if (one) {
+    // Only the bins between the workgroup's smallest and largest key are
+    // cleared and flushed (a few hundred of the 8192 for a typical block).
+    if (!do_hist) return;
+    __shared__ uint32_t rng[8];
+    uint32_t bk[kRowU];
+    uint32_t lo = kBins0, hi = 0;
+#pragma unroll
+    for (int u = 0; u < kRowU; ++u) {
+      const bool ok = cv && r0 + rs + 2 * u < r1;
+      bk[u] = ok ? orderable(weight_score(v[u], fc)) >> kShift0 : (uint32_t)kBins0;  // kBins0: no element
+      lo = ok && bk[u] < lo ? bk[u] : lo;
+      hi = ok && bk[u] > hi ? bk[u] : hi;
+    }
+    lo = wave_extreme<false>(lo);
+    hi = wave_extreme<true>(hi);
+    const int wv = tid >> 6;
+    if ((tid & 63) == 0) {
+      rng[wv] = lo;
+      rng[4 + wv] = hi;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      lo = min(lo, rng[w]);
+      hi = max(hi, rng[4 + w]);
+    }
+    for (int i = (int)lo + tid; i <= (int)hi; i += 256) lh[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kRowU; ++u)
+      if (bk[u] < (uint32_t)kBins0) atomicAdd(&lh[bk[u]], 1u);
+    __syncthreads();
+    for (int i = (int)lo + tid; i <= (int)hi; i += 256)
+      if (lh[i]) atomicAdd(&hist[i], lh[i]);
+    return;
+  }
   if (do_hist)
     for (int i = tid; i < kBins0; i += 256) lh[i] = 0;
   __syncthreads();
-  for_rows(Wc, ldw, r0, r1, rs, cv, [&](int r, float w) {
-    const float S = weight_score(w, fc);
-    if (scores_out) scores_out[(int64_t)r * ldw + j0 + c] = S;
-    if (do_hist) atomicAdd(&lh[orderable(S) >> kShift0], 1u);
-  });
+  {
+    for_rows(Wc, ldw, r0, r1, rs, cv, [&](int r, float w) {
+      const float S = weight_score(w, fc);
+      if (scores_out) scores_out[(int64_t)r * ldw + j0 + c] = S;
+      if (do_hist) atomicAdd(&lh[orderable(S) >> kShift0], 1u);
+    });
+  }
   if (!do_hist) return;
   __syncthreads();
   for (int i = tid; i < kBins0; i += 256)
@@ -166,15 +231,49 @@ __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict
                                                          unsigned long long* cand) {
   __shared__ uint32_t sh[16];
   const int tid = threadIdx.x;
-  uint32_t bin, rank, cnt;
-  find_bucket<kBins0 / 256>(hist, z, sh, bin, rank, cnt);
-  if (cnt > (uint32_t)kSelCap) return;  // the resolving launch reads the block itself
   const int rpw = (n + gridDim.x - 1) / gridDim.x;
   const int r0 = blockIdx.x * rpw, r1 = min(n, r0 + rpw);
   const int c = min(tid & 127, Bb - 1), rs = tid >> 7;
   const bool cv = (tid & 127) < Bb;
   const float fc = fac[j0 + c];
   const float* Wc = W + j0 + c;
+  // Usual case: the thread's rows fit one batch.  They are loaded before the
+  // bucket search (both loads in flight together) and kept for both passes.
+  const bool one = r1 - r0 <= 2 * kRowU;  // uniform
+  uint32_t key1[kRowU];
+  uint32_t vm = 0;  // bit u: row r0 + rs + 2u is in range (and the column is)
+  if (one) {
+#pragma unroll
+    for (int u = 0; u < kRowU; ++u) {
+      const int r = r0 + rs + 2 * u;
+      key1[u] = orderable(weight_score(Wc[(int64_t)(r < r1 ? r : min(r0, n - 1)) * ldw], fc));
+      vm |= (cv && r < r1 ? 1u : 0u) << u;
+    }
+  }
+  uint32_t bin, rank, cnt;
+  find_bucket<kBins0 / 256>(hist, z, sh, bin, rank, cnt);
+  if (cnt > (uint32_t)kSelCap) return;  // the resolving launch reads the block itself
+  if (one) {
+    asm volatile("" : "+v"(vm));  // lane tests where they are used
+    uint32_t mine = 0;
+#pragma unroll
+    for (int u = 0; u < kRowU; ++u) mine += ((vm >> u) & 1u) && (key1[u] >> kShift0) == bin;
+    uint32_t tot;
+    const uint32_t incl = block_incl_scan(mine, sh + 4, tot);
+    if (tid == 0) sh[9] = tot ? atomicAdd(&st->ncand, tot) : 0u;
+    __syncthreads();
+    uint32_t pos = sh[9] + incl - mine;
+    asm volatile("" : "+v"(vm));
+#pragma unroll
+    for (int u = 0; u < kRowU; ++u)
+      if (((vm >> u) & 1u) && (key1[u] >> kShift0) == bin) {
+        if (pos < (uint32_t)kSelCap)
+          cand[pos] = ((unsigned long long)(key1[u] & ((1u << kShift0) - 1u)) << idx_bits) |
+                      (unsigned long long)((uint32_t)c * (uint32_t)n + (uint32_t)(r0 + rs + 2 * u));
+        ++pos;
+      }
+    return;
+  }
   uint32_t mine = 0;
   for_rows(Wc, ldw, r0, r1, rs, cv, [&](int, float w) { mine += (orderable(weight_score(w, fc)) >> kShift0) == bin; });
   uint32_t tot;
