@@ -404,6 +404,10 @@ constexpr int IB_I = kMaxBlock / IB_Q;    // columns per lane: c = q + 16 i
 constexpr int IB_ROWS = 256 / IB_Q;       // rows per workgroup
 constexpr int IB_QS = IB_I + 1;           // LDS stride between lanes (odd: no bank conflicts)
 constexpr int IB_JS = IB_Q * IB_QS;       // LDS floats per column step
+// LDS image of one block's operands, [lq | dq | il], padded to whole 4 KB
+// rows of a 256-thread copy (16 bytes per thread)
+constexpr int IB_IMG_USED = 2 * kMaxBlock * IB_JS + kMaxBlock;          // floats
+constexpr int IB_IMG = (IB_IMG_USED * 4 + 4095) / 4096 * 4096 / 4;      // floats (37888)
 
 // Lane O of every 16-lane row, broadcast to the row.
 template <int O>
@@ -564,65 +568,73 @@ __device__ __forceinline__ void ib_steps(IbRow& s, const float* lq, const float*
 // NM: the N:M variant (mode MODE_NM): the keep bits are chosen inside the
 // column loop, and the scores they used go to scores_out when it is set.
 // QUANT: joint RTN quantisation of the kept weights (grids per row and group).
+// The LDS image of block b (columns j0 = b*B .. j0+Bb) for inblock_kernel:
+// the live L and D entries of each lane's columns and 1 / L_jj, zeros
+// elsewhere (entries of columns <= j, past the ragged end, and the padding
+// slot of each lane).  One launch covers every block of the sweep.
+__global__ __launch_bounds__(256) void ib_image_kernel(const float* __restrict__ L, int64_t ldl,
+                                                       const float* __restrict__ D, int64_t ldd, int k, int B,
+                                                       float* __restrict__ img) {
+  const int b = blockIdx.x, j0 = b * B, Bb = min(B, k - j0);
+  float* out = img + (int64_t)b * IB_IMG;
+  for (int e = blockIdx.y * 256 + threadIdx.x; e < IB_IMG; e += gridDim.y * 256) {
+    float v = 0.f;
+    if (e < 2 * kMaxBlock * IB_JS) {
+      const bool isd = e >= kMaxBlock * IB_JS;
+      const int f = isd ? e - kMaxBlock * IB_JS : e;
+      const int j = f / IB_JS, rem = f % IB_JS, q = rem / IB_QS, i = rem % IB_QS;
+      const int c = q + IB_Q * i;
+      if (i < IB_I && c > j && c < Bb) {
+        if (isd)
+          v = D[(int64_t)(j0 + j) * ldd + j0 + c];
+        else
+          v = L[(int64_t)(j0 + c) * ldl + j0 + j] * (1.0f / L[(int64_t)(j0 + j) * ldl + j0 + j]);
+      }
+    } else if (e < IB_IMG_USED) {
+      const int j = e - 2 * kMaxBlock * IB_JS;
+      v = j < Bb ? 1.0f / L[(int64_t)(j0 + j) * ldl + j0 + j] : 1.f;
+    }
+    out[e] = v;
+  }
+}
+
 template <bool NM, bool QUANT>
 __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int64_t ew_ld,
-                                                      const float* __restrict__ L, int64_t ldl,
-                                                      const float* __restrict__ D, int64_t ldd,
                                                       const float* __restrict__ fac, const SelState* st, int mode,
                                                       const uint32_t* __restrict__ mask_in, float* __restrict__ EW,
                                                       uint8_t* __restrict__ bmask, IbOpts opt,
-                                                      float* __restrict__ scores_out) {
+                                                      float* __restrict__ scores_out, const float* __restrict__ img) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
   float* lq = sm;                       // [j][q][i]: L[j0+q+16i][j0+j] / L[j0+j][j0+j] where q+16i > j, else 0
   float* dq = sm + kMaxBlock * IB_JS;   // [j][q][i]: D[j0+j][j0+q+16i] where q+16i > j, else 0
   float* il = dq + kMaxBlock * IB_JS;   // [j]: 1 / L[j0+j][j0+j]
   const int tid = threadIdx.x;
-  if (tid < kMaxBlock) il[tid] = tid < Bb ? 1.0f / L[(int64_t)(j0 + tid) * ldl + j0 + tid] : 1.f;
-  __syncthreads();
-  // stage L: one wave covers 8 consecutive j of the 8 rows q + 16 i (one q);
-  // all of a thread's loads are issued before its LDS stores
-  constexpr int SPT = kMaxBlock * IB_Q * IB_I / 256;  // 64 elements per thread
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    float v[SPT / 2];
-#pragma unroll
-    for (int u = 0; u < SPT / 2; ++u) {
-      const int p = tid + 256 * (h * SPT / 2 + u);
-      const int jj = p & 7, i = (p >> 3) & 7, q = (p >> 6) & 15, j = ((p >> 10) << 3) + jj;
-      const int c = q + IB_Q * i;
-      v[u] = (c > j && c < Bb) ? L[(int64_t)(j0 + c) * ldl + j0 + j] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < SPT / 2; ++u) {
-      const int p = tid + 256 * (h * SPT / 2 + u);
-      const int jj = p & 7, i = (p >> 3) & 7, q = (p >> 6) & 15, j = ((p >> 10) << 3) + jj;
-      lq[j * IB_JS + q * IB_QS + i] = v[u] * il[j];
-    }
-  }
-  // stage D: one wave covers 64 consecutive columns of one row j
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    float v[SPT / 2];
-#pragma unroll
-    for (int u = 0; u < SPT / 2; ++u) {
-      const int p = tid + 256 * (h * SPT / 2 + u);
-      const int q = p & 15, i = (p >> 4) & 7, j = p >> 7;
-      const int c = q + IB_Q * i;
-      v[u] = (c > j && c < Bb && j < Bb) ? D[(int64_t)(j0 + j) * ldd + j0 + c] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < SPT / 2; ++u) {
-      const int p = tid + 256 * (h * SPT / 2 + u);
-      const int q = p & 15, i = (p >> 4) & 7, j = p >> 7;
-      dq[j * IB_JS + q * IB_QS + i] = v[u];
-    }
-  }
-  __syncthreads();
-
-  const int lane = tid & 63;
+  // The row's values and score factors are requested first; the block's LDS
+  // image (written once per sweep by ib_image_kernel) then streams straight
+  // into LDS (global_load_lds, 16 bytes per lane, no register staging), so
+  // the two latencies overlap.
   const int q = tid & 15;
   const int row = blockIdx.x * IB_ROWS + (tid >> 4);
   const bool rv = row < n;
+  float wv[IB_I], fv[IB_I];
+#pragma unroll
+  for (int i = 0; i < IB_I; ++i) {
+    const int c = q + IB_Q * i;
+    const bool cv = rv && c < Bb;
+    wv[i] = Wo[cv ? (int64_t)row * k + j0 + c : 0];
+    fv[i] = fac[c < Bb ? j0 + c : j0];
+  }
+  {
+    const uint8_t* src = (const uint8_t*)img + (tid >> 6) * 1024 + (tid & 63) * 16;
+    uint8_t* dst = (uint8_t*)sm + (tid >> 6) * 1024;
+#pragma unroll
+    for (int t = 0; t < IB_IMG * 4 / 4096; ++t)
+      __builtin_amdgcn_global_load_lds((const void*)(src + t * 4096),
+                                       (__attribute__((address_space(3))) void*)(dst + t * 4096), 16, 0, 0);
+  }
+  __syncthreads();  // (waits for every load of the thread, the image's included)
+
+  const int lane = tid & 63;
   uint32_t T = 0, tie = 0;
   if (mode == MODE_SELECT) {
     T = st->key;
@@ -634,17 +646,17 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
   for (int i = 0; i < IB_I; ++i) {
     const int c = q + IB_Q * i;
     const bool cv = rv && c < Bb;
-    s.w[i] = cv ? Wo[(int64_t)row * k + j0 + c] : 0.f;
+    s.w[i] = cv ? wv[i] : 0.f;
     s.e[i] = 0.f;
     s.w0[i] = 0.f;
     if constexpr (NM) {
-      s.f[i] = c < Bb ? fac[j0 + c] : 0.f;
+      s.f[i] = c < Bb ? fv[i] : 0.f;
       s.sc[i] = 0.f;
     }
     bool keep = true;
     if (cv) {
       if (mode == MODE_SELECT) {
-        const uint32_t key = orderable(weight_score(s.w[i], fac[j0 + c]));
+        const uint32_t key = orderable(weight_score(s.w[i], fv[i]));
         const uint32_t idx = (uint32_t)c * (uint32_t)n + (uint32_t)row;
         keep = !(key < T || (key == T && idx <= tie));
       } else if (mode == MODE_FORCED) {
@@ -720,6 +732,7 @@ struct SweepWs {
   unsigned long long* cand;
   float* EW;
   uint8_t* bmask;
+  float* img;  // LDS images of the blocks' L, D operands
   size_t bytes;
 };
 
@@ -731,6 +744,7 @@ SweepWs carve(void* ws, int64_t n, int64_t k, int B) {
   w.cand = c.take<unsigned long long>(kSelCap);
   w.EW = c.take<float>((size_t)n * 2 * super_width(B));
   w.bmask = c.take<uint8_t>((size_t)n * k);
+  w.img = c.take<float>((size_t)cdiv(k, B) * IB_IMG);
   w.bytes = c.off;
   return w;
 }
@@ -751,7 +765,10 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   DUO_LAUNCH_CHECK();
   hipLaunchKernelGGL(sel_reset_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist);
   DUO_LAUNCH_CHECK();
-  const size_t ib_lds = (size_t)(2 * kMaxBlock * IB_JS + kMaxBlock) * sizeof(float);
+  const size_t ib_lds = (size_t)IB_IMG * sizeof(float);
+  hipLaunchKernelGGL(ib_image_kernel, dim3((unsigned)cdiv(k, B), 16), dim3(256), 0, s, L, ldl, D, ldd, (int)k, B,
+                     w.img);
+  DUO_LAUNCH_CHECK();
   const bool nm = o.nm_n > 0 && !mask_in;
   const bool qt = o.q_bits > 0;
   auto ib_kern = nm ? (qt ? inblock_kernel<true, true> : inblock_kernel<true, false>)
@@ -798,8 +815,8 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     prof_begin(DUO_PROF_INBLOCK, s);
     const int64_t sb0 = j0 / S * S, sb1 = sb0 + S < k ? sb0 + S : k;
     hipLaunchKernelGGL(ib_kern, dim3((unsigned)cdiv(n, IB_ROWS)), dim3(256), ib_lds, s, W_out, (int)n, (int)k,
-                       (int)j0, Bb, (int64_t)2 * S, L, ldl, D, ldd, fac, (const SelState*)w.st, mode, mask_in,
-                       w.EW + (j0 - sb0), w.bmask, ibo, scores_out);
+                       (int)j0, Bb, (int64_t)2 * S, fac, (const SelState*)w.st, mode, mask_in,
+                       w.EW + (j0 - sb0), w.bmask, ibo, scores_out, (const float*)(w.img + (j0 / B) * IB_IMG));
     DUO_LAUNCH_CHECK();
     prof_end(DUO_PROF_INBLOCK, s);
     // inside the super-block: columns [j1, sb1) from this block (K = Bb);
