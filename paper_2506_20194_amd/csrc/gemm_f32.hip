@@ -272,8 +272,10 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmDesc d, int ntiles) {
 }
 
 // A launch with fewer 128 tiles than kSmallTiles runs on 64 tiles: four
-// times the workgroups, so that short products still cover the 256 CUs.
-constexpr int kSmallTiles = 512;
+// times the workgroups.  Short products then still cover the 256 CUs, and
+// launches of a few waves of 128 tiles lose less to the last, partly filled
+// wave (measured at k = 4096 and 11008: 2048 beats 512, 1024 and 4096).
+constexpr int kSmallTiles = 2048;
 
 template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
 duo_status launch(const GemmDesc& d, hipStream_t s) {
