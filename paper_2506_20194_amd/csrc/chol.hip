@@ -61,15 +61,18 @@ __global__ __launch_bounds__(256) void damp_kernel(float* H, int64_t ldh, int k,
 //   leaf     one wave factors A_JJ = V_JJ V_JJ^T and inverts it in the same
 //            sweep (column c of the working matrix drives both the rank-1
 //            update of the columns before it and the back substitution
-//            V N = I of the columns after it); the column and row of step c
-//            reach the wave's lanes through LDS, so the 32 steps need no
-//            workgroup barrier;
-//   panel    V_IJ = A_IJ N_JJ^T for the leaves I < J;
-//   update   A_II' -= V_IJ V_I'J^T for I, I' < J;
-// and finally the off-diagonal blocks of N by block back substitution,
-//   N_IJ = -N_II sum_{K=I+1..J} V_IK N_KJ, in order of J - I.
-// The small products run on all four waves with fp32 MFMA, one 32 x 32
-// block per wave.
+//            V N = I of the columns after it); column c reaches the wave's
+//            lanes as scalars read from its lane, so the 32 steps need no
+//            LDS round trip and no workgroup barrier;
+//   panel    V_IJ = A_IJ N_JJ^T for the leaves I < J, and beside it the
+//            finished inverse blocks N_JK = -N_JJ T_JK for K > J;
+//   update   A_II' -= V_IJ V_I'J^T for I <= I' < J, and beside it
+//            T_IK += V_IJ N_JK for I < J <= K,
+// so that T_JK = sum_{L=J+1..K} V_JL N_LK is complete when leaf J is done
+// (block back substitution N_JK = -N_JJ T_JK folded into the factorisation's
+// own rounds).  T_IK lives in the block (K, I) below the diagonal, which the
+// factorisation never reads.  The small products run on all four waves with
+// fp32 MFMA, one 32 x 32 block per wave and task.
 // Padding rows/columns beyond s are an identity block.
 constexpr int DS = kTile + 2;  // LDS row stride of the working matrices (rows 2 banks apart)
 constexpr int LF = 32;         // leaf width
@@ -180,14 +183,14 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
       const float w = (c < s) ? v[u] : (r == c ? 1.f : 0.f);
       if (r <= c) {
         A[r * DS + c] = w;
-        A[c * DS + r] = w;
+        A[c * DS + r] = r / LF == c / LF ? w : 0.f;  // below the diagonal blocks: T accumulators
       }
-      N[r * DS + c] = 0.f;
     }
   }
   if (tid == 0) *fail_sh = -1;
   __syncthreads();
-  for (int J = kTile / LF - 1; J >= 0; --J) {
+  constexpr int NB = kTile / LF;
+  for (int J = NB - 1; J >= 0; --J) {
     const int j0 = J * LF;
     if (wave == 0) {
       const int q = lane & (LF - 1);
@@ -205,41 +208,41 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
       if (lane == 0 && fail >= 0 && *fail_sh < 0) *fail_sh = j0 + fail;
     }
     __syncthreads();
+    // NB - 1 products, one per wave: the panel V_IJ = A_IJ N_JJ^T for I < J
+    // (in place: only this wave reads A_IJ in this round), and the finished
+    // blocks N_JK = -N_JJ T_JK for K > J
+    if (wave < NB - 1) {
+      f4 acc[2][2] = {};
+      if (wave < J) {
+        wave_gemm32<true>(&A[wave * LF * DS + j0], &N[j0 * DS + j0], acc, lane);
+        store32(&A[wave * LF * DS + j0], acc, lane, 1.f, false);
+      } else {
+        const int K = wave + 1;
+        wave_gemm32<false>(&N[j0 * DS + j0], &A[K * LF * DS + j0], acc, lane);
+        store32(&N[j0 * DS + K * LF], acc, lane, -1.f, false);
+      }
+    }
+    __syncthreads();
     if (J == 0) break;
-    // panel: V_IJ = A_IJ N_JJ^T for I < J (one wave per block), kept in registers
-    // until every wave has read A_IJ
-    f4 acc[2][2] = {};
-    if (wave < J) {
-      wave_gemm32<true>(&A[wave * LF * DS + j0], &N[j0 * DS + j0], acc, lane);
-    }
-    __syncthreads();
-    if (wave < J) store32(&A[wave * LF * DS + j0], acc, lane, 1.f, false);
-    __syncthreads();
-    // update: A_II' -= V_IJ V_I'J^T for I, I' < J (both triangles)
-    for (int blk = wave; blk < J * J; blk += 4) {
-      const int I = blk / J, I2 = blk % J;
+    // Schur update A_II' -= V_IJ V_I'J^T for I <= I' < J, and T_IK += V_IJ N_JK
+    // for I < J <= K (T_IK sits in the free block (K, I) below the diagonal)
+    const int nsch = J * (J + 1) / 2, ntot = nsch + J * (NB - J);
+    for (int task = wave; task < ntot; task += 4) {
       f4 u[2][2] = {};
-      wave_gemm32<true>(&A[I * LF * DS + j0], &A[I2 * LF * DS + j0], u, lane);
-      store32(&A[I * LF * DS + I2 * LF], u, lane, -1.f, true);
-    }
-    __syncthreads();
-  }
-  // off-diagonal blocks of N, by distance D = J - I
-  constexpr int NB = kTile / LF;
-  for (int D = 1; D < NB; ++D) {
-    const int nblk = NB - D;
-    f4 acc[2][2] = {};
-    if (wave < nblk) {  // T_I = sum_{K=I+1..I+D} V_IK N_{K,I+D}
-      const int I = wave, J = wave + D;
-      for (int K = I + 1; K <= J; ++K) wave_gemm32<false>(&A[I * LF * DS + K * LF], &N[K * LF * DS + J * LF], acc, lane);
-      store32(&A[(wave + 1) * LF * DS], acc, lane, 1.f, false);  // A's lower blocks are free by now
-    }
-    __syncthreads();
-    if (wave < nblk) {  // N_IJ = -N_II T_I
-      const int I = wave, J = wave + D;
-      f4 n2[2][2] = {};
-      wave_gemm32<false>(&N[I * LF * DS + I * LF], &A[(wave + 1) * LF * DS], n2, lane);
-      store32(&N[I * LF * DS + J * LF], n2, lane, -1.f, false);
+      if (task < nsch) {
+        int I = 0, r = task;
+        while (r >= J - I) {
+          r -= J - I;
+          ++I;
+        }
+        const int I2 = I + r;
+        wave_gemm32<true>(&A[I * LF * DS + j0], &A[I2 * LF * DS + j0], u, lane);
+        store32(&A[I * LF * DS + I2 * LF], u, lane, -1.f, true);
+      } else {
+        const int r = task - nsch, I = r / (NB - J), K = J + r % (NB - J);
+        wave_gemm32<false>(&A[I * LF * DS + j0], &N[j0 * DS + K * LF], u, lane);
+        store32(&A[K * LF * DS + I * LF], u, lane, 1.f, true);
+      }
     }
     __syncthreads();
   }
