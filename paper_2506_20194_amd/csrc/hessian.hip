@@ -172,30 +172,37 @@ __global__ __launch_bounds__(256) void act_select_wave_kernel(const uint16_t* __
     for (int j = 0; j < 8; ++j) mag[8 * u + j] = ok ? (w[j >> 1] >> (16 * (j & 1))) & 0x7fffu : 0xffffffffu;
   }
   // v = the smallest magnitude with count(mag <= v) >= z, from two LDS
-  // histograms of the wave's own: the top 8 of the 15 magnitude bits (lane l
-  // scans bins 4l .. 4l+3), then the low 7 bits of the entries in the bin of
-  // the z-th entry (lane l: bins 2l, 2l+1).  Within a wave the LDS operations
-  // run in order, so no barrier is needed.
-  __shared__ uint32_t hist_w[4][256 + 128];
+  // histograms of the wave's own: the top 10 of the 15 magnitude bits (lane l
+  // scans bins 16l .. 16l+15), then the low 5 bits of the entries in the bin of
+  // the z-th entry (lane l < 32: bin l).  Coarse bins of exponent plus two
+  // mantissa bits spread a token's entries over four times as many bins as
+  // the exponent alone, so fewer lanes of an atomic collide on one address.
+  // Within a wave the LDS operations run in order, so no barrier is needed.
+  constexpr int kFineBits = 5, kCoarse = 1 << (15 - kFineBits), kFine = 1 << kFineBits;
+  __shared__ __attribute__((aligned(16))) uint32_t hist_w[4][kCoarse + kFine];
   uint32_t* hc = hist_w[threadIdx.x >> 6];
-  uint32_t* hf = hc + 256;
-  for (int i = lane; i < 256 + 128; i += 64) hc[i] = 0u;
+  uint32_t* hf = hc + kCoarse;
+  for (int i = lane; i < (kCoarse + kFine) / 4; i += 64) ((u32x4*)hc)[i] = u32x4{0u, 0u, 0u, 0u};
   __builtin_amdgcn_wave_barrier();
 #pragma unroll
   for (int e = 0; e < 8 * V; ++e)
-    if (mag[e] < 0x8000u) atomicAdd(&hc[mag[e] >> 7], 1u);
+    if (mag[e] < 0x8000u) atomicAdd(&hc[mag[e] >> kFineBits], 1u);
   __builtin_amdgcn_wave_barrier();
-  int h[4], loc = 0;
+  constexpr int PER = kCoarse / 64;
+  int h[PER], loc = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    h[i] = (int)hc[4 * lane + i];
-    loc += h[i];
+  for (int i = 0; i < PER / 4; ++i) {
+    const u32x4 q = ((const u32x4*)hc)[(PER / 4) * lane + i];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) h[4 * i + j] = (int)q[j];
   }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) loc += h[i];
   int incl = wave_incl_scan(loc), run = incl - loc, cb = -1, below = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < PER; ++i) {
     if (run < z && z <= run + h[i]) {
-      cb = 4 * lane + i;
+      cb = PER * lane + i;
       below = run;
     }
     run += h[i];
@@ -205,21 +212,18 @@ __global__ __launch_bounds__(256) void act_select_wave_kernel(const uint16_t* __
   below = __shfl(below, src);
 #pragma unroll
   for (int e = 0; e < 8 * V; ++e)
-    if ((int)(mag[e] >> 7) == cb) atomicAdd(&hf[mag[e] & 127u], 1u);
+    if ((int)(mag[e] >> kFineBits) == cb) atomicAdd(&hf[mag[e] & (kFine - 1u)], 1u);
   __builtin_amdgcn_wave_barrier();
-  const int f0 = (int)hf[2 * lane], f1 = (int)hf[2 * lane + 1];
-  incl = wave_incl_scan(f0 + f1);
-  run = below + incl - f0 - f1;
+  const int f0 = lane < kFine ? (int)hf[lane] : 0;
+  incl = wave_incl_scan(f0);
+  run = below + incl - f0;
   int fb = -1, lt = 0;
   if (run < z && z <= run + f0) {
-    fb = 2 * lane;
+    fb = lane;
     lt = run;
-  } else if (run + f0 < z && z <= run + f0 + f1) {
-    fb = 2 * lane + 1;
-    lt = run + f0;
   }
   const int src2 = __builtin_ctzll(__ballot(fb >= 0));
-  const uint32_t v = ((uint32_t)cb << 7) | (uint32_t)__shfl(fb, src2);
+  const uint32_t v = ((uint32_t)cb << kFineBits) | (uint32_t)__shfl(fb, src2);
   int need = z - __shfl(lt, src2);  // 1 <= need <= number of ties
   // the need-th tie in channel order (u, lane, j)
 #pragma unroll
