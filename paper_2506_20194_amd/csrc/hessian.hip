@@ -576,6 +576,7 @@ struct GramArgs {
   float* G;
   int64_t ldg;
   float* part;  // [nseg][ntiles][256 * 256] when nseg > 1
+  int vec4;     // k, ldh, ldg multiples of 4 and H, G 16-byte aligned: 16-byte reduction path
 };
 
 // Tiles are numbered H first, then G.  Within each kind, bands of 4 row blocks
@@ -892,6 +893,69 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A) {
   const float* p0 = A.part + (int64_t)tile * GT * GT;
   float* C = isg ? A.G : A.H;
   const int64_t ldc = isg ? A.ldg : A.ldh;
+  if (A.vec4) {
+    // 16-byte path (k and the leading dimensions multiples of 4): thread
+    // (r, c4) sums rows r, r + 16, r + 32, r + 48 at columns c4 .. c4 + 3, with
+    // every segment's loads issued before the sums need them
+    const int c4 = (threadIdx.x & 15) * 4, r0 = threadIdx.x >> 4;
+    float4 sum[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) sum[p] = make_float4(0.f, 0.f, 0.f, 0.f);
+    // (nseg <= 8; segments past the last re-read the last one, and are not added)
+    float4 v[8][4];
+#pragma unroll
+    for (int sg = 0; sg < 8; ++sg)
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+        v[sg][p] = *(const float4*)(p0 + min(sg, A.nseg - 1) * stride + (sr + r0 + 16 * p) * GT + sc + c4);
+#pragma unroll
+    for (int sg = 0; sg < 8; ++sg)
+      if (sg < A.nseg) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          sum[p].x += v[sg][p].x;
+          sum[p].y += v[sg][p].y;
+          sum[p].z += v[sg][p].z;
+          sum[p].w += v[sg][p].w;
+        }
+      }
+    const int col = J * GT + sc + c4;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int rr = r0 + 16 * p, row = I * GT + sr + rr;
+      if (row < A.k && col < A.k) {
+        float4* cp = (float4*)(C + (int64_t)row * ldc + col);
+        float4 c = *cp;
+        c.x += sum[p].x;
+        c.y += sum[p].y;
+        c.z += sum[p].z;
+        c.w += sum[p].w;
+        *cp = c;
+      }
+      tr[rr][c4] = sum[p].x;
+      tr[rr][c4 + 1] = sum[p].y;
+      tr[rr][c4 + 2] = sum[p].z;
+      tr[rr][c4 + 3] = sum[p].w;
+    }
+    if (!isg && I != J) {
+      __syncthreads();
+      const int hcol = I * GT + sr + c4;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int cc = r0 + 16 * p, hrow = J * GT + sc + cc;
+        if (hrow < A.k && hcol < A.k) {
+          float4* hp = (float4*)(A.H + (int64_t)hrow * A.ldh + hcol);
+          float4 h = *hp;
+          h.x += tr[c4][cc];
+          h.y += tr[c4 + 1][cc];
+          h.z += tr[c4 + 2][cc];
+          h.w += tr[c4 + 3][cc];
+          *hp = h;
+        }
+      }
+    }
+    return;
+  }
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int rr = ty; rr < 64; rr += 4) {
     const int e = (sr + rr) * GT + sc + tx;
@@ -1105,6 +1169,10 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
     A.G = G;
     A.ldg = ldg;
     A.part = w.part;
+    {
+      auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+      A.vec4 = k % 4 == 0 && (!want_h || (ldh % 4 == 0 && al16(H))) && (!want_g || (ldg % 4 == 0 && al16(G)));
+    }
     prof_begin(DUO_PROF_GRAM, s);
     if constexpr (sizeof(T) == 2)
       st = lo ? launch_gram<T, true>(A, s) : launch_gram<T, false>(A, s);
