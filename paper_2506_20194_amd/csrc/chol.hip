@@ -398,13 +398,16 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
   const int T = (int)cdiv(k, kTile);
   hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, H, ldh, (int)k, damp, w.st);
   DUO_LAUNCH_CHECK();
-  for (int b = T - 1; b >= 0; --b) {
+  // Blocks are factored from the last one.  The leading matrix receives the
+  // rank updates of two consecutive blocks b, b - 1 in one two-term product
+  // (K = 2 x 128): before block b - 1 is factored only its own block column
+  // gets block b's update (a 128-column strip).
+  auto factor = [&](int b, int sz) -> duo_status {
     const int r0 = b * kTile;
-    const int sz = (int)((int64_t)r0 + kTile <= k ? kTile : k - r0);
     hipLaunchKernelGGL(diag_factor_kernel, dim3(1), dim3(256), kDiagLds, s, (const float*)H, ldh, r0, sz,
                        w.vinv + (int64_t)b * kTile * kTile, w.st);
     DUO_LAUNCH_CHECK();
-    if (r0 == 0) break;
+    if (r0 == 0) return DUO_OK;
     // panel: H[0:r0, r0:r0+sz] <- H[0:r0, r0:r0+sz] * Vinv_bb^T   (in place: one tile column)
     GemmDesc p{};
     p.M = r0;
@@ -415,20 +418,63 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
     p.tri = TRI_ALL;
     p.nterms = 1;
     p.t[0] = GemmTerm{H + r0, ldh, 1, w.vinv + (int64_t)b * kTile * kTile, kTile, 0, sz, 1.f, KLO_ZERO, KHI_FULL};
-    duo_status st = gemm_f32(p, s);
+    return gemm_f32(p, s);
+  };
+  // the term -P_b P_b^T of block b's panel P_b = H[:, r0 : r0 + sz]
+  auto panel_term = [&](int b, int sz) {
+    const int r0 = b * kTile;
+    return GemmTerm{H + r0, ldh, 1, H + r0, ldh, 0, sz, -1.f, KLO_ZERO, KHI_FULL};
+  };
+  for (int b = T - 1; b >= 0;) {
+    const int sz = (int)((int64_t)b * kTile + kTile <= k ? kTile : k - (int64_t)b * kTile);
+    duo_status st = factor(b, sz);
     if (st != DUO_OK) return st;
-    // leading block (upper tiles): H[0:r0, 0:r0] -= P P^T
-    GemmDesc u{};
-    u.M = r0;
-    u.N = r0;
-    u.C = H;
-    u.ldc = ldh;
-    u.beta = 1.f;
-    u.tri = TRI_UPPER;
-    u.nterms = 1;
-    u.t[0] = GemmTerm{H + r0, ldh, 1, H + r0, ldh, 0, sz, -1.f, KLO_ZERO, KHI_FULL};
-    st = gemm_f32(u, s);
-    if (st != DUO_OK) return st;
+    if (b == 0) break;
+    if (b >= 2) {
+      // strip: H[0:r0, r1:r0] -= P_b P_b[r1:r0]^T with r1 = (b - 1) * 128
+      const int r0 = b * kTile, r1 = r0 - kTile;
+      GemmDesc g{};
+      g.M = r0;
+      g.N = kTile;
+      g.C = H + r1;
+      g.ldc = ldh;
+      g.beta = 1.f;
+      g.tri = TRI_ALL;
+      g.nterms = 1;
+      g.t[0] = GemmTerm{H + r0, ldh, 1, H + (int64_t)r1 * ldh + r0, ldh, 0, sz, -1.f, KLO_ZERO, KHI_FULL};
+      st = gemm_f32(g, s);
+      if (st != DUO_OK) return st;
+      st = factor(b - 1, kTile);
+      if (st != DUO_OK) return st;
+      // leading block (upper tiles): H[0:r1, 0:r1] -= P_b P_b^T + P_{b-1} P_{b-1}^T
+      GemmDesc u{};
+      u.M = r1;
+      u.N = r1;
+      u.C = H;
+      u.ldc = ldh;
+      u.beta = 1.f;
+      u.tri = TRI_UPPER;
+      u.nterms = 2;
+      u.t[0] = panel_term(b, sz);
+      u.t[1] = panel_term(b - 1, kTile);
+      st = gemm_f32(u, s);
+      if (st != DUO_OK) return st;
+      b -= 2;
+    } else {
+      // b == 1: leading block H[0:128, 0:128] -= P_1 P_1^T
+      GemmDesc u{};
+      u.M = kTile;
+      u.N = kTile;
+      u.C = H;
+      u.ldc = ldh;
+      u.beta = 1.f;
+      u.tri = TRI_UPPER;
+      u.nterms = 1;
+      u.t[0] = panel_term(b, sz);
+      st = gemm_f32(u, s);
+      if (st != DUO_OK) return st;
+      b -= 1;
+    }
   }
   hipLaunchKernelGGL(place_diag_kernel, dim3(T), dim3(256), 0, s, H, ldh, (int)k, (const float*)w.vinv);
   DUO_LAUNCH_CHECK();

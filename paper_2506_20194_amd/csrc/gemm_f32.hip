@@ -317,6 +317,7 @@ duo_status gemm_f32(const GemmDesc& d, hipStream_t s) {
   }
   const int c2 = d.t[1].a_row * 2 + d.t[1].b_row;
   if (c1 == 2 && c2 == 3) return launch<true, false, true, true, true>(d, s);
+  if (c1 == 2 && c2 == 2) return launch<true, false, true, false, true>(d, s);
   return DUO_ERR_UNSUPPORTED;
 }
 
