@@ -29,7 +29,18 @@ namespace {
 __global__ __launch_bounds__(256) void damp_kernel(float* H, int64_t ldh, int k, double damp, CholStatus* st) {
   __shared__ double red[256];
   double s = 0.0;
-  for (int i = threadIdx.x; i < k; i += 256) s += (double)H[(int64_t)i * ldh + i];
+  // 16 diagonal loads per thread in flight at a time (clamped, masked)
+  for (int i0 = 0; i0 < k; i0 += 256 * 16) {
+    float v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int i = min(i0 + 256 * u + (int)threadIdx.x, k - 1);
+      v[u] = H[(int64_t)i * ldh + i];
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (i0 + 256 * u + (int)threadIdx.x < k) s += (double)v[u];
+  }
   red[threadIdx.x] = s;
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
@@ -264,9 +275,21 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
 }
 
 // Copy the inverted diagonal blocks into place (full 128 x 128 incl. zeros).
-__global__ __launch_bounds__(256) void place_diag_kernel(float* H, int64_t ldh, int k, const float* vinv) {
+// Workgroup (b, y) copies rows 16y .. 16y + 15 of block b; with k and ldh
+// multiples of 4 and H 16-byte aligned, as 16-byte vectors.
+__global__ __launch_bounds__(256) void place_diag_kernel(float* H, int64_t ldh, int k, const float* vinv, int vec) {
   const int b = blockIdx.x;
   const float* src = vinv + (int64_t)b * kTile * kTile;
+  if (vec) {
+    const int rl = 16 * blockIdx.y + (threadIdx.x >> 4), c4 = 4 * (threadIdx.x & 15);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = b * kTile + rl, c = b * kTile + c4 + 64 * h;
+      if (r < k && c < k) *(float4*)(H + (int64_t)r * ldh + c) = *(const float4*)(src + rl * kTile + c4 + 64 * h);
+    }
+    return;
+  }
+  if (blockIdx.y) return;
   for (int e = threadIdx.x; e < kTile * kTile; e += 256) {
     const int r = b * kTile + e / kTile, c = b * kTile + e % kTile;
     if (r < k && c < k) H[(int64_t)r * ldh + c] = src[e];
@@ -476,7 +499,9 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
       b -= 1;
     }
   }
-  hipLaunchKernelGGL(place_diag_kernel, dim3(T), dim3(256), 0, s, H, ldh, (int)k, (const float*)w.vinv);
+  const int pvec = k % 4 == 0 && ldh % 4 == 0 && (reinterpret_cast<uintptr_t>(H) & 15) == 0;
+  hipLaunchKernelGGL(place_diag_kernel, dim3(T, kTile / 16), dim3(256), 0, s, H, ldh, (int)k, (const float*)w.vinv,
+                     pvec);
   DUO_LAUNCH_CHECK();
   duo_status st = trinv(H, ldh, k, T, w.X, s);
   if (st != DUO_OK) return st;

@@ -714,6 +714,50 @@ __global__ void finalize_kernel(const float* Wo, const uint8_t* bmask, int n, in
   }
 }
 
+// 16-byte forms of init_w_kernel and finalize_kernel for k a multiple of 32,
+// ldw a multiple of 4 and aligned buffers: one thread per 4 elements (per
+// 32 mask bits); the same values as the element kernels.
+__global__ void init_w4_kernel(const void* W, int dtype, int64_t ldw, int n, int k, float* Wo) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, k4 = k / 4;
+  if (id >= (int64_t)n * k4) return;
+  const int64_t r = id / k4, c = 4 * (id % k4);
+  float4 v;
+  if (dtype == DUO_BF16) {
+    const uint2 b = *(const uint2*)((const uint16_t*)W + r * ldw + c);
+    v = make_float4(bf16_bits_to_f32((uint16_t)(b.x & 0xFFFFu)), bf16_bits_to_f32((uint16_t)(b.x >> 16)),
+                    bf16_bits_to_f32((uint16_t)(b.y & 0xFFFFu)), bf16_bits_to_f32((uint16_t)(b.y >> 16)));
+  } else {
+    v = *(const float4*)((const float*)W + r * ldw + c);
+  }
+  ((float4*)Wo)[id] = v;
+}
+
+__global__ void finalize4_kernel(const float* Wo, const uint8_t* bmask, int n, int k, int dtype, void* lowp,
+                                 uint32_t* mask_out) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (mask_out && id < (int64_t)n * (k / 32)) {
+    // 32 byte flags (0 or 1) -> 32 bits: each 4-byte group gives a nibble
+    // ((v & 0x01010101) * 0x01020408) >> 24 (no carries: at most 15)
+    const u32x4* f = (const u32x4*)(bmask + id * 32);
+    const u32x4 a = f[0], b = f[1];
+    uint32_t bits = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      bits |= (((a[i] & 0x01010101u) * 0x01020408u) >> 24) << (4 * i);
+      bits |= (((b[i] & 0x01010101u) * 0x01020408u) >> 24) << (4 * i + 16);
+    }
+    mask_out[id] = bits;
+  }
+  if (lowp && id < (int64_t)n * k / 4) {
+    const float4 v = ((const float4*)Wo)[id];
+    if (dtype == DUO_BF16)
+      ((uint2*)lowp)[id] = make_uint2((uint32_t)f32_to_bf16_bits(v.x) | ((uint32_t)f32_to_bf16_bits(v.y) << 16),
+                                      (uint32_t)f32_to_bf16_bits(v.z) | ((uint32_t)f32_to_bf16_bits(v.w) << 16));
+    else
+      ((float4*)lowp)[id] = v;
+  }
+}
+
 // Two-level lazy update.  The weight update that a processed block owes the
 // columns to its right is linear in that block's (E, W0) pair, so it may be
 // applied in pieces: right after block [j0, j1) only the columns up to the
@@ -760,8 +804,15 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   const SweepWs w = carve(ws, n, k, B);
   const int64_t nk = n * k;
   const int64_t S = super_width(B);
-  hipLaunchKernelGGL(init_w_kernel, dim3((unsigned)cdiv(nk, 256)), dim3(256), 0, s, W, (int)w_dtype, ldw, (int)n,
-                     (int)k, W_out);
+  auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+  const bool v4 = k % 32 == 0 && ldw % 4 == 0 && (reinterpret_cast<uintptr_t>(W) & 7) == 0 && al16(W_out) &&
+                  (!W_out_lowp || al16(W_out_lowp)) && al16(ws);
+  if (v4)
+    hipLaunchKernelGGL(init_w4_kernel, dim3((unsigned)cdiv(nk / 4, 256)), dim3(256), 0, s, W, (int)w_dtype, ldw,
+                       (int)n, (int)k, W_out);
+  else
+    hipLaunchKernelGGL(init_w_kernel, dim3((unsigned)cdiv(nk, 256)), dim3(256), 0, s, W, (int)w_dtype, ldw, (int)n,
+                       (int)k, W_out);
   DUO_LAUNCH_CHECK();
   hipLaunchKernelGGL(sel_reset_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist);
   DUO_LAUNCH_CHECK();
@@ -842,9 +893,15 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   }
   if (mask_out || W_out_lowp) {
     const int64_t words = cdiv(k, 32);
-    const int64_t cnt = nk > n * words ? nk : n * words;
-    hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)cdiv(cnt, 256)), dim3(256), 0, s, (const float*)W_out,
-                       (const uint8_t*)w.bmask, (int)n, (int)k, (int)w_dtype, W_out_lowp, mask_out);
+    if (v4) {
+      const int64_t cnt = nk / 4 > n * words ? nk / 4 : n * words;
+      hipLaunchKernelGGL(finalize4_kernel, dim3((unsigned)cdiv(cnt, 256)), dim3(256), 0, s, (const float*)W_out,
+                         (const uint8_t*)w.bmask, (int)n, (int)k, (int)w_dtype, W_out_lowp, mask_out);
+    } else {
+      const int64_t cnt = nk > n * words ? nk : n * words;
+      hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)cdiv(cnt, 256)), dim3(256), 0, s, (const float*)W_out,
+                         (const uint8_t*)w.bmask, (int)n, (int)k, (int)w_dtype, W_out_lowp, mask_out);
+    }
     DUO_LAUNCH_CHECK();
   }
   return DUO_OK;
