@@ -281,7 +281,7 @@ def main():
     if args.quant and (args.act_order or not 2 <= args.quant <= 8):
         sys.exit("bench.py: --quant takes 2..8 bits and is timed without --act-order")
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: the solver runs on one GPU only (asked for --gpus {args.gpus}); "
               "the multi-GPU path is a design note, not implemented", file=sys.stderr)
         sys.exit(2)
     if args.copy_probe:

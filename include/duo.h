@@ -57,7 +57,7 @@ typedef int32_t duo_status;
 enum {
   DUO_OK = 0,
   DUO_ERR_INVALID_ARG = 1,  /* null pointer, bad size/stride/ratio/dtype */
-  DUO_ERR_UNSUPPORTED = 2,  /* valid but outside this build's limits      */
+  DUO_ERR_UNSUPPORTED = 2,  /* valid but outside the library's limits    */
   DUO_ERR_WORKSPACE = 3,    /* workspace missing, too small or misaligned  */
   DUO_ERR_NOT_PD = 4,       /* damped Hessian not positive definite        */
   DUO_ERR_NONFINITE = 5,    /* NaN/Inf met where a finite value is needed  */

@@ -81,7 +81,7 @@ __global__ __launch_bounds__(256) void damp_kernel(float* H, int64_t ldh, int k,
 //            T_IK += V_IJ N_JK for I < J <= K,
 // so that T_JK = sum_{L=J+1..K} V_JL N_LK is complete when leaf J is done
 // (block back substitution N_JK = -N_JJ T_JK folded into the factorisation's
-// own rounds).  T_IK lives in the block (K, I) below the diagonal, which the
+// own steps).  T_IK lives in the block (K, I) below the diagonal, which the
 // factorisation never reads.  The small products run on all four waves with
 // fp32 MFMA, one 32 x 32 block per wave and task.
 // Padding rows/columns beyond s are an identity block.
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
     }
     __syncthreads();
     // NB - 1 products, one per wave: the panel V_IJ = A_IJ N_JJ^T for I < J
-    // (in place: only this wave reads A_IJ in this round), and the finished
+    // (in place: only this wave reads A_IJ at this step), and the finished
     // blocks N_JK = -N_JJ T_JK for K > J
     if (wave < NB - 1) {
       f4 acc[2][2] = {};
