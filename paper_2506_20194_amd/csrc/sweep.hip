@@ -42,7 +42,9 @@ struct SelState {
   uint32_t ncand;    // candidates gathered for the current block
   uint32_t key;      // threshold: an element is pruned iff
   uint32_t tie;      //   (key, column*n + row) <= (key, tie)
-  uint32_t pad;
+  uint32_t bin;      // bucket of the z-th key, the rank inside it and its
+  uint32_t rank;     //   count, as the gathering launch found them
+  uint32_t cnt;
 };
 
 __global__ void sel_reset_kernel(SelState* st, uint32_t* hist) {
@@ -252,6 +254,11 @@ __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict
   }
   uint32_t bin, rank, cnt;
   find_bucket<kBins0 / 256>(hist, z, sh, bin, rank, cnt);
+  if (blockIdx.x == 0 && tid == 0) {  // for the resolving launch
+    st->bin = bin;
+    st->rank = rank;
+    st->cnt = cnt;
+  }
   if (cnt > (uint32_t)kSelCap) return;  // the resolving launch reads the block itself
   if (one) {
     asm volatile("" : "+v"(vm));  // lane tests where they are used
@@ -292,7 +299,8 @@ __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict
   });
 }
 
-// 3. one workgroup: the rank-th composite of the bucket, then the histogram is
+// 3. one workgroup: the rank-th composite of the bucket (bin, rank and count
+//    as the gathering launch left them in the state), then the histogram is
 //    cleared for the next block.  Gathered candidates (at most kSelCap) stay
 //    in registers, 32 per thread: radix passes of up to kDigitR bits narrow
 //    them to the prefix that holds the rank-th composite until at most 256
@@ -310,15 +318,15 @@ __global__ __launch_bounds__(256) void sel_resolve_kernel(const float* __restric
   uint32_t* lh = sel_sm + 16;                                              // [1 << kDigitR]
   unsigned long long* lr = (unsigned long long*)(lh + (1 << kDigitR));     // [kRankMax]
   const int tid = threadIdx.x;
-  if (tid == 0) sh[12] = 0;  // compaction counter (published by find_bucket's barriers)
+  if (tid == 0) sh[12] = 0;  // compaction counter
+  __syncthreads();
   // every one of the kSelCap candidate slots exists: they are loaded before
-  // the bucket is known, so both loads are in flight together
+  // the bucket is read, so both loads are in flight together
   constexpr int NU = kSelCap / 256;
   unsigned long long v[NU];
 #pragma unroll
   for (int u = 0; u < NU; ++u) v[u] = cand[256 * u + tid];
-  uint32_t bin, rank, cnt;
-  find_bucket<kBins0 / 256>(hist, z, sh, bin, rank, cnt);
+  const uint32_t bin = st->bin, rank = st->rank, cnt = st->cnt;
   const int tb = kShift0 + idx_bits;  // composite bits
   unsigned long long pref = 0;
   if (cnt <= (uint32_t)kSelCap) {
