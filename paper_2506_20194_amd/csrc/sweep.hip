@@ -31,10 +31,13 @@ namespace duo {
 namespace {
 
 enum { MODE_SELECT = 0, MODE_FORCED = 1, MODE_KEEP_ALL = 2, MODE_PRUNE_ALL = 3, MODE_NM = 4 };
-constexpr int kShift0 = 19;                 // launch 0 histograms key bits 31..19
-constexpr int kBins0 = 1 << (32 - kShift0); // 8192 bins
-constexpr int kDigit = 8;                   // radix digit of the final select
-constexpr int kSelCap = 8192;               // largest bucket gathered into LDS
+// The first launch histograms key bits 31..sh0: sh0 = 19 (8192 bins) for
+// blocks of fewer than 2^20 scores, 17 (32768 bins, a quarter of the bucket)
+// for larger ones, so that the bucket of the z-th key stays within kSelCap.
+constexpr int kShift0 = 17;                 // smallest sh0
+constexpr int kBins0 = 1 << (32 - kShift0); // largest bin count (128 KB of LDS)
+constexpr int kDigit = 8;                   // radix digit of the W-stream fallback
+constexpr int kSelCap = 16384;              // largest bucket gathered (64 candidates per resolving thread)
 constexpr int kSelWG = 128;                 // workgroups of a selection launch (at most)
 constexpr int kRowU = 16;                   // rows loaded per batch by one thread
 
@@ -45,6 +48,8 @@ struct SelState {
   uint32_t bin;      // bucket of the z-th key, the rank inside it and its
   uint32_t rank;     //   count, as the gathering launch found them
   uint32_t cnt;
+  uint32_t nlo;      // kBins0 - 1 - (lowest occupied bin) and the highest
+  uint32_t hi;       //   occupied bin of the block's histogram (atomic max)
 };
 
 __global__ void sel_reset_kernel(SelState* st, uint32_t* hist) {
@@ -109,6 +114,38 @@ __device__ void find_bucket(const uint32_t* h, uint32_t rank, uint32_t* sh, uint
   __syncthreads();
 }
 
+// find_bucket over the bins [lo, hi] of h (all others are empty): thread t
+// sums a contiguous chunk of the range; the thread whose chunk holds the
+// rank-th element finds the bin by reading its chunk again.
+__device__ void find_bucket_range(const uint32_t* h, int lo, int hi, uint32_t rank, uint32_t* sh, uint32_t& bin,
+                                  uint32_t& rank_in, uint32_t& cnt) {
+  const int nb = hi >= lo ? hi - lo + 1 : 0;
+  const int per = (nb + 255) / 256;
+  const int b0 = lo + (int)threadIdx.x * per, b1 = min(hi + 1, b0 + per);
+  uint32_t mine = 0;
+  for (int b = b0; b < b1; ++b) mine += h[b];
+  uint32_t tot;
+  const uint32_t incl = block_incl_scan(mine, sh + 4, tot);
+  const uint32_t excl = incl - mine;
+  if (excl < rank && rank <= incl) {
+    uint32_t cum = excl;
+    for (int b = b0; b < b1; ++b) {
+      const uint32_t hv = h[b];
+      if (rank > cum && rank <= cum + hv) {
+        sh[0] = (uint32_t)b;
+        sh[1] = rank - cum;
+        sh[2] = hv;
+      }
+      cum += hv;
+    }
+  }
+  __syncthreads();
+  bin = sh[0];
+  rank_in = sh[1];
+  cnt = sh[2];
+  __syncthreads();
+}
+
 // f(row, w) for rows r0+rs, r0+rs+2, ... < r1 of one column.  Loads are
 // issued kRowU at a time, unconditionally (clamped to a valid row), so that
 // they are all in flight together; the trip count is uniform per wave.
@@ -148,11 +185,17 @@ __device__ __forceinline__ uint32_t wave_extreme(uint32_t v) {
 // Workgroup b of the first two owns rows [b*rpw, (b+1)*rpw); thread t handles
 // column t % 128 (clamped to Bb - 1 and masked) of every second row.
 
-// 1. histogram of key bits 31..19 over the block (optionally writing S)
+// 1. histogram of key bits 31..17 over the block (optionally writing S).
+//    HB: batches of kRowU rows a thread holds in registers (1 or 2), or 0
+//    for the streaming form of any height.  Only the bins between the
+//    workgroup's smallest and largest key are cleared and flushed, and that
+//    range also widens the block's [lo, hi] in the selection state.
+template <int HB>
 __global__ __launch_bounds__(256) void sel_hist_kernel(const float* __restrict__ W, int64_t ldw, int n, int Bb, int j0,
                                                        const float* __restrict__ fac, uint32_t* hist,
-                                                       float* scores_out, int do_hist) {
-  __shared__ uint32_t lh[kBins0];
+                                                       float* scores_out, int do_hist, SelState* st, int sh0) {
+  extern __shared__ __attribute__((aligned(16))) uint32_t lh[];  // [kBins0]
+  __shared__ uint32_t rng[8];
   const int tid = threadIdx.x;
   const int rpw = (n + gridDim.x - 1) / gridDim.x;
   const int r0 = blockIdx.x * rpw, r1 = min(n, r0 + rpw);
@@ -160,37 +203,29 @@ __global__ __launch_bounds__(256) void sel_hist_kernel(const float* __restrict__
   const bool cv = (tid & 127) < Bb;
   const float fc = fac[j0 + c];
   const float* Wc = W + j0 + c;
-  // usual case: the thread's rows fit one batch, loaded before the histogram
-  // is cleared so that the two overlap
-  const bool one = r1 - r0 <= 2 * kRowU && !scores_out;  // uniform
-  float v[kRowU];
-  if (one) {
+  uint32_t lo = kBins0, hi = 0;
+  if constexpr (HB > 0) {
+    if (!do_hist) return;  // (launched with HB > 0 only without scores_out)
+    constexpr int NV = HB * kRowU;
+    float v[NV];
 #pragma unroll
-    for (int u = 0; u < kRowU; ++u) {
+    for (int u = 0; u < NV; ++u) {
       const int r = r0 + rs + 2 * u;
       v[u] = Wc[(int64_t)(r < r1 ? r : min(r0, n - 1)) * ldw];
     }
-  }
-  if (one) {
-    // Only the bins between the workgroup's smallest and largest key are
-    // cleared and flushed (a few hundred of the 8192 for a typical block).
-    if (!do_hist) return;
-    __shared__ uint32_t rng[8];
-    uint32_t bk[kRowU];
-    uint32_t lo = kBins0, hi = 0;
+    uint32_t bk[NV];
 #pragma unroll
-    for (int u = 0; u < kRowU; ++u) {
+    for (int u = 0; u < NV; ++u) {
       const bool ok = cv && r0 + rs + 2 * u < r1;
-      bk[u] = ok ? orderable(weight_score(v[u], fc)) >> kShift0 : (uint32_t)kBins0;  // kBins0: no element
+      bk[u] = ok ? orderable(weight_score(v[u], fc)) >> sh0 : (uint32_t)kBins0;  // kBins0: no element
       lo = ok && bk[u] < lo ? bk[u] : lo;
       hi = ok && bk[u] > hi ? bk[u] : hi;
     }
     lo = wave_extreme<false>(lo);
     hi = wave_extreme<true>(hi);
-    const int wv = tid >> 6;
     if ((tid & 63) == 0) {
-      rng[wv] = lo;
-      rng[4 + wv] = hi;
+      rng[tid >> 6] = lo;
+      rng[4 + (tid >> 6)] = hi;
     }
     __syncthreads();
 #pragma unroll
@@ -201,36 +236,54 @@ __global__ __launch_bounds__(256) void sel_hist_kernel(const float* __restrict__
     for (int i = (int)lo + tid; i <= (int)hi; i += 256) lh[i] = 0;
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < kRowU; ++u)
+    for (int u = 0; u < NV; ++u)
       if (bk[u] < (uint32_t)kBins0) atomicAdd(&lh[bk[u]], 1u);
+  } else {
+    if (do_hist)
+      for (int i = tid; i < kBins0 / 4; i += 256) ((u32x4*)lh)[i] = u32x4{0u, 0u, 0u, 0u};
     __syncthreads();
-    for (int i = (int)lo + tid; i <= (int)hi; i += 256)
-      if (lh[i]) atomicAdd(&hist[i], lh[i]);
-    return;
-  }
-  if (do_hist)
-    for (int i = tid; i < kBins0; i += 256) lh[i] = 0;
-  __syncthreads();
-  {
     for_rows(Wc, ldw, r0, r1, rs, cv, [&](int r, float w) {
       const float S = weight_score(w, fc);
       if (scores_out) scores_out[(int64_t)r * ldw + j0 + c] = S;
-      if (do_hist) atomicAdd(&lh[orderable(S) >> kShift0], 1u);
+      if (do_hist) {
+        const uint32_t b = orderable(S) >> sh0;
+        atomicAdd(&lh[b], 1u);
+        lo = b < lo ? b : lo;
+        hi = b > hi ? b : hi;
+      }
     });
+    if (!do_hist) return;
+    lo = wave_extreme<false>(lo);
+    hi = wave_extreme<true>(hi);
+    if ((tid & 63) == 0) {
+      rng[tid >> 6] = lo;
+      rng[4 + (tid >> 6)] = hi;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      lo = min(lo, rng[w]);
+      hi = max(hi, rng[4 + w]);
+    }
   }
-  if (!do_hist) return;
   __syncthreads();
-  for (int i = tid; i < kBins0; i += 256)
+  for (int i = (int)lo + tid; i <= (int)hi; i += 256)
     if (lh[i]) atomicAdd(&hist[i], lh[i]);
+  if (tid == 0 && lo <= hi) {
+    atomicMax(&st->nlo, (uint32_t)(kBins0 - 1) - lo);
+    atomicMax(&st->hi, hi);
+  }
 }
 
-// 2. every workgroup locates the bucket of the z-th key in the histogram and
-//    appends its elements of that bucket as (low 19 key bits, index)
-//    composites; one atomic per workgroup reserves its slots
+// 2. every workgroup locates the bucket of the z-th key in the histogram
+//    (scanning only the block's occupied range [lo, hi]) and appends its
+//    elements of that bucket as (low 17 key bits, index) composites; one
+//    atomic per workgroup reserves its slots.  HB as for the histogram.
+template <int HB>
 __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict__ W, int64_t ldw, int n, int Bb, int j0,
                                                          const float* __restrict__ fac, uint32_t z, int idx_bits,
                                                          const uint32_t* hist, SelState* st,
-                                                         unsigned long long* cand) {
+                                                         unsigned long long* cand, int sh0) {
   __shared__ uint32_t sh[16];
   const int tid = threadIdx.x;
   const int rpw = (n + gridDim.x - 1) / gridDim.x;
@@ -239,32 +292,35 @@ __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict
   const bool cv = (tid & 127) < Bb;
   const float fc = fac[j0 + c];
   const float* Wc = W + j0 + c;
-  // Usual case: the thread's rows fit one batch.  They are loaded before the
-  // bucket search (both loads in flight together) and kept for both passes.
-  const bool one = r1 - r0 <= 2 * kRowU;  // uniform
-  uint32_t key1[kRowU];
+  // With HB > 0 the thread's rows are loaded before the bucket search (both
+  // loads in flight together) and kept for both passes.
+  constexpr int NV = HB > 0 ? HB * kRowU : 1;
+  uint32_t key1[NV];
   uint32_t vm = 0;  // bit u: row r0 + rs + 2u is in range (and the column is)
-  if (one) {
+  if constexpr (HB > 0) {
 #pragma unroll
-    for (int u = 0; u < kRowU; ++u) {
+    for (int u = 0; u < NV; ++u) {
       const int r = r0 + rs + 2 * u;
       key1[u] = orderable(weight_score(Wc[(int64_t)(r < r1 ? r : min(r0, n - 1)) * ldw], fc));
       vm |= (cv && r < r1 ? 1u : 0u) << u;
     }
   }
   uint32_t bin, rank, cnt;
-  find_bucket<kBins0 / 256>(hist, z, sh, bin, rank, cnt);
+  if (sh0 == kShift0 + 2)  // 8192 bins: all of them, without waiting for the range
+    find_bucket<(1 << (30 - kShift0)) / 256>(hist, z, sh, bin, rank, cnt);
+  else
+    find_bucket_range(hist, (int)(kBins0 - 1 - st->nlo), (int)st->hi, z, sh, bin, rank, cnt);
   if (blockIdx.x == 0 && tid == 0) {  // for the resolving launch
     st->bin = bin;
     st->rank = rank;
     st->cnt = cnt;
   }
   if (cnt > (uint32_t)kSelCap) return;  // the resolving launch reads the block itself
-  if (one) {
+  if constexpr (HB > 0) {
     asm volatile("" : "+v"(vm));  // lane tests where they are used
     uint32_t mine = 0;
 #pragma unroll
-    for (int u = 0; u < kRowU; ++u) mine += ((vm >> u) & 1u) && (key1[u] >> kShift0) == bin;
+    for (int u = 0; u < NV; ++u) mine += ((vm >> u) & 1u) && (key1[u] >> sh0) == bin;
     uint32_t tot;
     const uint32_t incl = block_incl_scan(mine, sh + 4, tot);
     if (tid == 0) sh[9] = tot ? atomicAdd(&st->ncand, tot) : 0u;
@@ -272,17 +328,17 @@ __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict
     uint32_t pos = sh[9] + incl - mine;
     asm volatile("" : "+v"(vm));
 #pragma unroll
-    for (int u = 0; u < kRowU; ++u)
-      if (((vm >> u) & 1u) && (key1[u] >> kShift0) == bin) {
+    for (int u = 0; u < NV; ++u)
+      if (((vm >> u) & 1u) && (key1[u] >> sh0) == bin) {
         if (pos < (uint32_t)kSelCap)
-          cand[pos] = ((unsigned long long)(key1[u] & ((1u << kShift0) - 1u)) << idx_bits) |
+          cand[pos] = ((unsigned long long)(key1[u] & ((1u << sh0) - 1u)) << idx_bits) |
                       (unsigned long long)((uint32_t)c * (uint32_t)n + (uint32_t)(r0 + rs + 2 * u));
         ++pos;
       }
     return;
   }
   uint32_t mine = 0;
-  for_rows(Wc, ldw, r0, r1, rs, cv, [&](int, float w) { mine += (orderable(weight_score(w, fc)) >> kShift0) == bin; });
+  for_rows(Wc, ldw, r0, r1, rs, cv, [&](int, float w) { mine += (orderable(weight_score(w, fc)) >> sh0) == bin; });
   uint32_t tot;
   const uint32_t incl = block_incl_scan(mine, sh + 4, tot);
   if (tid == 0) sh[9] = tot ? atomicAdd(&st->ncand, tot) : 0u;
@@ -290,9 +346,9 @@ __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict
   uint32_t pos = sh[9] + incl - mine;
   for_rows(Wc, ldw, r0, r1, rs, cv, [&](int r, float w) {
     const uint32_t key = orderable(weight_score(w, fc));
-    if ((key >> kShift0) == bin) {
+    if ((key >> sh0) == bin) {
       if (pos < (uint32_t)kSelCap)
-        cand[pos] = ((unsigned long long)(key & ((1u << kShift0) - 1u)) << idx_bits) |
+        cand[pos] = ((unsigned long long)(key & ((1u << sh0) - 1u)) << idx_bits) |
                     (unsigned long long)((uint32_t)c * (uint32_t)n + (uint32_t)r);
       ++pos;
     }
@@ -309,10 +365,11 @@ __global__ __launch_bounds__(256) void sel_gather_kernel(const float* __restrict
 //    kSelCap is resolved by 8-bit passes straight over the block.
 constexpr int kDigitR = 11;
 constexpr int kRankMax = 256;
+template <int NU>
 __global__ __launch_bounds__(256) void sel_resolve_kernel(const float* __restrict__ W, int64_t ldw, int n, int Bb,
                                                           int j0, const float* __restrict__ fac, uint32_t z,
                                                           int idx_bits, uint32_t* hist, SelState* st,
-                                                          const unsigned long long* cand) {
+                                                          const unsigned long long* cand, int sh0) {
   extern __shared__ __attribute__((aligned(16))) uint32_t sel_sm[];
   uint32_t* sh = sel_sm;                                                   // [16]
   uint32_t* lh = sel_sm + 16;                                              // [1 << kDigitR]
@@ -320,16 +377,17 @@ __global__ __launch_bounds__(256) void sel_resolve_kernel(const float* __restric
   const int tid = threadIdx.x;
   if (tid == 0) sh[12] = 0;  // compaction counter
   __syncthreads();
-  // every one of the kSelCap candidate slots exists: they are loaded before
-  // the bucket is read, so both loads are in flight together
-  constexpr int NU = kSelCap / 256;
+  // NU candidates per thread (NU * 256 <= kSelCap slots, all of which exist):
+  // they are loaded before the bucket is read, so both loads are in flight
+  // together
+  static_assert(NU * 256 <= kSelCap, "candidate slots");
   unsigned long long v[NU];
 #pragma unroll
   for (int u = 0; u < NU; ++u) v[u] = cand[256 * u + tid];
   const uint32_t bin = st->bin, rank = st->rank, cnt = st->cnt;
-  const int tb = kShift0 + idx_bits;  // composite bits
+  const int tb = sh0 + idx_bits;  // composite bits
   unsigned long long pref = 0;
-  if (cnt <= (uint32_t)kSelCap) {
+  if (cnt <= (uint32_t)(NU * 256)) {
     // slots past cnt become all-ones, which matches no prefix (composites
     // are below 2^50)
 #pragma unroll
@@ -383,8 +441,8 @@ __global__ __launch_bounds__(256) void sel_resolve_kernel(const float* __restric
       const int hs = s + kDigit;
       for_rows(Wc, ldw, 0, n, rs, cv, [&](int r, float w) {
         const uint32_t key = orderable(weight_score(w, fc));
-        if ((key >> kShift0) == bin) {
-          const unsigned long long v = ((unsigned long long)(key & ((1u << kShift0) - 1u)) << idx_bits) |
+        if ((key >> sh0) == bin) {
+          const unsigned long long v = ((unsigned long long)(key & ((1u << sh0) - 1u)) << idx_bits) |
                                        (unsigned long long)((uint32_t)c * (uint32_t)n + (uint32_t)r);
           if ((v >> hs) == (pref >> hs)) atomicAdd(&lh[(uint32_t)(v >> s) & ((1u << kDigit) - 1u)], 1u);
         }
@@ -396,11 +454,15 @@ __global__ __launch_bounds__(256) void sel_resolve_kernel(const float* __restric
       rk = rk2;
     }
   }
-  for (int i = tid; i < kBins0; i += 256) hist[i] = 0;
+  // the histogram is empty outside [lo, hi]: clear that range for the next block
+  for (int i = (int)(kBins0 - 1 - st->nlo) + tid; i <= (int)st->hi; i += 256) hist[i] = 0;
+  __syncthreads();  // every thread has read the range before it is reset
   if (tid == 0) {
-    st->key = (bin << kShift0) | (uint32_t)(pref >> idx_bits);
+    st->key = (bin << sh0) | (uint32_t)(pref >> idx_bits);
     st->tie = (uint32_t)(pref & ((1ull << idx_bits) - 1ull));
     st->ncand = 0;
+    st->nlo = 0;
+    st->hi = 0;
   }
 }
 
@@ -835,8 +897,21 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   const IbOpts ibo{o.nm_n, o.q_bits, qt ? o.q_group : kMaxBlock, o.q_scale, o.q_zero};
   if (duo_status d = set_max_lds((const void*)ib_kern, ib_lds); d != DUO_OK) return d;
   const size_t sel_lds = (size_t)(16 + (1 << kDigitR)) * sizeof(uint32_t) + (size_t)kRankMax * sizeof(unsigned long long);
-  if (duo_status d = set_max_lds((const void*)sel_resolve_kernel, sel_lds); d != DUO_OK) return d;
+  for (const void* f : {(const void*)sel_resolve_kernel<kSelCap / 512>, (const void*)sel_resolve_kernel<kSelCap / 256>})
+    if (duo_status d = set_max_lds(f, sel_lds); d != DUO_OK) return d;
   const int P = (int)(cdiv(n, 32) < kSelWG ? cdiv(n, 32) : kSelWG);
+  // rows a selection thread holds in registers: one or two batches of kRowU
+  // (two threads per column, rpw rows per workgroup), else streamed
+  const int64_t rpw = cdiv(n, P);
+  const int hb = rpw <= 2 * kRowU ? 1 : (rpw <= 4 * kRowU ? 2 : 0);
+  const int sh0 = n * (int64_t)(k < B ? k : B) >= ((int64_t)1 << 20) ? kShift0 : kShift0 + 2;
+  // half the candidate registers for the 8192-bin histogram's smaller buckets
+  auto resolve_k = sh0 == kShift0 + 2 ? sel_resolve_kernel<kSelCap / 512> : sel_resolve_kernel<kSelCap / 256>;
+  auto hist_k = hb == 1 ? sel_hist_kernel<1> : (hb == 2 ? sel_hist_kernel<2> : sel_hist_kernel<0>);
+  auto gather_k = hb == 1 ? sel_gather_kernel<1> : (hb == 2 ? sel_gather_kernel<2> : sel_gather_kernel<0>);
+  const size_t hist_lds = (size_t)kBins0 * sizeof(uint32_t);
+  for (const void* f : {(const void*)sel_hist_kernel<0>, (const void*)sel_hist_kernel<1>, (const void*)sel_hist_kernel<2>})
+    if (duo_status d = set_max_lds(f, hist_lds); d != DUO_OK) return d;
   int64_t prev = 0;
   for (int64_t j0 = 0; j0 < k; j0 += B) {
     const int Bb = (int)(k - j0 < B ? k - j0 : B);
@@ -858,16 +933,17 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     while (idx_bits < 31 && ((int64_t)1 << idx_bits) < total) ++idx_bits;
     prof_begin(DUO_PROF_SELECT, s);
     if (mode == MODE_SELECT || (scores_out && mode != MODE_NM)) {
-      hipLaunchKernelGGL(sel_hist_kernel, dim3(P), dim3(256), 0, s, (const float*)W_out, k, (int)n, Bb, (int)j0, fac,
-                         w.hist, scores_out, mode == MODE_SELECT ? 1 : 0);
+      hipLaunchKernelGGL(scores_out ? sel_hist_kernel<0> : hist_k, dim3(P), dim3(256), hist_lds, s,
+                         (const float*)W_out, k, (int)n, Bb, (int)j0, fac, w.hist, scores_out,
+                         mode == MODE_SELECT ? 1 : 0, w.st, sh0);
       DUO_LAUNCH_CHECK();
     }
     if (mode == MODE_SELECT) {
-      hipLaunchKernelGGL(sel_gather_kernel, dim3(P), dim3(256), 0, s, (const float*)W_out, k, (int)n, Bb, (int)j0,
-                         fac, (uint32_t)z, idx_bits, (const uint32_t*)w.hist, w.st, w.cand);
+      hipLaunchKernelGGL(gather_k, dim3(P), dim3(256), 0, s, (const float*)W_out, k, (int)n, Bb, (int)j0, fac,
+                         (uint32_t)z, idx_bits, (const uint32_t*)w.hist, w.st, w.cand, sh0);
       DUO_LAUNCH_CHECK();
-      hipLaunchKernelGGL(sel_resolve_kernel, dim3(1), dim3(256), sel_lds, s, (const float*)W_out, k, (int)n, Bb,
-                         (int)j0, fac, (uint32_t)z, idx_bits, w.hist, w.st, (const unsigned long long*)w.cand);
+      hipLaunchKernelGGL(resolve_k, dim3(1), dim3(256), sel_lds, s, (const float*)W_out, k, (int)n, Bb,
+                         (int)j0, fac, (uint32_t)z, idx_bits, w.hist, w.st, (const unsigned long long*)w.cand, sh0);
       DUO_LAUNCH_CHECK();
     }
     prof_end(DUO_PROF_SELECT, s);
