@@ -421,10 +421,6 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
   const int T = (int)cdiv(k, kTile);
   hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, H, ldh, (int)k, damp, w.st);
   DUO_LAUNCH_CHECK();
-  // Blocks are factored from the last one.  The leading matrix receives the
-  // rank updates of two consecutive blocks b, b - 1 in one two-term product
-  // (K = 2 x 128): before block b - 1 is factored only its own block column
-  // gets block b's update (a 128-column strip).
   auto factor = [&](int b, int sz) -> duo_status {
     const int r0 = b * kTile;
     hipLaunchKernelGGL(diag_factor_kernel, dim3(1), dim3(256), kDiagLds, s, (const float*)H, ldh, r0, sz,
@@ -443,61 +439,54 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
     p.t[0] = GemmTerm{H + r0, ldh, 1, w.vinv + (int64_t)b * kTile * kTile, kTile, 0, sz, 1.f, KLO_ZERO, KHI_FULL};
     return gemm_f32(p, s);
   };
-  // the term -P_b P_b^T of block b's panel P_b = H[:, r0 : r0 + sz]
-  auto panel_term = [&](int b, int sz) {
-    const int r0 = b * kTile;
-    return GemmTerm{H + r0, ldh, 1, H + r0, ldh, 0, sz, -1.f, KLO_ZERO, KHI_FULL};
-  };
-  for (int b = T - 1; b >= 0;) {
-    const int sz = (int)((int64_t)b * kTile + kTile <= k ? kTile : k - (int64_t)b * kTile);
-    duo_status st = factor(b, sz);
-    if (st != DUO_OK) return st;
-    if (b == 0) break;
-    if (b >= 2) {
-      // strip: H[0:r0, r1:r0] -= P_b P_b[r1:r0]^T with r1 = (b - 1) * 128
-      const int r0 = b * kTile, r1 = r0 - kTile;
-      GemmDesc g{};
-      g.M = r0;
-      g.N = kTile;
-      g.C = H + r1;
-      g.ldc = ldh;
-      g.beta = 1.f;
-      g.tri = TRI_ALL;
-      g.nterms = 1;
-      g.t[0] = GemmTerm{H + r0, ldh, 1, H + (int64_t)r1 * ldh + r0, ldh, 0, sz, -1.f, KLO_ZERO, KHI_FULL};
-      st = gemm_f32(g, s);
+  // Groups of kGroup blocks, from the last one.  Inside a group, before block
+  // b is factored its own block column (rows 0 .. r_b + 128) takes the rank
+  // updates of the group's blocks already factored (one product: their
+  // panels are adjacent columns of H, so K = 128 per block); after the group,
+  // the leading matrix takes all of the group's updates in one product with
+  // K = 128 kGroup.  Every column still receives every update before its own
+  // block is factored; only the fp32 summation order changes.
+  constexpr int kGroup = 4;
+  for (int top = T - 1; top >= 0;) {
+    const int lo = top - kGroup + 1 > 0 ? top - kGroup + 1 : 0;
+    const int64_t top_end = (int64_t)top * kTile + kTile <= k ? (int64_t)top * kTile + kTile : k;
+    for (int b = top; b >= lo; --b) {
+      const int rb = b * kTile;
+      const int sz = (int)((int64_t)rb + kTile <= k ? kTile : k - rb);
+      if (b < top) {
+        // strip: H[0:rb+128, rb:rb+128] -= Pp Pp[rb:rb+128]^T, Pp = H[:, rb+128 : top_end]
+        const int rp = rb + kTile;
+        GemmDesc g{};
+        g.M = rp;
+        g.N = kTile;
+        g.C = H + rb;
+        g.ldc = ldh;
+        g.beta = 1.f;
+        g.tri = TRI_ALL;
+        g.nterms = 1;
+        g.t[0] = GemmTerm{H + rp, ldh, 1, H + (int64_t)rb * ldh + rp, ldh, 0, (int)(top_end - rp), -1.f, KLO_ZERO,
+                          KHI_FULL};
+        duo_status st = gemm_f32(g, s);
+        if (st != DUO_OK) return st;
+      }
+      duo_status st = factor(b, sz);
       if (st != DUO_OK) return st;
-      st = factor(b - 1, kTile);
-      if (st != DUO_OK) return st;
-      // leading block (upper tiles): H[0:r1, 0:r1] -= P_b P_b^T + P_{b-1} P_{b-1}^T
-      GemmDesc u{};
-      u.M = r1;
-      u.N = r1;
-      u.C = H;
-      u.ldc = ldh;
-      u.beta = 1.f;
-      u.tri = TRI_UPPER;
-      u.nterms = 2;
-      u.t[0] = panel_term(b, sz);
-      u.t[1] = panel_term(b - 1, kTile);
-      st = gemm_f32(u, s);
-      if (st != DUO_OK) return st;
-      b -= 2;
-    } else {
-      // b == 1: leading block H[0:128, 0:128] -= P_1 P_1^T
-      GemmDesc u{};
-      u.M = kTile;
-      u.N = kTile;
-      u.C = H;
-      u.ldc = ldh;
-      u.beta = 1.f;
-      u.tri = TRI_UPPER;
-      u.nterms = 1;
-      u.t[0] = panel_term(b, sz);
-      st = gemm_f32(u, s);
-      if (st != DUO_OK) return st;
-      b -= 1;
     }
+    if (lo == 0) break;
+    // leading block (upper tiles): H[0:r, 0:r] -= Pg Pg^T, Pg = H[0:r, r : top_end], r = lo * 128
+    const int r = lo * kTile;
+    GemmDesc u{};
+    u.M = r;
+    u.N = r;
+    u.C = H;
+    u.ldc = ldh;
+    u.beta = 1.f;
+    u.tri = TRI_UPPER;
+    u.nterms = 1;
+    u.t[0] = GemmTerm{H + r, ldh, 1, H + r, ldh, 0, (int)(top_end - r), -1.f, KLO_ZERO, KHI_FULL};
+    duo_status st = gemm_f32(u, s);
+    if (st != DUO_OK) return st;
+    top = lo - 1;
   }
   const int pvec = k % 4 == 0 && ldh % 4 == 0 && (reinterpret_cast<uintptr_t>(H) & 15) == 0;
   hipLaunchKernelGGL(place_diag_kernel, dim3(T, kTile / 16), dim3(256), 0, s, H, ldh, (int)k, (const float*)w.vinv,
