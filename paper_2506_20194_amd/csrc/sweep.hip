@@ -4,15 +4,17 @@
 // Per block of B columns [j0, j0+Bb):
 //   select   S = W[:, blk]^2 * fac[blk]; the z lowest by (S, column, row) are
 //            pruned.  Every element has the unique key (bits of S,
-//            column*n + row).  One launch histograms the top 13 key bits over
-//            the block; the next gathers the elements of the bucket that
+//            column*n + row).  One launch histograms the top 13 key bits
+//            (15 for blocks of 2^20 scores or more) over the block; the next
+//            gathers the elements of the bucket that
 //            holds the z-th key (normally a few thousand), and a third, one
 //            workgroup, finds the exact threshold among them (radix passes
 //            in registers down to at most 256, then direct ranking; a bucket
-//            larger than kSelCap is read from the block itself).  Counting
+//            too large for the registers is read from the block itself).  Counting
 //            uses integer atomics only, so the result is deterministic.
 //   in-block one row per 16 lanes (one DPP row), each lane owning the 8 columns
-//            c = lane%16 + 16i; L[blk, blk] and D[blk, blk] sit in LDS.  For
+//            c = lane%16 + 16i; L[blk, blk] and D[blk, blk] sit in LDS (an image
+//            laid out once per sweep and streamed in per block).  For
 //            column j the owner's current value w0 reaches the other 15 lanes
 //            by a DPP row broadcast; p = w0 * m_j, e = (w0 - p) / L_jj, and
 //            later columns get w -= e L[c][j] - w0 D[j][c].  The 128 steps are
