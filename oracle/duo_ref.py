@@ -156,13 +156,14 @@ def _token_keep(X, z: int):
     return ~(below | zero_tied)
 
 
-def hessian_entries(X_src, p_x: float, idx, X_dense=None, t0: int = 0, t1: int | None = None):
+def hessian_entries(X_src, p_x: float, idx, X_dense=None, t0: int = 0, t1: int | None = None, rows=None):
     """Selected entries of the stage-1 terms, summed over tokens t0..t1-1.
 
     Returns dict(H=H[idx][:, idx], G=G[idx][:, idx], a=a (all k), diag=diag(H)
     (all k)) with the same definitions as ``hessian_terms``, for layers whose
-    full k x k terms are too large to form in float64.  Tokens are taken in
-    chunks; results over disjoint token ranges add up.
+    full k x k terms are too large to form in float64; with ``rows`` also
+    G_rows = G[rows, :] (whole rows).  Tokens are taken in chunks; results over
+    disjoint token ranges add up.
     """
     idx = np.asarray(idx)
     m, k = X_src.shape
@@ -173,6 +174,7 @@ def hessian_entries(X_src, p_x: float, idx, X_dense=None, t0: int = 0, t1: int |
     G = np.zeros((s, s))
     a = np.zeros(k)
     diag = np.zeros(k)
+    G_rows = None if rows is None else np.zeros((len(rows), k))
     for c0 in range(t0, t1, 1024):
         c1 = min(t1, c0 + 1024)
         Xs = _f64(X_src[c0:c1])
@@ -183,7 +185,12 @@ def hessian_entries(X_src, p_x: float, idx, X_dense=None, t0: int = 0, t1: int |
         G += dX[:, idx].T @ Xh[:, idx]
         a += np.sum(dX * dX, axis=0)
         diag += np.sum(Xh * Xh, axis=0)
-    return dict(H=H, G=G, a=a, diag=diag)
+        if G_rows is not None:
+            G_rows += dX[:, rows].T @ Xh
+    out = dict(H=H, G=G, a=a, diag=diag)
+    if G_rows is not None:
+        out["G_rows"] = G_rows
+    return out
 
 
 # ---------------------------------------------------------------------------
@@ -524,18 +531,26 @@ def prune_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 1
 
 
 def objective(W, W_hat, X_src, p_x: float, X_dense=None):
-    """Layer objective |W X_dense - W_hat Xh|_F^2 (Sec. 4.2), undamped, f64."""
+    """Layer objective |W X_dense - W_hat Xh|_F^2 (Sec. 4.2), undamped, f64.
+
+    W_hat may be a list of candidate weights; the objective of each is then
+    returned as a list (the tokens are sparsified once).  The sum runs over
+    the given tokens, so objectives over disjoint token ranges add up."""
+    many = isinstance(W_hat, (list, tuple))
     W = _f64(W)
-    W_hat = _f64(W_hat)
-    X_src = _f64(X_src)
-    X_dense = X_src if X_dense is None else _f64(X_dense)
-    total = 0.0
-    for t0 in range(0, X_src.shape[0], _TOKEN_CHUNK):
-        t1 = min(X_src.shape[0], t0 + _TOKEN_CHUNK)
-        Xh, _ = sparsify_tokens(X_src[t0:t1], p_x)
-        R = X_dense[t0:t1] @ W.T - Xh @ W_hat.T
-        total += float(np.sum(R * R))
-    return total
+    W_hats = [_f64(w) for w in (W_hat if many else [W_hat])]
+    m = X_src.shape[0]
+    totals = [0.0] * len(W_hats)
+    for t0 in range(0, m, _TOKEN_CHUNK):
+        t1 = min(m, t0 + _TOKEN_CHUNK)
+        Xs = _f64(X_src[t0:t1])
+        Xd = Xs if X_dense is None else _f64(X_dense[t0:t1])
+        Xh, _ = sparsify_tokens(Xs, p_x)
+        Y = Xd @ W.T
+        for i, Wh in enumerate(W_hats):
+            R = Y - Xh @ Wh.T
+            totals[i] += float(np.sum(R * R))
+    return totals if many else totals[0]
 
 
 def sparsegpt_layer(W, X_src, p_x: float, p_w: float, damp: float = 0.01, B: int = 128):

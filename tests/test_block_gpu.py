@@ -130,34 +130,28 @@ def _tiny_run(duo, p_x, p_w):
     return c, W, out, ref
 
 
-def _group_checks(duo, c, W, out, ref, p_x, p_w, strict_first=True):
-    """Per linear: exact counts; the reference run on its own streams, forced
-    to the GPU mask, must show every disagreement to be a near-tie of its
-    scores and must match the GPU weights.  The first group's inputs are the
-    same on both sides: the layer solver's bars apply (gap 1e-5, W 1e-3).
-    Later groups' inputs differ by delta (relative Frobenius) from single-unit
-    bf16 differences upstream; without activation sparsity the scores, being
-    quadratic in the inputs, move by a small multiple of that: gap and weight
-    difference are allowed 20 * delta more.  With activation sparsity a
-    single-unit difference between two equal-magnitude entries at a token's
-    selection threshold swaps which one is kept, which moves that channel's
-    Hessian entries by a whole token's contribution; those groups are held to
-    a sensitivity bar instead (agreement >= 98 %, W within 5e-2 of the forced
-    run; the measured worst case is about 1e-2)."""
-    first = True
-    for names, (xs, xd) in ref["inputs"].items():
+def _group_checks(duo, c, W, out, ref, p_x, p_w):
+    """Per group, teacher-forced (reading c16): the oracle solves each group on
+    the GPU's own captured group inputs (sparse and dense stream), so the
+    layer solver's bars apply to every group: exact counts, mask agreement
+    >= 99.9 % with the oracle's free run, every disagreement a near-tie (the
+    oracle forced to the GPU mask finds the selection within a relative score
+    gap of 1e-5), W within 1e-3 of that forced run and the group objective
+    within 1e-3 of the oracle's.  The streams themselves are compared with
+    the oracle's own forward pass separately (_stream_checks)."""
+    for names in ref["inputs"]:
         gs, gd = (f64(t) for t in out["inputs"][names])
-        delta = max(relfro(gs, xs), relfro(gd, xd))
         for nm in names:
             n, k = W[nm].shape
             keep = duo.unpack_mask(out["mask"][nm], k).cpu().numpy()
             Wg = f64(out["W_out"][nm])
-            assert (~keep).sum() == sum(R.block_prune_counts(n, k, p_w, c["block"]))
-            agree = float(np.mean(keep == ref["keep"][nm]))
-            scores = []
-            forced = R.prune_layer(W[nm], xs, p_x, p_w, damp=c["damp"], B=c["block"], X_dense=xd, mask_in=keep,
-                                   scores_out=scores)
             counts = R.block_prune_counts(n, k, p_w, c["block"])
+            assert (~keep).sum() == sum(counts)
+            free = R.prune_layer(W[nm], gs, p_x, p_w, damp=c["damp"], B=c["block"], X_dense=gd)
+            agree = float(np.mean(keep == free["keep"]))
+            scores = []
+            forced = R.prune_layer(W[nm], gs, p_x, p_w, damp=c["damp"], B=c["block"], X_dense=gd, mask_in=keep,
+                                   scores_out=scores)
             gap = 0.0
             for bi, j0 in enumerate(range(0, k, c["block"])):
                 S = scores[bi]
@@ -167,16 +161,28 @@ def _group_checks(duo, c, W, out, ref, p_x, p_w, strict_first=True):
                 T = np.sort(S.T.reshape(-1), kind="stable")[counts[bi] - 1]
                 gap = max(gap, (S[~kb].max() - T) / T, (T - S[kb].min()) / T)
             err = relfro(Wg, forced["W_hat"])
-            say(f"{nm}: input delta {delta:.1e}, mask agreement {agree:.5f}, near-tie gap {gap:.1e}, "
-                f"W rel err (forced) {err:.1e}")
-            if first and strict_first:
-                assert delta == 0.0
-                assert agree >= 0.999 and gap < 1e-5 and err < 1e-3, nm
-            elif p_x == 0.0:
-                assert gap < 1e-5 + 20 * delta, nm
-                assert err < 1e-3 + 20 * delta, nm
-            else:
-                assert agree >= 0.98 and err < 5e-2, nm
+            J_gpu, J_ref = R.objective(W[nm], [Wg, free["W_hat"]], gs, p_x, X_dense=gd)
+            say(f"{nm}: mask agreement {agree:.5f}, near-tie gap {gap:.1e}, W rel err (forced) {err:.1e}, "
+                f"objective rel {abs(J_gpu - J_ref) / J_ref:.1e}")
+            assert agree >= 0.999 and gap < 1e-5 and err < 1e-3, nm
+            assert abs(J_gpu - J_ref) <= 1e-3 * J_ref, nm
+
+
+def _stream_checks(out, ref, p_x):
+    """The GPU's group inputs against the oracle's own forward pass of both
+    streams (each side rounds to bf16 at the same points, reading R16).  The
+    first group's inputs are identical; later groups inherit single-unit bf16
+    differences, which the per-token activation selection can turn into a
+    swapped entry at a token's threshold, so the streams are held to a
+    relative Frobenius bound (2^-6) rather than element bars."""
+    first = True
+    for names, (xs, xd) in ref["inputs"].items():
+        gs, gd = (f64(t) for t in out["inputs"][names])
+        ds, dd = relfro(gs, xs), relfro(gd, xd)
+        say(f"streams at {names}: sparse {ds:.1e}, dense {dd:.1e}")
+        if first:
+            assert ds == 0.0 and dd == 0.0
+        assert ds < 2.0 ** -6 and dd < 2.0 ** -6, names
         first = False
 
 
@@ -194,30 +200,30 @@ def test_tiny_block_without_sparsity(duo):
 
 
 def test_tiny_block_weight_sparsity(duo):
-    """p_x = 0, p_w = 0.5: the streams differ only through the pruned
-    weights; every disagreement is a near-tie within 20 delta and the weights
-    match the forced run within 1e-3 + 20 delta; overall agreement >= 99.8 %
-    (99.9 % for the first group, whose inputs are identical)."""
+    """p_x = 0, p_w = 0.5: every group, solved by the oracle on the GPU's own
+    group inputs, meets the layer bars (_group_checks), and the streams agree
+    with the oracle's forward pass (_stream_checks)."""
     say("tiny block, weight sparsity only")
     c, W, out, ref = _tiny_run(duo, 0.0, 0.5)
     _group_checks(duo, c, W, out, ref, 0.0, 0.5)
+    _stream_checks(out, ref, 0.0)
     for nm in synth.BLOCK_LINEARS:
         k = W[nm].shape[1]
         keep = duo.unpack_mask(out["mask"][nm], k).cpu().numpy()
-        # every disagreement was checked above to be a near-tie; this floor only
-        # guards against wholesale differences
-        assert np.mean(keep == ref["keep"][nm]) >= 0.998, nm
+        # against the oracle's whole-block run on its own streams (not
+        # teacher-forced), reported only: the later groups' inputs differ by
+        # the stream differences above, which move near-tied scores
+        say(f"{nm}: mask agreement with the oracle's own-stream run {np.mean(keep == ref['keep'][nm]):.5f}")
 
 
 def test_tiny_block_duogpt(duo):
-    """The block's own setting (p_x = p_w = 0.5).  The first group sees
-    identical inputs on both sides and must match exactly as a single layer
-    does; later groups inherit near-tie swaps of the per-token activation
-    selection (bf16 values one unit apart) and are held to the sensitivity
-    bar of _group_checks."""
+    """The block's own setting (p_x = p_w = 0.5): every group meets the layer
+    bars on the GPU's own group inputs (teacher-forced streams, reading c16),
+    and the streams agree with the oracle's forward pass."""
     say("tiny block, activation and weight sparsity")
     c, W, out, ref = _tiny_run(duo, c_px := synth.BLOCKS["tiny_block"]["p_x"], synth.BLOCKS["tiny_block"]["p_w"])
     _group_checks(duo, c, W, out, ref, c_px, c["p_w"])
+    _stream_checks(out, ref, c_px)
 
 
 def test_llama2_7b_block_full_size(duo):
@@ -272,3 +278,34 @@ def test_llama2_7b_block_full_size(duo):
         ok, e = close(g, r, ulps=u, atol_rel=1e-5 if nm == "x1" else 2.0 ** -8)
         say(f"dense stream {nm}: worst error / bound {e:.3f}")
         assert ok, (nm, e)
+    # the two-stream stage 1 at full size (Sec. 4.2 multi-layer case): each
+    # group's H, G and a recomputed by the library on the captured streams,
+    # against the oracle's sums over all 262144 tokens of the same streams on
+    # sampled channels.  Bars: 4e-5 sqrt(H_ii H_jj) as for one stream (fp32
+    # sums of exact products); G also carries the hi + lo representation of
+    # dX (at most 2^-17 relative per entry, so 2^-17 sqrt(a_i H_jj) more by
+    # Cauchy-Schwarz): 5e-5 sqrt(a_i H_jj).
+    from tests import oracle_par as P
+
+    del h
+    rng = np.random.default_rng(4)
+    for names, (xs, xd) in out["inputs"].items():
+        k = xs.shape[1]
+        idx = np.sort(rng.choice(k, 48, replace=False))
+        it = torch.tensor(idx, device=DEV)
+        H = torch.zeros((k, k), dtype=torch.float32, device=DEV)
+        G = torch.zeros((k, k), dtype=torch.float32, device=DEV)
+        a = torch.zeros(k, dtype=torch.float32, device=DEV)
+        duo.duo_hessian_accum(xs, H, c["p_x"], X_dense=xd, G=G, a=a)
+        Hs, Gs = H[it][:, it].double().cpu().numpy(), G[it][:, it].double().cpu().numpy()
+        ag, dg = a.double().cpu().numpy(), H.diagonal().double().cpu().numpy()
+        del H, G, a
+        ref = P.hessian_entries(xs.float().cpu().numpy(), c["p_x"], idx, X_dense=xd.float().cpu().numpy())
+        dH = np.sqrt(ref["diag"][idx])
+        eH = np.max(np.abs(Hs - ref["H"]) / (4e-5 * np.outer(dH, dH) + 1e-30))
+        eG = np.max(np.abs(Gs - ref["G"]) / (5e-5 * np.outer(np.sqrt(ref["a"][idx]), dH) + 1e-30))
+        ea = np.max(np.abs(ag - ref["a"]) / (4e-5 * ref["a"] + 1e-30))
+        ed = np.max(np.abs(dg - ref["diag"]) / (4e-5 * ref["diag"] + 1e-30))
+        say(f"two-stream stage 1 at {names}: worst error / bound H {eH:.3f} G {eG:.3f} a {ea:.3f} diag {ed:.3f}")
+        assert eH <= 1 and eG <= 1 and ea <= 1 and ed <= 1, names
+        torch.cuda.empty_cache()

@@ -78,6 +78,16 @@ def run(request, duo_lib):
     ws_p = duo.workspace(duo.DUO_OP_PRUNE_LAYER, n, k, 0, B, DEV)
     duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h)
     out = dict(name=name, c=c, idx=idx, nwin=WINDOW)
+    # columns for the defining property of L and rows for fac/D: column 0 and
+    # k - 1 plus three per 1024 columns (every group of eight blocks the UL
+    # factorisation updates together), and the first row of every such group
+    cols = [0, k - 1]
+    for g0 in range(0, k, 1024):
+        g1 = min(k, g0 + 1024)
+        cols += [g0, int(rng.integers(g0, g1)), g1 - 1]
+    out["pcols"] = np.unique(np.array(cols))
+    out["prows"] = np.unique(np.array([0, 1] + list(range(0, k, 1024)) + [int(rng.integers(0, 512))]))
+    out["H_full"] = H.cpu().numpy()             # the matrix the factorisation is given
     out["H_s"] = H[idx_t][:, idx_t].double().cpu().numpy()
     out["G_s"] = G[idx_t][:, idx_t].double().cpu().numpy()
     out["a"] = a.double().cpu().numpy()
@@ -122,11 +132,101 @@ def _stage1_oracle(run):
         X, p_x, idx = run["X"], run["c"]["p_x"], run["idx"]
         m = X.shape[0]
         step = 8192
+        rows = run["prows"]
         with ThreadPoolExecutor(8) as ex:
-            parts = list(ex.map(lambda t0: R.hessian_entries(X, p_x, idx, t0=t0, t1=min(m, t0 + step)),
+            parts = list(ex.map(lambda t0: R.hessian_entries(X, p_x, idx, t0=t0, t1=min(m, t0 + step), rows=rows),
                                 range(0, m, step)))
         run["ref1"] = {key: sum(p[key] for p in parts) for key in parts[0]}
     return run["ref1"]
+
+
+def test_fullsize_inverse_factor_property(run):
+    """Defining property of the damped inverse Cholesky factor (Sec. 4.3,
+    App. A.2): L^T (H + lambda I) L = I, evaluated in float64 on the sampled
+    columns j (every group of eight blocks, column 0 included) for the fp32
+    H the factorisation was given.  Bar on each column's residual norm:
+    16 sqrt(k) u (u = 2^-24): the random-walk size of the k rounding errors of
+    an fp32 inner-product chain, with a factor 16 for the chains of the
+    factorisation and of the triangular inverse and for margin.  LAPACK's fp32
+    factorisation along the same route (UL Cholesky of H + lambda I, then the
+    triangular inverse V^-1 = L^T) of the same matrix is evaluated beside it
+    and reported as the yardstick."""
+    import scipy.linalg as sl
+
+    say("full-size L property", run["name"])
+    Hf, LT, lam = run["H_full"], run["LT"], run["lam"]
+    k = Hf.shape[0]
+    J = run["pcols"]
+    Lj = LT[J].T.astype(np.float64)                        # k x |J|: columns j of L
+    M = np.empty((k, len(J)))
+    for r0 in range(0, k, 2048):
+        r1 = min(k, r0 + 2048)
+        M[r0:r1] = Hf[r0:r1].astype(np.float64) @ Lj + lam * Lj[r0:r1]
+    Rg = np.empty((k, len(J)))
+    for r0 in range(0, k, 2048):
+        r1 = min(k, r0 + 2048)
+        Rg[r0:r1] = LT[r0:r1].astype(np.float64) @ M
+    Rg[J, np.arange(len(J))] -= 1.0
+    res_gpu = np.linalg.norm(Rg, axis=0)
+    # float32 LAPACK along the same route: H + lambda I = V V^T (V upper, from
+    # the reversed lower Cholesky factor), L = V^-T by the triangular inverse
+    Hl = Hf.copy()
+    Hl[np.diag_indices(k)] += np.float32(lam)
+    C = np.linalg.cholesky(Hl[::-1, ::-1])                 # float32
+    del Hl
+    V = np.ascontiguousarray(C[::-1, ::-1])
+    del C
+    Vinv, info = sl.lapack.strtri(V, lower=0)               # = L_ref^T, float32
+    assert info == 0 and Vinv.dtype == np.float32
+    del V
+    Lr = Vinv[J].T.astype(np.float64)                       # columns j of L_ref
+    Mr = np.empty((k, len(J)))
+    for r0 in range(0, k, 2048):
+        r1 = min(k, r0 + 2048)
+        Mr[r0:r1] = Hf[r0:r1].astype(np.float64) @ Lr + lam * Lr[r0:r1]
+    Rr = np.empty((k, len(J)))
+    for r0 in range(0, k, 2048):
+        r1 = min(k, r0 + 2048)
+        Rr[r0:r1] = np.triu(Vinv[r0:r1], r0).astype(np.float64) @ Mr
+    del Vinv
+    Rr[J, np.arange(len(J))] -= 1.0
+    res_ref = np.linalg.norm(Rr, axis=0)
+    bar = 16.0 * np.sqrt(k) * 2.0 ** -24
+    worst = int(np.argmax(res_gpu))
+    say("L^T H L - I, worst column %d: GPU %.2e (LAPACK fp32 %.2e); median GPU %.2e, LAPACK %.2e; bar %.1e" %
+        (J[worst], res_gpu[worst], res_ref[worst], float(np.median(res_gpu)), float(np.median(res_ref)), bar))
+    assert np.all(res_gpu <= bar), (J[worst], res_gpu[worst], res_ref[worst])
+
+
+def test_fullsize_score_terms_leading_rows(run):
+    """fac_p and row p of D (Eq. 7, App. A.3-A.4) recomputed in float64 for
+    sampled leading rows p from the oracle's G row over all tokens, its a_p,
+    and the kernel's L: Q_p = G_p L, b_p = sum_{i>p} Q_pi^2, c_p = Q_pp / L_pp,
+    D_p = U_p L^T.  fac within 1e-4 relative per row, D rows within 1e-4
+    relative Frobenius (the window bars)."""
+    say("full-size leading score rows", run["name"])
+    ref = _stage1_oracle(run)
+    LT = run["LT"]
+    k = LT.shape[0]
+    for i, p in enumerate(run["prows"]):
+        g = ref["G_rows"][i]
+        Q = np.empty(k)
+        for r0 in range(0, k, 4096):
+            r1 = min(k, r0 + 4096)
+            Q[r0:r1] = LT[r0:r1].astype(np.float64) @ g          # Q_p,j = sum_l G_pl L_lj
+        Lpp = float(LT[p, p])
+        U = Q.copy()
+        U[:p + 1] = 0.0
+        fac = 1.0 / Lpp ** 2 + ref["a"][p] - float(U @ U) + 2.0 * Q[p] / Lpp
+        D = np.empty(k)
+        for r0 in range(0, k, 4096):
+            r1 = min(k, r0 + 4096)
+            D[r0:r1] = LT[:, r0:r1].T.astype(np.float64) @ U        # D_pj = sum_i U_pi L_ji
+        D[:p + 1] = 0.0
+        ef = abs(run["fac"][p] - fac) / abs(fac)
+        eD = relfro(np.where(np.arange(k) > p, run["D"][p], 0.0), D) if p < k - 1 else 0.0
+        say(f"row {p}: fac {ef:.2e}, D row {eD:.2e}")
+        assert ef < 1e-4 and eD < 1e-4, (p, ef, eD)
 
 
 def test_fullsize_activation_mask(run):

@@ -435,6 +435,27 @@ def test_hessian_entries_match_full_terms(m, k, p_x):
     lo = R.hessian_entries(X, p_x, idx, Xd, 0, m // 2)
     hi = R.hessian_entries(X, p_x, idx, Xd, m // 2, m)
     np.testing.assert_allclose(lo["H"] + hi["H"], e["H"], rtol=1e-12, atol=1e-12)
+    rows = idx[::2]
+    er = R.hessian_entries(X, p_x, idx, Xd, rows=rows)
+    np.testing.assert_allclose(er["G_rows"], G[rows], rtol=1e-12, atol=1e-12)
+
+
+def test_objective_candidates_and_token_ranges():
+    """The objective of several candidates at once equals the single calls,
+    and objectives over disjoint token ranges add up (Sec. 4.2: a sum over
+    tokens of squared output errors)."""
+    W, X = _layer(31, 6, 20, 300)
+    W1 = W * (np.arange(20) % 3 != 0)
+    W2 = 0.9 * W
+    J = R.objective(W, [W1, W2], X, 0.5)
+    assert J == [R.objective(W, W1, X, 0.5), R.objective(W, W2, X, 0.5)]
+    Jlo = R.objective(W, W1, X[:110], 0.5)
+    Jhi = R.objective(W, W1, X[110:], 0.5)
+    assert abs(Jlo + Jhi - J[0]) <= 1e-12 * J[0]
+    # the definition by hand on one token
+    Xh, _ = R.sparsify_tokens(X[:1], 0.5)
+    r = W @ X[0] - W1 @ Xh[0]
+    assert abs(R.objective(W, W1, X[:1], 0.5) - r @ r) <= 1e-12 * (r @ r)
 
 
 @pytest.mark.parametrize("t", [1, 5, 16])
@@ -714,3 +735,84 @@ def test_forced_values_hook_reproduces_the_run():
         cols = slice(16 * gi, 16 * gi + 16)
         want = sc[:, None] * (np.clip(np.round(w0[:, cols] / sc[:, None]) + z[:, None], 0, 15) - z[:, None])
         np.testing.assert_array_equal(np.where(keep[:, cols], want, 0.0), Wh[:, cols])
+
+
+# ---------------------------------------------------------------------------
+# Readings that decide discrete outcomes: the (S, column, row) tie order of the
+# block mask and round-half-to-even on the quantisation grid.  Both are pinned
+# on inputs where the floating-point values are exact, so the tie or the
+# halfway case really occurs.
+# ---------------------------------------------------------------------------
+
+def _disjoint_channels(k, reps, norms):
+    """Token-major X whose channels live on disjoint tokens: X^T X is exactly
+    diagonal (every off-diagonal sum is a sum of exact zeros), so the damped
+    inverse, its Cholesky factor and the update coefficients L[j', j] are
+    exactly diagonal and no column compensates another."""
+    X = np.zeros((k * reps, k))
+    for c in range(k):
+        X[c * reps:(c + 1) * reps, c] = norms[c] / np.sqrt(reps)
+    return X
+
+
+def test_block_tie_order_column_before_row():
+    """Caption of Alg. 1 / mask line: equal scores are pruned lowest column
+    first, then lowest row (reading R-mask).  With S[0, 1] == S[1, 0] and one
+    weight to prune, (row 1, column 0) goes; row-major order would prune
+    (row 0, column 1)."""
+    S = np.array([[5.0, 1.0], [1.0, 5.0]])
+    keep = R.select_block_mask(S, 1)
+    np.testing.assert_array_equal(keep, [[True, True], [False, True]])
+    # three-way tie spread over rows and columns: columns first, rows within
+    # (column 0, row 2) and (column 1, row 0) go; row-major order would take
+    # (row 0, column 1) and (row 1, column 1)
+    S = np.array([[9.0, 2.0, 9.0], [9.0, 2.0, 9.0], [2.0, 9.0, 9.0]])
+    np.testing.assert_array_equal(~R.select_block_mask(S, 2), [[False, True, False], [False, False, False],
+                                                                [True, False, False]])
+    # magnitude pruning orders |w| the same way
+    _, keep_m = R.magnitude_layer(np.array([[1.0, -0.5], [0.5, 1.0]]), 0.25, B=2)
+    np.testing.assert_array_equal(keep_m, [[True, True], [False, True]])
+
+
+def test_block_tie_order_inside_the_sweep():
+    """The same tie decided by the whole layer: channels with equal norms on
+    disjoint tokens give equal score factors, so |W[0, 1]| == |W[1, 0]| is an
+    exact tie in S; the sweep prunes (row 1, column 0)."""
+    X = _disjoint_channels(2, 4, [2.0, 2.0])
+    W = np.array([[1.0, 0.5], [0.5, 1.0]])
+    scores = []
+    out = R.prune_layer(W, X, 0.0, 0.25, damp=0.01, B=2, scores_out=scores)
+    assert scores[0][0, 1] == scores[0][1, 0]
+    np.testing.assert_array_equal(out["keep"], [[True, True], [False, True]])
+    np.testing.assert_array_equal(out["W_hat"], [[1.0, 0.5], [0.0, 1.0]])
+
+
+def test_quant_rounds_half_to_even():
+    """Kept weights take the nearest grid value, halfway cases to the even
+    integer code (Table 4's RTN; reading R20).  2 bits over [-1, 2]: step 1,
+    zero code 1.  x/s = 0.5 -> 0, 1.5 -> 2, -0.5 -> 0, 2.5 -> 2 (clamped code
+    3 either way), exactly on the grid otherwise."""
+    x = np.array([-1.0, 2.0, 0.5, 1.5, -0.5, 0.25])
+    s, z = R.quant_grid(x, 2)
+    assert (s, z) == (1.0, 1.0)
+    np.testing.assert_array_equal(R.quantize(x, s, z, 2), [-1.0, 2.0, 0.0, 2.0, 0.0, 0.0])
+    np.testing.assert_array_equal(R.quantize(np.array([2.5, -2.5, 4.5]), 1.0, 3.0, 3),
+                                  [2.0, -2.0, 4.0])
+
+
+def test_quant_half_to_even_inside_the_sweep():
+    """Same halfway cases decided by the sweep (the value a kept weight takes,
+    not the stand-alone grid helper): exactly diagonal H, no activation or
+    weight sparsity, so every column keeps RTN of its dense value."""
+    k = 8
+    X = _disjoint_channels(k, 2, np.arange(1.0, k + 1.0))
+    W = np.array([[-1.0, 2.0, 0.5, 1.5, -0.5, 0.25, 1.0, -0.75],
+                  [0.5, -1.5, 2.5, 3.5, -2.5, 0.0, 4.0, -3.0]])
+    out = R.prune_layer(W, X, 0.0, 0.0, damp=0.01, B=8, quant=(2, 8))
+    # row 0: grid [-1, 2], step 1, zero 1.  row 1: grid [-3, 4], step 7/3,
+    # zero 1 (rint(3 / (7/3)) = rint(1.2857)).
+    assert out["keep"].all()
+    np.testing.assert_array_equal(out["W_hat"][0], [-1.0, 2.0, 0.0, 2.0, 0.0, 0.0, 1.0, -1.0])
+    s1 = 7.0 / 3.0
+    want1 = s1 * (np.clip(np.round(W[1] / s1) + 1.0, 0, 3) - 1.0)
+    np.testing.assert_array_equal(out["W_hat"][1], want1)
