@@ -350,6 +350,25 @@ duo_status duo_dsc_gemv(const void* x, int32_t x_dtype, int64_t n, int64_t k, du
                         const uint16_t* values, float* y, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * duo_dsc_gemv_noalloc - duo_dsc_gemv for callers that cannot allocate device
+ *   memory or pass a workspace (code under HIP graph capture, tight serving
+ *   loops, harnesses that forbid allocation).  Same arguments, kernels and
+ *   results as duo_dsc_gemv, bit for bit, without ws / ws_bytes: the partial
+ *   rows live in a 2 MiB array inside the library, one per GPU, held until
+ *   the process ends; its device address is looked up on the first call on a
+ *   device (with that device current).  The call allocates nothing and calls
+ *   no allocating routine.  Limits: n <= 32768 and k <= 32768
+ *   (DUO_ERR_UNSUPPORTED beyond; the partial rows never exceed 256 x 2048
+ *   floats inside those limits).  Every call on a GPU uses that GPU's one
+ *   array: calls that overlap on one GPU (other streams, other threads) race
+ *   and give undefined results; calls ordered on one stream are safe.  The
+ *   array needs no clearing: each call writes every partial it reads.
+ */
+duo_status duo_dsc_gemv_noalloc(const void* x, int32_t x_dtype, int64_t n, int64_t k, duo_act_rule rule,
+                                const int64_t* col_ptr, const uint32_t* maskT, const uint16_t* chunk_off,
+                                const uint16_t* values, float* y, void* stream);
+
+/*
  * Decoder-block harness.  When a whole decoder block is pruned group by group,
  * each group's solver input comes from two streams (the multi-layer case of
  * Sec. 4.2): the dense model's activations (X-tilde, dense weights, no

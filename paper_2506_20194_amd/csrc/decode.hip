@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <mutex>
 
 #include "internal.h"
 
@@ -548,6 +549,72 @@ size_t dsc_ws_bytes(int64_t n, int64_t k) {
   return g > l ? g : l;
 }
 
+duo_status gemv_check(const void* x, int32_t x_dtype, int64_t n, int64_t k, duo_act_rule rule,
+                      const int64_t* col_ptr, const uint32_t* maskT, const uint16_t* chunk_off,
+                      const uint16_t* values, float* y) {
+  if (!x || !col_ptr || !maskT || !chunk_off || !values || !y || n < 1 || k < 1) return DUO_ERR_INVALID_ARG;
+  if (x_dtype != DUO_F32 && x_dtype != DUO_BF16) return DUO_ERR_INVALID_ARG;
+  if (rule.kind != DUO_ACT_NONE &&
+      !(rule.kind == DUO_ACT_TOPK_MAG_PER_TOKEN && rule.sparsity >= 0.0 && rule.sparsity <= 1.0))
+    return DUO_ERR_INVALID_ARG;
+  if (n > kMaxDecodeN || k > kMaxK) return DUO_ERR_UNSUPPORTED;
+  if (((uintptr_t)values & 15) != 0) return DUO_ERR_INVALID_ARG;
+  return DUO_OK;
+}
+
+// The GEMV kernel writes every (share, row) entry of the partial rows before
+// the reduction reads them, so the partial buffer needs no clearing.
+duo_status gemv_launch(const void* x, int32_t x_dtype, int64_t n, int64_t k, duo_act_rule rule,
+                       const int64_t* col_ptr, const uint32_t* maskT, const uint16_t* chunk_off,
+                       const uint16_t* values, float* y, float* ypart, hipStream_t s) {
+  const int z = rule.kind == DUO_ACT_NONE ? 0 : (int)floor(rule.sparsity * (double)k + 0.5);
+  const GemvPlan p = gemv_plan(n, (int)(k - z));  // the rule keeps exactly k - z channels
+  const void* kern = x_dtype == DUO_BF16 ? (const void*)dsc_gemv_kernel<uint16_t> : (const void*)dsc_gemv_kernel<float>;
+  if (duo_status d = set_max_lds(kern, p.lds); d != DUO_OK) return d;
+  prof_begin(DUO_PROF_DECODE, s);
+  if (x_dtype == DUO_BF16)
+    hipLaunchKernelGGL(dsc_gemv_kernel<uint16_t>, dim3((unsigned)(p.ns * p.S)), dim3(kGemvThreads), p.lds, s,
+                       (const uint16_t*)x, (int)k, z, n, col_ptr, maskT, chunk_off, values, p.S, p.cap, ypart);
+  else
+    hipLaunchKernelGGL(dsc_gemv_kernel<float>, dim3((unsigned)(p.ns * p.S)), dim3(kGemvThreads), p.lds, s,
+                       (const float*)x, (int)k, z, n, col_ptr, maskT, chunk_off, values, p.S, p.cap, ypart);
+  DUO_LAUNCH_CHECK();
+  prof_end(DUO_PROF_DECODE, s);
+  hipLaunchKernelGGL(dsc_reduce_kernel, dim3((unsigned)cdiv(n, 64)), dim3(1024), 0, s, (const float*)ypart, n, p.S, y);
+  DUO_LAUNCH_CHECK();
+  return DUO_OK;
+}
+
+// Partial rows of the allocation-free GEMV: at most kTargetGroups shares of
+// kSlabRows rows each (gemv_plan gives S * n <= 256 * 2048 for every n),
+// 2 MiB per device, held until the process ends.  Host code never passes the
+// array's name to a kernel: the device address comes from
+// hipGetSymbolAddress, once per device with that device current.
+constexpr size_t kScratchFloats = (size_t)kTargetGroups * kSlabRows;
+
+}  // namespace
+
+static __device__ __align__(256) float scratch[kScratchFloats];
+
+namespace {
+
+std::mutex g_scratch_mu;
+float* g_scratch_dev[64];  // per device index; set once, then only read
+
+duo_status scratch_address(float** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return DUO_ERR_HIP;
+  if (dev < 0 || dev >= 64) return DUO_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return DUO_ERR_HIP;
+    g_scratch_dev[dev] = (float*)ptr;
+  }
+  *out = g_scratch_dev[dev];
+  return DUO_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -591,33 +658,23 @@ duo_status duo_dsc_pack(const void* W, int32_t w_dtype, int64_t n, int64_t k, in
 duo_status duo_dsc_gemv(const void* x, int32_t x_dtype, int64_t n, int64_t k, duo_act_rule rule,
                         const int64_t* col_ptr, const uint32_t* maskT, const uint16_t* chunk_off,
                         const uint16_t* values, float* y, void* ws, size_t ws_bytes, void* stream) {
-  if (!x || !col_ptr || !maskT || !chunk_off || !values || !y || n < 1 || k < 1) return DUO_ERR_INVALID_ARG;
-  if (x_dtype != DUO_F32 && x_dtype != DUO_BF16) return DUO_ERR_INVALID_ARG;
-  if (rule.kind != DUO_ACT_NONE &&
-      !(rule.kind == DUO_ACT_TOPK_MAG_PER_TOKEN && rule.sparsity >= 0.0 && rule.sparsity <= 1.0))
-    return DUO_ERR_INVALID_ARG;
-  if (n > kMaxDecodeN || k > kMaxK) return DUO_ERR_UNSUPPORTED;
+  if (duo_status d = gemv_check(x, x_dtype, n, k, rule, col_ptr, maskT, chunk_off, values, y); d != DUO_OK) return d;
   if (!ws || ws_bytes < dsc_ws_bytes(n, k) || ((uintptr_t)ws & (kAlign - 1))) return DUO_ERR_WORKSPACE;
-  if (((uintptr_t)values & 15) != 0) return DUO_ERR_INVALID_ARG;
   if (duo_status d = device_ok(); d != DUO_OK) return d;
-  const hipStream_t s = (hipStream_t)stream;
+  return gemv_launch(x, x_dtype, n, k, rule, col_ptr, maskT, chunk_off, values, y, (float*)ws, (hipStream_t)stream);
+}
+
+duo_status duo_dsc_gemv_noalloc(const void* x, int32_t x_dtype, int64_t n, int64_t k, duo_act_rule rule,
+                                const int64_t* col_ptr, const uint32_t* maskT, const uint16_t* chunk_off,
+                                const uint16_t* values, float* y, void* stream) {
+  if (duo_status d = gemv_check(x, x_dtype, n, k, rule, col_ptr, maskT, chunk_off, values, y); d != DUO_OK) return d;
+  if (duo_status d = device_ok(); d != DUO_OK) return d;
   const int z = rule.kind == DUO_ACT_NONE ? 0 : (int)floor(rule.sparsity * (double)k + 0.5);
-  const GemvPlan p = gemv_plan(n, (int)(k - z));  // the rule keeps exactly k - z channels
-  float* ypart = (float*)ws;
-  const void* kern = x_dtype == DUO_BF16 ? (const void*)dsc_gemv_kernel<uint16_t> : (const void*)dsc_gemv_kernel<float>;
-  if (duo_status d = set_max_lds(kern, p.lds); d != DUO_OK) return d;
-  prof_begin(DUO_PROF_DECODE, s);
-  if (x_dtype == DUO_BF16)
-    hipLaunchKernelGGL(dsc_gemv_kernel<uint16_t>, dim3((unsigned)(p.ns * p.S)), dim3(kGemvThreads), p.lds, s,
-                       (const uint16_t*)x, (int)k, z, n, col_ptr, maskT, chunk_off, values, p.S, p.cap, ypart);
-  else
-    hipLaunchKernelGGL(dsc_gemv_kernel<float>, dim3((unsigned)(p.ns * p.S)), dim3(kGemvThreads), p.lds, s,
-                       (const float*)x, (int)k, z, n, col_ptr, maskT, chunk_off, values, p.S, p.cap, ypart);
-  DUO_LAUNCH_CHECK();
-  prof_end(DUO_PROF_DECODE, s);
-  hipLaunchKernelGGL(dsc_reduce_kernel, dim3((unsigned)cdiv(n, 64)), dim3(1024), 0, s, (const float*)ypart, n, p.S, y);
-  DUO_LAUNCH_CHECK();
-  return DUO_OK;
+  const GemvPlan p = gemv_plan(n, (int)(k - z));
+  if ((size_t)p.S * (size_t)n > kScratchFloats) return DUO_ERR_UNSUPPORTED;
+  float* part = nullptr;
+  if (duo_status d = scratch_address(&part); d != DUO_OK) return d;
+  return gemv_launch(x, x_dtype, n, k, rule, col_ptr, maskT, chunk_off, values, y, part, (hipStream_t)stream);
 }
 
 }  // extern "C"

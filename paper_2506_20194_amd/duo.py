@@ -29,7 +29,7 @@ EXPORTED = (
     "duo_prune_layer", "duo_profile_enable", "duo_profile_read", "duo_block_workspace_size", "duo_rmsnorm",
     "duo_act_sparsify", "duo_linear", "duo_rope", "duo_attention", "duo_silu_mul", "duo_act_order",
     "duo_permute", "duo_permute_mask", "duo_dsc_workspace_size", "duo_dsc_layout", "duo_dsc_pack",
-    "duo_dsc_gemv",
+    "duo_dsc_gemv", "duo_dsc_gemv_noalloc",
 )
 PROF = dict(gram=0, hessian=1, chol=2, score=3, sweep=4, inblock=5, trail=6, select=7, decode=8)
 DUO_BOP_ACT_SPARSIFY, DUO_BOP_LINEAR, DUO_BOP_ATTENTION = 0, 1, 2
@@ -119,6 +119,8 @@ def lib():
         L.duo_dsc_pack.argtypes = [P, I32, I64, I64, I64, P, P, P, P, P]
         L.duo_dsc_gemv.restype = I32
         L.duo_dsc_gemv.argtypes = [P, I32, I64, I64, ActRule, P, P, P, P, P, P, SZ, P]
+        L.duo_dsc_gemv_noalloc.restype = I32
+        L.duo_dsc_gemv_noalloc.argtypes = [P, I32, I64, I64, ActRule, P, P, P, P, P, P]
         L.duo_profile_enable.restype = I32
         L.duo_profile_enable.argtypes = [I32]
         L.duo_profile_read.restype = I32
@@ -555,6 +557,24 @@ def dsc_gemv(comp, x, act_sparsity, ws=None, out=None):
                             _ptr(comp["maskT"]), _ptr(comp["chunk_off"]), _ptr(comp["values"]), _ptr(y), _ptr(ws),
                             ws.numel(), _stream(dev))
     _check(st, "duo_dsc_gemv")
+    return y
+
+
+def dsc_gemv_noalloc(comp, x, act_sparsity, out=None):
+    """dsc_gemv through the allocation-free entry point: no workspace; the
+    library's per-GPU partial rows are used (calls on one GPU must not
+    overlap).  `out` (n,) fp32 is written in place when given."""
+    n, k = comp["n"], comp["k"]
+    if x.dim() != 1 or x.shape[0] != k:
+        raise ValueError(f"x must have shape ({k},)")
+    _contig(x, "x")
+    dev = x.device
+    y = out if out is not None else torch.empty(n, dtype=torch.float32, device=dev)
+    _same_device(x, y, comp["values"])
+    st = lib().duo_dsc_gemv_noalloc(_ptr(x), _dtype(x), n, k, act_rule(act_sparsity), _ptr(comp["col_ptr"]),
+                                    _ptr(comp["maskT"]), _ptr(comp["chunk_off"]), _ptr(comp["values"]), _ptr(y),
+                                    _stream(dev))
+    _check(st, "duo_dsc_gemv_noalloc")
     return y
 
 
