@@ -120,7 +120,10 @@ duo_status duo_act_sparsify_mask(const void* X, int32_t x_dtype, int64_t m, int6
  * duo_hessian_accum - stage 1 (Algorithm 1, H <- Xh Xh^T; Sec. 4.3 a-term).
  *   X_src    m x k, ldx, x_dtype: the input to sparsify (Xh = sparsify(X_src)).
  *   X_dense  m x k, ldx, x_dtype, or NULL (= X_src): the dense stream.
- *   H        k x k fp32, ldh: H += Xh^T Xh over the m tokens (both triangles).
+ *   H        k x k fp32, ldh: H += Xh^T Xh over the m tokens; the sums are
+ *            added to the upper triangle (diagonal included), and the lower
+ *            triangle is then set to its mirror image, so H is returned
+ *            exactly symmetric.
  *   G, a     optional (both NULL or both set): G += dX^T Xh with dX = X_dense - Xh,
  *            a[p] += sum_t dX[t][p]^2.  G is k x k fp32 with row stride ldg.
  *   hdiag    NULL or k doubles: hdiag[p] += sum_t Xh[t][p]^2 summed in fp64
@@ -137,6 +140,19 @@ duo_status duo_hessian_accum(const void* X_src, const void* X_dense, int32_t x_d
                              int64_t k, int64_t ldx, duo_act_rule rule, float* H, int64_t ldh,
                              float* G, int64_t ldg, float* a, double* hdiag, void* ws,
                              size_t ws_bytes, void* stream);
+
+/*
+ * duo_hessian_status - non-finite input check of stage 1 (the calibration
+ *   input must be finite for the sums of Sec. 4.2-4.3 to mean anything).
+ *   Every duo_hessian_accum, duo_residual_term and duo_act_sparsify_mask call
+ *   records in its workspace whether any entry of X_src or X_dense was NaN or
+ *   +-inf (such entries are still selected by their magnitude bits, NaN above
+ *   inf above every finite value, so H and G then hold non-finite sums).
+ *   This call waits for `stream` and returns DUO_ERR_NONFINITE if the last
+ *   such call on workspace `ws` met one, else DUO_OK; ws and ws_bytes are the
+ *   workspace that call used (ws_bytes >= 256).
+ */
+duo_status duo_hessian_status(const void* ws, size_t ws_bytes, void* stream);
 
 /*
  * duo_residual_term - stage 1, residual part only (Sec. 4.3: G = dX Xh^T,

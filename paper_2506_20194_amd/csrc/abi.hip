@@ -194,6 +194,13 @@ duo_status duo_residual_term(const void* X_dense, const void* X_src, int32_t x_d
                         false);
 }
 
+duo_status duo_hessian_status(const void* ws, size_t ws_bytes, void* stream) {
+  if (!ws || ws_bytes < 256 || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0) return DUO_ERR_INVALID_ARG;
+  duo_status d = device_ok();
+  if (d != DUO_OK) return d;
+  return hessian_status_run(ws, (hipStream_t)stream);
+}
+
 duo_status duo_chol_inv(float* H_inout, int64_t k, int64_t ldh, double damp_ratio, duo_chol_info* info, void* ws,
                         size_t ws_bytes, void* stream) {
   if (!H_inout || ldh < k || !std::isfinite(damp_ratio) || damp_ratio < 0.0) return DUO_ERR_INVALID_ARG;

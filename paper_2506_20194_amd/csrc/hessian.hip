@@ -27,6 +27,7 @@ struct Elem;
 template <>
 struct Elem<uint16_t> {  // bf16 stored as raw bits
   static constexpr int kMagBits = 15;
+  static constexpr uint32_t kInfMag = 0x7f80u;  // magnitudes >= this are inf or NaN
   __device__ static inline uint32_t mag(uint16_t v) { return v & 0x7fffu; }
   __device__ static inline float to_f32(uint16_t v) { return bf16_bits_to_f32(v); }
   __device__ static inline uint16_t from_f32(float f) { return f32_to_bf16_bits(f); }
@@ -34,6 +35,7 @@ struct Elem<uint16_t> {  // bf16 stored as raw bits
 template <>
 struct Elem<float> {
   static constexpr int kMagBits = 31;
+  static constexpr uint32_t kInfMag = 0x7f800000u;
   __device__ static inline uint32_t mag(float v) { return __float_as_uint(v) & 0x7fffffffu; }
   __device__ static inline float to_f32(float v) { return v; }
   __device__ static inline float from_f32(float f) { return f; }
@@ -62,24 +64,35 @@ __device__ inline int block_sum256(int v, int* red, int slot) {
 // (mag(x) << 32 | c) > thr[t] (signed compare).  thr = -1 keeps everything,
 // INT64_MAX drops everything.
 // ---------------------------------------------------------------------------
+// Non-finite inputs (NaN or +-inf: the magnitude's exponent field all ones)
+// are reported by setting *nf (when not null) to 1; they still take part in
+// the selection with their magnitude bits (NaN above inf above any finite
+// value), so the kept set stays a function of the bit patterns.
+__device__ inline void flag_nonfinite(bool bad, uint32_t* nf) {
+  if (nf && __ballot(bad) != 0 && (threadIdx.x & 63) == 0) atomicOr(nf, 1u);
+}
+
 template <typename T, int C>
 __global__ __launch_bounds__(256) void act_select_kernel(const T* __restrict__ X, int64_t ldx, int m,
-                                                         int k, int z, int64_t* __restrict__ thr) {
+                                                         int k, int z, int64_t* __restrict__ thr,
+                                                         uint32_t* __restrict__ nf) {
   __shared__ int red[8];
   __shared__ int scan[4];
   const int t = blockIdx.x;
   if (t >= m) return;
+  const T* row = X + (int64_t)t * ldx;
+  uint32_t mag[C];
+  bool bad = false;
+#pragma unroll
+  for (int e = 0; e < C; ++e) {
+    const int c = threadIdx.x + 256 * e;  // coalesced: consecutive threads, consecutive channels
+    mag[e] = c < k ? Elem<T>::mag(row[c]) : 0xffffffffu;
+    bad |= c < k && mag[e] >= Elem<T>::kInfMag;
+  }
+  flag_nonfinite(bad, nf);
   if (z <= 0 || z >= k) {
     if (threadIdx.x == 0) thr[t] = z <= 0 ? (int64_t)-1 : INT64_MAX;
     return;
-  }
-  const T* row = X + (int64_t)t * ldx;
-  const int c0 = threadIdx.x * C;
-  uint32_t mag[C];
-#pragma unroll
-  for (int e = 0; e < C; ++e) {
-    const int c = c0 + e;
-    mag[e] = c < k ? Elem<T>::mag(row[c]) : 0xffffffffu;
   }
   // smallest v with count(mag <= v) >= z
   uint32_t lo = 0, hi = (1u << Elem<T>::kMagBits) - 1u;
@@ -97,35 +110,38 @@ __global__ __launch_bounds__(256) void act_select_kernel(const T* __restrict__ X
       lo = mid + 1;
   }
   const uint32_t v = lo;
-  int lt = 0, eq = 0;
+  int lt = 0;
+#pragma unroll
+  for (int e = 0; e < C; ++e) lt += mag[e] < v;
+  lt = block_sum256(lt, red, slot);
+  slot ^= 1;
+  int need = z - lt;  // 1 <= need <= (number of ties)
+  // the need-th tie in channel order, i.e. in (e, thread) order
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
 #pragma unroll
   for (int e = 0; e < C; ++e) {
-    lt += mag[e] < v;
-    eq += mag[e] == v;
-  }
-  lt = block_sum256(lt, red, slot);
-  const int r = z - lt;  // 1 <= r <= (number of ties)
-  // exclusive prefix of tie counts in channel order
-  int incl = eq;
-  const int lane = threadIdx.x & 63;
+    const int eq = mag[e] == v;
+    int incl = eq;
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(incl, o);
-    if (lane >= o) incl += y;
-  }
-  if (lane == 63) scan[threadIdx.x >> 6] = incl;
-  __syncthreads();
-  int base = 0;
-  for (int w = 0; w < (int)(threadIdx.x >> 6); ++w) base += scan[w];
-  const int excl = base + incl - eq;
-  if (eq > 0 && excl < r && r <= excl + eq) {
-    int need = r - excl;
-#pragma unroll
-    for (int e = 0; e < C; ++e) {
-      if (mag[e] == v) {
-        if (--need == 0) thr[t] = ((int64_t)v << 32) | (int64_t)(c0 + e);
-      }
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
     }
+    if (lane == 63) red[slot * 4 + wv] = incl;
+    __syncthreads();
+    int base = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int q = red[slot * 4 + w];
+      base += w < wv ? q : 0;
+      tot += q;
+    }
+    slot ^= 1;
+    if (need <= tot) {  // uniform
+      if (eq && base + incl == need) thr[t] = ((int64_t)v << 32) | (int64_t)(threadIdx.x + 256 * e);
+      return;
+    }
+    need -= tot;
   }
 }
 
@@ -153,23 +169,29 @@ __device__ inline int wave_incl_scan(int v) {
 
 template <int V>
 __global__ __launch_bounds__(256) void act_select_wave_kernel(const uint16_t* __restrict__ X, int64_t ldx, int m,
-                                                              int k, int z, int64_t* __restrict__ thr) {
+                                                              int k, int z, int64_t* __restrict__ thr,
+                                                              uint32_t* __restrict__ nf) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (t >= m) return;  // uniform per wave
-  if (z <= 0 || z >= k) {
-    if (lane == 0) thr[t] = z <= 0 ? (int64_t)-1 : INT64_MAX;
-    return;
-  }
   const uint16_t* row = X + (int64_t)t * ldx;
   uint32_t mag[8 * V];
+  bool bad = false;
 #pragma unroll
   for (int u = 0; u < V; ++u) {
     const int c = 512 * u + 8 * lane;
     const bool ok = c < k;
     const u32x4 w = *(const u32x4*)(row + (ok ? c : 0));
 #pragma unroll
-    for (int j = 0; j < 8; ++j) mag[8 * u + j] = ok ? (w[j >> 1] >> (16 * (j & 1))) & 0x7fffu : 0xffffffffu;
+    for (int j = 0; j < 8; ++j) {
+      mag[8 * u + j] = ok ? (w[j >> 1] >> (16 * (j & 1))) & 0x7fffu : 0xffffffffu;
+      bad |= ok && mag[8 * u + j] >= 0x7f80u;
+    }
+  }
+  flag_nonfinite(bad, nf);
+  if (z <= 0 || z >= k) {
+    if (lane == 0) thr[t] = z <= 0 ? (int64_t)-1 : INT64_MAX;
+    return;
   }
   // v = the smallest magnitude with count(mag <= v) >= z, from two LDS
   // histograms of the wave's own: the top 10 of the 15 magnitude bits (lane l
@@ -246,6 +268,146 @@ __global__ __launch_bounds__(256) void act_select_wave_kernel(const uint16_t* __
   }
 }
 
+// One 256-thread workgroup per token (bf16, 16-byte aligned rows, k % 8 == 0,
+// 8192 < k <= 2048 V): thread i holds channels 2048u + 8i + j (u < V, j < 8)
+// in registers, loaded as 16-byte vectors (coalesced); the two histograms of
+// the wave kernel (top 10 magnitude bits, then the low 5 of the z-th entry's
+// bin) are shared by the workgroup, and ties are resolved in channel order
+// (u, thread, j) with one block scan per u until the need-th tie is reached.
+template <int V>
+__global__ __launch_bounds__(256) void act_select_block_kernel(const uint16_t* __restrict__ X, int64_t ldx, int m,
+                                                               int k, int z, int64_t* __restrict__ thr,
+                                                               uint32_t* __restrict__ nf) {
+  constexpr int kFineBits = 5, kCoarse = 1 << (15 - kFineBits), kFine = 1 << kFineBits;
+  __shared__ __attribute__((aligned(16))) uint32_t hc[kCoarse];
+  __shared__ uint32_t hf[kFine];
+  __shared__ int wsum[2][4];
+  __shared__ int found[2];
+  __shared__ int tie_w[4][V];
+  const int t = blockIdx.x;
+  if (t >= m) return;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const uint16_t* row = X + (int64_t)t * ldx;
+  // the raw bf16 pairs (two channels per register: 8 V values in 4 V
+  // registers, so the largest form still fits without spilling); vector u is
+  // valid when 2048 u + 8 tid < k (k % 8 == 0)
+  uint32_t w[4 * V];
+  bool bad = false;
+#pragma unroll
+  for (int u = 0; u < V; ++u) {
+    const bool ok = 2048 * u + 8 * tid < k;
+    const u32x4 x4 = *(const u32x4*)(row + (ok ? 2048 * u + 8 * tid : 0));
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      w[4 * u + h] = x4[h];
+      bad |= ok && (x4[h] & 0x7f80u) == 0x7f80u;
+      bad |= ok && (x4[h] & 0x7f800000u) == 0x7f800000u;
+    }
+  }
+  flag_nonfinite(bad, nf);
+  if (z <= 0 || z >= k) {
+    if (tid == 0) thr[t] = z <= 0 ? (int64_t)-1 : INT64_MAX;
+    return;
+  }
+#define DUO_MAG(u, j) ((w[4 * (u) + ((j) >> 1)] >> (16 * ((j) & 1))) & 0x7fffu)
+  ((u32x4*)hc)[tid] = u32x4{0u, 0u, 0u, 0u};  // 256 x 4 = kCoarse bins
+  if (tid < kFine) hf[tid] = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < V; ++u)
+    if (2048 * u + 8 * tid < k)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) atomicAdd(&hc[DUO_MAG(u, j) >> kFineBits], 1u);
+  __syncthreads();
+  // thread i owns coarse bins 4i .. 4i + 3: block exclusive scan of their sums
+  const u32x4 q = ((const u32x4*)hc)[tid];
+  const int loc = (int)(q[0] + q[1] + q[2] + q[3]);
+  int incl = wave_incl_scan(loc);
+  if (lane == 63) wsum[0][wv] = incl;
+  __syncthreads();
+  int run = incl - loc;
+#pragma unroll
+  for (int ww = 0; ww < 4; ++ww) run += ww < wv ? wsum[0][ww] : 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (run < z && z <= run + (int)q[i]) {
+      found[0] = 4 * tid + i;
+      found[1] = run;
+    }
+    run += (int)q[i];
+  }
+  __syncthreads();
+  const int cb = found[0], below = found[1];
+#pragma unroll
+  for (int u = 0; u < V; ++u)
+    if (2048 * u + 8 * tid < k)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if ((int)(DUO_MAG(u, j) >> kFineBits) == cb) atomicAdd(&hf[DUO_MAG(u, j) & (kFine - 1u)], 1u);
+  __syncthreads();
+  if (wv == 0) {
+    const int f0 = lane < kFine ? (int)hf[lane] : 0;
+    const int fi = wave_incl_scan(f0);
+    const int r0 = below + fi - f0;
+    if (lane < kFine && r0 < z && z <= r0 + f0) {
+      wsum[1][0] = lane;
+      wsum[1][1] = r0;
+    }
+  }
+  __syncthreads();
+  const uint32_t v = ((uint32_t)cb << kFineBits) | (uint32_t)wsum[1][0];
+  int need = z - wsum[1][1];  // 1 <= need <= number of ties
+  // ties in channel order (u, thread, j): per-u totals from one block
+  // reduction, then a scan over the threads for the u that holds the need-th
+  // tie (static register indices throughout: u is selected, never indexed)
+  int cnt[V];
+#pragma unroll
+  for (int u = 0; u < V; ++u) {
+    const bool ok = 2048 * u + 8 * tid < k;
+    int e = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) e += ok && DUO_MAG(u, j) == v;
+    cnt[u] = e;
+    const int ws_ = wave_sum(e);
+    if (lane == 0) tie_w[wv][u] = ws_;
+  }
+  __syncthreads();
+  int us = V - 1, base_u = 0;
+  {
+    int acc = 0;
+    bool hit = false;
+#pragma unroll
+    for (int u = 0; u < V; ++u) {
+      const int tu = tie_w[0][u] + tie_w[1][u] + tie_w[2][u] + tie_w[3][u];
+      if (!hit && need <= acc + tu) {
+        hit = true;
+        us = u;
+        base_u = acc;
+      }
+      acc += tu;
+    }
+  }
+  int e = 0, wbase = 0;
+#pragma unroll
+  for (int u = 0; u < V; ++u)
+    if (u == us) {
+      e = cnt[u];
+#pragma unroll
+      for (int ww = 0; ww < 4; ++ww) wbase += ww < wv ? tie_w[ww][u] : 0;
+    }
+  const int wi = wave_incl_scan(e);
+  int c0 = base_u + wbase + wi - e;  // ties before this thread's in channel order
+  if (e > 0 && c0 < need && need <= c0 + e) {
+#pragma unroll
+    for (int u = 0; u < V; ++u)
+      if (u == us)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (DUO_MAG(u, j) == v && ++c0 == need) thr[t] = ((int64_t)v << 32) | (int64_t)(2048 * u + 8 * tid + j);
+  }
+}
+#undef DUO_MAG
+
 // Whether the bf16 fast paths apply: 16-byte aligned rows of whole 8-channel
 // vectors.
 __host__ inline bool bf16_vec_ok(const void* X, int64_t ldx, int64_t k) {
@@ -253,14 +415,15 @@ __host__ inline bool bf16_vec_ok(const void* X, int64_t ldx, int64_t k) {
 }
 
 template <typename T>
-static duo_status launch_act_select(const T* X, int64_t ldx, int m, int k, int z, int64_t* thr,
+static duo_status launch_act_select(const T* X, int64_t ldx, int m, int k, int z, int64_t* thr, uint32_t* nf,
                                     hipStream_t s) {
   if (m <= 0) return DUO_OK;
   if constexpr (sizeof(T) == 2) {
     if (bf16_vec_ok(X, ldx, k) && k <= 8192) {
       const int v = (int)cdiv(k, 512);
       dim3 g((unsigned)cdiv(m, 4)), b(256);
-#define DUO_WSEL(VV) hipLaunchKernelGGL((act_select_wave_kernel<VV>), g, b, 0, s, (const uint16_t*)X, ldx, m, k, z, thr)
+#define DUO_WSEL(VV) \
+  hipLaunchKernelGGL((act_select_wave_kernel<VV>), g, b, 0, s, (const uint16_t*)X, ldx, m, k, z, thr, nf)
       if (v <= 1)
         DUO_WSEL(1);
       else if (v <= 2)
@@ -275,10 +438,27 @@ static duo_status launch_act_select(const T* X, int64_t ldx, int m, int k, int z
       DUO_LAUNCH_CHECK();
       return DUO_OK;
     }
+    if (bf16_vec_ok(X, ldx, k) && k <= 32768) {
+      const int v = (int)cdiv(k, 2048);
+      dim3 g((unsigned)m), b(256);
+#define DUO_BSEL(VV) \
+  hipLaunchKernelGGL((act_select_block_kernel<VV>), g, b, 0, s, (const uint16_t*)X, ldx, m, k, z, thr, nf)
+      if (v <= 6)
+        DUO_BSEL(6);
+      else if (v <= 8)
+        DUO_BSEL(8);
+      else if (v <= 12)
+        DUO_BSEL(12);
+      else
+        DUO_BSEL(16);
+#undef DUO_BSEL
+      DUO_LAUNCH_CHECK();
+      return DUO_OK;
+    }
   }
   const int per = (int)cdiv(k, 256);
   dim3 g(m), b(256);
-#define DUO_SEL(CC) hipLaunchKernelGGL((act_select_kernel<T, CC>), g, b, 0, s, X, ldx, m, k, z, thr)
+#define DUO_SEL(CC) hipLaunchKernelGGL((act_select_kernel<T, CC>), g, b, 0, s, X, ldx, m, k, z, thr, nf)
   if (per <= 1)
     DUO_SEL(1);
   else if (per <= 2)
@@ -302,8 +482,9 @@ static duo_status launch_act_select(const T* X, int64_t ldx, int m, int k, int z
 
 duo_status act_threshold_run(const void* X, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z, int64_t* thr,
                              hipStream_t s) {
-  if (dtype == DUO_BF16) return launch_act_select<uint16_t>((const uint16_t*)X, ldx, (int)m, (int)k, z, thr, s);
-  return launch_act_select<float>((const float*)X, ldx, (int)m, (int)k, z, thr, s);
+  if (dtype == DUO_BF16)
+    return launch_act_select<uint16_t>((const uint16_t*)X, ldx, (int)m, (int)k, z, thr, nullptr, s);
+  return launch_act_select<float>((const float*)X, ldx, (int)m, (int)k, z, thr, nullptr, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -556,10 +737,11 @@ __global__ __launch_bounds__(256) void a_reduce_kernel(const float* __restrict__
 
 // ---------------------------------------------------------------------------
 // gram: C = [Xh ; Z] Xh^T restricted to the tiles the method needs.
-// 256 x 256 output tiles; row block I < T is an H tile (I, J) with J <= I,
-// row block I >= T is a G tile (I - T, J) for every J.  H and G together cost
-// 1.5 k^2 m multiply-adds (H's upper triangle is never computed, except inside
-// the T diagonal tiles).
+// 256 x 256 output tiles: H tiles (I, J) with I <= J (the upper triangle,
+// added in place with coalesced writes; mirror_lower_kernel copies it to the
+// lower triangle once per call) and G tiles (I, J) for every I, J.  H and G
+// together cost 1.5 k^2 m multiply-adds (H's lower triangle is never
+// computed, except inside the T diagonal tiles).
 // ---------------------------------------------------------------------------
 constexpr int GT = 256;  // gram tile edge (channels)
 
@@ -579,13 +761,19 @@ struct GramArgs {
   int vec4;     // k, ldh, ldg multiples of 4 and H, G 16-byte aligned: 16-byte reduction path
 };
 
-// Tiles are numbered H first, then G.  Within each kind, bands of 4 row blocks
-// are walked column by column, so neighbouring ids share operand tiles; the
+// Tiles are numbered H first, then G.  H tiles cover the upper triangle of H
+// (row block I <= column block J; the lower triangle is mirrored once per
+// call), G tiles all of G.  Within each kind, bands of 4 blocks
+// are walked across, so neighbouring ids share operand tiles; the
 // XCD remap below gives each XCD a contiguous id range (and so its own L2 set).
 __device__ inline void gram_tile(int t, int nh, int nt, int* isg, int* I, int* J) {
   constexpr int GB = 4;
-  if (t < nh) {  // lower triangle of nt x nt, bands of GB rows
+  if (t < nh) {  // upper triangle of nt x nt (I <= J), bands of GB columns
     *isg = 0;
+    // enumerated as the lower triangle (bands of GB rows), then transposed
+    int* const tmp = I;
+    I = J;
+    J = tmp;
     for (int b0 = 0; b0 < nt; b0 += GB) {
       const int b1 = min(nt, b0 + GB), h = b1 - b0;
       const int cnt = b0 * h + h * (h + 1) / 2;
@@ -851,6 +1039,53 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
   // epilogue.  Accumulator element r of block (a, b) sits at row
   // 16a + 4*(lane/16) + r, column 16b + lane%16 of the wave's 128 x 64 part.
   const int rq = (lane >> 4) * 4, cc = lane & 15;
+  float* C = isg ? A.G : A.H;
+  const int64_t ldc = isg ? A.ldg : A.ldh;
+  if (A.vec4) {
+    // Staged through the (now idle) LDS ring, one half tile (128 rows) at a
+    // time, so that every global access is a coalesced 16-byte one: the
+    // partial tile is stored, or the output read, added to and written back.
+    constexpr int LS = GT + 4;  // row stride of the staged rows, floats
+    constexpr int HR = 128 * LS * 4 <= NS * STAGE_B ? 128 : 64;  // rows per pass
+    static_assert(HR * LS * 4 <= NS * STAGE_B, "staging fits the ring");
+    float* st = (float*)smem;
+    __syncthreads();  // every wave is done with the ring
+#pragma unroll
+    for (int h = 0; h < GT / HR; ++h) {
+      if (wi == h * HR / 128)
+#pragma unroll
+        for (int a = 0; a < 8; ++a)
+          if (HR == 128 || a / 4 == h % 2)
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                st[((a * 16) % HR + rq + r) * LS + wj * 64 + b * 16 + cc] = acc[a][b][r];
+      __syncthreads();
+#pragma unroll 4
+      for (int q = tid; q < HR * (GT / 4); q += 512) {
+        const int rr = q / (GT / 4), c4 = (q % (GT / 4)) * 4;
+        const float4 v = *(const float4*)&st[rr * LS + c4];
+        if (A.nseg > 1) {
+          float* base = A.part + ((int64_t)seg * A.ntiles + tile) * GT * GT;
+          *(float4*)&base[(h * HR + rr) * GT + c4] = v;
+        } else {
+          const int row = I * GT + h * HR + rr, col = J * GT + c4;
+          if (row < A.k && col < A.k) {
+            float4* cp = (float4*)(C + (int64_t)row * ldc + col);
+            float4 c = *cp;
+            c.x += v.x;
+            c.y += v.y;
+            c.z += v.z;
+            c.w += v.w;
+            *cp = c;
+          }
+        }
+      }
+      __syncthreads();
+    }
+    return;
+  }
   if (A.nseg > 1) {
     float* base = A.part + ((int64_t)seg * A.ntiles + tile) * GT * GT;
 #pragma unroll
@@ -862,8 +1097,6 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
           base[(wi * 128 + a * 16 + rq + r) * GT + wj * 64 + b * 16 + cc] = acc[a][b][r];
     return;
   }
-  float* C = isg ? A.G : A.H;
-  const int64_t ldc = isg ? A.ldg : A.ldh;
 #pragma unroll
   for (int a = 0; a < 8; ++a)
 #pragma unroll
@@ -871,20 +1104,15 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = I * GT + wi * 128 + a * 16 + rq + r, col = J * GT + wj * 64 + b * 16 + cc;
-        if (row < A.k && col < A.k) {
-          C[(int64_t)row * ldc + col] += acc[a][b][r];
-          if (!isg && I != J) A.H[(int64_t)col * A.ldh + row] += acc[a][b][r];
-        }
+        if (row < A.k && col < A.k) C[(int64_t)row * ldc + col] += acc[a][b][r];
       }
 }
 
-// Fixed-order sum of the per-segment partial tiles into H and G.  Block
-// (tile, q) takes the 64 x 64 sub-block q: its rows are added with coalesced
-// accesses, and for an off-diagonal H tile the mirrored entries H[col][row]
-// pass through an LDS transpose so that those writes are coalesced too.
+// Fixed-order sum of the per-segment partial tiles into H (upper tiles) and
+// G.  Block (tile, q) takes the 64 x 64 sub-block q; its rows are added with
+// coalesced accesses.
 template <typename T>
 __global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A) {
-  __shared__ float tr[64][65];
   const int tile = blockIdx.x;
   int isg, I, J;
   gram_tile(tile, A.nh, A.nt, &isg, &I, &J);
@@ -932,27 +1160,6 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A) {
         c.w += sum[p].w;
         *cp = c;
       }
-      tr[rr][c4] = sum[p].x;
-      tr[rr][c4 + 1] = sum[p].y;
-      tr[rr][c4 + 2] = sum[p].z;
-      tr[rr][c4 + 3] = sum[p].w;
-    }
-    if (!isg && I != J) {
-      __syncthreads();
-      const int hcol = I * GT + sr + c4;
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int cc = r0 + 16 * p, hrow = J * GT + sc + cc;
-        if (hrow < A.k && hcol < A.k) {
-          float4* hp = (float4*)(A.H + (int64_t)hrow * A.ldh + hcol);
-          float4 h = *hp;
-          h.x += tr[c4][cc];
-          h.y += tr[c4 + 1][cc];
-          h.z += tr[c4 + 2][cc];
-          h.w += tr[c4 + 3][cc];
-          *hp = h;
-        }
-      }
     }
     return;
   }
@@ -963,14 +1170,26 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A) {
     for (int sg = 0; sg < A.nseg; ++sg) s += p0[sg * stride + e];
     const int row = I * GT + sr + rr, col = J * GT + sc + tx;
     if (row < A.k && col < A.k) C[(int64_t)row * ldc + col] += s;
-    tr[rr][tx] = s;
   }
-  if (!isg && I != J) {
-    __syncthreads();
-    for (int cc = ty; cc < 64; cc += 4) {
-      const int hrow = J * GT + sc + cc, hcol = I * GT + sr + tx;
-      if (hrow < A.k && hcol < A.k) A.H[(int64_t)hrow * A.ldh + hcol] += tr[tx][cc];
-    }
+}
+
+// H's lower triangle from its upper one: block (bi, bj), bi >= bj, of 64 x 64
+// takes the transpose of block (bj, bi) through LDS (coalesced reads and
+// writes); inside a diagonal block only the entries below the diagonal are
+// written.
+__global__ __launch_bounds__(256) void mirror_lower_kernel(float* __restrict__ H, int64_t ldh, int k) {
+  __shared__ float tr[64][65];
+  int bi, bj;
+  tri_pair(blockIdx.x, &bi, &bj);
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int rr = ty; rr < 64; rr += 4) {  // source rows bj*64 + rr, columns bi*64 + tx
+    const int r = bj * 64 + rr, c = bi * 64 + tx;
+    tr[rr][tx] = (r < k && c < k) ? H[(int64_t)r * ldh + c] : 0.f;
+  }
+  __syncthreads();
+  for (int rr = ty; rr < 64; rr += 4) {  // target rows bi*64 + rr, columns bj*64 + tx
+    const int r = bi * 64 + rr, c = bj * 64 + tx;
+    if (r < k && c < k && r > c) H[(int64_t)r * ldh + c] = tr[tx][rr];
   }
 }
 
@@ -986,12 +1205,20 @@ int64_t hessian_chunk_tokens(int64_t m, int64_t k) {
   return m < ch ? (m < 1 ? 1 : m) : ch;
 }
 
-int gram_split(int64_t ntiles) {
+// Token segments per output tile: more segments fill the last wave of a
+// launch with too few tiles for 256 CUs, at the price of summing the partial
+// tiles afterwards.  Model: a full-length tile costs 2 * 256^2 * ch flop at
+// about 4.5 TFLOP/s per CU; the fixed-order sum of s partials reads s tiles
+// and reads and writes the output, (s + 2) * 256 KB per tile at about 4 TB/s.
+int gram_split(int64_t ntiles, int64_t ch, int64_t kp) {
+  (void)kp;
+  const double t_tile = 2.0 * GT * GT * (double)ch / 4.5e12;
+  const double t_sum = (double)GT * GT * 4.0 / 4e12;
   int best = 1;
   double best_cost = 1e30;
   for (int s = 1; s <= 8; ++s) {
-    const double cost = (double)cdiv(ntiles * s, 256) / s + (s > 1 ? 0.03 * s : 0.0);
-    if (cost < best_cost - 1e-12) {
+    const double cost = (double)cdiv(ntiles * s, 256) / s * t_tile + (s > 1 ? (double)ntiles * (s + 2) * t_sum : 0.0);
+    if (cost < best_cost * (1.0 - 1e-9)) {
       best_cost = cost;
       best = s;
     }
@@ -1037,7 +1264,10 @@ __global__ void hdiag_reduce_kernel(const double* __restrict__ dpart, int nsl, i
   hdiag[c] += s;
 }
 
+__global__ void clear_flags_kernel(uint32_t* f) { f[threadIdx.x] = 0u; }
+
 struct HessWs {
+  uint32_t* flags;  // [0]: a non-finite input was met by the last call on this workspace
   int64_t* thr;
   uint8_t* Ph;
   uint8_t* Pz;
@@ -1064,10 +1294,11 @@ static HessWs carve_hessian(void* ws, int64_t m, int64_t k) {
   const int64_t tokp = rup(ch, 256);
   const int64_t T = kp / GT;
   const int64_t ntiles = T * (T + 1) / 2 + T * T;
-  const int nseg = gram_split(ntiles);
+  const int nseg = gram_split(ntiles, ch, kp);
   Carver c(ws);
   HessWs h;
-  h.thr = c.take<int64_t>(tokp);
+  h.flags = c.take<uint32_t>(64);
+  h.thr = c.take<int64_t>(2 * tokp);  // sparse stream, then the dense stream's (checked only)
   h.Ph = c.take<uint8_t>((size_t)tokp * kp * 4);  // sized for fp32; bf16 uses half
   h.Pz = c.take<uint8_t>((size_t)tokp * kp * 4);
   h.Pl = c.take<uint8_t>((size_t)tokp * kp * 2);  // low part exists for bf16 only
@@ -1079,6 +1310,15 @@ static HessWs carve_hessian(void* ws, int64_t m, int64_t k) {
 }
 
 size_t hessian_ws_bytes(int64_t m, int64_t k) { return carve_hessian(nullptr, m, k).bytes; }
+
+duo_status hessian_status_run(const void* ws, hipStream_t s) {
+  // the flags are the workspace's first slot whatever m and k were
+  const uint32_t* flags = carve_hessian(const_cast<void*>(ws), 1, 1).flags;
+  uint32_t f = 0;
+  DUO_HIP_TRY(hipMemcpyAsync(&f, flags, sizeof(f), hipMemcpyDeviceToHost, s));
+  DUO_HIP_TRY(hipStreamSynchronize(s));
+  return f ? DUO_ERR_NONFINITE : DUO_OK;
+}
 
 template <typename T, bool LO>
 static duo_status launch_gram(const GramArgs<T>& A, hipStream_t s) {
@@ -1106,13 +1346,19 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
   const int64_t kp = rup(k, GT);
   const int nt = (int)(kp / GT);
   const int nh_all = nt * (nt + 1) / 2;
-  const int nseg = gram_split(nh_all + nt * nt);  // the same split the workspace was sized for
+  const int nseg = gram_split(nh_all + nt * nt, ch, kp);  // the same split the workspace was sized for
+  hipLaunchKernelGGL(clear_flags_kernel, dim3(1), dim3(64), 0, s, w.flags);
+  DUO_LAUNCH_CHECK();
   for (int64_t t0 = 0; t0 < m; t0 += ch) {
     const int mc = (int)(m - t0 < ch ? m - t0 : ch);
     const T* xs = Xs + t0 * ldx;
     const T* xd = two ? Xd + t0 * ldx : nullptr;
-    duo_status st = launch_act_select<T>(xs, ldx, mc, (int)k, z, w.thr, s);
+    duo_status st = launch_act_select<T>(xs, ldx, mc, (int)k, z, w.thr, w.flags, s);
     if (st != DUO_OK) return st;
+    if (two) {  // the dense stream is checked too (its values enter G and a)
+      st = launch_act_select<T>(xd, ldx, mc, (int)k, 0, w.thr + rup(ch, 256), w.flags, s);
+      if (st != DUO_OK) return st;
+    }
     dim3 pg((unsigned)(kp / 256), (unsigned)cdiv(mc, 256));
     if constexpr (sizeof(T) == 2) {
       if (bf16_vec_ok(xs, ldx, k) && (!two || bf16_vec_ok(xd, ldx, k))) {
@@ -1185,6 +1431,11 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
       DUO_LAUNCH_CHECK();
     }
   }
+  if (want_h) {
+    const int64_t nb = cdiv(k, 64);
+    hipLaunchKernelGGL(mirror_lower_kernel, dim3((unsigned)(nb * (nb + 1) / 2)), dim3(256), 0, s, H, ldh, (int)k);
+    DUO_LAUNCH_CHECK();
+  }
   return DUO_OK;
 }
 
@@ -1203,19 +1454,21 @@ duo_status act_mask_run(const void* X, int32_t dtype, int64_t m, int64_t k, int6
   const HessWs w = carve_hessian(ws, m, k);
   const int64_t ch = hessian_chunk_tokens(m, k);
   const int64_t words = cdiv(k, 32);
+  hipLaunchKernelGGL(clear_flags_kernel, dim3(1), dim3(64), 0, s, w.flags);
+  DUO_LAUNCH_CHECK();
   for (int64_t t0 = 0; t0 < m; t0 += ch) {
     const int mc = (int)(m - t0 < ch ? m - t0 : ch);
     const int64_t n = mc * words;
     duo_status st;
     if (dtype == DUO_BF16) {
       const uint16_t* x = (const uint16_t*)X + t0 * ldx;
-      st = launch_act_select<uint16_t>(x, ldx, mc, (int)k, z, w.thr, s);
+      st = launch_act_select<uint16_t>(x, ldx, mc, (int)k, z, w.thr, w.flags, s);
       if (st != DUO_OK) return st;
       hipLaunchKernelGGL(act_mask_kernel<uint16_t>, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, x, ldx, mc,
                          (int)k, (const int64_t*)w.thr, mask + t0 * words);
     } else {
       const float* x = (const float*)X + t0 * ldx;
-      st = launch_act_select<float>(x, ldx, mc, (int)k, z, w.thr, s);
+      st = launch_act_select<float>(x, ldx, mc, (int)k, z, w.thr, w.flags, s);
       if (st != DUO_OK) return st;
       hipLaunchKernelGGL(act_mask_kernel<float>, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, x, ldx, mc, (int)k,
                          (const int64_t*)w.thr, mask + t0 * words);

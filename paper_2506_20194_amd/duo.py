@@ -29,7 +29,7 @@ EXPORTED = (
     "duo_prune_layer", "duo_profile_enable", "duo_profile_read", "duo_block_workspace_size", "duo_rmsnorm",
     "duo_act_sparsify", "duo_linear", "duo_rope", "duo_attention", "duo_silu_mul", "duo_act_order",
     "duo_permute", "duo_permute_mask", "duo_dsc_workspace_size", "duo_dsc_layout", "duo_dsc_pack",
-    "duo_dsc_gemv", "duo_dsc_gemv_noalloc",
+    "duo_dsc_gemv", "duo_dsc_gemv_noalloc", "duo_hessian_status",
 )
 PROF = dict(gram=0, hessian=1, chol=2, score=3, sweep=4, inblock=5, trail=6, select=7, decode=8)
 DUO_BOP_ACT_SPARSIFY, DUO_BOP_LINEAR, DUO_BOP_ATTENTION = 0, 1, 2
@@ -79,6 +79,8 @@ def lib():
         L.duo_act_sparsify_mask.argtypes = [P, I32, I64, I64, I64, ActRule, P, P, SZ, P]
         L.duo_hessian_accum.restype = I32
         L.duo_hessian_accum.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, I64, P, P, P, SZ, P]
+        L.duo_hessian_status.restype = I32
+        L.duo_hessian_status.argtypes = [P, SZ, P]
         L.duo_residual_term.restype = I32
         L.duo_residual_term.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, P, SZ, P]
         L.duo_chol_inv.restype = I32
@@ -215,7 +217,9 @@ def duo_act_sparsify_mask(X, act_sparsity, mask_out=None, ws=None):
     return mask_out
 
 
-def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=None, hdiag=None):
+def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=None, hdiag=None, check=False):
+    """Stage 1 (H, and G and a when given).  check=True waits for the stream
+    and raises DuoError(DUO_ERR_NONFINITE) if the inputs held NaN or inf."""
     m, k = X_src.shape
     _same_device(X_src, X_dense, H, G, a, ws, hdiag)
     _shape(H, (k, k), "H")
@@ -234,6 +238,8 @@ def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=N
                                  _ptr(H), _ld(H), _ptr(G), _ld(G) if G is not None else k, _ptr(a), _ptr(hdiag),
                                  _ptr(ws), ws.numel(), _stream(X_src.device))
     _check(st, "duo_hessian_accum")
+    if check and m > 0:
+        _check(lib().duo_hessian_status(_ptr(ws), ws.numel(), _stream(X_src.device)), "duo_hessian_accum")
 
 
 def duo_residual_term(X_dense, G, a, act_sparsity, X_src=None, ws=None):
@@ -484,7 +490,7 @@ def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=N
     G = torch.zeros((k, k), dtype=torch.float32, device=dev)
     a = torch.zeros(k, dtype=torch.float32, device=dev)
     hdiag = torch.zeros(k, dtype=torch.float64, device=dev) if act_order else None
-    duo_hessian_accum(X, H, act_sparsity, X_dense=X_dense, G=G, a=a, hdiag=hdiag)
+    duo_hessian_accum(X, H, act_sparsity, X_dense=X_dense, G=G, a=a, hdiag=hdiag, check=True)
     perm = None
     if act_order:
         perm, inv = duo_act_order(hdiag)

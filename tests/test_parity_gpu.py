@@ -55,7 +55,9 @@ def inputs(n, k, m, dtype, seed, kind="lognormal", sigma=1.0, outliers=0):
 
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 @pytest.mark.parametrize("m,k,p_x", [(300, 200, 0.5), (257, 4096, 0.5), (64, 11008, 0.6), (100, 129, 0.0),
-                                     (50, 33, 1.0), (70, 1, 0.5)])
+                                     (50, 33, 1.0), (70, 1, 0.5), (40, 8200, 0.5), (33, 12296, 0.3),
+                                     (20, 16392, 0.7), (17, 28672, 0.5), (9, 32768, 0.5), (12, 9000, 0.0),
+                                     (12, 9000, 1.0)])
 def test_act_mask_bit_exact(duo, dtype, m, k, p_x):
     say("act_mask", dtype, m, k, p_x)
     _, X = inputs(1, k, m, dtype, seed=k + m)
@@ -332,3 +334,39 @@ def test_deterministic(duo):
     a = duo.prune_linear(W.to(DEV), X.to(DEV), 0.5, 0.5, block=64)
     b = duo.prune_linear(W.to(DEV), X.to(DEV), 0.5, 0.5, block=64)
     assert torch.equal(a["W_out"], b["W_out"]) and torch.equal(a["mask"], b["mask"])
+
+
+@pytest.mark.parametrize("k,dtype", [(96, torch.float32), (4096, torch.bfloat16), (11008, torch.bfloat16),
+                                     (300, torch.bfloat16)])
+def test_nonfinite_input_is_reported(duo, k, dtype):
+    """Stage 1 flags NaN and inf calibration inputs (DUO_ERR_NONFINITE from
+    the status check) and not finite ones, for the sparse and the dense
+    stream; the largest finite bf16 magnitude is not flagged."""
+    say("non-finite input", k, dtype)
+    m = 40
+    _, X = inputs(1, k, m, dtype, seed=k)
+    X = X.to(DEV)
+    H = torch.zeros((k, k), dtype=torch.float32, device=DEV)
+    G = torch.zeros_like(H)
+    a = torch.zeros(k, dtype=torch.float32, device=DEV)
+    ws = duo.workspace(duo.DUO_OP_HESSIAN, 0, k, m, 0, DEV)
+    big = X.clone()
+    big[3, 5] = torch.finfo(dtype).max
+    duo.duo_hessian_accum(big, H, 0.5, G=G, a=a, ws=ws, check=True)      # finite: no error
+    for val, where in ((float("nan"), "src"), (float("inf"), "src"), (float("-inf"), "dense")):
+        bad = X.clone()
+        bad[m - 1, k - 1] = val
+        H.zero_(), G.zero_(), a.zero_()
+        with pytest.raises(duo.DuoError) as e:
+            if where == "src":
+                duo.duo_hessian_accum(bad, H, 0.5, G=G, a=a, ws=ws, check=True)
+            else:
+                duo.duo_hessian_accum(X, H, 0.5, X_dense=bad, G=G, a=a, ws=ws, check=True)
+        assert e.value.status == duo.DUO_ERR_NONFINITE
+        # the flag belongs to the last call: a clean call clears it
+        duo.duo_hessian_accum(X, H, 0.5, G=G, a=a, ws=ws, check=True)
+    # the activation-mask hook records it too
+    bad = X.clone()
+    bad[0, 0] = float("nan")
+    duo.duo_act_sparsify_mask(bad, 0.5, ws=ws)
+    assert duo.lib().duo_hessian_status(duo._ptr(ws), ws.numel(), duo._stream(DEV)) == duo.DUO_ERR_NONFINITE
