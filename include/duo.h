@@ -418,9 +418,10 @@ duo_status duo_act_sparsify(const void* X, int64_t m, int64_t k, int64_t ldx, du
 
 /* duo_linear - Y = X W^T (+ R): X m x k (ldx), W n x k (ldw, a Linear's
  *   out x in weights), optional residual R m x n (ldr; NULL for none), Y m x n
- *   (ldy; may equal R).  bf16 in and out, fp32 accumulation, one rounding.
- *   Computed by rocBLAS (gemm_ex) on the caller's stream, with its scratch
- *   memory taken from the workspace.  Workspace: DUO_BOP_LINEAR. */
+ *   (ldy; may equal R).  bf16 in and out, fp32 accumulation, one rounding
+ *   (of the fp32 sum plus R).  bf16 MFMA tiles of this library; rows that are
+ *   not 16-byte aligned or k % 8 != 0 take a slower per-element path.  Needs
+ *   no scratch memory: ws may be NULL (DUO_BOP_LINEAR is 0 bytes). */
 duo_status duo_linear(const void* X, int64_t m, int64_t k, int64_t ldx, const void* W, int64_t n, int64_t ldw,
                       const void* R, int64_t ldr, void* Y, int64_t ldy, void* ws, size_t ws_bytes, void* stream);
 
@@ -434,10 +435,12 @@ duo_status duo_rope(void* X, int64_t m, int64_t heads, int64_t head_dim, int64_t
  *   for each sequence and head h, O_h = softmax(Q_h K_h^T / sqrt(head_dim)
  *   with positions j > i masked) V_h, where Q_h is columns
  *   [h*head_dim, (h+1)*head_dim) of the sequence's rows of Q.  Q, K, V share
- *   the row stride ld; O has ldo.  Scores are fp32 (rocBLAS batched products),
- *   the row softmax is fp32 and the probabilities are rounded to bf16 before
- *   the product with V.  Workspace: DUO_BOP_ATTENTION with the same seq_len
- *   and heads (fp32 and bf16 score planes of one sequence). */
+ *   the row stride ld; O has ldo.  Scores, row maxima and sums are fp32 (two
+ *   passes over the key blocks), the normalised probabilities are rounded to
+ *   bf16 before the product with V, and O is accumulated in fp32.  head_dim
+ *   64 or 128, ld % 8 == 0 and 16-byte aligned Q, K, V (else
+ *   DUO_ERR_UNSUPPORTED).  Needs no scratch memory: ws may be NULL
+ *   (DUO_BOP_ATTENTION is 0 bytes). */
 duo_status duo_attention(const void* Q, const void* K, const void* V, int64_t ld, int64_t nseq, int64_t seq_len,
                          int64_t heads, int64_t head_dim, void* O, int64_t ldo, void* ws, size_t ws_bytes,
                          void* stream);

@@ -6,8 +6,9 @@ sparse stream (the block's pruned weights, every linear input sparsified per
 token).  The linears are pruned in groups that share one Hessian -- [q, k, v],
 then o, then [gate, up], then down -- and each group's solver input is the
 pair (sparse stream, dense stream) at that point, computed with the earlier
-groups already pruned.  Every step runs in libduo's kernels (and rocBLAS for
-the block's plain products); this module only sequences the calls.
+groups already pruned.  Every step runs in libduo's own kernels (the block's
+products included: bf16 MFMA linears and causal attention); this module only
+sequences the calls.
 """
 
 from __future__ import annotations

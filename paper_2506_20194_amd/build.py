@@ -46,8 +46,7 @@ def build(verbose: bool = False) -> str:
             if o.strip():
                 print(o, file=sys.stderr)
     tmp = LIB + f".tmp{os.getpid()}"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp, "-L/opt/rocm/lib", "-lrocblas",
-          "-Wl,-rpath,/opt/rocm/lib"])
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)
     return LIB
 

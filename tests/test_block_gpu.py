@@ -77,7 +77,9 @@ def test_act_sparsify_bit_exact(duo, m, k, p):
     assert np.array_equal(y.double().numpy(), ref)
 
 
-@pytest.mark.parametrize("m,k,n,res", [(200, 128, 352, False), (257, 4096, 640, True), (64, 11008, 4096, True)])
+@pytest.mark.parametrize("m,k,n,res", [(200, 128, 352, False), (257, 4096, 640, True), (64, 11008, 4096, True),
+                                       (70, 352, 200, True), (33, 100, 50, True), (1, 8, 1, False),
+                                       (384, 256, 128, False)])
 def test_linear(duo, m, k, n, res):
     say("linear", m, k, n, res)
     x, w = bf((m, k), 1), bf((n, k), 2, 0.02)
@@ -98,7 +100,18 @@ def test_rope(duo):
     assert ok, e
 
 
-@pytest.mark.parametrize("nseq,L,heads,hd", [(2, 96, 2, 64), (1, 520, 4, 128)])
+def test_linear_residual_in_place(duo):
+    """Y may be the residual R itself (the block adds its residual in place)."""
+    say("linear in place")
+    x, w, r = bf((130, 256), 11), bf((300, 256), 12, 0.02), bf((130, 300), 13)
+    y = r.to(DEV)
+    duo.duo_linear(x.to(DEV), w.to(DEV), R=y, out=y)
+    ok, e = close(f64(y), BR.linear(x.double().numpy(), w.double().numpy(), r.double().numpy()))
+    assert ok, e
+
+
+@pytest.mark.parametrize("nseq,L,heads,hd", [(2, 96, 2, 64), (1, 520, 4, 128), (3, 64, 2, 128), (2, 1, 1, 64),
+                                             (1, 2048, 2, 128)])
 def test_attention(duo, nseq, L, heads, hd):
     say("attention", nseq, L, heads, hd)
     q, k, v = (bf((nseq * L, heads * hd), s) for s in (5, 6, 7))
