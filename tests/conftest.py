@@ -23,6 +23,11 @@ def duo_lib():
     """The built library; builds it once if it is missing."""
     from paper_2506_20194_amd import duo
 
+    # another build of the same library (the AddressSanitizer build of the
+    # ABI tests) can be named through DUO_TEST_LIB
+    if os.environ.get("DUO_TEST_LIB"):
+        duo.LIB_PATH = os.environ["DUO_TEST_LIB"]
+        return duo
     if not os.path.exists(duo.LIB_PATH):
         from paper_2506_20194_amd import build
 
