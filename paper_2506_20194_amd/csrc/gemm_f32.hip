@@ -208,6 +208,27 @@ __device__ inline int xcd_remap_g(int b, int nblocks) {
   return (b % 8) * per + b / 8;
 }
 
+// Tile (ti, tj) of the 128 grid with enumeration index pid (the triangular
+// filters and the tile orders are defined on that grid).
+__device__ inline void tile_of(const GemmDesc& d, int pid, int* ti, int* tj) {
+  if (d.tri == TRI_ALL) {
+    const int tn = (int)cdiv(d.N, kTile);
+    *ti = pid / tn;
+    *tj = pid % tn;
+  } else if (d.tri == TRI_LOWER) {
+    tri_pair(pid, ti, tj);
+  } else if (d.order == ORDER_DIAG) {
+    // group s holds the s + 1 tiles at distance T - 1 - s from the diagonal
+    const int T = (int)cdiv(d.N, kTile);
+    int sgrp, off;
+    tri_pair(pid, &sgrp, &off);
+    *ti = off;
+    *tj = off + (T - 1 - sgrp);
+  } else {
+    tri_pair(pid, tj, ti);
+  }
+}
+
 // Tiles are enumerated on the 128 grid (the triangular filters and the tile
 // orders are defined there); with TE = 64 each 128 tile is split into its
 // four quarters, which are consecutive ids.
@@ -228,22 +249,7 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmDesc d, int ntiles) {
   }
   const int pid = id / (SUB * SUB), sub = id % (SUB * SUB);
   int ti, tj;  // on the 128 grid
-  if (d.tri == TRI_ALL) {
-    const int tn = (int)cdiv(d.N, kTile);
-    ti = pid / tn;
-    tj = pid % tn;
-  } else if (d.tri == TRI_LOWER) {
-    tri_pair(pid, &ti, &tj);
-  } else if (d.order == ORDER_DIAG) {
-    // group s holds the s + 1 tiles at distance T - 1 - s from the diagonal
-    const int T = (int)cdiv(d.N, kTile);
-    int sgrp, off;
-    tri_pair(pid, &sgrp, &off);
-    ti = off;
-    tj = off + (T - 1 - sgrp);
-  } else {
-    tri_pair(pid, &tj, &ti);
-  }
+  tile_of(d, pid, &ti, &tj);
   const int i0 = ti * kTile + (sub / SUB) * TE, j0 = tj * kTile + (sub % SUB) * TE;
   if (i0 >= d.M || j0 >= d.N) return;
   f4 acc[G::NA][G::NA];
@@ -271,11 +277,210 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmDesc d, int ntiles) {
       }
 }
 
+// ---------------------------------------------------------------------------
+// Fast path for launches whose tiles all lie inside M x N with 16-byte aligned
+// operands (every DuoGPT product at k a multiple of 128): A row-major (K
+// contiguous); B either K-contiguous (b_row = 0, "NT") or row-major (b_row = 1,
+// "NN").  128 x 128 tile, 2 x 2 waves of 64 x 64, K staged 16 at a time
+// through a ring of four 16 KB LDS stages filled by direct global->LDS loads
+// (no register staging), three stages in flight.
+//
+// K order inside a stage: MFMA step s (of 4) takes k = 4g + s in lane group g,
+// so that a K-contiguous operand's fragment for all four steps is one 16-byte
+// chunk (k = 4g .. 4g + 3) per lane.  Both operands use the same order, so
+// the sum is unchanged.  Layouts (16-byte chunks):
+//   K-contiguous operand, 128 lines x 4 chunks: chunk c of line r at
+//     r * 4 + (c ^ ((r >> 2) & 3)), so the 16 lines of a fragment read hit 16
+//     distinct bank groups;
+//   row-major B, 16 k-rows x 32 chunks: chunk c of row k at
+//     k * 32 + (c ^ (4 * ((k >> 2) & 3))), so the four lane groups (k four apart)
+//     read disjoint bank groups.
+// ---------------------------------------------------------------------------
+constexpr int FK = 16;                 // K per stage
+constexpr int FNS = 4;                 // ring depth
+constexpr int FOP = kTile * FK * 4;    // bytes per operand per stage (8 KB)
+constexpr int FSTAGE = 2 * FOP;        // 16 KB
+
+__device__ __forceinline__ void wait_vm(int n) {
+  // at most n of this wave's vector-memory operations outstanding (n <= 12)
+  switch (n) {
+    case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
+    case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
+    case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
+    default: __builtin_amdgcn_s_waitcnt(0x0F7C); break;  // 12
+  }
+}
+
+template <bool BR>
+__device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* smem, f4 (&acc)[4][4]) {
+  const int64_t klo = lo_of<kTile>(t.klo, i0, j0);
+  const int64_t khi = hi_of<kTile>(t.khi, i0, j0, t.K);
+  if (klo >= khi) return;
+  const int nst = (int)((khi - klo) / FK);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wi = wave >> 1, wj = wave & 1;
+  // this lane's two chunks of each operand per stage (wave-wide loads 2w, 2w + 1)
+  const float* ga[2];
+  const float* gb[2];
+  uint32_t la[2], lb[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int pos = (2 * wave + q) * 64 + lane;  // 16-byte position in the operand's stage image
+    {
+      const int r = pos >> 2, c = (pos & 3) ^ ((r >> 2) & 3);
+      ga[q] = t.A + (int64_t)(i0 + r) * t.lda + klo + 4 * c;
+    }
+    if (BR) {
+      const int k = pos >> 5, c = (pos & 31) ^ (4 * ((k >> 2) & 3));
+      gb[q] = t.B + (klo + k) * t.ldb + j0 + 4 * c;
+    } else {
+      const int r = pos >> 2, c = (pos & 3) ^ ((r >> 2) & 3);
+      gb[q] = t.B + (int64_t)(j0 + r) * t.ldb + klo + 4 * c;
+    }
+    la[q] = (uint32_t)((2 * wave + q) * 64 * 16);
+    lb[q] = (uint32_t)(FOP + (2 * wave + q) * 64 * 16);
+  }
+  const int64_t da = FK, db = BR ? (int64_t)FK * t.ldb : FK;  // element step per stage
+  const float alpha = t.alpha;
+  auto issue = [&](int st) {
+    uint8_t* base = smem + (st % FNS) * FSTAGE;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      __builtin_amdgcn_global_load_lds((const void*)(ga[q] + st * da),
+                                       (__attribute__((address_space(3))) void*)(base + la[q]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(gb[q] + st * db),
+                                       (__attribute__((address_space(3))) void*)(base + lb[q]), 16, 0, 0);
+    }
+  };
+  const int g = lane >> 4, l16 = lane & 15;
+  auto compute = [&](int st) {
+    const u32x4* sa = (const u32x4*)(smem + (st % FNS) * FSTAGE);
+    const uint8_t* sbb = smem + (st % FNS) * FSTAGE + FOP;
+    float av[4][4], bv[4][4];  // [block][step]
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const int r = wi * 64 + a * 16 + l16;
+      const u32x4 v = sa[r * 4 + (g ^ ((r >> 2) & 3))];
+#pragma unroll
+      for (int s2 = 0; s2 < 4; ++s2) av[a][s2] = alpha * __uint_as_float(v[s2]);
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int col = wj * 64 + b * 16 + l16;
+      if (BR) {
+        const float* sb = (const float*)sbb;
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) {
+          const int k = 4 * g + s2;
+          bv[b][s2] = sb[k * 128 + (((col >> 2) ^ (4 * ((k >> 2) & 3))) << 2) + (col & 3)];
+        }
+      } else {
+        const u32x4 v = ((const u32x4*)sbb)[col * 4 + (g ^ ((col >> 2) & 3))];
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) bv[b][s2] = __uint_as_float(v[s2]);
+      }
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2)
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a][s2], bv[b][s2], acc[a][b], 0, 0, 0);
+  };
+  lds_barrier();  // the previous user of the ring (an earlier term) is done with it
+  for (int st = 0; st < min(nst, FNS - 1); ++st) issue(st);
+  for (int st = 0; st < nst; ++st) {
+    wait_vm(4 * min(FNS - 2, nst - 1 - st));  // stage st landed (this wave's part)
+    lds_barrier();                            // every wave's part landed; stage st - 1 is free
+    if (st + FNS - 1 < nst) issue(st + FNS - 1);
+    compute(st);
+  }
+}
+
+template <bool B1R, bool B2R, bool TWO>
+__global__ __launch_bounds__(256, 2) void gemm_fast_kernel(GemmDesc d, int ntiles) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];  // FNS stages; reused by the epilogue
+  const int id = d.order == ORDER_XCD ? xcd_remap_g(blockIdx.x, gridDim.x) : (int)blockIdx.x;
+  if (id >= ntiles) return;
+  if (blockIdx.y) {
+    const int64_t z = blockIdx.y;
+    d.C += z * d.sC;
+    d.t[0].A += z * d.sA[0];
+    d.t[0].B += z * d.sB[0];
+    d.t[1].A += z * d.sA[1];
+    d.t[1].B += z * d.sB[1];
+  }
+  int ti, tj;
+  tile_of(d, id, &ti, &tj);
+  const int i0 = ti * kTile, j0 = tj * kTile;
+  f4 acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
+  fast_term<B1R>(d.t[0], i0, j0, smem, acc);
+  if (TWO) fast_term<B2R>(d.t[1], i0, j0, smem, acc);
+
+  // epilogue through LDS: C = beta C + acc with coalesced 16-byte accesses
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wi = wave >> 1, wj = wave & 1;
+  constexpr int LS = kTile + 4;  // kTile * LS floats: the dynamic LDS is sized for it
+  float* st = (float*)smem;
+  lds_barrier();
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        st[(wi * 64 + a * 16 + (lane >> 4) * 4 + r) * LS + wj * 64 + b * 16 + (lane & 15)] = acc[a][b][r];
+  lds_barrier();
+#pragma unroll 4
+  for (int q = tid; q < kTile * kTile / 4; q += 256) {
+    const int r = q >> 5, c4 = (q & 31) * 4;
+    const float4 v = *(const float4*)&st[r * LS + c4];
+    float4* cp = (float4*)(d.C + (int64_t)(i0 + r) * d.ldc + j0 + c4);
+    if (d.beta != 0.f) {
+      const float4 c = *cp;
+      *cp = make_float4(d.beta * c.x + v.x, d.beta * c.y + v.y, d.beta * c.z + v.z, d.beta * c.w + v.w);
+    } else {
+      *cp = v;
+    }
+  }
+}
+
 // A launch with fewer 128 tiles than kSmallTiles runs on 64 tiles: four
 // times the workgroups.  Short products then still cover the 256 CUs, and
 // launches of a few waves of 128 tiles lose less to the last, partly filled
 // wave (measured at k = 4096 and 11008: 2048 beats 512, 1024 and 4096).
 constexpr int kSmallTiles = 2048;
+
+constexpr size_t kFastLds = (size_t)kTile * (kTile + 4) * 4;  // >= FNS * FSTAGE (epilogue image)
+static_assert(kFastLds >= (size_t)FNS * FSTAGE, "fast-path LDS");
+
+// Whether every tile of a 128-tile launch can take the fast path: interior
+// tiles, 16-byte aligned operands and rows, K ranges in whole stages.
+bool fast_ok(const GemmDesc& d) {
+  if (d.M % kTile != 0 || d.N % kTile != 0 || (d.ldc & 3) != 0 || (reinterpret_cast<uintptr_t>(d.C) & 15) != 0)
+    return false;
+  for (int i = 0; i < d.nterms; ++i) {
+    const GemmTerm& t = d.t[i];
+    if (!t.a_row || t.K % FK != 0 || (t.lda & 3) != 0 || (t.ldb & 3) != 0) return false;
+    if ((reinterpret_cast<uintptr_t>(t.A) & 15) != 0 || (reinterpret_cast<uintptr_t>(t.B) & 15) != 0) return false;
+    if (d.batch > 1 && ((d.sA[i] & 3) != 0 || (d.sB[i] & 3) != 0)) return false;
+  }
+  if (d.batch > 1 && (d.sC & 3) != 0) return false;
+  return true;
+}
+
+template <bool B1R, bool B2R, bool TWO>
+duo_status launch_fast(const GemmDesc& d, int ntiles, int nb, hipStream_t s) {
+  auto kern = gemm_fast_kernel<B1R, B2R, TWO>;
+  if (duo_status st = set_max_lds((const void*)kern, kFastLds); st != DUO_OK) return st;
+  hipLaunchKernelGGL(kern, dim3((unsigned)rup(ntiles, 8), nb), dim3(256), kFastLds, s, d, ntiles);
+  DUO_LAUNCH_CHECK();
+  return DUO_OK;
+}
 
 template <bool A1R, bool B1R, bool A2R, bool B2R, bool TWO>
 duo_status launch(const GemmDesc& d, hipStream_t s) {
@@ -283,6 +488,9 @@ duo_status launch(const GemmDesc& d, hipStream_t s) {
   const int ntiles = d.tri == TRI_ALL ? tm * tn : tm * (tm + 1) / 2;
   if (ntiles <= 0) return DUO_OK;
   const int nb = d.batch > 1 ? d.batch : 1;
+  if constexpr (A1R && A2R) {
+    if ((int64_t)ntiles * nb >= kSmallTiles && fast_ok(d)) return launch_fast<B1R, B2R, TWO>(d, ntiles, nb, s);
+  }
   if ((int64_t)ntiles * nb < kSmallTiles) {
     const int grid = (int)rup(4 * ntiles, 8);
     hipLaunchKernelGGL((gemm_kernel<64, A1R, B1R, A2R, B2R, TWO>), dim3(grid, nb), dim3(256), 0, s, d, 4 * ntiles);
