@@ -362,25 +362,27 @@ def _check_mask_in(mask_in, n, k):
     return mask_in
 
 
-def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
-                qparams_out=None, values_in=None, w0_out=None):
-    """Column sweep with every column's update applied to all later columns at once.
+def _sweep(W, L, D, fac, p_w, B, lazy, mask_in, scores_out, nm, quant, qparams_out, values_in, w0_out):
+    """The column sweep, in either of its two equivalent forms.
 
-    Processing column j: w0 = W[:, j]; p = w0 * m_j; e = (w0 - p) / L_jj and
-    every later column j' gets  W[:, j'] -= e * L[j', j] - w0 * D[j, j'].
+    Processing column j leaves it at the value p it keeps (w0, or its grid
+    value, where kept; 0 where pruned), w0 being its value at that moment, and
+    records what every later column j' owes it: the compensation of its
+    error, e * L[j', j] with e = (w0 - p) / L_jj, minus its residual term
+    w0 * D[j, j'] (Eq. 7; App. A.4).
+      lazy=False: the debt is paid to every later column at once (the
+        definition, column by column);
+      lazy=True: it is paid at once only inside the block; the columns after
+        the block receive the debts of the whole block together as one product
+        E L[rest, blk]^T - W0 D[blk, rest], E and W0 collecting the block's e and
+        w0 (Alg. 1, lazy batch updates; reading R-lazy: W0 holds the values
+        before pruning).  The two forms give the same result up to rounding.
     The mask of each block is chosen when the sweep reaches the block, from
-    S = W[:, blk]^2 * fac[blk].  With nm = (N, M) the mask is instead chosen
-    per row for each group of M columns when the sweep reaches the group, from
-    the group's current S (select_nm_mask); p_w is then not used.
-    quant = (bits, group): joint pruning and quantisation (Table 4): when the
-    sweep reaches a group of `group` columns, every row's grid is fixed from
-    the group's current values (quant_grid); a kept weight becomes its grid
-    value and a pruned one 0, and the compensation carries both errors.
-    qparams_out (a list) receives (scale, zero) arrays of shape (n,) per group.
-    Test hooks: values_in (n x k) replaces the value every kept weight takes
-    (as mask_in replaces the mask); w0_out (n x k) receives each column's value
-    when it was processed.  Returns (W_hat, keep).
-    """
+    S = W[:, blk]^2 * fac[blk] (select_block_mask); with nm = (N, M) it is
+    instead chosen per row for each group of M columns when the sweep reaches
+    the group (select_nm_mask).  quant = (bits, group): a grid per row and
+    group is fixed from the group's current values when the sweep reaches it
+    (quant_grid)."""
     W = _f64(W).copy()
     L = _f64(L)
     D = _f64(D)
@@ -399,56 +401,9 @@ def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None,
             keep[:, j0:j1] = select_block_mask(S, counts[bi]) if mask_in is None else mask_in[:, j0:j1]
         elif mask_in is not None:
             keep[:, j0:j1] = mask_in[:, j0:j1]
-        for j in range(j0, j1):
-            if nm is not None and j % nm[1] == 0:
-                S[:, j - j0:j - j0 + nm[1]] = W[:, j:j + nm[1]] ** 2 * fac[j:j + nm[1]]
-                if mask_in is None:
-                    keep[:, j:j + nm[1]] = select_nm_mask(S[:, j - j0:j - j0 + nm[1]], nm[0])
-            if quant is not None and j % quant[1] == 0:
-                qs, qz = _group_grids(W[:, j:j + quant[1]], quant[0], qparams_out)
-            w0 = W[:, j].copy()
-            p = _kept_value(w0, keep[:, j], quant, qs, qz)
-            if values_in is not None:
-                p = np.where(keep[:, j], _f64(values_in[:, j]), 0.0)
-            if w0_out is not None:
-                w0_out[:, j] = w0
-            e = (w0 - p) / L[j, j]
-            W[:, j] = p
-            W[:, j + 1:] -= np.outer(e, L[j + 1:, j]) - np.outer(w0, D[j, j + 1:])
-        if scores_out is not None:
-            scores_out.append(S.copy())
-    return W * keep, keep
-
-
-def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
-                  qparams_out=None, values_in=None, w0_out=None):
-    """Algorithm 1: in-block sequential updates, then one lazy batch update
-    W[:, rest] -= E L[rest, blk]^T - W0 D[blk, rest] per block (reading R-lazy:
-    W0 holds each column's value at the time it was processed).  nm, quant,
-    qparams_out, values_in and w0_out as in sweep_eager.  scores_out receives, per block, the scores each weight's
-    selection used.  Returns (W_hat, keep).
-    """
-    W = _f64(W).copy()
-    L = _f64(L)
-    D = _f64(D)
-    fac = _f64(fac)
-    n, k = W.shape
-    mask_in = _check_mask_in(mask_in, n, k)
-    nm = _check_nm(nm, k, B)
-    quant = _check_quant(quant, B)
-    keep = np.ones((n, k), dtype=bool)
-    counts = block_prune_counts(n, k, p_w, B)
-    qs = qz = None
-    for bi, j0 in enumerate(range(0, k, B)):
-        j1 = min(k, j0 + B)
-        Bb = j1 - j0
-        S = W[:, j0:j1] ** 2 * fac[j0:j1]
-        if nm is None:
-            keep[:, j0:j1] = select_block_mask(S, counts[bi]) if mask_in is None else mask_in[:, j0:j1]
-        elif mask_in is not None:
-            keep[:, j0:j1] = mask_in[:, j0:j1]
-        E = np.zeros((n, Bb))
-        W0 = np.zeros((n, Bb))
+        E = np.zeros((n, j1 - j0))
+        W0 = np.zeros((n, j1 - j0))
+        reach = j1 if lazy else k  # columns paid at once
         for j in range(j0, j1):
             if nm is not None and j % nm[1] == 0:
                 S[:, j - j0:j - j0 + nm[1]] = W[:, j:j + nm[1]] ** 2 * fac[j:j + nm[1]]
@@ -463,15 +418,35 @@ def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=Non
             if w0_out is not None:
                 w0_out[:, j] = w0
             e = (w0 - p) / L[j, j]
+            W[:, j] = p
+            W[:, j + 1:reach] -= np.outer(e, L[j + 1:reach, j]) - np.outer(w0, D[j, j + 1:reach])
             E[:, j - j0] = e
             W0[:, j - j0] = w0
-            W[:, j] = p
-            W[:, j + 1:j1] -= np.outer(e, L[j + 1:j1, j]) - np.outer(w0, D[j, j + 1:j1])
-        if j1 < k:
-            W[:, j1:] -= E @ L[j1:, j0:j1].T - W0 @ D[j0:j1, j1:]
+        if reach < k:
+            W[:, reach:] -= E @ L[reach:, j0:j1].T - W0 @ D[j0:j1, reach:]
         if scores_out is not None:
             scores_out.append(S.copy())
     return W * keep, keep
+
+
+def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
+                qparams_out=None, values_in=None, w0_out=None):
+    """Column sweep by definition: every column's update reaches all later
+    columns at once (see _sweep).  qparams_out (a list) receives (scale,
+    zero) arrays of shape (n,) per quantisation group.  Test hooks: values_in
+    (n x k) replaces the value every kept weight takes (as mask_in replaces
+    the mask); w0_out (n x k) receives each column's value when it was
+    processed.  Returns (W_hat, keep)."""
+    return _sweep(W, L, D, fac, p_w, B, False, mask_in, scores_out, nm, quant, qparams_out, values_in, w0_out)
+
+
+def sweep_blocked(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
+                  qparams_out=None, values_in=None, w0_out=None):
+    """Column sweep with the lazy batch update of Algorithm 1 (see _sweep):
+    one product per block carries the block's debts to the later columns.
+    Arguments as in sweep_eager; scores_out receives, per block, the scores
+    each weight's selection used.  Returns (W_hat, keep)."""
+    return _sweep(W, L, D, fac, p_w, B, True, mask_in, scores_out, nm, quant, qparams_out, values_in, w0_out)
 
 
 # ---------------------------------------------------------------------------
