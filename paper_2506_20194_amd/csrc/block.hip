@@ -50,6 +50,32 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
   for (int c = threadIdx.x; c < d; c += 256) y[c] = f32_to_bf16_bits(ld_bf16(x + c) * inv);
 }
 
+// 16-byte form (k, ldx, ldy multiples of 8, aligned rows): one workgroup row
+// of threads per token, 8 channels per thread.
+__global__ __launch_bounds__(256) void act_apply8_kernel(const uint16_t* __restrict__ X, int64_t ldx, int k,
+                                                         const int64_t* __restrict__ thr, uint16_t* __restrict__ Y,
+                                                         int64_t ldy) {
+  const int cpr = (k + 2047) / 2048;  // workgroups per token
+  const int t = (int)(blockIdx.x / cpr);
+  const int c0 = ((int)(blockIdx.x % cpr) * 256 + threadIdx.x) * 8;
+  if (c0 >= k) return;
+  const int64_t th = thr[t];
+  const u32x4 x = *(const u32x4*)(X + (int64_t)t * ldx + c0);
+  u32x4 y;
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    uint32_t o = 0;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t v = (x[h] >> (16 * j)) & 0xFFFFu;
+      const int64_t key = ((int64_t)(v & 0x7fffu) << 32) | (c0 + 2 * h + j);
+      o |= (key > th ? v : 0u) << (16 * j);
+    }
+    y[h] = o;
+  }
+  *(u32x4*)(Y + (int64_t)t * ldy + c0) = y;
+}
+
 __global__ void act_apply_kernel(const uint16_t* __restrict__ X, int64_t ldx, int m, int k,
                                  const int64_t* __restrict__ thr, uint16_t* __restrict__ Y, int64_t ldy) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -60,24 +86,55 @@ __global__ void act_apply_kernel(const uint16_t* __restrict__ X, int64_t ldx, in
   Y[(int64_t)t * ldy + c] = key > thr[t] ? x : (uint16_t)0;
 }
 
-// Thread (token, head, i) rotates the pair (i, i + d/2) of that head by
-// angle pos * theta^(-2i/d), pos = token % seq_len.  Angles in fp64.
-__global__ void rope_kernel(uint16_t* __restrict__ X, int64_t ldx, int m, int heads, int hd, int seq_len,
-                            double theta) {
+// One workgroup per token: the half = head_dim / 2 rotation angles
+// pos * theta^(-2i/head_dim) (pos = token % seq_len) and their cosines and
+// sines are computed once in fp64 and shared by every head; each thread then
+// rotates pairs (i, i + half) of the token's heads in fp32.
+__global__ __launch_bounds__(256) void rope_kernel(uint16_t* __restrict__ X, int64_t ldx, int heads, int hd,
+                                                   int seq_len, double theta) {
+  __shared__ float cs[2][256];
   const int half = hd / 2;
-  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (id >= (int64_t)m * heads * half) return;
-  const int i = (int)(id % half);
-  const int h = (int)((id / half) % heads);
-  const int t = (int)(id / ((int64_t)half * heads));
-  const double ang = (double)(t % seq_len) * pow(theta, -2.0 * (double)i / (double)hd);
-  double sd, cd;
-  sincos(ang, &sd, &cd);
-  const float s = (float)sd, c = (float)cd;
-  uint16_t* p = X + (int64_t)t * ldx + (int64_t)h * hd;
-  const float x1 = bf16_bits_to_f32(p[i]), x2 = bf16_bits_to_f32(p[i + half]);
-  p[i] = f32_to_bf16_bits(x1 * c - x2 * s);
-  p[i + half] = f32_to_bf16_bits(x2 * c + x1 * s);
+  const int t = blockIdx.x;
+  for (int i = threadIdx.x; i < half; i += 256) {
+    const double ang = (double)(t % seq_len) * pow(theta, -2.0 * (double)i / (double)hd);
+    double sd, cd;
+    sincos(ang, &sd, &cd);
+    cs[0][i] = (float)cd;
+    cs[1][i] = (float)sd;
+  }
+  __syncthreads();
+  uint16_t* row = X + (int64_t)t * ldx;
+  for (int e = threadIdx.x; e < heads * half; e += 256) {
+    const int h = e / half, i = e % half;
+    uint16_t* p = row + (int64_t)h * hd;
+    const float c = cs[0][i], s = cs[1][i];
+    const float x1 = bf16_bits_to_f32(p[i]), x2 = bf16_bits_to_f32(p[i + half]);
+    p[i] = f32_to_bf16_bits(x1 * c - x2 * s);
+    p[i + half] = f32_to_bf16_bits(x2 * c + x1 * s);
+  }
+}
+
+// 16-byte form of silu_mul_kernel (n, ld, ldy multiples of 8, aligned rows).
+__global__ __launch_bounds__(256) void silu_mul8_kernel(const uint16_t* __restrict__ G, const uint16_t* __restrict__ U,
+                                                        int64_t ld, int n, uint16_t* __restrict__ Y, int64_t ldy) {
+  const int cpr = (n + 2047) / 2048;  // workgroups per token
+  const int t = (int)(blockIdx.x / cpr);
+  const int c0 = ((int)(blockIdx.x % cpr) * 256 + threadIdx.x) * 8;
+  if (c0 >= n) return;
+  const u32x4 g = *(const u32x4*)(G + (int64_t)t * ld + c0);
+  const u32x4 u = *(const u32x4*)(U + (int64_t)t * ld + c0);
+  u32x4 y;
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    uint32_t o = 0;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const float gv = bf16_bits_to_f32((uint16_t)(g[h] >> (16 * j))), uv = bf16_bits_to_f32((uint16_t)(u[h] >> (16 * j)));
+      o |= (uint32_t)f32_to_bf16_bits(gv / (1.0f + expf(-gv)) * uv) << (16 * j);
+    }
+    y[h] = o;
+  }
+  *(u32x4*)(Y + (int64_t)t * ldy + c0) = y;
 }
 
 __global__ void silu_mul_kernel(const uint16_t* __restrict__ G, const uint16_t* __restrict__ U, int64_t ld, int m,
@@ -427,8 +484,12 @@ duo_status duo_act_sparsify(const void* X, int64_t m, int64_t k, int64_t ldx, du
   duo_status st = act_threshold_run(X, DUO_BF16, m, k, ldx, act_zeros(rule, k), thr, s);
   if (st != DUO_OK) return st;
   const int64_t tot = m * k;
-  hipLaunchKernelGGL(act_apply_kernel, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, s, (const uint16_t*)X, ldx,
-                     (int)m, (int)k, (const int64_t*)thr, (uint16_t*)Y, ldy);
+  if (k % 8 == 0 && ldx % 8 == 0 && ldy % 8 == 0 && aligned16(X) && aligned16(Y) && m * cdiv(k, 2048) <= INT32_MAX)
+    hipLaunchKernelGGL(act_apply8_kernel, dim3((unsigned)(m * cdiv(k, 2048))), dim3(256), 0, s,
+                       (const uint16_t*)X, ldx, (int)k, (const int64_t*)thr, (uint16_t*)Y, ldy);
+  else
+    hipLaunchKernelGGL(act_apply_kernel, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, s, (const uint16_t*)X, ldx,
+                       (int)m, (int)k, (const int64_t*)thr, (uint16_t*)Y, ldy);
   DUO_LAUNCH_CHECK();
   return DUO_OK;
 }
@@ -465,9 +526,8 @@ duo_status duo_rope(void* X, int64_t m, int64_t heads, int64_t head_dim, int64_t
   if (m == 0) return DUO_OK;
   if (!X || m > INT32_MAX) return DUO_ERR_INVALID_ARG;
   if (duo_status d = device_ok(); d != DUO_OK) return d;
-  const int64_t tot = m * heads * (head_dim / 2);
-  hipLaunchKernelGGL(rope_kernel, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, (hipStream_t)stream, (uint16_t*)X, ldx,
-                     (int)m, (int)heads, (int)head_dim, (int)seq_len, theta);
+  hipLaunchKernelGGL(rope_kernel, dim3((unsigned)m), dim3(256), 0, (hipStream_t)stream, (uint16_t*)X, ldx, (int)heads,
+                     (int)head_dim, (int)seq_len, theta);
   DUO_LAUNCH_CHECK();
   return DUO_OK;
 }
@@ -507,8 +567,13 @@ duo_status duo_silu_mul(const void* G, const void* U, int64_t m, int64_t n, int6
   if (!G || !U || !Y) return DUO_ERR_INVALID_ARG;
   if (duo_status d = device_ok(); d != DUO_OK) return d;
   const int64_t tot = m * n;
-  hipLaunchKernelGGL(silu_mul_kernel, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, (hipStream_t)stream,
-                     (const uint16_t*)G, (const uint16_t*)U, ld, (int)m, (int)n, (uint16_t*)Y, ldy);
+  if (n % 8 == 0 && ld % 8 == 0 && ldy % 8 == 0 && aligned16(G) && aligned16(U) && aligned16(Y) &&
+      m * cdiv(n, 2048) <= INT32_MAX)
+    hipLaunchKernelGGL(silu_mul8_kernel, dim3((unsigned)(m * cdiv(n, 2048))), dim3(256), 0,
+                       (hipStream_t)stream, (const uint16_t*)G, (const uint16_t*)U, ld, (int)n, (uint16_t*)Y, ldy);
+  else
+    hipLaunchKernelGGL(silu_mul_kernel, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, (hipStream_t)stream,
+                       (const uint16_t*)G, (const uint16_t*)U, ld, (int)m, (int)n, (uint16_t*)Y, ldy);
   DUO_LAUNCH_CHECK();
   return DUO_OK;
 }

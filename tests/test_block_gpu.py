@@ -123,9 +123,10 @@ def test_attention(duo, nseq, L, heads, hd):
     assert relfro(f64(o), ref) < 2.0 ** -8
 
 
-def test_silu_mul(duo):
-    say("silu_mul")
-    g, u = bf((70, 352), 8, 3.0), bf((70, 352), 9)
+@pytest.mark.parametrize("n", [352, 350])
+def test_silu_mul(duo, n):
+    say("silu_mul", n)
+    g, u = bf((70, n), 8, 3.0), bf((70, n), 9)
     ok, e = close(f64(duo.duo_silu_mul(g.to(DEV), u.to(DEV))), BR.silu_mul(g.double().numpy(), u.double().numpy()))
     assert ok, e
 
