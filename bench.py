@@ -454,10 +454,15 @@ def main():
 
     per = lambda name: prof[name][0] / max(prof[name][1], 1)     # ms per launch
     per_step = lambda name: prof[name][0] / args.steps              # ms per layer
-    gram_flop_step = (k * (k + 1) + 2 * k * k) * m                  # H lower triangle + G
+    # Stage 1's algorithmic work: H on and above its diagonal, k(k+1)/2 dot
+    # products over m tokens (2 flop per multiply-add), and the part of G the
+    # solver reads, likewise its upper triangle (Eq. 7 uses Q = G L only on and
+    # above its diagonal); all of G (2 k^2 m) with act_order, which permutes it
+    g_flop = 2 * k * k * m if args.act_order else k * (k + 1) * m
+    gram_flop_step = k * (k + 1) * m + g_flop
     gram_launches = prof["gram"][1] / args.steps
     gram_tflops = gram_flop_step / gram_launches / (per("gram") * 1e-3) / 1e12
-    hess_flop = (3 * k * k + k) * m
+    hess_flop = gram_flop_step
     hess_tflops = hess_flop / (per_step("hessian") * 1e-3) / 1e12
     sweep_bytes = 16 * n * k
     sweep_ms = per_step("select") + per_step("inblock")

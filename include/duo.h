@@ -79,6 +79,17 @@ typedef struct {
   double sparsity; /* p^x in [0, 1] */
 } duo_act_rule;
 
+/* Which part of G stage 1 accumulates (duo_hessian_accum, duo_residual_term).
+ * The solver reads only G's upper triangle, diagonal included: Eq. 7 uses
+ * Q = G L only on and above its diagonal (U = strict upper(Q), c = diag(Q) /
+ * diag(L)), and with L lower triangular Q[p][i], i >= p, involves G[p][l]
+ * for l >= i >= p alone.  DUO_G_UPPER accumulates those entries (about half
+ * of G's work): G[p][q] for p / 256 <= q / 256, i.e. the upper triangle plus
+ * the lower halves of the 256 x 256 diagonal tiles, and leaves every other
+ * entry as it was; DUO_G_FULL accumulates all of G (needed when the channels
+ * are permuted afterwards, as for act_order). */
+enum { DUO_G_UPPER = 0, DUO_G_FULL = 1 };
+
 /* operations, for duo_workspace_size */
 enum {
   DUO_OP_HESSIAN = 0,     /* duo_hessian_accum and duo_residual_term (uses m, k) */
@@ -126,6 +137,9 @@ duo_status duo_act_sparsify_mask(const void* X, int32_t x_dtype, int64_t m, int6
  *            exactly symmetric.
  *   G, a     optional (both NULL or both set): G += dX^T Xh with dX = X_dense - Xh,
  *            a[p] += sum_t dX[t][p]^2.  G is k x k fp32 with row stride ldg.
+ *   g_part   DUO_G_UPPER: G[p][q] for p / 256 <= q / 256 (the upper triangle
+ *            the solver reads, plus the rest of the diagonal 256 x 256 tiles);
+ *            DUO_G_FULL: all of G.
  *   hdiag    NULL or k doubles: hdiag[p] += sum_t Xh[t][p]^2 summed in fp64
  *            (each square exact), the diagonal of H at the precision that
  *            decides the act_order channel order (duo_act_order).
@@ -138,7 +152,7 @@ duo_status duo_act_sparsify_mask(const void* X, int32_t x_dtype, int64_t m, int6
  */
 duo_status duo_hessian_accum(const void* X_src, const void* X_dense, int32_t x_dtype, int64_t m,
                              int64_t k, int64_t ldx, duo_act_rule rule, float* H, int64_t ldh,
-                             float* G, int64_t ldg, float* a, double* hdiag, void* ws,
+                             float* G, int64_t ldg, int32_t g_part, float* a, double* hdiag, void* ws,
                              size_t ws_bytes, void* stream);
 
 /*
@@ -161,7 +175,7 @@ duo_status duo_hessian_status(const void* ws, size_t ws_bytes, void* stream);
  */
 duo_status duo_residual_term(const void* X_dense, const void* X_src, int32_t x_dtype, int64_t m,
                              int64_t k, int64_t ldx, duo_act_rule rule, float* G, int64_t ldg,
-                             float* a, void* ws, size_t ws_bytes, void* stream);
+                             int32_t g_part, float* a, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * duo_chol_inv - stage 2 (Sec. 4.3 Hessian synchronisation; Algorithm 1
@@ -184,7 +198,8 @@ duo_status duo_chol_inv(float* H_inout, int64_t k, int64_t ldh, double damp_rati
 /*
  * duo_score_terms - stage 3 precompute (Eq. 7; App. A.3-A.4; Algorithm 1
  *   lines Q, U, a, b, c, D).
- *   L (ldl, strictly upper triangle zero), G (ldg), a (k) -> D (k x k, ldd)
+ *   L (ldl, strictly upper triangle zero), G (ldg; only its upper triangle,
+ *   diagonal included, is read), a (k) -> D (k x k, ldd)
  *   and fac (k):  Q = G L, U = strict upper(Q), b = diag(U U^T),
  *   c = diag(Q) / diag(L), D = U L^T (strictly upper; its lower triangle and
  *   diagonal are written as 0 inside the diagonal 128 x 128 tiles and are not

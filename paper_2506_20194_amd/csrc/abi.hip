@@ -156,8 +156,10 @@ duo_status duo_act_sparsify_mask(const void* X, int32_t x_dtype, int64_t m, int6
 
 static duo_status hessian_common(const void* X_src, const void* X_dense, int32_t x_dtype, int64_t m, int64_t k,
                                  int64_t ldx, duo_act_rule rule, float* H, int64_t ldh, float* G, int64_t ldg,
-                                 float* a, double* hdiag, void* ws, size_t ws_bytes, void* stream, bool want_h) {
+                                 int32_t g_part, float* a, double* hdiag, void* ws, size_t ws_bytes, void* stream,
+                                 bool want_h) {
   if (!dtype_ok(x_dtype) || m < 0 || !rule_ok(rule)) return DUO_ERR_INVALID_ARG;
+  if (g_part != DUO_G_UPPER && g_part != DUO_G_FULL) return DUO_ERR_INVALID_ARG;
   if (!k_ok(k)) return k < 1 ? DUO_ERR_INVALID_ARG : DUO_ERR_UNSUPPORTED;
   if (ldx < k) return DUO_ERR_INVALID_ARG;
   if (want_h && (!H || ldh < k)) return DUO_ERR_INVALID_ARG;
@@ -171,27 +173,27 @@ static duo_status hessian_common(const void* X_src, const void* X_dense, int32_t
   duo_status d = device_ok();
   if (d != DUO_OK) return d;
   prof_begin(DUO_PROF_HESSIAN, (hipStream_t)stream);
-  duo_status r = hessian_run(X_src, X_dense, x_dtype, m, k, ldx, zero_count(rule, k), H, ldh, G, ldg, a, hdiag,
-                             ws, want_h, (hipStream_t)stream);
+  duo_status r = hessian_run(X_src, X_dense, x_dtype, m, k, ldx, zero_count(rule, k), H, ldh, G, ldg,
+                             g_part == DUO_G_FULL ? 1 : 0, a, hdiag, ws, want_h, (hipStream_t)stream);
   prof_end(DUO_PROF_HESSIAN, (hipStream_t)stream);
   return r;
 }
 
 duo_status duo_hessian_accum(const void* X_src, const void* X_dense, int32_t x_dtype, int64_t m, int64_t k,
-                             int64_t ldx, duo_act_rule rule, float* H, int64_t ldh, float* G, int64_t ldg, float* a,
-                             double* hdiag, void* ws, size_t ws_bytes, void* stream) {
-  return hessian_common(X_src, X_dense, x_dtype, m, k, ldx, rule, H, ldh, G, ldg, a, hdiag, ws, ws_bytes, stream,
-                        true);
+                             int64_t ldx, duo_act_rule rule, float* H, int64_t ldh, float* G, int64_t ldg,
+                             int32_t g_part, float* a, double* hdiag, void* ws, size_t ws_bytes, void* stream) {
+  return hessian_common(X_src, X_dense, x_dtype, m, k, ldx, rule, H, ldh, G, ldg, g_part, a, hdiag, ws, ws_bytes,
+                        stream, true);
 }
 
 duo_status duo_residual_term(const void* X_dense, const void* X_src, int32_t x_dtype, int64_t m, int64_t k,
-                             int64_t ldx, duo_act_rule rule, float* G, int64_t ldg, float* a, void* ws,
+                             int64_t ldx, duo_act_rule rule, float* G, int64_t ldg, int32_t g_part, float* a, void* ws,
                              size_t ws_bytes, void* stream) {
   if (!G || !a) return DUO_ERR_INVALID_ARG;
   if (m > 0 && !X_dense) return DUO_ERR_INVALID_ARG;
   const void* src = X_src ? X_src : X_dense;
-  return hessian_common(src, X_dense, x_dtype, m, k, ldx, rule, nullptr, k, G, ldg, a, nullptr, ws, ws_bytes, stream,
-                        false);
+  return hessian_common(src, X_dense, x_dtype, m, k, ldx, rule, nullptr, k, G, ldg, g_part, a, nullptr, ws, ws_bytes,
+                        stream, false);
 }
 
 duo_status duo_hessian_status(const void* ws, size_t ws_bytes, void* stream) {

@@ -14,6 +14,8 @@
 //   reductions  fixed-order sums of per-segment partials (deterministic).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "internal.h"
 
@@ -752,6 +754,7 @@ struct GramArgs {
   const T* Pl;  // packed low part of dX (two bf16 streams), else unused
   int kp, k, nt;     // padded channels, channels, kp / 256
   int nh, ntiles;    // H tiles (0 when H is not wanted) and H + G tiles
+  int g_full;        // G tiles: all nt x nt (1) or the upper triangle I <= J (0)
   int nseg, seg_len, ntb;
   float* H;
   int64_t ldh;
@@ -766,10 +769,14 @@ struct GramArgs {
 // call), G tiles all of G.  Within each kind, bands of 4 blocks
 // are walked across, so neighbouring ids share operand tiles; the
 // XCD remap below gives each XCD a contiguous id range (and so its own L2 set).
-__device__ inline void gram_tile(int t, int nh, int nt, int* isg, int* I, int* J) {
+__device__ inline void gram_tile(int t, int nh, int nt, int g_full, int* isg, int* I, int* J) {
   constexpr int GB = 4;
-  if (t < nh) {  // upper triangle of nt x nt (I <= J), bands of GB columns
-    *isg = 0;
+  // H tiles, and G tiles when only G's upper triangle is wanted, walk the
+  // upper triangle of nt x nt (I <= J) in bands of GB columns
+  const bool tri = t < nh || !g_full;
+  *isg = t < nh ? 0 : 1;
+  if (t >= nh && tri) t -= nh;
+  if (tri) {
     // enumerated as the lower triangle (bands of GB rows), then transposed
     int* const tmp = I;
     I = J;
@@ -800,7 +807,6 @@ __device__ inline void gram_tile(int t, int nh, int nt, int* isg, int* I, int* J
     return;
   }
   t -= nh;
-  *isg = 1;
   const int b0 = (t / (GB * nt)) * GB;
   const int h = min(GB, nt - b0);
   const int r = t - b0 * nt;
@@ -892,7 +898,7 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
   const int seg = u / A.ntiles;
   const int tile = u % A.ntiles;
   int isg, I, J;
-  gram_tile(tile, A.nh, A.nt, &isg, &I, &J);
+  gram_tile(tile, A.nh, A.nt, A.g_full, &isg, &I, &J);
   const int tb0 = seg * A.seg_len;
   const int tb1 = min(A.ntb, tb0 + A.seg_len);
 
@@ -1115,7 +1121,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void gram_reduce_kernel(GramArgs<T> A) {
   const int tile = blockIdx.x;
   int isg, I, J;
-  gram_tile(tile, A.nh, A.nt, &isg, &I, &J);
+  gram_tile(tile, A.nh, A.nt, A.g_full, &isg, &I, &J);
   const int sr = (blockIdx.y >> 2) * 64, sc = (blockIdx.y & 3) * 64;
   const int64_t stride = (int64_t)A.ntiles * GT * GT;
   const float* p0 = A.part + (int64_t)tile * GT * GT;
@@ -1293,8 +1299,10 @@ static HessWs carve_hessian(void* ws, int64_t m, int64_t k) {
   const int64_t kp = rup(k, GT);
   const int64_t tokp = rup(ch, 256);
   const int64_t T = kp / GT;
-  const int64_t ntiles = T * (T + 1) / 2 + T * T;
-  const int nseg = gram_split(ntiles, ch, kp);
+  // partial tiles: enough for either G form (all of G, or its upper triangle)
+  const int64_t nt_full = T * (T + 1) / 2 + T * T, nt_up = T * (T + 1);
+  const int64_t part_tiles = std::max(gram_split(nt_full, ch, kp) > 1 ? gram_split(nt_full, ch, kp) * nt_full : 0,
+                                      gram_split(nt_up, ch, kp) > 1 ? gram_split(nt_up, ch, kp) * nt_up : 0);
   Carver c(ws);
   HessWs h;
   h.flags = c.take<uint32_t>(64);
@@ -1303,7 +1311,7 @@ static HessWs carve_hessian(void* ws, int64_t m, int64_t k) {
   h.Pz = c.take<uint8_t>((size_t)tokp * kp * 4);
   h.Pl = c.take<uint8_t>((size_t)tokp * kp * 2);  // low part exists for bf16 only
   h.apart = c.take<float>((size_t)(tokp / 256) * kp);
-  h.part = c.take<float>(nseg > 1 ? (size_t)nseg * ntiles * GT * GT : 1);
+  h.part = c.take<float>(part_tiles > 0 ? (size_t)part_tiles * GT * GT : 1);
   h.dpart = c.take<double>((size_t)diag_slices(kp, kDiagSlices) * kp);
   h.bytes = c.off;
   return h;
@@ -1336,8 +1344,8 @@ static duo_status launch_gram(const GramArgs<T>& A, hipStream_t s) {
 
 template <typename T>
 static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, int64_t ldx, int z, float* H,
-                                int64_t ldh, float* G, int64_t ldg, float* a, double* hdiag, void* ws, bool want_h,
-                                hipStream_t s) {
+                                int64_t ldh, float* G, int64_t ldg, int g_full, float* a, double* hdiag, void* ws,
+                                bool want_h, hipStream_t s) {
   const bool want_g = G != nullptr;
   const bool two = Xd != nullptr && Xd != Xs;
   const bool lo = two && sizeof(T) == 2;
@@ -1346,7 +1354,8 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
   const int64_t kp = rup(k, GT);
   const int nt = (int)(kp / GT);
   const int nh_all = nt * (nt + 1) / 2;
-  const int nseg = gram_split(nh_all + nt * nt, ch, kp);  // the same split the workspace was sized for
+  const int ng = want_g ? (g_full ? nt * nt : nh_all) : 0;
+  const int nseg = gram_split((want_h ? nh_all : 0) + ng, ch, kp);  // within what the workspace was sized for
   hipLaunchKernelGGL(clear_flags_kernel, dim3(1), dim3(64), 0, s, w.flags);
   DUO_LAUNCH_CHECK();
   for (int64_t t0 = 0; t0 < m; t0 += ch) {
@@ -1406,7 +1415,8 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
     A.k = (int)k;
     A.nt = nt;
     A.nh = want_h ? nh_all : 0;
-    A.ntiles = A.nh + (want_g ? nt * nt : 0);
+    A.ntiles = A.nh + ng;
+    A.g_full = g_full;
     A.nseg = nseg;
     A.ntb = (int)cdiv(mc, kTokBlk);
     A.seg_len = (int)cdiv(A.ntb, nseg);
@@ -1440,12 +1450,12 @@ static duo_status hessian_typed(const T* Xs, const T* Xd, int64_t m, int64_t k, 
 }
 
 duo_status hessian_run(const void* Xs, const void* Xd, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z,
-                       float* H, int64_t ldh, float* G, int64_t ldg, float* a, double* hdiag, void* ws, bool want_h,
-                       hipStream_t s) {
+                       float* H, int64_t ldh, float* G, int64_t ldg, int g_full, float* a, double* hdiag, void* ws,
+                       bool want_h, hipStream_t s) {
   if (dtype == DUO_BF16)
-    return hessian_typed<uint16_t>((const uint16_t*)Xs, (const uint16_t*)Xd, m, k, ldx, z, H, ldh, G, ldg, a,
+    return hessian_typed<uint16_t>((const uint16_t*)Xs, (const uint16_t*)Xd, m, k, ldx, z, H, ldh, G, ldg, g_full, a,
                                    hdiag, ws, want_h, s);
-  return hessian_typed<float>((const float*)Xs, (const float*)Xd, m, k, ldx, z, H, ldh, G, ldg, a, hdiag, ws,
+  return hessian_typed<float>((const float*)Xs, (const float*)Xd, m, k, ldx, z, H, ldh, G, ldg, g_full, a, hdiag, ws,
                               want_h, s);
 }
 

@@ -14,8 +14,8 @@ int64_t hessian_chunk_tokens(int64_t m, int64_t k);
 int gram_split(int64_t ntiles, int64_t ch, int64_t kp);
 size_t hessian_ws_bytes(int64_t m, int64_t k);
 duo_status hessian_run(const void* Xs, const void* Xd, int32_t dtype, int64_t m, int64_t k, int64_t ldx, int z,
-                       float* H, int64_t ldh, float* G, int64_t ldg, float* a, double* hdiag, void* ws, bool want_h,
-                       hipStream_t s);
+                       float* H, int64_t ldh, float* G, int64_t ldg, int g_full, float* a, double* hdiag, void* ws,
+                       bool want_h, hipStream_t s);
 // DUO_ERR_NONFINITE when the last stage-1 call on this workspace met a NaN or
 // inf input (waits for the stream), else DUO_OK.
 duo_status hessian_status_run(const void* ws, hipStream_t s);

@@ -22,6 +22,7 @@ DUO_ERR_NOT_PD, DUO_ERR_NONFINITE, DUO_ERR_HIP, DUO_ERR_NO_DEVICE = 4, 5, 6, 7
 DUO_F32, DUO_BF16 = 0, 1
 DUO_ACT_NONE, DUO_ACT_TOPK_MAG_PER_TOKEN = 0, 1
 DUO_OP_HESSIAN, DUO_OP_CHOL_INV, DUO_OP_SCORE_TERMS, DUO_OP_SWEEP, DUO_OP_PRUNE_LAYER = 0, 1, 2, 3, 4
+DUO_G_UPPER, DUO_G_FULL = 0, 1
 
 EXPORTED = (
     "duo_workspace_size", "duo_status_string", "duo_version", "duo_act_sparsify_mask",
@@ -78,11 +79,11 @@ def lib():
         L.duo_act_sparsify_mask.restype = I32
         L.duo_act_sparsify_mask.argtypes = [P, I32, I64, I64, I64, ActRule, P, P, SZ, P]
         L.duo_hessian_accum.restype = I32
-        L.duo_hessian_accum.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, I64, P, P, P, SZ, P]
+        L.duo_hessian_accum.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, I64, I32, P, P, P, SZ, P]
         L.duo_hessian_status.restype = I32
         L.duo_hessian_status.argtypes = [P, SZ, P]
         L.duo_residual_term.restype = I32
-        L.duo_residual_term.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, P, P, SZ, P]
+        L.duo_residual_term.argtypes = [P, P, I32, I64, I64, I64, ActRule, P, I64, I32, P, P, SZ, P]
         L.duo_chol_inv.restype = I32
         L.duo_chol_inv.argtypes = [P, I64, I64, F64, ctypes.POINTER(CholInfo), P, SZ, P]
         L.duo_score_terms.restype = I32
@@ -217,9 +218,15 @@ def duo_act_sparsify_mask(X, act_sparsity, mask_out=None, ws=None):
     return mask_out
 
 
-def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=None, hdiag=None, check=False):
+def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=None, hdiag=None, check=False,
+                      g_full=None):
     """Stage 1 (H, and G and a when given).  check=True waits for the stream
-    and raises DuoError(DUO_ERR_NONFINITE) if the inputs held NaN or inf."""
+    and raises DuoError(DUO_ERR_NONFINITE) if the inputs held NaN or inf.
+    g_full: accumulate all of G (True) or only its upper triangle, diagonal
+    included, which is all the solver reads (False); by default all of G
+    exactly when hdiag is given (act_order permutes G afterwards)."""
+    if g_full is None:
+        g_full = hdiag is not None
     m, k = X_src.shape
     _same_device(X_src, X_dense, H, G, a, ws, hdiag)
     _shape(H, (k, k), "H")
@@ -235,14 +242,15 @@ def duo_hessian_accum(X_src, H, act_sparsity, X_dense=None, G=None, a=None, ws=N
     if X_dense is not None and (X_dense.shape != X_src.shape or X_dense.stride() != X_src.stride()):
         raise ValueError("X_dense must have the shape and strides of X_src")
     st = lib().duo_hessian_accum(_ptr(X_src), _ptr(X_dense), _dtype(X_src), m, k, _ld(X_src), act_rule(act_sparsity),
-                                 _ptr(H), _ld(H), _ptr(G), _ld(G) if G is not None else k, _ptr(a), _ptr(hdiag),
+                                 _ptr(H), _ld(H), _ptr(G), _ld(G) if G is not None else k,
+                                 DUO_G_FULL if g_full else DUO_G_UPPER, _ptr(a), _ptr(hdiag),
                                  _ptr(ws), ws.numel(), _stream(X_src.device))
     _check(st, "duo_hessian_accum")
     if check and m > 0:
         _check(lib().duo_hessian_status(_ptr(ws), ws.numel(), _stream(X_src.device)), "duo_hessian_accum")
 
 
-def duo_residual_term(X_dense, G, a, act_sparsity, X_src=None, ws=None):
+def duo_residual_term(X_dense, G, a, act_sparsity, X_src=None, ws=None, g_full=False):
     m, k = X_dense.shape
     _same_device(X_dense, X_src, G, a, ws)
     _shape(X_src, (m, k), "X_src")
@@ -254,7 +262,8 @@ def duo_residual_term(X_dense, G, a, act_sparsity, X_src=None, ws=None):
     if ws is None:
         ws = workspace(DUO_OP_HESSIAN, 0, k, m, 0, X_dense.device)
     st = lib().duo_residual_term(_ptr(X_dense), _ptr(X_src), _dtype(X_dense), m, k, _ld(X_dense),
-                                 act_rule(act_sparsity), _ptr(G), _ld(G), _ptr(a), _ptr(ws), ws.numel(),
+                                 act_rule(act_sparsity), _ptr(G), _ld(G), DUO_G_FULL if g_full else DUO_G_UPPER,
+                                 _ptr(a), _ptr(ws), ws.numel(),
                                  _stream(X_dense.device))
     _check(st, "duo_residual_term")
 

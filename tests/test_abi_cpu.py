@@ -65,8 +65,8 @@ def test_hessian_argument_errors(duo_lib):
     big = 10 ** 10
 
     def call(X=FAKE, Xd=None, dt=1, m=64, k=32, ldx=32, rule=None, H=FAKE, ldh=32, G=None, ldg=32, a=None, ws=WS,
-             wsb=big, hdiag=None):
-        return L.duo_hessian_accum(X, Xd, dt, m, k, ldx, rule or _rule(), H, ldh, G, ldg, a, hdiag, ws, wsb, None)
+             wsb=big, hdiag=None, gp=0):
+        return L.duo_hessian_accum(X, Xd, dt, m, k, ldx, rule or _rule(), H, ldh, G, ldg, gp, a, hdiag, ws, wsb, None)
 
     assert call() == NODEV
     assert call(X=None) == E
@@ -87,8 +87,12 @@ def test_hessian_argument_errors(duo_lib):
     assert call(ws=ctypes.c_void_p((256 << 20) + 8)) == duo_lib.DUO_ERR_WORKSPACE
     assert call(m=0) == duo_lib.DUO_OK           # nothing to do, nothing enqueued
     assert call(hdiag=FAKE) == NODEV
-    assert L.duo_residual_term(None, None, 1, 64, 32, 32, _rule(), FAKE, 32, FAKE, WS, big, None) == E
-    assert L.duo_residual_term(FAKE, None, 1, 64, 32, 32, _rule(), FAKE, 32, FAKE, WS, big, None) == NODEV
+    assert call(G=FAKE, a=FAKE, gp=1) == NODEV   # all of G
+    assert call(G=FAKE, a=FAKE, gp=2) == E       # no such G part
+    assert L.duo_residual_term(None, None, 1, 64, 32, 32, _rule(), FAKE, 32, 0, FAKE, WS, big, None) == E
+    assert L.duo_residual_term(FAKE, None, 1, 64, 32, 32, _rule(), FAKE, 32, 0, FAKE, WS, big, None) == NODEV
+    assert L.duo_residual_term(FAKE, None, 1, 64, 32, 32, _rule(), FAKE, 32, 1, FAKE, WS, big, None) == NODEV
+    assert L.duo_residual_term(FAKE, None, 1, 64, 32, 32, _rule(), FAKE, 32, 2, FAKE, WS, big, None) == E
 
 
 def test_chol_and_sweep_argument_errors(duo_lib):

@@ -8,7 +8,8 @@ hold at any size:
 
 * activation masks bit-exact on sampled tokens (the oracle's per-token rule);
 * H and G on a sampled set of channels (random channels plus a trailing
-  window), and all of a and diag(H), summed by the oracle over every token;
+  window; G on and above its diagonal, the part stage 1 accumulates), and
+  all of a and diag(H), summed by the oracle over every token;
   fp32 sums of exact bf16 products: each entry within 4e-5 * sqrt(H_ii H_jj)
   (resp. sqrt(a_i H_jj)), the worst-case relative error of a recursive fp32
   sum of ~600 partial sums (u = 6e-8);
@@ -244,7 +245,11 @@ def test_fullsize_stage1_entries(run):
     bound = tol * np.outer(dH, dH) + 1e-30
     assert np.all(np.abs(run["H_s"] - ref["H"]) <= bound), float(np.max(np.abs(run["H_s"] - ref["H"]) / bound))
     bound_G = tol * np.outer(np.sqrt(ref["a"][idx]), dH) + 1e-30
-    assert np.all(np.abs(run["G_s"] - ref["G"]) <= bound_G), float(np.max(np.abs(run["G_s"] - ref["G"]) / bound_G))
+    # stage 1 accumulates G on and above its diagonal 256-tiles (all the solver reads); below them G stays zero
+    up = idx[:, None] // 256 <= idx[None, :] // 256
+    errG = np.where(up, np.abs(run["G_s"] - ref["G"]), 0.0)
+    assert np.all(errG <= bound_G), float(np.max(errG / bound_G))
+    assert np.all(run["G_s"][~up] == 0.0)
     assert np.all(np.abs(run["a"] - ref["a"]) <= tol * ref["a"] + 1e-30)
     assert np.all(np.abs(run["diag"] - ref["diag"]) <= tol * ref["diag"] + 1e-30)
 

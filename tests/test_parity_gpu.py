@@ -69,29 +69,40 @@ def test_act_mask_bit_exact(duo, dtype, m, k, p_x):
     assert np.array_equal(mask, keep)
 
 
-def _check_gram(H, G, a, Hr, Gr, ar, tol):
+def _check_gram(H, G, a, Hr, Gr, ar, tol, g_full=False):
+    """H and a against the oracle; G on the entries stage 1 accumulates
+    without g_full (p / 256 <= q / 256: its upper triangle and the diagonal
+    256 x 256 tiles), the rest left as the caller set it (zero), or all of G
+    with g_full.  H is returned exactly symmetric (its lower triangle mirrors
+    the upper one)."""
     dH = np.sqrt(np.maximum(np.diag(Hr), 0))
     bound_H = tol * np.outer(dH, dH) + 1e-30
     assert np.all(np.abs(H - Hr) <= bound_H), float(np.max(np.abs(H - Hr) / bound_H))
+    assert np.array_equal(H, H.T)
     if G is not None:
         bound_G = tol * np.outer(np.sqrt(np.maximum(ar, 0)), dH) + 1e-30
-        assert np.all(np.abs(G - Gr) <= bound_G), float(np.max(np.abs(G - Gr) / bound_G))
+        tb = np.arange(G.shape[0]) // 256
+        part = np.ones_like(G, dtype=bool) if g_full else tb[:, None] <= tb[None, :]
+        err = np.where(part, np.abs(G - Gr), 0.0)
+        assert np.all(err <= bound_G), float(np.max(err / bound_G))
+        assert np.all(G[~part] == 0.0)
         assert np.all(np.abs(a - ar) <= tol * ar + 1e-30)
 
 
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
-@pytest.mark.parametrize("m,k", [(1000, 300), (4096, 512), (2500, 640), (33, 130)])
-def test_hessian_terms(duo, dtype, m, k):
-    say("hessian", dtype, m, k)
+@pytest.mark.parametrize("m,k", [(1000, 300), (4096, 512), (2500, 640), (33, 130), (600, 1800)])
+@pytest.mark.parametrize("g_full", [False, True])
+def test_hessian_terms(duo, dtype, m, k, g_full):
+    say("hessian", dtype, m, k, g_full)
     _, X = inputs(1, k, m, dtype, seed=3 * k + m, outliers=2)
     Xd = X.to(DEV)
     H = torch.zeros((k, k), device=DEV)
     G = torch.zeros((k, k), device=DEV)
     a = torch.zeros(k, device=DEV)
-    duo.duo_hessian_accum(Xd, H, 0.5, G=G, a=a)
+    duo.duo_hessian_accum(Xd, H, 0.5, G=G, a=a, g_full=g_full)
     torch.cuda.synchronize()
     Hr, Gr, ar = R.hessian_terms(X.float().numpy(), 0.5)
-    _check_gram(f64(H), f64(G), f64(a), Hr, Gr, ar, 2e-5)
+    _check_gram(f64(H), f64(G), f64(a), Hr, Gr, ar, 2e-5, g_full)
 
 
 def test_hessian_accumulates_over_chunks(duo):
@@ -119,14 +130,17 @@ def test_two_stream_residual(duo, dtype):
     H = torch.zeros((k, k), device=DEV)
     G = torch.zeros((k, k), device=DEV)
     a = torch.zeros(k, device=DEV)
-    duo.duo_hessian_accum(Xs_.to(DEV), H, 0.5, X_dense=Xd_.to(DEV), G=G, a=a)
+    duo.duo_hessian_accum(Xs_.to(DEV), H, 0.5, X_dense=Xd_.to(DEV), G=G, a=a, g_full=True)
     Hr, Gr, ar = R.hessian_terms(Xs_.float().numpy(), 0.5, Xd_.float().numpy())
-    _check_gram(f64(H), f64(G), f64(a), Hr, Gr, ar, 2e-5 if dtype == torch.float32 else 6e-5)
-    # the residual-only entry point gives the same G and a
-    G2 = torch.zeros((k, k), device=DEV)
-    a2 = torch.zeros(k, device=DEV)
-    duo.duo_residual_term(Xd_.to(DEV), G2, a2, 0.5, X_src=Xs_.to(DEV))
-    assert torch.equal(G2, G) and torch.equal(a2, a)
+    _check_gram(f64(H), f64(G), f64(a), Hr, Gr, ar, 2e-5 if dtype == torch.float32 else 6e-5, g_full=True)
+    # the residual-only entry point gives the same G and a, in either form
+    for g_full in (True, False):
+        G2 = torch.zeros((k, k), device=DEV)
+        a2 = torch.zeros(k, device=DEV)
+        duo.duo_residual_term(Xd_.to(DEV), G2, a2, 0.5, X_src=Xs_.to(DEV), g_full=g_full)
+        assert torch.equal(a2, a)
+        tb = torch.arange(k, device=DEV) // 256
+        assert torch.equal(G2, G if g_full else torch.where(tb[:, None] <= tb[None, :], G, 0.0))
 
 
 # ---------------------------------------------------------------------------
