@@ -282,8 +282,10 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmDesc d, int ntiles) {
 // operands (every DuoGPT product at k a multiple of 128): A row-major (K
 // contiguous); B either K-contiguous (b_row = 0, "NT") or row-major (b_row = 1,
 // "NN").  128 x 128 tile, 2 x 2 waves of 64 x 64, K staged 16 at a time
-// through a ring of four 16 KB LDS stages filled by direct global->LDS loads
-// (no register staging), three stages in flight.
+// through a ring of FNS LDS stages filled by direct global->LDS loads (no
+// register staging), FNS - 1 stages in flight.  Three workgroups share a CU
+// (48 KB of LDS each, 112 VGPRs), so while one waits at a stage barrier or for
+// its fragment reads the other two keep the matrix core busy.
 //
 // K order inside a stage: MFMA step s (of 4) takes k = 4g + s in lane group g,
 // so that a K-contiguous operand's fragment for all four steps is one 16-byte
@@ -297,17 +299,26 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmDesc d, int ntiles) {
 //     read disjoint bank groups.
 // ---------------------------------------------------------------------------
 constexpr int FK = 16;                 // K per stage
-constexpr int FNS = 4;                 // ring depth
+constexpr int FNS = 3;                 // ring depth
+constexpr int FOCC = 3;                // workgroups per CU
+constexpr int FEP = 64;                // tile rows per epilogue pass
 constexpr int FOP = kTile * FK * 4;    // bytes per operand per stage (8 KB)
 constexpr int FSTAGE = 2 * FOP;        // 16 KB
 
+template <int N>
+__device__ __forceinline__ void wait_vm_n() {
+  // vmcnt N (bits 3:0 and 15:14), expcnt and lgkmcnt not waited for
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
 __device__ __forceinline__ void wait_vm(int n) {
-  // at most n of this wave's vector-memory operations outstanding (n <= 12)
-  switch (n) {
-    case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-    case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
-    case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
-    default: __builtin_amdgcn_s_waitcnt(0x0F7C); break;  // 12
+  // at most n of this wave's vector-memory operations outstanding (n a
+  // multiple of 4, at most 12)
+  static_assert(4 * (FNS - 2) <= 12, "ring depth");
+  switch (n >> 2) {
+    case 0: wait_vm_n<0>(); break;
+    case 1: wait_vm_n<4>(); break;
+    case 2: wait_vm_n<8>(); break;
+    default: wait_vm_n<12>(); break;
   }
 }
 
@@ -398,7 +409,7 @@ __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* sme
 }
 
 template <bool B1R, bool B2R, bool TWO>
-__global__ __launch_bounds__(256, 2) void gemm_fast_kernel(GemmDesc d, int ntiles) {
+__global__ __launch_bounds__(256, FOCC) void gemm_fast_kernel(GemmDesc d, int ntiles) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];  // FNS stages; reused by the epilogue
   const int id = d.order == ORDER_XCD ? xcd_remap_g(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   if (id >= ntiles) return;
@@ -421,30 +432,36 @@ __global__ __launch_bounds__(256, 2) void gemm_fast_kernel(GemmDesc d, int ntile
   fast_term<B1R>(d.t[0], i0, j0, smem, acc);
   if (TWO) fast_term<B2R>(d.t[1], i0, j0, smem, acc);
 
-  // epilogue through LDS: C = beta C + acc with coalesced 16-byte accesses
+  // epilogue through LDS: C = beta C + acc with coalesced 16-byte accesses,
+  // FEP rows of the tile per pass (the waves holding them stage them)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wi = wave >> 1, wj = wave & 1;
-  constexpr int LS = kTile + 4;  // kTile * LS floats: the dynamic LDS is sized for it
+  constexpr int LS = kTile + 4;  // FEP * LS floats: the dynamic LDS is sized for it
   float* st = (float*)smem;
-  lds_barrier();
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int e0 = 0; e0 < kTile; e0 += FEP) {
+    lds_barrier();
+    if (wi * 64 >= e0 && wi * 64 < e0 + FEP) {
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+      for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        st[(wi * 64 + a * 16 + (lane >> 4) * 4 + r) * LS + wj * 64 + b * 16 + (lane & 15)] = acc[a][b][r];
-  lds_barrier();
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            st[(wi * 64 - e0 + a * 16 + (lane >> 4) * 4 + r) * LS + wj * 64 + b * 16 + (lane & 15)] = acc[a][b][r];
+    }
+    lds_barrier();
 #pragma unroll 4
-  for (int q = tid; q < kTile * kTile / 4; q += 256) {
-    const int r = q >> 5, c4 = (q & 31) * 4;
-    const float4 v = *(const float4*)&st[r * LS + c4];
-    float4* cp = (float4*)(d.C + (int64_t)(i0 + r) * d.ldc + j0 + c4);
-    if (d.beta != 0.f) {
-      const float4 c = *cp;
-      *cp = make_float4(d.beta * c.x + v.x, d.beta * c.y + v.y, d.beta * c.z + v.z, d.beta * c.w + v.w);
-    } else {
-      *cp = v;
+    for (int q = tid; q < FEP * kTile / 4; q += 256) {
+      const int r = q >> 5, c4 = (q & 31) * 4;
+      const float4 v = *(const float4*)&st[r * LS + c4];
+      float4* cp = (float4*)(d.C + (int64_t)(i0 + e0 + r) * d.ldc + j0 + c4);
+      if (d.beta != 0.f) {
+        const float4 c = *cp;
+        *cp = make_float4(d.beta * c.x + v.x, d.beta * c.y + v.y, d.beta * c.z + v.z, d.beta * c.w + v.w);
+      } else {
+        *cp = v;
+      }
     }
   }
 }
@@ -455,8 +472,9 @@ __global__ __launch_bounds__(256, 2) void gemm_fast_kernel(GemmDesc d, int ntile
 // wave (measured at k = 4096 and 11008: 2048 beats 512, 1024 and 4096).
 constexpr int kSmallTiles = 2048;
 
-constexpr size_t kFastLds = (size_t)kTile * (kTile + 4) * 4;  // >= FNS * FSTAGE (epilogue image)
-static_assert(kFastLds >= (size_t)FNS * FSTAGE, "fast-path LDS");
+constexpr size_t kFastEpi = (size_t)FEP * (kTile + 4) * 4;  // epilogue image
+constexpr size_t kFastLds = (size_t)FNS * FSTAGE > kFastEpi ? (size_t)FNS * FSTAGE : kFastEpi;
+static_assert(kFastLds * FOCC <= 160 * 1024, "fast-path LDS");
 
 // Whether every tile of a 128-tile launch can take the fast path: interior
 // tiles, 16-byte aligned operands and rows, K ranges in whole stages.
