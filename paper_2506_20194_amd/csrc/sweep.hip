@@ -621,6 +621,10 @@ __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* 
     s.e[g] = u * b.il;
     s.w0[g] = v;
   }
+  // materialise the owner's record here: left to itself the compiler keeps
+  // every step's u and 1 / L_JJ to the end of the block (about 350 registers,
+  // most of them AGPR spill slots)
+  asm volatile("" : "+v"(s.e[g]), "+v"(s.w0[g]));
   // columns c = q + 16 i > J; the LDS entries of columns <= J are zero
 #pragma unroll
   for (int i = g; i < IB_I; ++i) s.w[i] = fmaf(-u, b.l[i], fmaf(v, b.d[i], s.w[i]));

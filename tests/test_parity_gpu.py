@@ -275,6 +275,45 @@ def test_sweep_select(duo, n, k, B, p_w):
         assert relfro(f64(W_out), Wr) < 1e-5
 
 
+@pytest.mark.parametrize("n,k,B,p_w", [(200, 336, 128, 0.5), (300, 1152, 128, 0.55), (150, 640, 64, 0.5),
+                                       (90, 544, 16, 0.45), (4200, 256, 128, 0.5), (8200, 128, 128, 0.6),
+                                       (50, 160, 32, 0.0), (40, 96, 16, 1.0)])
+def test_sweep_select_shapes(duo, n, k, B, p_w):
+    """Rows and the last block ragged, several 512-column super-blocks, 8 and
+    32 blocks per super-block, row counts of several selection workgroups'
+    batches, and no or every weight pruned."""
+    say("sweep select shapes", n, k, B, p_w)
+    W, X, L, D, fac = _sweep_inputs(n, k, 3 * k, seed=5 * n + k)
+    Wr, keep_r = R.sweep_blocked(W.float().numpy(), L, D, fac, p_w, B)
+    t = lambda x: torch.tensor(x, device=DEV)
+    W_out, _, mask, _ = duo.duo_sweep(W.to(DEV), t(L), t(D), t(fac), p_w, B)
+    keep = duo.unpack_mask(mask, k).cpu().numpy()
+    assert np.isfinite(f64(W_out)).all()
+    assert (~keep).sum() == (~keep_r).sum()
+    assert np.mean(keep == keep_r) >= 0.999
+    _attribute(W.float().numpy(), L, D, fac, p_w, B, keep)
+    if np.array_equal(keep, keep_r):
+        assert relfro(f64(W_out), Wr) < 1e-5, relfro(f64(W_out), Wr)
+
+
+def test_sweep_ties_large_bucket(duo):
+    """A bucket of equal scores larger than the gathered-candidate capacity
+    (the threshold is then resolved from the block itself); ties broken by
+    (column, row)."""
+    say("sweep ties, large bucket")
+    n, k, B = 1024, 256, 128
+    W = torch.ones((n, k), dtype=torch.float32)
+    W[::3] = 2.0
+    L = np.eye(k, dtype=np.float32)
+    D = np.zeros((k, k), dtype=np.float32)
+    fac = np.ones(k, dtype=np.float32)
+    Wr, keep_r = R.sweep_blocked(W.numpy(), L, D, fac, 0.5, B)
+    t = lambda x: torch.tensor(x, device=DEV)
+    W_out, _, mask, _ = duo.duo_sweep(W.to(DEV), t(L), t(D), t(fac), 0.5, B)
+    assert np.array_equal(duo.unpack_mask(mask, k).cpu().numpy(), keep_r)
+    assert np.array_equal(f64(W_out), Wr)
+
+
 def test_sweep_ties(duo):
     """Many exactly equal scores: ties are broken by (column, row)."""
     say("sweep ties")
