@@ -23,17 +23,17 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3    # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
-# HBM bytes per gram_kernel launch on this workload, from rocprofv3 --pmc
-# FETCH_SIZE and WRITE_SIZE runs (profiles/gram_kernel_llama2_7b_q_proj_hbm_traffic.md),
+# Bytes from beyond L2 per gram_kernel launch on this workload, from rocprofv3
+# --pmc FETCH_SIZE and WRITE_SIZE runs (profiles/gram_kernel_llama2_70b_down_proj_hbm_traffic.md),
 # each scaled by what the same counter reads for a plain 1 GiB streaming kernel
 # (FETCH_SIZE x2.0, WRITE_SIZE x1.0).  Valid only for the kernel source they
 # were taken on: any change to that file makes the figure unknown (null).
 GRAM_TRAFFIC = {
     "source": "paper_2506_20194_amd/csrc/hessian.hip",
-    "sha256": "60702a9709114ffbd979095fc530239ab6658a4846d88e84fd5f204a0c550aa6",
-    "workload": "llama2_7b_q_proj",
-    "fetch_kib": 5611819.7, "fetch_scale": 2.0,
-    "write_kib": 502103.3, "write_scale": 1.0,
+    "sha256": "66f9a165d6f3b0b7d772fcf53b2d9e8a33fda939c4a172896ab0f6806bd8a34f",
+    "workload": "llama2_70b_down_proj",
+    "fetch_kib": 205590067.8, "fetch_scale": 2.0,
+    "write_kib": 3239936.0, "write_scale": 1.0,
 }
 
 
