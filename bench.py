@@ -475,6 +475,9 @@ def main():
     # Cholesky, full products) and is printed beside it
     chol_score_flop = 4 * k ** 3 / 3
     chol_score_flop_plain = 8 * k ** 3 / 3
+    # the Gram kernel multiplies in the calibration input's precision: bf16
+    # MFMA for bf16 inputs, fp32 MFMA for fp32 inputs
+    gram_peak = PEAK_BF16_TFLOPS if c["x_dtype"] == torch.bfloat16 else PEAK_FP32_TFLOPS
     line = {
         "metric": "s/layer for OBC prune of LLaMA-shaped linears; Hessian TFLOP/s; sweep GB/s",
         "value": ms_step / 1e3,
@@ -486,7 +489,7 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 MFMA (H, G) + fp32",
+        "dtype": ("bf16" if gram_peak == PEAK_BF16_TFLOPS else "fp32") + " MFMA (H, G) + fp32",
         "data": "synthetic",
         "config": {"workload": args.workload, "n": n, "k": k, "m": m, "p_x": c["p_x"], "p_w": c["p_w"],
                    "block": B, "damp": c["damp"], "x_dtype": str(c["x_dtype"]).replace("torch.", ""),
@@ -494,10 +497,10 @@ def main():
                    "mask": f"{args.nm}:4" if args.nm else "unstructured",
                    "quant": f"int{args.quant} g128" if args.quant else None, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "gram_kernel (H, G)", "achieved": gram_tflops,
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": gram_tflops / PEAK_BF16_TFLOPS,
+                     "peak": gram_peak, "unit": "TFLOP/s", "frac": gram_tflops / gram_peak,
                      "traffic": gram_traffic(args.workload), "ms_per_launch": per("gram"), "flop_per_launch": gram_flop_step / gram_launches},
         "hessian_tflops": hess_tflops,
-        "hessian_frac": hess_tflops / PEAK_BF16_TFLOPS,
+        "hessian_frac": hess_tflops / gram_peak,
         "sweep_gbs": sweep_gbs,
         "sweep_frac": sweep_gbs / PEAK_HBM_GBS,
         "trailing_tflops": trail_tflops,
