@@ -281,29 +281,42 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmDesc d, int ntiles) {
 // Fast path for launches whose tiles all lie inside M x N with 16-byte aligned
 // operands (every DuoGPT product at k a multiple of 128): A row-major (K
 // contiguous); B either K-contiguous (b_row = 0, "NT") or row-major (b_row = 1,
-// "NN").  128 x 128 tile, 2 x 2 waves of 64 x 64, K staged 16 at a time
-// through a ring of FNS LDS stages filled by direct global->LDS loads (no
-// register staging), FNS - 1 stages in flight.  Three workgroups share a CU
-// (48 KB of LDS each, 112 VGPRs), so while one waits at a stage barrier or for
-// its fragment reads the other two keep the matrix core busy.
+// "NN").  TF x TF tile (128, or 64 for launches too small to fill the chip),
+// 2 x 2 waves of TF/2 x TF/2, K staged 16 at a time through a ring of LDS stages
+// filled by direct global->LDS loads (no register staging), all but one
+// stage in flight.  The 128 tile needs 112 VGPRs and 48 KB of LDS, so three
+// workgroups share a CU (the 64 tile: 24 KB, five): while one waits at a
+// stage barrier or for its fragment reads, the others keep the matrix core
+// busy.
 //
 // K order inside a stage: MFMA step s (of 4) takes k = 4g + s in lane group g,
 // so that a K-contiguous operand's fragment for all four steps is one 16-byte
 // chunk (k = 4g .. 4g + 3) per lane.  Both operands use the same order, so
 // the sum is unchanged.  Layouts (16-byte chunks):
-//   K-contiguous operand, 128 lines x 4 chunks: chunk c of line r at
+//   K-contiguous operand, TF lines x 4 chunks: chunk c of line r at
 //     r * 4 + (c ^ ((r >> 2) & 3)), so the 16 lines of a fragment read hit 16
 //     distinct bank groups;
-//   row-major B, 16 k-rows x 32 chunks: chunk c of row k at
-//     k * 32 + (c ^ (4 * ((k >> 2) & 3))), so the four lane groups (k four apart)
-//     read disjoint bank groups.
+//   row-major B, 16 k-rows x TF/4 chunks: chunk c of row k at
+//     k * TF/4 + (c ^ (4 * ((k >> 2) & 3))), so the four lane groups (k four
+//     apart) read disjoint bank groups.
 // ---------------------------------------------------------------------------
 constexpr int FK = 16;                 // K per stage
-constexpr int FNS = 3;                 // ring depth
-constexpr int FOCC = 3;                // workgroups per CU
 constexpr int FEP = 64;                // tile rows per epilogue pass
-constexpr int FOP = kTile * FK * 4;    // bytes per operand per stage (8 KB)
-constexpr int FSTAGE = 2 * FOP;        // 16 KB
+
+template <int TF>
+struct FGeo {
+  static constexpr int OP = TF * FK * 4;  // bytes per operand per stage
+  static constexpr int STAGE = 2 * OP;
+  static constexpr int Q = TF / 64;       // 16-byte chunks per thread per operand per stage
+  static constexpr int NB = TF / 32;      // 16 x 16 blocks per wave and dimension
+  static constexpr int HW = TF / 2;       // wave tile edge
+  static constexpr int NS = TF == kTile ? 3 : 3;   // ring depth (stages)
+  static constexpr int OCC = TF == kTile ? 3 : 5;  // workgroups per CU
+  static constexpr size_t EPI = (size_t)FEP * (TF + 4) * 4;
+  static constexpr size_t LDS = (size_t)NS * STAGE > EPI ? (size_t)NS * STAGE : EPI;
+  static_assert(2 * Q * (NS - 2) <= 8, "loads in flight beyond wait_vm's range");
+  static_assert(LDS * OCC <= 160 * 1024, "fast-path LDS");
+};
 
 template <int N>
 __device__ __forceinline__ void wait_vm_n() {
@@ -311,52 +324,58 @@ __device__ __forceinline__ void wait_vm_n() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 __device__ __forceinline__ void wait_vm(int n) {
-  // at most n of this wave's vector-memory operations outstanding (n a
-  // multiple of 4, at most 12)
-  static_assert(4 * (FNS - 2) <= 12, "ring depth");
-  switch (n >> 2) {
+  // at most n of this wave's vector-memory operations outstanding (n <= 8)
+  switch (n) {
     case 0: wait_vm_n<0>(); break;
-    case 1: wait_vm_n<4>(); break;
-    case 2: wait_vm_n<8>(); break;
-    default: wait_vm_n<12>(); break;
+    case 1: wait_vm_n<1>(); break;
+    case 2: wait_vm_n<2>(); break;
+    case 3: wait_vm_n<3>(); break;
+    case 4: wait_vm_n<4>(); break;
+    case 5: wait_vm_n<5>(); break;
+    case 6: wait_vm_n<6>(); break;
+    case 7: wait_vm_n<7>(); break;
+    default: wait_vm_n<8>(); break;
   }
 }
 
-template <bool BR>
-__device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* smem, f4 (&acc)[4][4]) {
-  const int64_t klo = lo_of<kTile>(t.klo, i0, j0);
-  const int64_t khi = hi_of<kTile>(t.khi, i0, j0, t.K);
+template <int TF, bool BR>
+__device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* smem,
+                                 f4 (&acc)[FGeo<TF>::NB][FGeo<TF>::NB]) {
+  using G = FGeo<TF>;
+  constexpr int NB = G::NB, Q = G::Q, CPR = TF / 4;  // CPR: chunks per row-major B row
+  const int64_t klo = lo_of<TF>(t.klo, i0, j0);
+  const int64_t khi = hi_of<TF>(t.khi, i0, j0, t.K);
   if (klo >= khi) return;
   const int nst = (int)((khi - klo) / FK);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wi = wave >> 1, wj = wave & 1;
-  // this lane's two chunks of each operand per stage (wave-wide loads 2w, 2w + 1)
-  const float* ga[2];
-  const float* gb[2];
-  uint32_t la[2], lb[2];
+  // this lane's Q chunks of each operand per stage (wave-wide loads Q w .. Q w + Q - 1)
+  const float* ga[Q];
+  const float* gb[Q];
+  uint32_t la[Q], lb[Q];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int pos = (2 * wave + q) * 64 + lane;  // 16-byte position in the operand's stage image
+  for (int q = 0; q < Q; ++q) {
+    const int pos = (Q * wave + q) * 64 + lane;  // 16-byte position in the operand's stage image
     {
       const int r = pos >> 2, c = (pos & 3) ^ ((r >> 2) & 3);
       ga[q] = t.A + (int64_t)(i0 + r) * t.lda + klo + 4 * c;
     }
     if (BR) {
-      const int k = pos >> 5, c = (pos & 31) ^ (4 * ((k >> 2) & 3));
+      const int k = pos / CPR, c = (pos % CPR) ^ (4 * ((k >> 2) & 3));
       gb[q] = t.B + (klo + k) * t.ldb + j0 + 4 * c;
     } else {
       const int r = pos >> 2, c = (pos & 3) ^ ((r >> 2) & 3);
       gb[q] = t.B + (int64_t)(j0 + r) * t.ldb + klo + 4 * c;
     }
-    la[q] = (uint32_t)((2 * wave + q) * 64 * 16);
-    lb[q] = (uint32_t)(FOP + (2 * wave + q) * 64 * 16);
+    la[q] = (uint32_t)((Q * wave + q) * 64 * 16);
+    lb[q] = (uint32_t)(G::OP + (Q * wave + q) * 64 * 16);
   }
   const int64_t da = FK, db = BR ? (int64_t)FK * t.ldb : FK;  // element step per stage
   const float alpha = t.alpha;
   auto issue = [&](int st) {
-    uint8_t* base = smem + (st % FNS) * FSTAGE;
+    uint8_t* base = smem + (st % G::NS) * G::STAGE;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < Q; ++q) {
       __builtin_amdgcn_global_load_lds((const void*)(ga[q] + st * da),
                                        (__attribute__((address_space(3))) void*)(base + la[q]), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)(gb[q] + st * db),
@@ -365,25 +384,25 @@ __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* sme
   };
   const int g = lane >> 4, l16 = lane & 15;
   auto compute = [&](int st) {
-    const u32x4* sa = (const u32x4*)(smem + (st % FNS) * FSTAGE);
-    const uint8_t* sbb = smem + (st % FNS) * FSTAGE + FOP;
-    float av[4][4], bv[4][4];  // [block][step]
+    const u32x4* sa = (const u32x4*)(smem + (st % G::NS) * G::STAGE);
+    const uint8_t* sbb = smem + (st % G::NS) * G::STAGE + G::OP;
+    float av[NB][4], bv[NB][4];  // [block][step]
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const int r = wi * 64 + a * 16 + l16;
+    for (int a = 0; a < NB; ++a) {
+      const int r = wi * G::HW + a * 16 + l16;
       const u32x4 v = sa[r * 4 + (g ^ ((r >> 2) & 3))];
 #pragma unroll
       for (int s2 = 0; s2 < 4; ++s2) av[a][s2] = alpha * __uint_as_float(v[s2]);
     }
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int col = wj * 64 + b * 16 + l16;
+    for (int b = 0; b < NB; ++b) {
+      const int col = wj * G::HW + b * 16 + l16;
       if (BR) {
         const float* sb = (const float*)sbb;
 #pragma unroll
         for (int s2 = 0; s2 < 4; ++s2) {
           const int k = 4 * g + s2;
-          bv[b][s2] = sb[k * 128 + (((col >> 2) ^ (4 * ((k >> 2) & 3))) << 2) + (col & 3)];
+          bv[b][s2] = sb[k * TF + (((col >> 2) ^ (4 * ((k >> 2) & 3))) << 2) + (col & 3)];
         }
       } else {
         const u32x4 v = ((const u32x4*)sbb)[col * 4 + (g ^ ((col >> 2) & 3))];
@@ -394,23 +413,28 @@ __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* sme
 #pragma unroll
     for (int s2 = 0; s2 < 4; ++s2)
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int a = 0; a < NB; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a][s2], bv[b][s2], acc[a][b], 0, 0, 0);
+        for (int b = 0; b < NB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a][s2], bv[b][s2], acc[a][b], 0, 0, 0);
   };
   lds_barrier();  // the previous user of the ring (an earlier term) is done with it
-  for (int st = 0; st < min(nst, FNS - 1); ++st) issue(st);
+  for (int st = 0; st < min(nst, G::NS - 1); ++st) issue(st);
   for (int st = 0; st < nst; ++st) {
-    wait_vm(4 * min(FNS - 2, nst - 1 - st));  // stage st landed (this wave's part)
-    lds_barrier();                            // every wave's part landed; stage st - 1 is free
-    if (st + FNS - 1 < nst) issue(st + FNS - 1);
+    wait_vm(2 * Q * min(G::NS - 2, nst - 1 - st));  // stage st landed (this wave's part)
+    lds_barrier();                                // every wave's part landed; stage st - 1 is free
+    if (st + G::NS - 1 < nst) issue(st + G::NS - 1);
     compute(st);
   }
 }
 
-template <bool B1R, bool B2R, bool TWO>
-__global__ __launch_bounds__(256, FOCC) void gemm_fast_kernel(GemmDesc d, int ntiles) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];  // FNS stages; reused by the epilogue
+// Tiles are enumerated on the 128 grid (the triangular filters and the tile
+// orders are defined there); with TF = 64 each 128 tile is split into its
+// four quarters, which are consecutive ids (a quarter outside M x N exits).
+template <int TF, bool B1R, bool B2R, bool TWO>
+__global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc d, int ntiles) {
+  using G = FGeo<TF>;
+  constexpr int NB = G::NB, SUB = kTile / TF;
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];  // the ring; reused by the epilogue
   const int id = d.order == ORDER_XCD ? xcd_remap_g(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   if (id >= ntiles) return;
   if (blockIdx.y) {
@@ -421,39 +445,43 @@ __global__ __launch_bounds__(256, FOCC) void gemm_fast_kernel(GemmDesc d, int nt
     d.t[1].A += z * d.sA[1];
     d.t[1].B += z * d.sB[1];
   }
+  const int pid = id / (SUB * SUB), sub = id % (SUB * SUB);
   int ti, tj;
-  tile_of(d, id, &ti, &tj);
-  const int i0 = ti * kTile, j0 = tj * kTile;
-  f4 acc[4][4];
+  tile_of(d, pid, &ti, &tj);
+  const int i0 = ti * kTile + (sub / SUB) * TF, j0 = tj * kTile + (sub % SUB) * TF;
+  if (i0 >= d.M || j0 >= d.N) return;
+  f4 acc[NB][NB];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < NB; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
-  fast_term<B1R>(d.t[0], i0, j0, smem, acc);
-  if (TWO) fast_term<B2R>(d.t[1], i0, j0, smem, acc);
+    for (int b = 0; b < NB; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
+  fast_term<TF, B1R>(d.t[0], i0, j0, smem, acc);
+  if (TWO) fast_term<TF, B2R>(d.t[1], i0, j0, smem, acc);
 
   // epilogue through LDS: C = beta C + acc with coalesced 16-byte accesses,
   // FEP rows of the tile per pass (the waves holding them stage them)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wi = wave >> 1, wj = wave & 1;
-  constexpr int LS = kTile + 4;  // FEP * LS floats: the dynamic LDS is sized for it
+  constexpr int LS = TF + 4;  // FEP * LS floats: the dynamic LDS is sized for it
+  constexpr int CPR = TF / 4;
   float* st = (float*)smem;
 #pragma unroll
-  for (int e0 = 0; e0 < kTile; e0 += FEP) {
+  for (int e0 = 0; e0 < TF; e0 += FEP) {
     lds_barrier();
-    if (wi * 64 >= e0 && wi * 64 < e0 + FEP) {
+    if (wi * G::HW >= e0 && wi * G::HW < e0 + FEP) {
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int a = 0; a < NB; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            st[(wi * 64 - e0 + a * 16 + (lane >> 4) * 4 + r) * LS + wj * 64 + b * 16 + (lane & 15)] = acc[a][b][r];
+            st[(wi * G::HW - e0 + a * 16 + (lane >> 4) * 4 + r) * LS + wj * G::HW + b * 16 + (lane & 15)] =
+                acc[a][b][r];
     }
     lds_barrier();
 #pragma unroll 4
-    for (int q = tid; q < FEP * kTile / 4; q += 256) {
-      const int r = q >> 5, c4 = (q & 31) * 4;
+    for (int q = tid; q < FEP * TF / 4; q += 256) {
+      const int r = q / CPR, c4 = (q % CPR) * 4;
       const float4 v = *(const float4*)&st[r * LS + c4];
       float4* cp = (float4*)(d.C + (int64_t)(i0 + e0 + r) * d.ldc + j0 + c4);
       if (d.beta != 0.f) {
@@ -472,14 +500,11 @@ __global__ __launch_bounds__(256, FOCC) void gemm_fast_kernel(GemmDesc d, int nt
 // wave (measured at k = 4096 and 11008: 2048 beats 512, 1024 and 4096).
 constexpr int kSmallTiles = 2048;
 
-constexpr size_t kFastEpi = (size_t)FEP * (kTile + 4) * 4;  // epilogue image
-constexpr size_t kFastLds = (size_t)FNS * FSTAGE > kFastEpi ? (size_t)FNS * FSTAGE : kFastEpi;
-static_assert(kFastLds * FOCC <= 160 * 1024, "fast-path LDS");
-
-// Whether every tile of a 128-tile launch can take the fast path: interior
-// tiles, 16-byte aligned operands and rows, K ranges in whole stages.
+// Whether every TF tile of a launch can take the fast path: interior tiles,
+// 16-byte aligned operands and rows, K ranges in whole stages.
+template <int TF>
 bool fast_ok(const GemmDesc& d) {
-  if (d.M % kTile != 0 || d.N % kTile != 0 || (d.ldc & 3) != 0 || (reinterpret_cast<uintptr_t>(d.C) & 15) != 0)
+  if (d.M % TF != 0 || d.N % TF != 0 || (d.ldc & 3) != 0 || (reinterpret_cast<uintptr_t>(d.C) & 15) != 0)
     return false;
   for (int i = 0; i < d.nterms; ++i) {
     const GemmTerm& t = d.t[i];
@@ -491,11 +516,11 @@ bool fast_ok(const GemmDesc& d) {
   return true;
 }
 
-template <bool B1R, bool B2R, bool TWO>
-duo_status launch_fast(const GemmDesc& d, int ntiles, int nb, hipStream_t s) {
-  auto kern = gemm_fast_kernel<B1R, B2R, TWO>;
-  if (duo_status st = set_max_lds((const void*)kern, kFastLds); st != DUO_OK) return st;
-  hipLaunchKernelGGL(kern, dim3((unsigned)rup(ntiles, 8), nb), dim3(256), kFastLds, s, d, ntiles);
+template <int TF, bool B1R, bool B2R, bool TWO>
+duo_status launch_fast(const GemmDesc& d, int ids, int nb, hipStream_t s) {
+  auto kern = gemm_fast_kernel<TF, B1R, B2R, TWO>;
+  if (duo_status st = set_max_lds((const void*)kern, FGeo<TF>::LDS); st != DUO_OK) return st;
+  hipLaunchKernelGGL(kern, dim3((unsigned)rup(ids, 8), nb), dim3(256), FGeo<TF>::LDS, s, d, ids);
   DUO_LAUNCH_CHECK();
   return DUO_OK;
 }
@@ -507,7 +532,11 @@ duo_status launch(const GemmDesc& d, hipStream_t s) {
   if (ntiles <= 0) return DUO_OK;
   const int nb = d.batch > 1 ? d.batch : 1;
   if constexpr (A1R && A2R) {
-    if ((int64_t)ntiles * nb >= kSmallTiles && fast_ok(d)) return launch_fast<B1R, B2R, TWO>(d, ntiles, nb, s);
+    if ((int64_t)ntiles * nb >= kSmallTiles) {
+      if (fast_ok<kTile>(d)) return launch_fast<kTile, B1R, B2R, TWO>(d, ntiles, nb, s);
+    } else if (fast_ok<64>(d)) {
+      return launch_fast<64, B1R, B2R, TWO>(d, 4 * ntiles, nb, s);
+    }
   }
   if ((int64_t)ntiles * nb < kSmallTiles) {
     const int grid = (int)rup(4 * ntiles, 8);
