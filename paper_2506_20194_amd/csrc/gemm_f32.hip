@@ -459,14 +459,30 @@ __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc 
   if (TWO) fast_term<TF, B2R>(d.t[1], i0, j0, smem, acc);
 
   // epilogue through LDS: C = beta C + acc with coalesced 16-byte accesses,
-  // FEP rows of the tile per pass (the waves holding them stage them)
+  // FEP rows of the tile per pass (the waves holding them stage them).  Every
+  // read of C is issued before the staging starts, so the tile waits for one
+  // memory latency rather than one per batch of loads.
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wi = wave >> 1, wj = wave & 1;
   constexpr int LS = TF + 4;  // FEP * LS floats: the dynamic LDS is sized for it
   constexpr int CPR = TF / 4;
+  constexpr int NP = TF / FEP, QPT = FEP * TF / 4 / 256;  // passes, 16-byte pieces per thread and pass
+  static_assert(QPT * 256 * 4 == FEP * TF, "epilogue split");
+  float4 cv[NP][QPT];
+  const bool keep_c = d.beta != 0.f;
+  if (keep_c) {
+#pragma unroll
+    for (int e = 0; e < NP; ++e)
+#pragma unroll
+      for (int i = 0; i < QPT; ++i) {
+        const int q = tid + 256 * i, r = q / CPR, c4 = (q % CPR) * 4;
+        cv[e][i] = *(const float4*)(d.C + (int64_t)(i0 + e * FEP + r) * d.ldc + j0 + c4);
+      }
+  }
   float* st = (float*)smem;
 #pragma unroll
-  for (int e0 = 0; e0 < TF; e0 += FEP) {
+  for (int e = 0; e < NP; ++e) {
+    const int e0 = e * FEP;
     lds_barrier();
     if (wi * G::HW >= e0 && wi * G::HW < e0 + FEP) {
 #pragma unroll
@@ -479,17 +495,15 @@ __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc 
                 acc[a][b][r];
     }
     lds_barrier();
-#pragma unroll 4
-    for (int q = tid; q < FEP * TF / 4; q += 256) {
-      const int r = q / CPR, c4 = (q % CPR) * 4;
-      const float4 v = *(const float4*)&st[r * LS + c4];
-      float4* cp = (float4*)(d.C + (int64_t)(i0 + e0 + r) * d.ldc + j0 + c4);
-      if (d.beta != 0.f) {
-        const float4 c = *cp;
-        *cp = make_float4(d.beta * c.x + v.x, d.beta * c.y + v.y, d.beta * c.z + v.z, d.beta * c.w + v.w);
-      } else {
-        *cp = v;
+#pragma unroll
+    for (int i = 0; i < QPT; ++i) {
+      const int q = tid + 256 * i, r = q / CPR, c4 = (q % CPR) * 4;
+      float4 v = *(const float4*)&st[r * LS + c4];
+      if (keep_c) {
+        const float4 c = cv[e][i];
+        v = make_float4(d.beta * c.x + v.x, d.beta * c.y + v.y, d.beta * c.z + v.z, d.beta * c.w + v.w);
       }
+      *(float4*)(d.C + (int64_t)(i0 + e0 + r) * d.ldc + j0 + c4) = v;
     }
   }
 }
