@@ -13,6 +13,7 @@ import argparse
 import json
 import os
 import platform
+import statistics
 import sys
 import time
 
@@ -68,8 +69,8 @@ def gram_traffic(workload, t=None):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama2_70b_down_proj")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probes", action="store_true", help="skip the measured-peak probes")
@@ -422,17 +423,20 @@ def main():
     torch.cuda.synchronize()
     # the timed steps carry no per-kernel events; a second, profiled pass of
     # the same steps gives the stage split and the Gram kernel's launch time
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    # one event at every step boundary (markers on the stream, no kernel is
+    # touched): the mean over the K steps is the reported time, the median of
+    # the per-step times is reported beside it
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    e0.record()
-    for _ in range(args.steps):
+    ev[0].record()
+    for i in range(args.steps):
         step()
-    e1.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms_step = e0.elapsed_time(e1) / args.steps
+    ms_step = ev[0].elapsed_time(ev[-1]) / args.steps
+    ms_step_median = float(statistics.median(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)))
     duo.duo_profile_enable(True)
     for name in duo.PROF:
         duo.duo_profile_read(name)
@@ -510,6 +514,7 @@ def main():
         "chol_score_flop_count": "(4/3) k^3 (implemented route); plain route (8/3) k^3 gives "
                                  f"{chol_score_flop_plain / ((per_step('chol') + per_step('score')) * 1e-3) / 1e12:.1f} TFLOP/s",
         "stage_ms": {name: per_step(name) for name in duo.PROF},
+        "ms_per_step_median": ms_step_median,
         "ms_per_step_with_stage_events": ms_step_profiled,
         "wall_s_timed": wall,
         "lambda": lam,
