@@ -213,6 +213,15 @@ __device__ inline int xcd_remap_g(int b, int nblocks) {
 __device__ inline void tile_of(const GemmDesc& d, int pid, int* ti, int* tj) {
   if (d.tri == TRI_ALL) {
     const int tn = (int)cdiv(d.N, kTile);
+    if (d.order == ORDER_PLAIN && d.t[0].khi == KHI_COL && d.t[0].klo == KLO_ZERO) {
+      // K range [0, j0 + 128): by columns, from the last (the longest) down.
+      // (Row by row, the workgroups that share a CU in a launch of a few
+      // waves, 256 ids apart, all held tiles of one column.)
+      const int tm = (int)cdiv(d.M, kTile);
+      *tj = tn - 1 - pid / tm;
+      *ti = pid % tm;
+      return;
+    }
     *ti = pid / tn;
     *tj = pid % tn;
   } else if (d.tri == TRI_LOWER) {

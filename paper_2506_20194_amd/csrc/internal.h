@@ -65,7 +65,9 @@ struct GemmDesc {
   // tile order: ORDER_XCD gives each XCD a contiguous range of tiles (operand
   // reuse in its L2; for tiles of equal cost); ORDER_PLAIN deals tiles to the
   // XCDs round-robin in enumeration order (for upper tiles: by column, i.e.
-  // the longest first when the K range shrinks with the column); ORDER_DIAG
+  // the longest first when the K range shrinks with the column; for all tiles
+  // with a K range that grows with the column: by column from the last, else
+  // by row); ORDER_DIAG
   // (upper tiles only) deals them by decreasing distance from the diagonal
   // (the longest first when the K range grows with that distance)
   int order;
