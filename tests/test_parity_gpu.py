@@ -153,7 +153,10 @@ def _oracle_stage(k, m, seed, p_x=0.5, damp=0.01, dtype=torch.bfloat16):
     return X, H, G, a
 
 
-@pytest.mark.parametrize("k", [1, 100, 128, 300, 512, 1000])
+# 576 and 1344: the 64-tile products with 128-grid tiles half outside the
+# matrix, a ragged last group of diagonal blocks and a merge level with a tail
+# node; 2048: merges over several column tiles of the 128 grid
+@pytest.mark.parametrize("k", [1, 100, 128, 300, 512, 576, 1000, 1344, 2048])
 def test_chol_inv(duo, k):
     say("chol_inv", k)
     # k = 1 with p_x = 0.5 drops the only channel (H = 0): use dense input there
@@ -193,7 +196,7 @@ def test_chol_inv_reports_not_pd(duo):
     assert e.value.status == duo.DUO_ERR_NOT_PD
 
 
-@pytest.mark.parametrize("k", [64, 300, 512, 700])
+@pytest.mark.parametrize("k", [64, 300, 512, 576, 700, 1344])
 def test_score_terms(duo, k):
     say("score_terms", k)
     _, H, G, a = _oracle_stage(k, 4 * k, seed=2 * k)
@@ -277,7 +280,10 @@ def test_sweep_select(duo, n, k, B, p_w):
 
 @pytest.mark.parametrize("n,k,B,p_w", [(200, 336, 128, 0.5), (300, 1152, 128, 0.55), (150, 640, 64, 0.5),
                                        (90, 544, 16, 0.45), (4200, 256, 128, 0.5), (8200, 128, 128, 0.6),
-                                       (50, 160, 32, 0.0), (40, 96, 16, 1.0)])
+                                       (50, 160, 32, 0.0), (40, 96, 16, 1.0),
+                                       # n, k multiples of 64 but not of 128: the trailing
+                                       # products on 64 tiles with 128-grid tiles half outside
+                                       (192, 576, 128, 0.5), (320, 1728, 64, 0.5)])
 def test_sweep_select_shapes(duo, n, k, B, p_w):
     """Rows and the last block ragged, several 512-column super-blocks, 8 and
     32 blocks per super-block, row counts of several selection workgroups'
