@@ -78,7 +78,9 @@ __global__ __launch_bounds__(256) void damp_kernel(float* H, int64_t ldh, int k,
 //   panel    V_IJ = A_IJ N_JJ^T for the leaves I < J, and beside it the
 //            finished inverse blocks N_JK = -N_JJ T_JK for K > J;
 //   update   A_II' -= V_IJ V_I'J^T for I <= I' < J, and beside it
-//            T_IK += V_IJ N_JK for I < J <= K,
+//            T_IK += V_IJ N_JK for I < J <= K; wave 0 takes the update of
+//            the next leaf's own block and then factors that leaf while the
+//            other three waves do the rest of the update,
 // so that T_JK = sum_{L=J+1..K} V_JL N_LK is complete when leaf J is done
 // (block back substitution N_JK = -N_JJ T_JK folded into the factorisation's
 // own steps).  T_IK lives in the block (K, I) below the diagonal, which the
@@ -201,24 +203,27 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
   if (tid == 0) *fail_sh = -1;
   __syncthreads();
   constexpr int NB = kTile / LF;
+  // leaf J: wave 0 factors and inverts the diagonal block J in registers
+  auto leaf = [&](int J) {
+    const int j0 = J * LF;
+    const int q = lane & (LF - 1);
+    int fail = -1;
+    float x[LF];
+#pragma unroll
+    for (int i = 0; i < LF; ++i) x[i] = A[(j0 + i) * DS + j0 + q];
+    leaf_steps(x, q, fail, std::make_integer_sequence<int, LF>{});
+    if (lane < LF) {
+      int qs = q;
+      asm volatile("" : "+v"(qs));  // no hoisted per-row masks
+#pragma unroll
+      for (int i = 0; i < LF; ++i) N[(j0 + i) * DS + j0 + qs] = i <= qs ? x[i] : 0.f;
+    }
+    if (lane == 0 && fail >= 0 && *fail_sh < 0) *fail_sh = j0 + fail;
+  };
+  if (wave == 0) leaf(NB - 1);
+  __syncthreads();
   for (int J = NB - 1; J >= 0; --J) {
     const int j0 = J * LF;
-    if (wave == 0) {
-      const int q = lane & (LF - 1);
-      int fail = -1;
-      float x[LF];
-#pragma unroll
-      for (int i = 0; i < LF; ++i) x[i] = A[(j0 + i) * DS + j0 + q];
-      leaf_steps(x, q, fail, std::make_integer_sequence<int, LF>{});
-      if (lane < LF) {
-        int qs = q;
-        asm volatile("" : "+v"(qs));  // no hoisted per-row masks
-#pragma unroll
-        for (int i = 0; i < LF; ++i) N[(j0 + i) * DS + j0 + qs] = i <= qs ? x[i] : 0.f;
-      }
-      if (lane == 0 && fail >= 0 && *fail_sh < 0) *fail_sh = j0 + fail;
-    }
-    __syncthreads();
     // NB - 1 products, one per wave: the panel V_IJ = A_IJ N_JJ^T for I < J
     // (in place: only this wave reads A_IJ at this step), and the finished
     // blocks N_JK = -N_JJ T_JK for K > J
@@ -236,23 +241,35 @@ __global__ __launch_bounds__(256) void diag_factor_kernel(const float* H, int64_
     __syncthreads();
     if (J == 0) break;
     // Schur update A_II' -= V_IJ V_I'J^T for I <= I' < J, and T_IK += V_IJ N_JK
-    // for I < J <= K (T_IK sits in the free block (K, I) below the diagonal)
+    // for I < J <= K (T_IK sits in the free block (K, I) below the diagonal).
+    // Wave 0 updates the next leaf's own block (J - 1, J - 1), the last Schur
+    // task, and goes straight on to that leaf; the other waves share the rest,
+    // which no leaf step reads, so they run beside it.
     const int nsch = J * (J + 1) / 2, ntot = nsch + J * (NB - J);
-    for (int task = wave; task < ntot; task += 4) {
+    if (wave == 0) {
       f4 u[2][2] = {};
-      if (task < nsch) {
-        int I = 0, r = task;
-        while (r >= J - I) {
-          r -= J - I;
-          ++I;
+      const int I = J - 1;
+      wave_gemm32<true>(&A[I * LF * DS + j0], &A[I * LF * DS + j0], u, lane);
+      store32(&A[I * LF * DS + I * LF], u, lane, -1.f, true);
+      leaf(I);
+    } else {
+      for (int task = wave - 1; task < ntot; task += 3) {
+        if (task == nsch - 1) continue;  // wave 0's
+        f4 u[2][2] = {};
+        if (task < nsch) {
+          int I = 0, r = task;
+          while (r >= J - I) {
+            r -= J - I;
+            ++I;
+          }
+          const int I2 = I + r;
+          wave_gemm32<true>(&A[I * LF * DS + j0], &A[I2 * LF * DS + j0], u, lane);
+          store32(&A[I * LF * DS + I2 * LF], u, lane, -1.f, true);
+        } else {
+          const int r = task - nsch, I = r / (NB - J), K = J + r % (NB - J);
+          wave_gemm32<false>(&A[I * LF * DS + j0], &N[j0 * DS + K * LF], u, lane);
+          store32(&A[K * LF * DS + I * LF], u, lane, 1.f, true);
         }
-        const int I2 = I + r;
-        wave_gemm32<true>(&A[I * LF * DS + j0], &A[I2 * LF * DS + j0], u, lane);
-        store32(&A[I * LF * DS + I2 * LF], u, lane, -1.f, true);
-      } else {
-        const int r = task - nsch, I = r / (NB - J), K = J + r % (NB - J);
-        wave_gemm32<false>(&A[I * LF * DS + j0], &N[j0 * DS + K * LF], u, lane);
-        store32(&A[K * LF * DS + I * LF], u, lane, 1.f, true);
       }
     }
     __syncthreads();
