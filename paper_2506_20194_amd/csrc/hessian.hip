@@ -980,8 +980,25 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
     lds_barrier();
     read_b(tb0, fb);
     read_a(tb0, 0, fa0);
-    // (fb, fa0) hold stage t's B and first A half on entry to each stage
-    for (int t = tb0; t < tb1 - 1; ++t) {
+    // (fb, fa0) hold stage t's B and first A half on entry to each stage;
+    // two stages per trip with the fragment sets swapped, so no copies
+    int t = tb0;
+    for (; t + 2 < tb1; t += 2) {
+      v4u fa1[4], nb[4], na0[4];
+      read_a(t, 1, fa1);
+      mma_half(0, fa0, fb);
+      advance(t);
+      read_b(t + 1, nb);
+      read_a(t + 1, 0, na0);
+      mma_half(1, fa1, fb);
+      read_a(t + 1, 1, fa1);
+      mma_half(0, na0, nb);
+      advance(t + 1);
+      read_b(t + 2, fb);
+      read_a(t + 2, 0, fa0);
+      mma_half(1, fa1, nb);
+    }
+    if (t + 1 < tb1) {
       v4u fa1[4], nb[4], na0[4];
       read_a(t, 1, fa1);
       mma_half(0, fa0, fb);
@@ -994,6 +1011,7 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
         fb[i] = nb[i];
         fa0[i] = na0[i];
       }
+      ++t;
     }
     {
       v4u fa1[4];
