@@ -31,9 +31,9 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # were taken on: any change to that file makes the figure unknown (null).
 GRAM_TRAFFIC = {
     "source": "paper_2506_20194_amd/csrc/hessian.hip",
-    "sha256": "66f9a165d6f3b0b7d772fcf53b2d9e8a33fda939c4a172896ab0f6806bd8a34f",
+    "sha256": "e730e2ceb5d78a9e9651f63916cc13c7cf9b450e7cd01dde86780a9baf5f2fce",
     "workload": "llama2_70b_down_proj",
-    "fetch_kib": 205590067.8, "fetch_scale": 2.0,
+    "fetch_kib": 61316064.8, "fetch_scale": 2.0,
     "write_kib": 3239936.0, "write_scale": 1.0,
 }
 
