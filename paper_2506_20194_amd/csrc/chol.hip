@@ -454,6 +454,7 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
     p.tri = TRI_ALL;
     p.nterms = 1;
     p.t[0] = GemmTerm{H + r0, ldh, 1, w.vinv + (int64_t)b * kTile * kTile, kTile, 0, sz, 1.f, KLO_ZERO, KHI_FULL};
+    p.inplace = 1;
     return gemm_f32(p, s);
   };
   // Groups of kGroup blocks, from the last one.  Inside a group, before block

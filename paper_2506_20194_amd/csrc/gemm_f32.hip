@@ -439,10 +439,16 @@ __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* sme
 // Tiles are enumerated on the 128 grid (the triangular filters and the tile
 // orders are defined there); with TF = 64 each 128 tile is split into its
 // four quarters, which are consecutive ids (a quarter outside M x N exits).
-template <int TF, bool B1R, bool B2R, bool TWO>
+// PAIR (64 tiles, launches whose C overwrites the first term's A in place,
+// N <= 128): a workgroup takes both column quarters of a row quarter, runs
+// both K loops and only then writes, so no workgroup overwrites columns that
+// another one of the same rows has still to read.
+template <int TF, bool B1R, bool B2R, bool TWO, bool PAIR>
 __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc d, int ntiles) {
   using G = FGeo<TF>;
   constexpr int NB = G::NB, SUB = kTile / TF;
+  constexpr int NQ = PAIR ? 2 : 1;  // column quarters per workgroup
+  static_assert(!PAIR || TF == 64, "paired quarters on 64 tiles");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];  // the ring; reused by the epilogue
   const int id = d.order == ORDER_XCD ? xcd_remap_g(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   if (id >= ntiles) return;
@@ -454,18 +460,28 @@ __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc 
     d.t[1].A += z * d.sA[1];
     d.t[1].B += z * d.sB[1];
   }
-  const int pid = id / (SUB * SUB), sub = id % (SUB * SUB);
+  const int SPT = PAIR ? SUB : SUB * SUB;  // ids per 128 tile
+  const int pid = id / SPT, sub = id % SPT;
   int ti, tj;
   tile_of(d, pid, &ti, &tj);
-  const int i0 = ti * kTile + (sub / SUB) * TF, j0 = tj * kTile + (sub % SUB) * TF;
-  if (i0 >= d.M || j0 >= d.N) return;
-  f4 acc[NB][NB];
+  const int i0 = ti * kTile + (PAIR ? sub : sub / SUB) * TF;
+  const int jb = tj * kTile + (PAIR ? 0 : (sub % SUB) * TF);  // first column quarter
+  if (i0 >= d.M || jb >= d.N) return;
+  f4 acc[NQ][NB][NB];
 #pragma unroll
-  for (int a = 0; a < NB; ++a)
+  for (int q = 0; q < NQ; ++q)
 #pragma unroll
-    for (int b = 0; b < NB; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
-  fast_term<TF, B1R>(d.t[0], i0, j0, smem, acc);
-  if (TWO) fast_term<TF, B2R>(d.t[1], i0, j0, smem, acc);
+    for (int a = 0; a < NB; ++a)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[q][a][b] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int j0 = jb + q * TF;
+    if (j0 < d.N) {  // uniform
+      fast_term<TF, B1R>(d.t[0], i0, j0, smem, acc[q]);
+      if (TWO) fast_term<TF, B2R>(d.t[1], i0, j0, smem, acc[q]);
+    }
+  }
 
   // epilogue through LDS: C = beta C + acc with coalesced 16-byte accesses,
   // FEP rows of the tile per pass (the waves holding them stage them).  Every
@@ -477,42 +493,47 @@ __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc 
   constexpr int CPR = TF / 4;
   constexpr int NP = TF / FEP, QPT = FEP * TF / 4 / 256;  // passes, 16-byte pieces per thread and pass
   static_assert(QPT * 256 * 4 == FEP * TF, "epilogue split");
-  float4 cv[NP][QPT];
   const bool keep_c = d.beta != 0.f;
-  if (keep_c) {
-#pragma unroll
-    for (int e = 0; e < NP; ++e)
-#pragma unroll
-      for (int i = 0; i < QPT; ++i) {
-        const int q = tid + 256 * i, r = q / CPR, c4 = (q % CPR) * 4;
-        cv[e][i] = *(const float4*)(d.C + (int64_t)(i0 + e * FEP + r) * d.ldc + j0 + c4);
-      }
-  }
   float* st = (float*)smem;
 #pragma unroll
-  for (int e = 0; e < NP; ++e) {
-    const int e0 = e * FEP;
-    lds_barrier();
-    if (wi * G::HW >= e0 && wi * G::HW < e0 + FEP) {
+  for (int q = 0; q < NQ; ++q) {
+    const int j0 = jb + q * TF;
+    if (j0 >= d.N) break;  // uniform
+    float4 cv[NP][QPT];
+    if (keep_c) {
 #pragma unroll
-      for (int a = 0; a < NB; ++a)
+      for (int e = 0; e < NP; ++e)
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            st[(wi * G::HW - e0 + a * 16 + (lane >> 4) * 4 + r) * LS + wj * G::HW + b * 16 + (lane & 15)] =
-                acc[a][b][r];
+        for (int i = 0; i < QPT; ++i) {
+          const int qq = tid + 256 * i, r = qq / CPR, c4 = (qq % CPR) * 4;
+          cv[e][i] = *(const float4*)(d.C + (int64_t)(i0 + e * FEP + r) * d.ldc + j0 + c4);
+        }
     }
-    lds_barrier();
 #pragma unroll
-    for (int i = 0; i < QPT; ++i) {
-      const int q = tid + 256 * i, r = q / CPR, c4 = (q % CPR) * 4;
-      float4 v = *(const float4*)&st[r * LS + c4];
-      if (keep_c) {
-        const float4 c = cv[e][i];
-        v = make_float4(d.beta * c.x + v.x, d.beta * c.y + v.y, d.beta * c.z + v.z, d.beta * c.w + v.w);
+    for (int e = 0; e < NP; ++e) {
+      const int e0 = e * FEP;
+      lds_barrier();
+      if (wi * G::HW >= e0 && wi * G::HW < e0 + FEP) {
+#pragma unroll
+        for (int a = 0; a < NB; ++a)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              st[(wi * G::HW - e0 + a * 16 + (lane >> 4) * 4 + r) * LS + wj * G::HW + b * 16 + (lane & 15)] =
+                  acc[q][a][b][r];
       }
-      *(float4*)(d.C + (int64_t)(i0 + e0 + r) * d.ldc + j0 + c4) = v;
+      lds_barrier();
+#pragma unroll
+      for (int i = 0; i < QPT; ++i) {
+        const int qq = tid + 256 * i, r = qq / CPR, c4 = (qq % CPR) * 4;
+        float4 v = *(const float4*)&st[r * LS + c4];
+        if (keep_c) {
+          const float4 c = cv[e][i];
+          v = make_float4(d.beta * c.x + v.x, d.beta * c.y + v.y, d.beta * c.z + v.z, d.beta * c.w + v.w);
+        }
+        *(float4*)(d.C + (int64_t)(i0 + e0 + r) * d.ldc + j0 + c4) = v;
+      }
     }
   }
 }
@@ -539,9 +560,9 @@ bool fast_ok(const GemmDesc& d) {
   return true;
 }
 
-template <int TF, bool B1R, bool B2R, bool TWO>
+template <int TF, bool B1R, bool B2R, bool TWO, bool PAIR = false>
 duo_status launch_fast(const GemmDesc& d, int ids, int nb, hipStream_t s) {
-  auto kern = gemm_fast_kernel<TF, B1R, B2R, TWO>;
+  auto kern = gemm_fast_kernel<TF, B1R, B2R, TWO, PAIR>;
   if (duo_status st = set_max_lds((const void*)kern, FGeo<TF>::LDS); st != DUO_OK) return st;
   hipLaunchKernelGGL(kern, dim3((unsigned)rup(ids, 8), nb), dim3(256), FGeo<TF>::LDS, s, d, ids);
   DUO_LAUNCH_CHECK();
@@ -554,6 +575,20 @@ duo_status launch(const GemmDesc& d, hipStream_t s) {
   const int ntiles = d.tri == TRI_ALL ? tm * tn : tm * (tm + 1) / 2;
   if (ntiles <= 0) return DUO_OK;
   const int nb = d.batch > 1 ? d.batch : 1;
+  if (d.inplace) {
+    if (d.N > kTile) return DUO_ERR_UNSUPPORTED;
+    if constexpr (A1R && A2R && !B1R && !B2R) {
+      if ((int64_t)ntiles * nb >= kSmallTiles) {
+        if (fast_ok<kTile>(d)) return launch_fast<kTile, B1R, B2R, TWO>(d, ntiles, nb, s);
+      } else if (fast_ok<64>(d)) {
+        return launch_fast<64, B1R, B2R, TWO, true>(d, 2 * ntiles, nb, s);
+      }
+    }
+    const int grid = (int)rup(ntiles, 8);
+    hipLaunchKernelGGL((gemm_kernel<kTile, A1R, B1R, A2R, B2R, TWO>), dim3(grid, nb), dim3(256), 0, s, d, ntiles);
+    DUO_LAUNCH_CHECK();
+    return DUO_OK;
+  }
   if constexpr (A1R && A2R) {
     if ((int64_t)ntiles * nb >= kSmallTiles) {
       if (fast_ok<kTile>(d)) return launch_fast<kTile, B1R, B2R, TWO>(d, ntiles, nb, s);

@@ -71,6 +71,10 @@ struct GemmDesc {
   // (upper tiles only) deals them by decreasing distance from the diagonal
   // (the longest first when the K range grows with that distance)
   int order;
+  // C is the first term's A operand, overwritten in place (N <= 128): every
+  // workgroup must then own whole rows of C, so the launch uses 128-wide
+  // tiles (a quarter tile would overwrite columns its row neighbour still reads)
+  int inplace;
 };
 enum { ORDER_XCD = 0, ORDER_PLAIN = 1, ORDER_DIAG = 2 };
 
