@@ -291,67 +291,57 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmDesc d, int ntiles) {
 // operands (every DuoGPT product at k a multiple of 128): A row-major (K
 // contiguous); B either K-contiguous (b_row = 0, "NT") or row-major (b_row = 1,
 // "NN").  TF x TF tile (128, or 64 for launches too small to fill the chip),
-// 2 x 2 waves of TF/2 x TF/2, K staged 16 at a time through a ring of LDS stages
-// filled by direct global->LDS loads (no register staging), all but one
-// stage in flight.  The 128 tile needs 112 VGPRs and 48 KB of LDS, so three
-// workgroups share a CU (the 64 tile: 24 KB, five): while one waits at a
-// stage barrier or for its fragment reads, the others keep the matrix core
-// busy.
+// 2 x 2 waves of TF/2 x TF/2, K staged 32 at a time through two LDS stages
+// filled by direct global->LDS loads (no register staging): the loads of
+// stage s + 1 are in flight while stage s is multiplied.  The 128 tile needs
+// about 150 VGPRs and 64 KB of LDS, so two workgroups share a CU (the 64
+// tile: 32 KB, five): while one waits at a stage barrier or for its fragment
+// reads, the other keeps the matrix core busy.  A stage is 128 MFMAs per
+// wave on the 128 tile; 16-deep stages (a barrier every 64 MFMAs, three
+// workgroups per CU) measured 1-4 % slower.
 //
-// K order inside a stage: MFMA step s (of 4) takes k = 4g + s in lane group g,
-// so that a K-contiguous operand's fragment for all four steps is one 16-byte
-// chunk (k = 4g .. 4g + 3) per lane.  Both operands use the same order, so
-// the sum is unchanged.  Layouts (16-byte chunks):
-//   K-contiguous operand, TF lines x 4 chunks: chunk c of line r at
-//     r * 4 + (c ^ ((r >> 2) & 3)), so the 16 lines of a fragment read hit 16
-//     distinct bank groups;
-//   row-major B, 16 k-rows x TF/4 chunks: chunk c of row k at
-//     k * TF/4 + (c ^ (4 * ((k >> 2) & 3))), so the four lane groups (k four
+// K order inside a stage: MFMA step s (of 8) takes k = 8g + s in lane group g,
+// so that a K-contiguous operand's fragment for all eight steps is two 16-byte
+// chunks (k = 8g .. 8g + 7) per lane.  Both operands use the same order, so
+// the sum is the same.  Layouts (16-byte chunks):
+//   K-contiguous operand, TF lines x 8 chunks: chunk c of line r at
+//     r * 8 + (c ^ ((r >> 1) & 7)), so the 16 lines of a fragment read hit 16
+//     distinct bank groups (the 8 lines of each parity, 8 distinct positions);
+//   row-major B, 32 k-rows x TF/4 chunks: chunk c of row k at
+//     k * TF/4 + (c ^ (4 * ((k >> 3) & 3))), so the four lane groups (k eight
 //     apart) read disjoint bank groups.
 // ---------------------------------------------------------------------------
-constexpr int FK = 16;                 // K per stage
-constexpr int FEP = 64;                // tile rows per epilogue pass
+constexpr int FK = 32;       // K per stage
+constexpr int FCH = FK / 4;  // 16-byte chunks per K-contiguous line = MFMA steps per stage
+constexpr int FEP = 64;      // tile rows per epilogue pass
 
 template <int TF>
 struct FGeo {
-  static constexpr int OP = TF * FK * 4;  // bytes per operand per stage
+  static constexpr int OP = TF * FK * 4;    // bytes per operand per stage
   static constexpr int STAGE = 2 * OP;
-  static constexpr int Q = TF / 64;       // 16-byte chunks per thread per operand per stage
-  static constexpr int NB = TF / 32;      // 16 x 16 blocks per wave and dimension
-  static constexpr int HW = TF / 2;       // wave tile edge
-  static constexpr int NS = TF == kTile ? 3 : 3;   // ring depth (stages)
-  static constexpr int OCC = TF == kTile ? 3 : 5;  // workgroups per CU
+  static constexpr int Q = TF * FK / 1024;  // 16-byte chunks per thread per operand per stage
+  static constexpr int NB = TF / 32;        // 16 x 16 blocks per wave and dimension
+  static constexpr int HW = TF / 2;         // wave tile edge
+  static constexpr int OCC = TF == kTile ? 2 : 5;  // workgroups per CU
   static constexpr size_t EPI = (size_t)FEP * (TF + 4) * 4;
-  static constexpr size_t LDS = (size_t)NS * STAGE > EPI ? (size_t)NS * STAGE : EPI;
-  static_assert(2 * Q * (NS - 2) <= 8, "loads in flight beyond wait_vm's range");
+  static constexpr size_t LDS = (size_t)2 * STAGE > EPI ? (size_t)2 * STAGE : EPI;
   static_assert(LDS * OCC <= 160 * 1024, "fast-path LDS");
 };
 
-template <int N>
-__device__ __forceinline__ void wait_vm_n() {
-  // vmcnt N (bits 3:0 and 15:14), expcnt and lgkmcnt not waited for
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-__device__ __forceinline__ void wait_vm(int n) {
-  // at most n of this wave's vector-memory operations outstanding (n <= 8)
-  switch (n) {
-    case 0: wait_vm_n<0>(); break;
-    case 1: wait_vm_n<1>(); break;
-    case 2: wait_vm_n<2>(); break;
-    case 3: wait_vm_n<3>(); break;
-    case 4: wait_vm_n<4>(); break;
-    case 5: wait_vm_n<5>(); break;
-    case 6: wait_vm_n<6>(); break;
-    case 7: wait_vm_n<7>(); break;
-    default: wait_vm_n<8>(); break;
-  }
+// chunk positions: K-contiguous line r, row-major B row k
+__device__ __forceinline__ int swa(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ int swb(int k) { return 4 * ((k >> 3) & 3); }
+
+__device__ __forceinline__ void wait_vm0() {
+  // vmcnt 0; expcnt and lgkmcnt not waited for
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
 }
 
 template <int TF, bool BR>
 __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* smem,
                                  f4 (&acc)[FGeo<TF>::NB][FGeo<TF>::NB]) {
   using G = FGeo<TF>;
-  constexpr int NB = G::NB, Q = G::Q, CPR = TF / 4;  // CPR: chunks per row-major B row
+  constexpr int NB = G::NB, Q = G::Q, CPR = TF / 4, CH = FCH;  // CPR: chunks per row-major B row
   const int64_t klo = lo_of<TF>(t.klo, i0, j0);
   const int64_t khi = hi_of<TF>(t.khi, i0, j0, t.K);
   if (klo >= khi) return;
@@ -366,23 +356,22 @@ __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* sme
   for (int q = 0; q < Q; ++q) {
     const int pos = (Q * wave + q) * 64 + lane;  // 16-byte position in the operand's stage image
     {
-      const int r = pos >> 2, c = (pos & 3) ^ ((r >> 2) & 3);
+      const int r = pos / CH, c = (pos % CH) ^ swa(r);
       ga[q] = t.A + (int64_t)(i0 + r) * t.lda + klo + 4 * c;
     }
     if (BR) {
-      const int k = pos / CPR, c = (pos % CPR) ^ (4 * ((k >> 2) & 3));
+      const int k = pos / CPR, c = (pos % CPR) ^ swb(k);
       gb[q] = t.B + (klo + k) * t.ldb + j0 + 4 * c;
     } else {
-      const int r = pos >> 2, c = (pos & 3) ^ ((r >> 2) & 3);
+      const int r = pos / CH, c = (pos % CH) ^ swa(r);
       gb[q] = t.B + (int64_t)(j0 + r) * t.ldb + klo + 4 * c;
     }
     la[q] = (uint32_t)((Q * wave + q) * 64 * 16);
     lb[q] = (uint32_t)(G::OP + (Q * wave + q) * 64 * 16);
   }
   const int64_t da = FK, db = BR ? (int64_t)FK * t.ldb : FK;  // element step per stage
-  const float alpha = t.alpha;
   auto issue = [&](int st) {
-    uint8_t* base = smem + (st % G::NS) * G::STAGE;
+    uint8_t* base = smem + (st & 1) * G::STAGE;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       __builtin_amdgcn_global_load_lds((const void*)(ga[q] + st * da),
@@ -393,15 +382,18 @@ __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* sme
   };
   const int g = lane >> 4, l16 = lane & 15;
   auto compute = [&](int st) {
-    const u32x4* sa = (const u32x4*)(smem + (st % G::NS) * G::STAGE);
-    const uint8_t* sbb = smem + (st % G::NS) * G::STAGE + G::OP;
-    float av[NB][4], bv[NB][4];  // [block][step]
+    const u32x4* sa = (const u32x4*)(smem + (st & 1) * G::STAGE);
+    const uint8_t* sbb = smem + (st & 1) * G::STAGE + G::OP;
+    float av[NB][CH], bv[NB][CH];  // [block][step]
 #pragma unroll
     for (int a = 0; a < NB; ++a) {
       const int r = wi * G::HW + a * 16 + l16;
-      const u32x4 v = sa[r * 4 + (g ^ ((r >> 2) & 3))];
 #pragma unroll
-      for (int s2 = 0; s2 < 4; ++s2) av[a][s2] = alpha * __uint_as_float(v[s2]);
+      for (int h = 0; h < CH / 4; ++h) {
+        const u32x4 v = sa[r * CH + (((CH / 4) * g + h) ^ swa(r))];
+#pragma unroll
+        for (int s2 = 0; s2 < 4; ++s2) av[a][4 * h + s2] = __uint_as_float(v[s2]);
+      }
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -409,29 +401,32 @@ __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* sme
       if (BR) {
         const float* sb = (const float*)sbb;
 #pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2) {
-          const int k = 4 * g + s2;
-          bv[b][s2] = sb[k * TF + (((col >> 2) ^ (4 * ((k >> 2) & 3))) << 2) + (col & 3)];
+        for (int s2 = 0; s2 < CH; ++s2) {
+          const int k = CH * g + s2;
+          bv[b][s2] = sb[k * TF + (((col >> 2) ^ swb(k)) << 2) + (col & 3)];
         }
       } else {
-        const u32x4 v = ((const u32x4*)sbb)[col * 4 + (g ^ ((col >> 2) & 3))];
 #pragma unroll
-        for (int s2 = 0; s2 < 4; ++s2) bv[b][s2] = __uint_as_float(v[s2]);
+        for (int h = 0; h < CH / 4; ++h) {
+          const u32x4 v = ((const u32x4*)sbb)[col * CH + (((CH / 4) * g + h) ^ swa(col))];
+#pragma unroll
+          for (int s2 = 0; s2 < 4; ++s2) bv[b][4 * h + s2] = __uint_as_float(v[s2]);
+        }
       }
     }
 #pragma unroll
-    for (int s2 = 0; s2 < 4; ++s2)
+    for (int s2 = 0; s2 < CH; ++s2)
 #pragma unroll
       for (int a = 0; a < NB; ++a)
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a][s2], bv[b][s2], acc[a][b], 0, 0, 0);
   };
-  lds_barrier();  // the previous user of the ring (an earlier term) is done with it
-  for (int st = 0; st < min(nst, G::NS - 1); ++st) issue(st);
+  lds_barrier();  // the previous user of the stages (an earlier term) is done with them
+  issue(0);
   for (int st = 0; st < nst; ++st) {
-    wait_vm(2 * Q * min(G::NS - 2, nst - 1 - st));  // stage st landed (this wave's part)
-    lds_barrier();                                // every wave's part landed; stage st - 1 is free
-    if (st + G::NS - 1 < nst) issue(st + G::NS - 1);
+    wait_vm0();     // stage st landed (this wave's part)
+    lds_barrier();  // every wave's part landed; every wave is done with stage st - 1
+    if (st + 1 < nst) issue(st + 1);
     compute(st);
   }
 }
@@ -474,12 +469,27 @@ __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc 
     for (int a = 0; a < NB; ++a)
 #pragma unroll
       for (int b = 0; b < NB; ++b) acc[q][a][b] = f4{0.f, 0.f, 0.f, 0.f};
+  // The terms are summed unscaled: acc = P0 (r P0 + P1 with r = alpha0 / alpha1
+  // for two terms) and the epilogue multiplies by alpha0 (alpha1), so the
+  // fragments go from LDS to the MFMAs untouched.  For alpha = +-1 the result
+  // is bit for bit that of accumulating the scaled products.
+  const float a0 = d.t[0].alpha, a1 = d.t[1].alpha;
+  const bool two = TWO && a1 != 0.f && d.t[1].K > 0;
+  const float ae = two ? a1 : a0, r01 = two ? a0 / a1 : 1.f;
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int j0 = jb + q * TF;
     if (j0 < d.N) {  // uniform
       fast_term<TF, B1R>(d.t[0], i0, j0, smem, acc[q]);
-      if (TWO) fast_term<TF, B2R>(d.t[1], i0, j0, smem, acc[q]);
+      if (two) {
+        if (r01 != 1.f) {
+#pragma unroll
+          for (int a = 0; a < NB; ++a)
+#pragma unroll
+            for (int b = 0; b < NB; ++b) acc[q][a][b] *= r01;
+        }
+        fast_term<TF, B2R>(d.t[1], i0, j0, smem, acc[q]);
+      }
     }
   }
 
@@ -528,6 +538,7 @@ __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc 
       for (int i = 0; i < QPT; ++i) {
         const int qq = tid + 256 * i, r = qq / CPR, c4 = (qq % CPR) * 4;
         float4 v = *(const float4*)&st[r * LS + c4];
+        v = make_float4(ae * v.x, ae * v.y, ae * v.z, ae * v.w);
         if (keep_c) {
           const float4 c = cv[e][i];
           v = make_float4(d.beta * c.x + v.x, d.beta * c.y + v.y, d.beta * c.z + v.z, d.beta * c.w + v.w);
