@@ -326,7 +326,9 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
  * every launch of the tracked kernels is bracketed by HIP events on the
  * stream it runs on.  duo_profile_read waits for the recorded events and
  * returns the summed time (milliseconds) and the number of launches since the
- * last read, then resets them.  Single-threaded use only.
+ * last read, then resets them.  A launch whose events could not be recorded
+ * is left out of both; DUO_ERR_HIP if a recorded pair could not be read
+ * (the others are still summed).  Single-threaded use only.
  */
 enum {
   DUO_PROF_GRAM = 0,     /* stage 1: MFMA Gram kernel (H, G)                   */

@@ -79,7 +79,6 @@ __global__ __launch_bounds__(256) void act_select_kernel(const T* __restrict__ X
                                                          int k, int z, int64_t* __restrict__ thr,
                                                          uint32_t* __restrict__ nf) {
   __shared__ int red[8];
-  __shared__ int scan[4];
   const int t = blockIdx.x;
   if (t >= m) return;
   const T* row = X + (int64_t)t * ldx;

@@ -5,7 +5,6 @@
 #include <hip/hip_runtime.h>
 
 #include <mutex>
-#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -14,10 +13,15 @@ namespace duo {
 
 namespace {
 
+struct Bracket {
+  hipEvent_t a, b;
+  bool ended;  // the end event was recorded
+};
+
 struct Profiler {
   std::mutex mu;
   bool on = false;
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[DUO_PROF_COUNT];
+  std::vector<Bracket> pending[DUO_PROF_COUNT];
   std::vector<hipEvent_t> pool;
   double total_ms[DUO_PROF_COUNT] = {};
   long long count[DUO_PROF_COUNT] = {};
@@ -31,6 +35,9 @@ struct Profiler {
     hipEvent_t e = nullptr;
     if (hipEventCreate(&e) != hipSuccess) return nullptr;
     return e;
+  }
+  void put(hipEvent_t e) {
+    if (e) pool.push_back(e);
   }
 };
 
@@ -46,16 +53,26 @@ void prof_begin(int id, hipStream_t s) {
   std::lock_guard<std::mutex> g(p.mu);
   if (!p.on) return;
   hipEvent_t a = p.get(), b = p.get();
-  if (!a || !b) return;
-  hipEventRecord(a, s);
-  p.pending[id].push_back({a, b});
+  if (!a || !b || hipEventRecord(a, s) != hipSuccess) {  // this launch goes untimed
+    p.put(a);
+    p.put(b);
+    return;
+  }
+  p.pending[id].push_back({a, b, false});
 }
 
 void prof_end(int id, hipStream_t s) {
   Profiler& p = prof();
   std::lock_guard<std::mutex> g(p.mu);
-  if (!p.on || p.pending[id].empty()) return;
-  hipEventRecord(p.pending[id].back().second, s);
+  if (!p.on || p.pending[id].empty() || p.pending[id].back().ended) return;
+  Bracket& br = p.pending[id].back();
+  if (hipEventRecord(br.b, s) == hipSuccess) {
+    br.ended = true;
+  } else {  // this launch goes untimed
+    p.put(br.a);
+    p.put(br.b);
+    p.pending[id].pop_back();
+  }
 }
 
 }  // namespace duo
@@ -75,21 +92,26 @@ duo_status duo_profile_read(int32_t kernel, double* total_ms, int64_t* launches)
   if (kernel < 0 || kernel >= DUO_PROF_COUNT || !total_ms || !launches) return DUO_ERR_INVALID_ARG;
   Profiler& p = prof();
   std::lock_guard<std::mutex> g(p.mu);
-  for (auto& pr : p.pending[kernel]) {
-    if (hipEventSynchronize(pr.second) != hipSuccess) return DUO_ERR_HIP;
+  duo_status st = DUO_OK;
+  for (const Bracket& br : p.pending[kernel]) {
     float ms = 0.f;
-    if (hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess) return DUO_ERR_HIP;
-    p.total_ms[kernel] += ms;
-    p.count[kernel] += 1;
-    p.pool.push_back(pr.first);
-    p.pool.push_back(pr.second);
+    if (br.ended) {  // a bracket left open (no end recorded) is dropped
+      if (hipEventSynchronize(br.b) == hipSuccess && hipEventElapsedTime(&ms, br.a, br.b) == hipSuccess) {
+        p.total_ms[kernel] += ms;
+        p.count[kernel] += 1;
+      } else {
+        st = DUO_ERR_HIP;
+      }
+    }
+    p.put(br.a);
+    p.put(br.b);
   }
   p.pending[kernel].clear();
   *total_ms = p.total_ms[kernel];
   *launches = p.count[kernel];
   p.total_ms[kernel] = 0.0;
   p.count[kernel] = 0;
-  return DUO_OK;
+  return st;
 }
 
 }  // extern "C"
