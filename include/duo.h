@@ -241,7 +241,24 @@ typedef struct {
   int32_t q_group;
   float* q_scale_out;
   float* q_zero_out;
+  int32_t residual_form;
 } duo_sweep_opts;
+
+/*
+ * residual_form (duo_prune_layer only; duo_sweep, given D, accepts AUTO and
+ * D): how the residual term of Algorithm 1's updates (W0 D, D = U L^T) is
+ * carried.  Both forms give the same weights up to fp32 rounding order.
+ *   DUO_FORM_D  D is formed (k^3 / 3 multiply-adds) and the lazy update is one
+ *               product with the two terms E L^T and W0 D.
+ *   DUO_FORM_Y  no D: the sweep carries Y = W0 U (W0: the values the columns
+ *               had when processed) beside W, since W0 D = Y L^T with the
+ *               terms of each column's own block added at the block's start;
+ *               two lazy products (W += (Y - E) L^T, Y += W0 U) of the same
+ *               total size.  Uses the workspace's D space for Y.  Not with
+ *               nm_n or q_bits (DUO_ERR_UNSUPPORTED).
+ *   DUO_FORM_AUTO  Y when k >= 6144 and neither nm_n nor q_bits is set, else D.
+ */
+enum { DUO_FORM_AUTO = 0, DUO_FORM_D = 1, DUO_FORM_Y = 2 };
 
 /*
  * duo_sweep - stage 3 sweep (Algorithm 1 outer/inner loops, lazy updates).

@@ -35,7 +35,7 @@ bool ws_ok(const void* ws, size_t ws_bytes, size_t need) {
 }
 
 struct PruneWs {
-  float* D;
+  float* D;  // D (k x k) in the D form, Y (n x k) in the Y form
   float* fac;
   void* score;
   void* sweep;
@@ -45,7 +45,7 @@ struct PruneWs {
 PruneWs carve_prune(void* ws, int64_t n, int64_t k, int B) {
   Carver c(ws);
   PruneWs w;
-  w.D = c.take<float>((size_t)k * k);
+  w.D = c.take<float>((size_t)(n > k ? n : k) * k);
   w.fac = c.take<float>((size_t)k);
   w.score = c.take<uint8_t>(score_ws_bytes(k));
   w.sweep = c.take<uint8_t>(sweep_ws_bytes(n, k, B));
@@ -54,6 +54,8 @@ PruneWs carve_prune(void* ws, int64_t n, int64_t k, int B) {
 }
 
 bool k_ok(int64_t k) { return k >= 1 && k <= kMaxK; }
+
+constexpr int64_t kYFormMinK = 6144;  // DUO_FORM_AUTO: the Y form from this k up
 
 }  // namespace
 
@@ -251,7 +253,10 @@ static duo_status sweep_args(const void* W, int32_t w_dtype, int64_t n, int64_t 
     if (nm < 0 || nm > 4 || (nm > 0 && (k % 4 != 0 || block % 4 != 0))) return DUO_ERR_INVALID_ARG;
     if (qb != 0 && (qb < 2 || qb > 8)) return DUO_ERR_INVALID_ARG;
     if (qb > 0 && !((qg == 16 || qg == 32 || qg == 64 || qg == 128) && block % qg == 0)) return DUO_ERR_INVALID_ARG;
-    *o = SweepOpts{nm, qb, qb > 0 ? qg : 0, qb > 0 ? opts->q_scale_out : nullptr, qb > 0 ? opts->q_zero_out : nullptr};
+    const int form = opts->residual_form;
+    if (form != DUO_FORM_AUTO && form != DUO_FORM_D && form != DUO_FORM_Y) return DUO_ERR_INVALID_ARG;
+    *o = SweepOpts{nm, qb, qb > 0 ? qg : 0, qb > 0 ? opts->q_scale_out : nullptr, qb > 0 ? opts->q_zero_out : nullptr,
+                   form};
   }
   if (!k_ok(k)) return k < 1 ? DUO_ERR_INVALID_ARG : DUO_ERR_UNSUPPORTED;
   if (n > INT32_MAX / 2 || n * k > ((int64_t)1 << 40)) return DUO_ERR_UNSUPPORTED;
@@ -265,7 +270,7 @@ duo_status duo_sweep(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   SweepOpts o;
   duo_status a = sweep_args(W, w_dtype, n, k, ldw, w_sparsity, opts, block, W_out, &o);
   if (a != DUO_OK) return a;
-  if (!L || !D || !fac || ldl < k || ldd < k) return DUO_ERR_INVALID_ARG;
+  if (!L || !D || !fac || ldl < k || ldd < k || o.form == DUO_FORM_Y) return DUO_ERR_INVALID_ARG;
   if (!ws_ok(ws, ws_bytes, sweep_ws_bytes(n, k, block))) return DUO_ERR_WORKSPACE;
   duo_status d = device_ok();
   if (d != DUO_OK) return d;
@@ -285,19 +290,31 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   duo_status e = sweep_args(W, w_dtype, n, k, ldw, w_sparsity, opts, block, W_out, &o);
   if (e != DUO_OK) return e;
   if (!L || !G || !a || ldl < k || ldg < k) return DUO_ERR_INVALID_ARG;
+  const bool plain = o.nm_n == 0 && o.q_bits == 0;
+  if (o.form == DUO_FORM_Y && !plain) return DUO_ERR_UNSUPPORTED;
   const PruneWs pw = carve_prune(nullptr, n, k, block);
   if (!ws_ok(ws, ws_bytes, pw.bytes)) return DUO_ERR_WORKSPACE;
   duo_status d = device_ok();
   if (d != DUO_OK) return d;
   const PruneWs w = carve_prune(ws, n, k, block);
   const hipStream_t s = (hipStream_t)stream;
+  // The unstructured, unquantised sweep may run in the Y form (no D = U L^T);
+  // N:4 and quantisation read values inside a block that the Y form would
+  // have to rebuild, and keep D.  Automatic choice: the Y form saves the
+  // k^3 / 3 of D but launches two more products per block (measured at
+  // n = k = 4096: 0.17 ms slower per layer; k = 11008: 2 ms faster).
+  const bool yform = o.form == DUO_FORM_Y || (o.form == DUO_FORM_AUTO && plain && k >= kYFormMinK);
   prof_begin(DUO_PROF_SCORE, s);
-  duo_status r = score_run(L, ldl, G, ldg, a, k, w.D, k, w.fac, w.score, s);
+  duo_status r = score_run(L, ldl, G, ldg, a, k, yform ? nullptr : w.D, k, w.fac, w.score, s);
   prof_end(DUO_PROF_SCORE, s);
   if (r != DUO_OK) return r;
   prof_begin(DUO_PROF_SWEEP, s);
-  r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, w.D, k, w.fac, w_sparsity, o, block, mask_in, W_out, W_out_lowp,
-                mask_out, block_scores_out, w.sweep, s);
+  if (yform)
+    r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, nullptr, 0, w.fac, w_sparsity, o, block, mask_in, W_out, W_out_lowp,
+                  mask_out, block_scores_out, w.sweep, s, score_u(w.score, k), k, w.D);
+  else
+    r = sweep_run(W, w_dtype, n, k, ldw, L, ldl, w.D, k, w.fac, w_sparsity, o, block, mask_in, W_out, W_out_lowp,
+                  mask_out, block_scores_out, w.sweep, s);
   prof_end(DUO_PROF_SWEEP, s);
   return r;
 }

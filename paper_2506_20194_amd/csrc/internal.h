@@ -93,8 +93,12 @@ duo_status chol_run(float* H, int64_t k, int64_t ldh, double damp, void* ws, hip
 
 // ---- stage 3 (score.hip, sweep.hip) ----
 size_t score_ws_bytes(int64_t k);
+// D = NULL: Q, fac only (no D = U L^T); U (the upper 128-tiles of Q with the
+// entries on and below the diagonal zeroed, k x k, ld k) stays in the
+// workspace, at score_u(ws, k).
 duo_status score_run(const float* L, int64_t ldl, const float* G, int64_t ldg, const float* a, int64_t k,
                      float* D, int64_t ldd, float* fac, void* ws, hipStream_t s);
+const float* score_u(const void* ws, int64_t k);
 
 size_t sweep_ws_bytes(int64_t n, int64_t k, int B);
 // Sweep options (validated by the caller).  nm_n > 0: the N:4 variant (nm_n
@@ -108,10 +112,15 @@ struct SweepOpts {
   int q_group = 0;
   float* q_scale = nullptr;
   float* q_zero = nullptr;
+  int form = 0;  // DUO_FORM_*
 };
+// U != NULL: the Y form (no D; D ignored): U is the strictly upper part of Q
+// (only entries U[i][j] with j > i are read, on 128-tiles at or above the
+// diagonal) and Y an n x k fp32 scratch matrix; not with nm_n or q_bits.
 duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L,
                      int64_t ldl, const float* D, int64_t ldd, const float* fac, double p_w, const SweepOpts& o, int B,
                      const uint32_t* mask_in, float* W_out, void* W_out_lowp, uint32_t* mask_out,
-                     float* scores_out, void* ws, hipStream_t s);
+                     float* scores_out, void* ws, hipStream_t s, const float* U = nullptr, int64_t ldu = 0,
+                     float* Y = nullptr);
 
 }  // namespace duo

@@ -59,6 +59,8 @@ ScoreWs carve(void* ws, int64_t k) {
 
 size_t score_ws_bytes(int64_t k) { return carve(nullptr, k).bytes; }
 
+const float* score_u(const void* ws, int64_t k) { return carve(const_cast<void*>(ws), k).Q; }
+
 duo_status score_run(const float* L, int64_t ldl, const float* G, int64_t ldg, const float* a, int64_t k, float* D,
                      int64_t ldd, float* fac, void* ws, hipStream_t s) {
   const ScoreWs w = carve(ws, k);
@@ -77,6 +79,7 @@ duo_status score_run(const float* L, int64_t ldl, const float* G, int64_t ldg, c
   if (st != DUO_OK) return st;
   hipLaunchKernelGGL(fac_kernel, dim3((unsigned)k), dim3(256), 0, s, w.Q, (int64_t)k, L, ldl, a, (int)k, fac);
   DUO_LAUNCH_CHECK();
+  if (!D) return DUO_OK;  // the Y form of the sweep reads U (score_u) instead
   // D = U L^T on upper tiles: D[p][j] = sum_{p < i <= j} U[p][i] L[j][i]
   GemmDesc d{};
   d.M = (int)k;

@@ -476,9 +476,9 @@ constexpr int IB_I = kMaxBlock / IB_Q;    // columns per lane: c = q + 16 i
 constexpr int IB_ROWS = 256 / IB_Q;       // rows per workgroup
 constexpr int IB_QS = IB_I + 1;           // LDS stride between lanes (odd: no bank conflicts)
 constexpr int IB_JS = IB_Q * IB_QS;       // LDS floats per column step
-// LDS image of one block's operands, [lq | dq | il], padded to whole 4 KB
+// LDS image of one block's operands, [lq | dq | il | lj], padded to whole 4 KB
 // rows of a 256-thread copy (16 bytes per thread)
-constexpr int IB_IMG_USED = 2 * kMaxBlock * IB_JS + kMaxBlock;          // floats
+constexpr int IB_IMG_USED = 2 * kMaxBlock * IB_JS + 2 * kMaxBlock;      // floats
 constexpr int IB_IMG = (IB_IMG_USED * 4 + 4095) / 4096 * 4096 / 4;      // floats (37888)
 
 // Lane O of every 16-lane row, broadcast to the row.
@@ -490,6 +490,7 @@ __device__ __forceinline__ float row_bcast(float v) {
 
 struct IbRow {
   float w[IB_I];     // current values of columns q + 16 i
+  float y[IB_I];     // Y form only: the block's own part of y = V U for columns q + 16 i
   float e[IB_I];     // E of the columns this lane owns
   float w0[IB_I];    // values before pruning of the columns this lane owns
   uint32_t kb[IB_I]; // keep bits of the row: bit o of kb[g] is column 16 g + o
@@ -507,11 +508,11 @@ struct IbOpts {
   float* q_zero;
 };
 
-// LDS operands of one column step: the staged L and D entries of this lane's
-// columns that are still live (i >= g) and 1 / L_JJ.
+// LDS operands of one column step: the staged L and D (Y form: U) entries of
+// this lane's columns that are still live (i >= g), 1 / L_JJ and L_JJ.
 struct IbBuf {
   float l[IB_I], d[IB_I];
-  float il;
+  float il, lj;
 };
 
 template <int J>
@@ -527,6 +528,7 @@ __device__ __forceinline__ void ib_load(IbBuf& b, const float* __restrict__ lq, 
       b.d[i] = dr[i];
     }
     b.il = il[J];
+    b.lj = il[kMaxBlock + J];
   }
 }
 
@@ -592,7 +594,12 @@ __device__ __forceinline__ void quant_grid(IbRow& s, const IbOpts& opt, int64_t 
   }
 }
 
-template <int J, bool NM, bool QUANT>
+// YR (the Y form of the sweep, no D): the lane also carries y, the block's
+// own part of y = V U for its columns.  Column J's value is w_J + y_J L_JJ;
+// after it, every later column c takes w_c += (y_J - e_J) L_cJ and
+// y_c += v U_Jc, which is the D-form step w_c += -e_J L_cJ + v D_Jc summed
+// over the block (D = U L^T).
+template <int J, bool NM, bool QUANT, bool YR>
 __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* __restrict__ lq,
                                         const float* __restrict__ dq, const float* __restrict__ il, int q,
                                         const IbOpts& opt, int64_t row, bool rv, int j0, int Bb, int ngroups) {
@@ -604,7 +611,9 @@ __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* 
     if (J < Bb && J % opt.q_group == 0) quant_grid<g>(s, opt, row, rv, q, (j0 + J) / opt.q_group, ngroups);
   }
   const IbBuf& b = buf[J % 3];
-  const float v = row_bcast<o>(s.w[g]);
+  float t = 0.f;  // YR: y_J L_JJ
+  if constexpr (YR) t = row_bcast<o>(s.y[g]) * b.lj;
+  const float v = YR ? row_bcast<o>(s.w[g]) + t : row_bcast<o>(s.w[g]);
   const bool kj = (s.kb[g] >> o) & 1u;
   // p: the value the column keeps (its grid value with QUANT), u = v - p the
   // error the later columns compensate
@@ -626,28 +635,39 @@ __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* 
   // most of them AGPR spill slots)
   asm volatile("" : "+v"(s.e[g]), "+v"(s.w0[g]));
   // columns c = q + 16 i > J; the LDS entries of columns <= J are zero
+  if constexpr (YR) {
+    const float tu = t - u;  // (y_J - e_J) L_JJ; the staged L column is divided by L_JJ
 #pragma unroll
-  for (int i = g; i < IB_I; ++i) s.w[i] = fmaf(-u, b.l[i], fmaf(v, b.d[i], s.w[i]));
+    for (int i = g; i < IB_I; ++i) {
+      s.w[i] = fmaf(tu, b.l[i], s.w[i]);
+      s.y[i] = fmaf(v, b.d[i], s.y[i]);
+    }
+  } else {
+#pragma unroll
+    for (int i = g; i < IB_I; ++i) s.w[i] = fmaf(-u, b.l[i], fmaf(v, b.d[i], s.w[i]));
+  }
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <bool NM, bool QUANT, int... Js>
+template <bool NM, bool QUANT, bool YR, int... Js>
 __device__ __forceinline__ void ib_steps(IbRow& s, const float* lq, const float* dq, const float* il, int q,
                                          const IbOpts& opt, int64_t row, bool rv, int j0, int Bb, int ngroups,
                                          std::integer_sequence<int, Js...>) {
   IbBuf buf[3];
   ib_load<0>(buf[0], lq, dq, il, q);
   ib_load<1>(buf[1], lq, dq, il, q);
-  (ib_step<Js, NM, QUANT>(s, buf, lq, dq, il, q, opt, row, rv, j0, Bb, ngroups), ...);
+  (ib_step<Js, NM, QUANT, YR>(s, buf, lq, dq, il, q, opt, row, rv, j0, Bb, ngroups), ...);
 }
 
 // NM: the N:M variant (mode MODE_NM): the keep bits are chosen inside the
 // column loop, and the scores they used go to scores_out when it is set.
 // QUANT: joint RTN quantisation of the kept weights (grids per row and group).
 // The LDS image of block b (columns j0 = b*B .. j0+Bb) for inblock_kernel:
-// the live L and D entries of each lane's columns and 1 / L_jj, zeros
+// the live L and D entries of each lane's columns, 1 / L_jj and L_jj, zeros
 // elsewhere (entries of columns <= j, past the ragged end, and the padding
-// slot of each lane).  One launch covers every block of the sweep.
+// slot of each lane).  In the Y form D is replaced by U: the entries read
+// (column c > j) are the same positions of Q, whose strictly upper part U is.
+// One launch covers every block of the sweep.
 __global__ __launch_bounds__(256) void ib_image_kernel(const float* __restrict__ L, int64_t ldl,
                                                        const float* __restrict__ D, int64_t ldd, int k, int B,
                                                        float* __restrict__ img) {
@@ -666,24 +686,31 @@ __global__ __launch_bounds__(256) void ib_image_kernel(const float* __restrict__
         else
           v = L[(int64_t)(j0 + c) * ldl + j0 + j] * (1.0f / L[(int64_t)(j0 + j) * ldl + j0 + j]);
       }
-    } else if (e < IB_IMG_USED) {
+    } else if (e < 2 * kMaxBlock * IB_JS + kMaxBlock) {
       const int j = e - 2 * kMaxBlock * IB_JS;
       v = j < Bb ? 1.0f / L[(int64_t)(j0 + j) * ldl + j0 + j] : 1.f;
+    } else if (e < IB_IMG_USED) {
+      const int j = e - 2 * kMaxBlock * IB_JS - kMaxBlock;
+      v = j < Bb ? L[(int64_t)(j0 + j) * ldl + j0 + j] : 0.f;
     }
     out[e] = v;
   }
 }
 
-template <bool NM, bool QUANT>
+// YR: the Y form (no D; see ib_step).  Yp is the n x k matrix of the earlier
+// blocks' part of y; the E slot of EW then receives z = y - e with y the
+// whole of it (earlier blocks' part plus the block's own).
+template <bool NM, bool QUANT, bool YR>
 __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int64_t ew_ld,
                                                       const float* __restrict__ fac, const SelState* st, int mode,
                                                       const uint32_t* __restrict__ mask_in, float* __restrict__ EW,
                                                       uint8_t* __restrict__ bmask, IbOpts opt,
-                                                      float* __restrict__ scores_out, const float* __restrict__ img) {
+                                                      float* __restrict__ scores_out, const float* __restrict__ img,
+                                                      const float* __restrict__ Yp) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
   float* lq = sm;                       // [j][q][i]: L[j0+q+16i][j0+j] / L[j0+j][j0+j] where q+16i > j, else 0
   float* dq = sm + kMaxBlock * IB_JS;   // [j][q][i]: D[j0+j][j0+q+16i] where q+16i > j, else 0
-  float* il = dq + kMaxBlock * IB_JS;   // [j]: 1 / L[j0+j][j0+j]
+  float* il = dq + kMaxBlock * IB_JS;   // [j]: 1 / L[j0+j][j0+j], then [kMaxBlock + j]: L[j0+j][j0+j]
   const int tid = threadIdx.x;
   // The row's values and score factors are requested first; the block's LDS
   // image (written once per sweep by ib_image_kernel) then streams straight
@@ -692,13 +719,14 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
   const int q = tid & 15;
   const int row = blockIdx.x * IB_ROWS + (tid >> 4);
   const bool rv = row < n;
-  float wv[IB_I], fv[IB_I];
+  float wv[IB_I], fv[IB_I], yv[IB_I];
 #pragma unroll
   for (int i = 0; i < IB_I; ++i) {
     const int c = q + IB_Q * i;
     const bool cv = rv && c < Bb;
     wv[i] = Wo[cv ? (int64_t)row * k + j0 + c : 0];
     fv[i] = fac[c < Bb ? j0 + c : j0];
+    if constexpr (YR) yv[i] = cv ? Yp[(int64_t)row * k + j0 + c] : 0.f;
   }
   {
     const uint8_t* src = (const uint8_t*)img + (tid >> 6) * 1024 + (tid & 63) * 16;
@@ -723,6 +751,7 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
     const int c = q + IB_Q * i;
     const bool cv = rv && c < Bb;
     s.w[i] = cv ? wv[i] : 0.f;
+    s.y[i] = 0.f;
     s.e[i] = 0.f;
     s.w0[i] = 0.f;
     if constexpr (NM) {
@@ -748,18 +777,25 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
   const int ngroups = QUANT ? (k + opt.q_group - 1) / opt.q_group : 0;
   s.qs = 1.f;
   s.qz = 0.f;
-  ib_steps<NM, QUANT>(s, lq, dq, il, q, opt, row, rv, j0, Bb, ngroups, std::make_integer_sequence<int, kMaxBlock>{});
+  ib_steps<NM, QUANT, YR>(s, lq, dq, il, q, opt, row, rv, j0, Bb, ngroups, std::make_integer_sequence<int, kMaxBlock>{});
 #pragma unroll
   for (int i = 0; i < IB_I; ++i) {
     const int c = q + IB_Q * i;
     if (rv && c < Bb) {
       Wo[(int64_t)row * k + j0 + c] = s.w[i];
-      EW[(int64_t)row * ew_ld + c] = s.e[i];
+      EW[(int64_t)row * ew_ld + c] = YR ? (yv[i] + s.y[i]) - s.e[i] : s.e[i];
       EW[(int64_t)row * ew_ld + (ew_ld >> 1) + c] = s.w0[i];
       bmask[(int64_t)row * k + j0 + c] = (uint8_t)((s.kb[i] >> q) & 1u);
       if (NM && scores_out) scores_out[(int64_t)row * k + j0 + c] = s.sc[i];
     }
   }
+}
+
+__global__ void zero_kernel(float* __restrict__ p, int64_t cnt) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cnt / 4; i += stride)
+    ((float4*)p)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int64_t i = cnt / 4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cnt; i += stride) p[i] = 0.f;
 }
 
 __global__ void init_w_kernel(const void* W, int dtype, int64_t ldw, int n, int k, float* Wo) {
@@ -842,6 +878,19 @@ __global__ void finalize4_kernel(const float* Wo, const uint8_t* bmask, int n, i
 // brings every column beyond it up to date.  Each block still sees, before
 // its selection, every update owed to it.  EW holds the super-block's pairs,
 // row-major with stride 2 S: E of column sb0 + c at c, W0 at S + c.
+//
+// Y form (U given instead of D; no D = U L^T is formed).  With V the values
+// of the processed columns when they were processed (the W0 above), the
+// residual terms owed to column c sum to (V D)_c = sum_{i <= c} L_ci y_i,
+// y = V U (U strictly upper: y_i depends only on columns before i).  So the
+// sweep carries Y, the earlier blocks' part of y, beside W, and a column
+// before its block starts holds W_c + sum_{i < block} (y_i - e_i) L_ci.  At
+// the start of a block W[:, blk] += Y[:, blk] L[blk, blk]^T adds the terms of
+// the block's own columns (L lower), which makes W[:, blk] the values the D
+// form has there; the in-block kernel carries the block's own part of y and
+// leaves z = y - e in the E slot; the lazy products become
+// W[:, rest] += Z L[rest, blk]^T and Y[:, rest] += V U[blk, rest].  Same
+// products in count and size as the D form, with the k^3 / 3 of D saved.
 constexpr int kSuper = 512;
 
 int super_width(int B) { return B * (kSuper / B > 1 ? kSuper / B : 1); }
@@ -876,8 +925,10 @@ size_t sweep_ws_bytes(int64_t n, int64_t k, int B) { return carve(nullptr, n, k,
 duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64_t ldw, const float* L, int64_t ldl,
                      const float* D, int64_t ldd, const float* fac, double p_w, const SweepOpts& o, int B,
                      const uint32_t* mask_in, float* W_out, void* W_out_lowp, uint32_t* mask_out, float* scores_out,
-                     void* ws, hipStream_t s) {
+                     void* ws, hipStream_t s, const float* U, int64_t ldu, float* Y) {
   const SweepWs w = carve(ws, n, k, B);
+  const bool yr = U != nullptr;  // Y form
+  if (yr && (o.nm_n > 0 || o.q_bits > 0 || !Y)) return DUO_ERR_UNSUPPORTED;
   const int64_t nk = n * k;
   const int64_t S = super_width(B);
   auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
@@ -893,13 +944,19 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   hipLaunchKernelGGL(sel_reset_kernel, dim3(1), dim3(256), 0, s, w.st, w.hist);
   DUO_LAUNCH_CHECK();
   const size_t ib_lds = (size_t)IB_IMG * sizeof(float);
-  hipLaunchKernelGGL(ib_image_kernel, dim3((unsigned)cdiv(k, B), 16), dim3(256), 0, s, L, ldl, D, ldd, (int)k, B,
-                     w.img);
+  hipLaunchKernelGGL(ib_image_kernel, dim3((unsigned)cdiv(k, B), 16), dim3(256), 0, s, L, ldl, yr ? U : D,
+                     yr ? ldu : ldd, (int)k, B, w.img);
   DUO_LAUNCH_CHECK();
+  if (yr) {
+    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)(cdiv(nk, 1024) < 8192 ? cdiv(nk, 1024) : 8192)), dim3(256), 0, s,
+                       Y, nk);
+    DUO_LAUNCH_CHECK();
+  }
   const bool nm = o.nm_n > 0 && !mask_in;
   const bool qt = o.q_bits > 0;
-  auto ib_kern = nm ? (qt ? inblock_kernel<true, true> : inblock_kernel<true, false>)
-                    : (qt ? inblock_kernel<false, true> : inblock_kernel<false, false>);
+  auto ib_kern = yr ? inblock_kernel<false, false, true>
+                    : nm ? (qt ? inblock_kernel<true, true, false> : inblock_kernel<true, false, false>)
+                         : (qt ? inblock_kernel<false, true, false> : inblock_kernel<false, false, false>);
   const IbOpts ibo{o.nm_n, o.q_bits, qt ? o.q_group : kMaxBlock, o.q_scale, o.q_zero};
   if (duo_status d = set_max_lds((const void*)ib_kern, ib_lds); d != DUO_OK) return d;
   const size_t sel_lds = (size_t)(16 + (1 << kDigitR)) * sizeof(uint32_t) + (size_t)kRankMax * sizeof(unsigned long long);
@@ -937,6 +994,23 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
       mode = MODE_PRUNE_ALL;
     int idx_bits = 1;
     while (idx_bits < 31 && ((int64_t)1 << idx_bits) < total) ++idx_bits;
+    if (yr && j0 > 0) {
+      // Y form: W[:, blk] += Y[:, blk] L[blk, blk]^T (the residual terms of the
+      // block's own columns owed by the earlier blocks)
+      GemmDesc c{};
+      c.M = (int)n;
+      c.N = Bb;
+      c.C = W_out + j0;
+      c.ldc = k;
+      c.beta = 1.f;
+      c.tri = TRI_ALL;
+      c.nterms = 1;
+      c.t[0] = GemmTerm{Y + j0, k, 1, L + j0 * ldl + j0, ldl, 0, Bb, 1.f, KLO_ZERO, KHI_FULL};
+      prof_begin(DUO_PROF_TRAIL, s);
+      duo_status st = gemm_f32(c, s);
+      prof_end(DUO_PROF_TRAIL, s);
+      if (st != DUO_OK) return st;
+    }
     prof_begin(DUO_PROF_SELECT, s);
     if (mode == MODE_SELECT || (scores_out && mode != MODE_NM)) {
       hipLaunchKernelGGL(scores_out ? sel_hist_kernel<0> : hist_k, dim3(P), dim3(256), hist_lds, s,
@@ -957,7 +1031,8 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     const int64_t sb0 = j0 / S * S, sb1 = sb0 + S < k ? sb0 + S : k;
     hipLaunchKernelGGL(ib_kern, dim3((unsigned)cdiv(n, IB_ROWS)), dim3(256), ib_lds, s, W_out, (int)n, (int)k,
                        (int)j0, Bb, (int64_t)2 * S, fac, (const SelState*)w.st, mode, mask_in,
-                       w.EW + (j0 - sb0), w.bmask, ibo, scores_out, (const float*)(w.img + (j0 / B) * IB_IMG));
+                       w.EW + (j0 - sb0), w.bmask, ibo, scores_out, (const float*)(w.img + (j0 / B) * IB_IMG),
+                       (const float*)Y);
     DUO_LAUNCH_CHECK();
     prof_end(DUO_PROF_INBLOCK, s);
     // inside the super-block: columns [j1, sb1) from this block (K = Bb);
@@ -973,12 +1048,26 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
       g.beta = 1.f;
       g.tri = TRI_ALL;
       g.nterms = 2;
-      g.t[0] = GemmTerm{w.EW + (u0 - sb0), 2 * S, 1, L + c0 * ldl + u0, ldl, 0, K, -1.f, KLO_ZERO, KHI_FULL};
-      g.t[1] = GemmTerm{w.EW + S + (u0 - sb0), 2 * S, 1, D + u0 * ldd + c0, ldd, 1, K, 1.f, KLO_ZERO, KHI_FULL};
-      prof_begin(DUO_PROF_TRAIL, s);
-      duo_status st = gemm_f32(g, s);
-      prof_end(DUO_PROF_TRAIL, s);
-      if (st != DUO_OK) return st;
+      if (yr) {
+        // W[:, c0:c1] += Z L[c0:c1, u0:j1]^T and Y[:, c0:c1] += V U[u0:j1, c0:c1]
+        g.nterms = 1;
+        g.t[0] = GemmTerm{w.EW + (u0 - sb0), 2 * S, 1, L + c0 * ldl + u0, ldl, 0, K, 1.f, KLO_ZERO, KHI_FULL};
+        GemmDesc y = g;
+        y.C = Y + c0;
+        y.t[0] = GemmTerm{w.EW + S + (u0 - sb0), 2 * S, 1, U + u0 * ldu + c0, ldu, 1, K, 1.f, KLO_ZERO, KHI_FULL};
+        prof_begin(DUO_PROF_TRAIL, s);
+        duo_status st = gemm_f32(g, s);
+        if (st == DUO_OK) st = gemm_f32(y, s);
+        prof_end(DUO_PROF_TRAIL, s);
+        if (st != DUO_OK) return st;
+      } else {
+        g.t[0] = GemmTerm{w.EW + (u0 - sb0), 2 * S, 1, L + c0 * ldl + u0, ldl, 0, K, -1.f, KLO_ZERO, KHI_FULL};
+        g.t[1] = GemmTerm{w.EW + S + (u0 - sb0), 2 * S, 1, D + u0 * ldd + c0, ldd, 1, K, 1.f, KLO_ZERO, KHI_FULL};
+        prof_begin(DUO_PROF_TRAIL, s);
+        duo_status st = gemm_f32(g, s);
+        prof_end(DUO_PROF_TRAIL, s);
+        if (st != DUO_OK) return st;
+      }
     }
   }
   if (mask_out || W_out_lowp) {

@@ -48,7 +48,12 @@ class ActRule(ctypes.Structure):
 
 class SweepOpts(ctypes.Structure):
     _fields_ = [("nm_n", ctypes.c_int32), ("q_bits", ctypes.c_int32), ("q_group", ctypes.c_int32),
-                ("q_scale_out", ctypes.c_void_p), ("q_zero_out", ctypes.c_void_p)]
+                ("q_scale_out", ctypes.c_void_p), ("q_zero_out", ctypes.c_void_p),
+                ("residual_form", ctypes.c_int32)]
+
+
+# residual_form of duo_prune_layer: None / "auto", "d", "y"
+FORMS = {None: 0, "auto": 0, "d": 1, "y": 2}
 
 
 class CholInfo(ctypes.Structure):
@@ -329,9 +334,12 @@ def _sweep_outputs(W, want_lowp, want_mask, want_scores):
     return W_out, lowp, mask, scores
 
 
-def _opts(W, nm_n, quant):
-    """(SweepOpts or None, q_scale, q_zero) for the sweep; quant = (bits, group)."""
-    if not nm_n and quant is None:
+def _opts(W, nm_n, quant, form=None):
+    """(SweepOpts or None, q_scale, q_zero) for the sweep; quant = (bits, group);
+    form: the residual form (FORMS)."""
+    if form not in FORMS:
+        raise ValueError(f"form must be one of {list(FORMS)}")
+    if not nm_n and quant is None and not FORMS[form]:
         return None, None, None
     n, k = W.shape
     qs = qz = None
@@ -341,7 +349,7 @@ def _opts(W, nm_n, quant):
         qs = torch.empty((n, ng), dtype=torch.float32, device=W.device)
         qz = torch.empty((n, ng), dtype=torch.float32, device=W.device)
     o = SweepOpts(int(nm_n), bits, group, qs.data_ptr() if qs is not None else None,
-                  qz.data_ptr() if qz is not None else None)
+                  qz.data_ptr() if qz is not None else None, FORMS[form])
     return o, qs, qz
 
 
@@ -373,9 +381,10 @@ def duo_sweep(W, L, D, fac, w_sparsity, block=128, mask_in=None, want_lowp=False
 
 
 def duo_prune_layer(W, L, G, a, w_sparsity, block=128, mask_in=None, want_lowp=False, want_mask=True,
-                    want_scores=False, ws=None, out=None, nm_n=0, quant=None):
+                    want_scores=False, ws=None, out=None, nm_n=0, quant=None, form=None):
     """Returns (W_out, W_lowp, mask, scores), plus (q_scale, q_zero) when
-    quant = (bits, group) is given."""
+    quant = (bits, group) is given.  form: residual form, None (automatic),
+    "d" or "y"."""
     n, k = W.shape
     _same_device(W, L, G, a, mask_in, ws)
     _shape(L, (k, k), "L")
@@ -388,7 +397,7 @@ def duo_prune_layer(W, L, G, a, w_sparsity, block=128, mask_in=None, want_lowp=F
         ws = workspace(DUO_OP_PRUNE_LAYER, n, k, 0, block, W.device)
     W_out, lowp, mask, scores = out if out is not None else _sweep_outputs(W, want_lowp, want_mask, want_scores)
     _check_outputs((W_out, lowp, mask, scores), W)
-    o, qs, qz = _opts(W, nm_n, quant)
+    o, qs, qz = _opts(W, nm_n, quant, form)
     st = lib().duo_prune_layer(_ptr(W), _dtype(W), n, k, _ld(W), _ptr(L), _ld(L), _ptr(G), _ld(G), _ptr(a),
                                float(w_sparsity), ctypes.byref(o) if o is not None else None, int(block),
                                _ptr(mask_in), _ptr(W_out), _ptr(lowp), _ptr(mask), _ptr(scores), _ptr(ws),
@@ -473,7 +482,7 @@ def duo_permute_mask(words, k, col_idx, out=None):
 
 
 def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=None, want_lowp=True,
-                 act_order=False, nm=None, quant=None):
+                 act_order=False, nm=None, quant=None, form=None):
     """DuoGPT on one linear layer (stages 1-3 on the device).
 
     W: n x k (out x in), X: m x k token-major calibration input of the pruned
@@ -485,6 +494,7 @@ def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=N
     quant: None, or (bits, group) for joint RTN quantisation (Table 4); the
     grids (q_scale, q_zero: n x ceil(k / group)) are returned too (in the
     permuted channel order when act_order is set, as their groups are).
+    form: residual form of the sweep (duo_prune_layer), None for automatic.
     Returns dict(W_out fp32, W_lowp in W's dtype, mask (bool n x k), lam, and
     perm when act_order).
     """
@@ -508,7 +518,7 @@ def prune_linear(W, X, act_sparsity, w_sparsity, damp=0.01, block=128, X_dense=N
         a = duo_permute(a.view(1, k), None, perm).view(k)
         W = duo_permute(W, None, perm)
     lam, _ = duo_chol_inv(H, damp)
-    res = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp, nm_n=nm_n, quant=quant)
+    res = duo_prune_layer(W, H, G, a, w_sparsity, block, want_lowp=want_lowp, nm_n=nm_n, quant=quant, form=form)
     W_out, lowp, mask = res[0], res[1], res[2]
     if act_order:
         W_out = duo_permute(W_out, None, inv)

@@ -110,9 +110,21 @@ def test_chol_and_sweep_argument_errors(duo_lib):
 
     from paper_2506_20194_amd.duo import SweepOpts
 
-    def sweep(W=FAKE, dt=1, n=32, k=64, ldw=64, p=0.5, B=16, Wo=FAKE, fn=L.duo_sweep, nm=0, qb=0, qg=0):
-        o = ctypes.byref(SweepOpts(nm, qb, qg, None, None)) if (nm or qb or qg) else None
+    def sweep(W=FAKE, dt=1, n=32, k=64, ldw=64, p=0.5, B=16, Wo=FAKE, fn=L.duo_sweep, nm=0, qb=0, qg=0, form=0):
+        o = ctypes.byref(SweepOpts(nm, qb, qg, None, None, form)) if (nm or qb or qg or form) else None
         return fn(W, dt, n, k, ldw, FAKE, 64, FAKE, 64, FAKE, p, o, B, None, Wo, None, None, None, WS, big, None)
+
+    # residual form: 0 automatic, 1 D, 2 Y (duo_prune_layer only; not with N:4 or quantisation)
+    assert sweep(form=1) == NODEV
+    assert sweep(form=2) == E
+    assert sweep(form=3) == E
+    assert sweep(form=-1) == E
+    P = L.duo_prune_layer
+    assert sweep(fn=P, form=1) == NODEV
+    assert sweep(fn=P, form=2) == NODEV
+    assert sweep(fn=P, form=3) == E
+    assert sweep(fn=P, form=2, nm=2) == duo_lib.DUO_ERR_UNSUPPORTED
+    assert sweep(fn=P, form=2, qb=4, qg=16) == duo_lib.DUO_ERR_UNSUPPORTED
 
     for fn in (L.duo_sweep, L.duo_prune_layer):
         assert sweep(fn=fn) == NODEV

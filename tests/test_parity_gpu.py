@@ -337,11 +337,79 @@ def test_sweep_ties(duo):
 
 
 # ---------------------------------------------------------------------------
+# stage 3 through duo_prune_layer in both residual forms (D formed, or the
+# sweep carrying Y = W0 U instead)
+# ---------------------------------------------------------------------------
+
+def _layer_terms(n, k, m, seed):
+    W, X = inputs(n, k, m, torch.bfloat16, seed=seed, outliers=2)
+    H, G, a = R.hessian_terms(X.float().numpy(), 0.5)
+    L, _ = R.inverse_cholesky(H, 0.01)
+    L32, G32, a32 = (np.ascontiguousarray(x.astype(np.float32)) for x in (L, G, a))
+    fac, D, _ = R.score_terms(G32.astype(np.float64), L32.astype(np.float64), a32.astype(np.float64))
+    return W, L32, G32, a32, D, fac
+
+
+@pytest.mark.parametrize("form", ["d", "y"])
+@pytest.mark.parametrize("n,k,B", [(100, 300, 128), (64, 256, 64), (37, 200, 48), (16, 64, 1), (300, 130, 128),
+                                   (96, 1152, 128), (80, 1344, 64), (192, 576, 128)])
+def test_prune_layer_forced_mask_forms(duo, n, k, B, form):
+    say("prune_layer forced", n, k, B, form)
+    W, L, G, a, D, fac = _layer_terms(n, k, 3 * k, seed=n + 3 * k)
+    Wf = W.float().numpy()
+    _, keep = R.sweep_blocked(Wf, L, D, fac, 0.5, B)
+    Wr, _ = R.sweep_blocked(Wf, L, D, fac, 0.5, B, mask_in=keep)
+    t = lambda x: torch.tensor(x, device=DEV)
+    W_out, _, mask, _ = duo.duo_prune_layer(W.to(DEV), t(L), t(G), t(a), 0.5, B, mask_in=_mask_words(keep).to(DEV),
+                                            form=form)
+    assert np.array_equal(duo.unpack_mask(mask, k).cpu().numpy(), keep)
+    assert relfro(f64(W_out), Wr) < 1e-5, relfro(f64(W_out), Wr)
+    assert np.all(f64(W_out)[~keep] == 0.0)
+
+
+@pytest.mark.parametrize("form", ["d", "y"])
+@pytest.mark.parametrize("n,k,B,p_w", [(200, 336, 128, 0.5), (300, 1152, 128, 0.55), (150, 640, 64, 0.5),
+                                       (90, 544, 16, 0.45), (4200, 256, 128, 0.5), (50, 160, 32, 0.0),
+                                       (40, 96, 16, 1.0), (320, 1728, 64, 0.5)])
+def test_prune_layer_select_forms(duo, n, k, B, p_w, form):
+    """Whole stage 3 (Q, fac, selection, sweep) against the oracle's sweep on
+    the same L, G, a; several super-blocks, ragged rows and blocks."""
+    say("prune_layer select", n, k, B, p_w, form)
+    W, L, G, a, D, fac = _layer_terms(n, k, 3 * k, seed=11 * n + k)
+    Wf = W.float().numpy()
+    Wr, keep_r = R.sweep_blocked(Wf, L, D, fac, p_w, B)
+    t = lambda x: torch.tensor(x, device=DEV)
+    W_out, _, mask, _ = duo.duo_prune_layer(W.to(DEV), t(L), t(G), t(a), p_w, B, form=form)
+    keep = duo.unpack_mask(mask, k).cpu().numpy()
+    assert np.isfinite(f64(W_out)).all()
+    assert (~keep).sum() == (~keep_r).sum()
+    assert np.mean(keep == keep_r) >= 0.999
+    _attribute(Wf, L, D, fac, p_w, B, keep)
+    if np.array_equal(keep, keep_r):
+        assert relfro(f64(W_out), Wr) < 1e-5, relfro(f64(W_out), Wr)
+
+
+def test_prune_layer_forms_agree(duo):
+    """The two forms on one layer: the same mask and weights within fp32
+    rounding (k = 2048, 4 super-blocks of 512)."""
+    say("prune_layer forms agree")
+    n, k, B = 256, 2048, 128
+    W, L, G, a, D, fac = _layer_terms(n, k, 3 * k, seed=77)
+    t = lambda x: torch.tensor(x, device=DEV)
+    Wd, _, md, _ = duo.duo_prune_layer(W.to(DEV), t(L), t(G), t(a), 0.6, B, form="d")
+    Wy, _, my, _ = duo.duo_prune_layer(W.to(DEV), t(L), t(G), t(a), 0.6, B, form="y")
+    kd, ky = (duo.unpack_mask(x, k).cpu().numpy() for x in (md, my))
+    assert np.mean(kd == ky) >= 0.999
+    if np.array_equal(kd, ky):
+        assert relfro(f64(Wy), f64(Wd)) < 1e-5
+
+
+# ---------------------------------------------------------------------------
 # whole layer
 # ---------------------------------------------------------------------------
 
-def _layer_case(duo, W, X, p_x, p_w, B, damp=0.01):
-    out = duo.prune_linear(W.to(DEV), X.to(DEV), p_x, p_w, damp=damp, block=B)
+def _layer_case(duo, W, X, p_x, p_w, B, damp=0.01, form=None):
+    out = duo.prune_linear(W.to(DEV), X.to(DEV), p_x, p_w, damp=damp, block=B, form=form)
     torch.cuda.synchronize()
     ref = R.prune_layer(W.float().numpy(), X.float().numpy(), p_x, p_w, damp=damp, B=B)
     keep = out["mask"].cpu().numpy()
@@ -365,11 +433,12 @@ def test_layer_tiny_linear_config(duo):
     assert abs(out["lam"] - ref["lam"]) <= 1e-5 * ref["lam"]
 
 
+@pytest.mark.parametrize("form", [None, "y"])
 @pytest.mark.parametrize("n,k,m,B", [(192, 384, 1536, 128), (100, 200, 700, 64)])
-def test_layer_bf16(duo, n, k, m, B):
-    say("layer bf16", n, k, m, B)
+def test_layer_bf16(duo, n, k, m, B, form):
+    say("layer bf16", n, k, m, B, form)
     W, X = inputs(n, k, m, torch.bfloat16, seed=n * k, outliers=3)
-    out, ref, keep, Wg, agree, J_g, J_r = _layer_case(duo, W, X, 0.5, 0.5, B)
+    out, ref, keep, Wg, agree, J_g, J_r = _layer_case(duo, W, X, 0.5, 0.5, B, form=form)
     assert agree >= 0.999, agree
     assert relfro(Wg, ref["W_hat"]) < 1e-3
     assert abs(J_g - J_r) <= 1e-3 * J_r
@@ -379,10 +448,11 @@ def test_layer_bf16(duo, n, k, m, B):
     assert J_g < R.objective(W.float().numpy(), Wm, X.float().numpy(), 0.5)
 
 
-def test_zero_sparsity_returns_weights_unchanged(duo):
-    say("zero sparsity")
+@pytest.mark.parametrize("form", [None, "y"])
+def test_zero_sparsity_returns_weights_unchanged(duo, form):
+    say("zero sparsity", form)
     W, X = inputs(64, 256, 800, torch.bfloat16, seed=3)
-    out = duo.prune_linear(W.to(DEV), X.to(DEV), 0.0, 0.0, block=64)
+    out = duo.prune_linear(W.to(DEV), X.to(DEV), 0.0, 0.0, block=64, form=form)
     assert torch.equal(out["W_out"].cpu(), W.float())
     assert out["mask"].all()
 
