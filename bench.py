@@ -471,13 +471,19 @@ def main():
     sweep_bytes = 16 * n * k
     sweep_ms = per_step("select") + per_step("inblock")
     sweep_gbs = sweep_bytes / (sweep_ms * 1e-3) / 1e9
-    trail_flop = 2 * n * k * (k - B)
+    # residual form of the sweep: the library's automatic choice (DUO_FORM_AUTO)
+    # is the Y form (no D) for the unstructured, unquantised sweep from k = 6144
+    yform = not args.nm and not args.quant and k >= 6144
+    # lazy updates: the two terms (E L^T and W0 D, or (Y - E) L^T and W0 U) of
+    # each block over the columns after it, 2 n k (k - B) flop; the Y form adds
+    # the block-start products Y[:, blk] L[blk, blk]^T, 2 n B (k - B)
+    trail_flop = 2 * n * k * (k - B) + (2 * n * B * (k - B) if yform else 0)
     trail_tflops = trail_flop / (per_step("trail") * 1e-3) / 1e12
     # A3 + A4 on the implemented route: UL factorisation k^3/3 + triangular
-    # inverse k^3/3 + upper triangle of Q = G L k^3/3 + D = U L^T k^3/3; the
-    # survey's count (8/3) k^3 is for the plain route (explicit inverse,
-    # Cholesky, full products) and is printed beside it
-    chol_score_flop = 4 * k ** 3 / 3
+    # inverse k^3/3 + upper triangle of Q = G L k^3/3 (+ D = U L^T k^3/3 in the
+    # D form); the survey's count (8/3) k^3 is for the plain route (explicit
+    # inverse, Cholesky, full products) and is printed beside it
+    chol_score_flop = (3 if yform else 4) * k ** 3 / 3
     chol_score_flop_plain = 8 * k ** 3 / 3
     # the Gram kernel multiplies in the calibration input's precision: bf16
     # MFMA for bf16 inputs, fp32 MFMA for fp32 inputs
@@ -499,7 +505,8 @@ def main():
                    "block": B, "damp": c["damp"], "x_dtype": str(c["x_dtype"]).replace("torch.", ""),
                    "inputs": c["kind"], "act_order": bool(args.act_order),
                    "mask": f"{args.nm}:4" if args.nm else "unstructured",
-                   "quant": f"int{args.quant} g128" if args.quant else None, "parallelism": "single GPU"},
+                   "quant": f"int{args.quant} g128" if args.quant else None,
+                   "residual_form": "Y" if yform else "D", "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "gram_kernel (H, G)", "achieved": gram_tflops,
                      "peak": gram_peak, "unit": "TFLOP/s", "frac": gram_tflops / gram_peak,
                      "traffic": gram_traffic(args.workload), "ms_per_launch": per("gram"), "flop_per_launch": gram_flop_step / gram_launches},
@@ -511,7 +518,8 @@ def main():
         "trailing_frac": trail_tflops / PEAK_FP32_TFLOPS,
         "chol_score_tflops": chol_score_flop / ((per_step("chol") + per_step("score")) * 1e-3) / 1e12,
         "chol_score_frac": chol_score_flop / ((per_step("chol") + per_step("score")) * 1e-3) / 1e12 / PEAK_FP32_TFLOPS,
-        "chol_score_flop_count": "(4/3) k^3 (implemented route); plain route (8/3) k^3 gives "
+        "chol_score_flop_count": ("k^3 (implemented route, Y form: no D)" if yform else "(4/3) k^3 (implemented route)")
+                                 + "; plain route (8/3) k^3 gives "
                                  f"{chol_score_flop_plain / ((per_step('chol') + per_step('score')) * 1e-3) / 1e12:.1f} TFLOP/s",
         "stage_ms": {name: per_step(name) for name in duo.PROF},
         "ms_per_step_median": ms_step_median,
