@@ -438,7 +438,9 @@ __device__ inline void fast_term(const GemmTerm& t, int i0, int j0, uint8_t* sme
 // N <= 128): a workgroup takes both column quarters of a row quarter, runs
 // both K loops and only then writes, so no workgroup overwrites columns that
 // another one of the same rows has still to read.
-template <int TF, bool B1R, bool B2R, bool TWO, bool PAIR>
+// DUAL: two independent one-term products (GemmDesc::dual), blockIdx.y
+// selects which.
+template <int TF, bool B1R, bool B2R, bool TWO, bool PAIR, bool DUAL>
 __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc d, int ntiles) {
   using G = FGeo<TF>;
   constexpr int NB = G::NB, SUB = kTile / TF;
@@ -447,7 +449,10 @@ __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];  // the ring; reused by the epilogue
   const int id = d.order == ORDER_XCD ? xcd_remap_g(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   if (id >= ntiles) return;
-  if (blockIdx.y) {
+  const int prob = DUAL ? (int)blockIdx.y : 0;  // the product this workgroup computes
+  if (DUAL) {
+    if (prob) d.C = d.C2;
+  } else if (blockIdx.y) {
     const int64_t z = blockIdx.y;
     d.C += z * d.sC;
     d.t[0].A += z * d.sA[0];
@@ -474,13 +479,16 @@ __global__ __launch_bounds__(256, FGeo<TF>::OCC) void gemm_fast_kernel(GemmDesc 
   // fragments go from LDS to the MFMAs untouched.  For alpha = +-1 the result
   // is bit for bit that of accumulating the scaled products.
   const float a0 = d.t[0].alpha, a1 = d.t[1].alpha;
-  const bool two = TWO && a1 != 0.f && d.t[1].K > 0;
-  const float ae = two ? a1 : a0, r01 = two ? a0 / a1 : 1.f;
+  const bool two = TWO && !DUAL && a1 != 0.f && d.t[1].K > 0;
+  const float ae = (DUAL && prob) || two ? a1 : a0, r01 = two ? a0 / a1 : 1.f;
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int j0 = jb + q * TF;
     if (j0 < d.N) {  // uniform
-      fast_term<TF, B1R>(d.t[0], i0, j0, smem, acc[q]);
+      if (DUAL && prob)
+        fast_term<TF, B2R>(d.t[1], i0, j0, smem, acc[q]);
+      else
+        fast_term<TF, B1R>(d.t[0], i0, j0, smem, acc[q]);
       if (two) {
         if (r01 != 1.f) {
 #pragma unroll
@@ -561,6 +569,7 @@ template <int TF>
 bool fast_ok(const GemmDesc& d) {
   if (d.M % TF != 0 || d.N % TF != 0 || (d.ldc & 3) != 0 || (reinterpret_cast<uintptr_t>(d.C) & 15) != 0)
     return false;
+  if (d.dual && (reinterpret_cast<uintptr_t>(d.C2) & 15) != 0) return false;
   for (int i = 0; i < d.nterms; ++i) {
     const GemmTerm& t = d.t[i];
     if (!t.a_row || t.K % FK != 0 || (t.lda & 3) != 0 || (t.ldb & 3) != 0) return false;
@@ -573,7 +582,17 @@ bool fast_ok(const GemmDesc& d) {
 
 template <int TF, bool B1R, bool B2R, bool TWO, bool PAIR = false>
 duo_status launch_fast(const GemmDesc& d, int ids, int nb, hipStream_t s) {
-  auto kern = gemm_fast_kernel<TF, B1R, B2R, TWO, PAIR>;
+  if constexpr (!PAIR && TWO && !B1R && B2R) {
+    if (d.dual) {
+      auto kern = gemm_fast_kernel<TF, B1R, B2R, TWO, false, true>;
+      if (duo_status st = set_max_lds((const void*)kern, FGeo<TF>::LDS); st != DUO_OK) return st;
+      hipLaunchKernelGGL(kern, dim3((unsigned)rup(ids, 8), nb), dim3(256), FGeo<TF>::LDS, s, d, ids);
+      DUO_LAUNCH_CHECK();
+      return DUO_OK;
+    }
+  }
+  if (d.dual) return DUO_ERR_UNSUPPORTED;
+  auto kern = gemm_fast_kernel<TF, B1R, B2R, TWO, PAIR, false>;
   if (duo_status st = set_max_lds((const void*)kern, FGeo<TF>::LDS); st != DUO_OK) return st;
   hipLaunchKernelGGL(kern, dim3((unsigned)rup(ids, 8), nb), dim3(256), FGeo<TF>::LDS, s, d, ids);
   DUO_LAUNCH_CHECK();
@@ -585,7 +604,7 @@ duo_status launch(const GemmDesc& d, hipStream_t s) {
   const int tm = (int)cdiv(d.M, kTile), tn = (int)cdiv(d.N, kTile);
   const int ntiles = d.tri == TRI_ALL ? tm * tn : tm * (tm + 1) / 2;
   if (ntiles <= 0) return DUO_OK;
-  const int nb = d.batch > 1 ? d.batch : 1;
+  const int nb = d.dual ? 2 : (d.batch > 1 ? d.batch : 1);
   if (d.inplace) {
     if (d.N > kTile) return DUO_ERR_UNSUPPORTED;
     if constexpr (A1R && A2R && !B1R && !B2R) {
@@ -601,11 +620,8 @@ duo_status launch(const GemmDesc& d, hipStream_t s) {
     return DUO_OK;
   }
   if constexpr (A1R && A2R) {
-    if ((int64_t)ntiles * nb >= kSmallTiles) {
-      if (fast_ok<kTile>(d)) return launch_fast<kTile, B1R, B2R, TWO>(d, ntiles, nb, s);
-    } else if (fast_ok<64>(d)) {
-      return launch_fast<64, B1R, B2R, TWO>(d, 4 * ntiles, nb, s);
-    }
+    if ((int64_t)ntiles * nb >= kSmallTiles && fast_ok<kTile>(d)) return launch_fast<kTile, B1R, B2R, TWO>(d, ntiles, nb, s);
+    if (fast_ok<64>(d)) return launch_fast<64, B1R, B2R, TWO>(d, 4 * ntiles, nb, s);
   }
   if ((int64_t)ntiles * nb < kSmallTiles) {
     const int grid = (int)rup(4 * ntiles, 8);
@@ -623,6 +639,20 @@ duo_status launch(const GemmDesc& d, hipStream_t s) {
 duo_status gemm_f32(const GemmDesc& d, hipStream_t s) {
   if (d.M <= 0 || d.N <= 0) return DUO_OK;
   if (d.tri != TRI_ALL && d.M != d.N) return DUO_ERR_UNSUPPORTED;
+  if (d.dual) {
+    if (d.nterms != 2 || d.batch > 1 || d.inplace || !d.C2) return DUO_ERR_UNSUPPORTED;
+    // one launch when the fast path takes both (A row-major, B of the first
+    // K-contiguous and of the second row-major); otherwise two
+    if (d.t[0].a_row && !d.t[0].b_row && d.t[1].a_row && d.t[1].b_row && fast_ok<64>(d))
+      return launch<true, false, true, true, true>(d, s);
+    GemmDesc p = d;
+    p.dual = 0;
+    p.nterms = 1;
+    if (duo_status st = gemm_f32(p, s); st != DUO_OK) return st;
+    p.C = d.C2;
+    p.t[0] = d.t[1];
+    return gemm_f32(p, s);
+  }
   const int c1 = d.t[0].a_row * 2 + d.t[0].b_row;
   if (d.nterms == 1) {
     // one-term products run the two-term kernel with an empty second term

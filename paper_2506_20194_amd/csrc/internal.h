@@ -75,6 +75,11 @@ struct GemmDesc {
   // workgroup must then own whole rows of C, so the launch uses 128-wide
   // tiles (a quarter tile would overwrite columns its row neighbour still reads)
   int inplace;
+  // two independent one-term products in one launch (two terms, batch 0):
+  // C = beta C + alpha0 A0 B0 and C2 = beta C2 + alpha1 A1 B1, C2 with the
+  // row stride ldc (for two products that would otherwise be two launches)
+  int dual;
+  float* C2;
 };
 enum { ORDER_XCD = 0, ORDER_PLAIN = 1, ORDER_DIAG = 2 };
 

@@ -1049,15 +1049,14 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
       g.tri = TRI_ALL;
       g.nterms = 2;
       if (yr) {
-        // W[:, c0:c1] += Z L[c0:c1, u0:j1]^T and Y[:, c0:c1] += V U[u0:j1, c0:c1]
-        g.nterms = 1;
+        // W[:, c0:c1] += Z L[c0:c1, u0:j1]^T and Y[:, c0:c1] += V U[u0:j1, c0:c1]:
+        // independent, one launch
+        g.dual = 1;
+        g.C2 = Y + c0;
         g.t[0] = GemmTerm{w.EW + (u0 - sb0), 2 * S, 1, L + c0 * ldl + u0, ldl, 0, K, 1.f, KLO_ZERO, KHI_FULL};
-        GemmDesc y = g;
-        y.C = Y + c0;
-        y.t[0] = GemmTerm{w.EW + S + (u0 - sb0), 2 * S, 1, U + u0 * ldu + c0, ldu, 1, K, 1.f, KLO_ZERO, KHI_FULL};
+        g.t[1] = GemmTerm{w.EW + S + (u0 - sb0), 2 * S, 1, U + u0 * ldu + c0, ldu, 1, K, 1.f, KLO_ZERO, KHI_FULL};
         prof_begin(DUO_PROF_TRAIL, s);
         duo_status st = gemm_f32(g, s);
-        if (st == DUO_OK) st = gemm_f32(y, s);
         prof_end(DUO_PROF_TRAIL, s);
         if (st != DUO_OK) return st;
       } else {
