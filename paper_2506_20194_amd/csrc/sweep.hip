@@ -473,7 +473,8 @@ __global__ __launch_bounds__(256) void sel_resolve_kernel(const float* __restric
 // ---------------------------------------------------------------------------
 constexpr int IB_Q = 16;                  // lanes per row (one DPP row)
 constexpr int IB_I = kMaxBlock / IB_Q;    // columns per lane: c = q + 16 i
-constexpr int IB_ROWS = 256 / IB_Q;       // rows per workgroup
+constexpr int IB_ROWS = 256 / IB_Q;       // rows per workgroup (IB_ROWS2 for row counts past one round)
+constexpr int IB_ROWS2 = 512 / IB_Q;
 constexpr int IB_QS = IB_I + 1;           // LDS stride between lanes (odd: no bank conflicts)
 constexpr int IB_JS = IB_Q * IB_QS;       // LDS floats per column step
 // LDS image of one block's operands, [lq | dq | il | lj], padded to whole 4 KB
@@ -700,8 +701,11 @@ __global__ __launch_bounds__(256) void ib_image_kernel(const float* __restrict__
 // YR: the Y form (no D; see ib_step).  Yp is the n x k matrix of the earlier
 // blocks' part of y; the E slot of EW then receives z = y - e with y the
 // whole of it (earlier blocks' part plus the block's own).
-template <bool NM, bool QUANT, bool YR>
-__global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int64_t ew_ld,
+// ROWS rows per workgroup (16 lanes each): IB_ROWS, or IB_ROWS2 when the
+// rows would otherwise need more than one workgroup per CU (the LDS image
+// allows one), so that a block finishes in one round over the CUs.
+template <bool NM, bool QUANT, bool YR, int ROWS>
+__global__ __launch_bounds__(ROWS * IB_Q) void inblock_kernel(float* __restrict__ Wo, int n, int k, int j0, int Bb, int64_t ew_ld,
                                                       const float* __restrict__ fac, const SelState* st, int mode,
                                                       const uint32_t* __restrict__ mask_in, float* __restrict__ EW,
                                                       uint8_t* __restrict__ bmask, IbOpts opt,
@@ -717,7 +721,7 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
   // into LDS (global_load_lds, 16 bytes per lane, no register staging), so
   // the two latencies overlap.
   const int q = tid & 15;
-  const int row = blockIdx.x * IB_ROWS + (tid >> 4);
+  const int row = blockIdx.x * ROWS + (tid >> 4);
   const bool rv = row < n;
   float wv[IB_I], fv[IB_I], yv[IB_I];
 #pragma unroll
@@ -728,7 +732,7 @@ __global__ __launch_bounds__(256) void inblock_kernel(float* __restrict__ Wo, in
     fv[i] = fac[c < Bb ? j0 + c : j0];
     if constexpr (YR) yv[i] = cv ? Yp[(int64_t)row * k + j0 + c] : 0.f;
   }
-  {
+  if (tid < 256) {  // the image in 4 KB rows of 256 x 16 bytes
     const uint8_t* src = (const uint8_t*)img + (tid >> 6) * 1024 + (tid & 63) * 16;
     uint8_t* dst = (uint8_t*)sm + (tid >> 6) * 1024;
 #pragma unroll
@@ -954,9 +958,12 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   }
   const bool nm = o.nm_n > 0 && !mask_in;
   const bool qt = o.q_bits > 0;
-  auto ib_kern = yr ? inblock_kernel<false, false, true>
-                    : nm ? (qt ? inblock_kernel<true, true, false> : inblock_kernel<true, false, false>)
-                         : (qt ? inblock_kernel<false, true, false> : inblock_kernel<false, false, false>);
+  const bool wide = !nm && !qt && cdiv(n, IB_ROWS) > 256;  // 32 rows per workgroup
+  const int ib_rows = wide ? IB_ROWS2 : IB_ROWS;
+  auto ib_kern = yr ? (wide ? inblock_kernel<false, false, true, IB_ROWS2> : inblock_kernel<false, false, true, IB_ROWS>)
+                 : nm ? (qt ? inblock_kernel<true, true, false, IB_ROWS> : inblock_kernel<true, false, false, IB_ROWS>)
+                 : qt ? inblock_kernel<false, true, false, IB_ROWS>
+                      : (wide ? inblock_kernel<false, false, false, IB_ROWS2> : inblock_kernel<false, false, false, IB_ROWS>);
   const IbOpts ibo{o.nm_n, o.q_bits, qt ? o.q_group : kMaxBlock, o.q_scale, o.q_zero};
   if (duo_status d = set_max_lds((const void*)ib_kern, ib_lds); d != DUO_OK) return d;
   const size_t sel_lds = (size_t)(16 + (1 << kDigitR)) * sizeof(uint32_t) + (size_t)kRankMax * sizeof(unsigned long long);
@@ -1029,7 +1036,7 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
     prof_end(DUO_PROF_SELECT, s);
     prof_begin(DUO_PROF_INBLOCK, s);
     const int64_t sb0 = j0 / S * S, sb1 = sb0 + S < k ? sb0 + S : k;
-    hipLaunchKernelGGL(ib_kern, dim3((unsigned)cdiv(n, IB_ROWS)), dim3(256), ib_lds, s, W_out, (int)n, (int)k,
+    hipLaunchKernelGGL(ib_kern, dim3((unsigned)cdiv(n, ib_rows)), dim3(ib_rows * IB_Q), ib_lds, s, W_out, (int)n, (int)k,
                        (int)j0, Bb, (int64_t)2 * S, fac, (const SelState*)w.st, mode, mask_in,
                        w.EW + (j0 - sb0), w.bmask, ibo, scores_out, (const float*)(w.img + (j0 / B) * IB_IMG),
                        (const float*)Y);
