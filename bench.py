@@ -82,6 +82,8 @@ def parse():
                     help="joint RTN quantisation of the kept weights (Table 4), one grid per row and 128 columns")
     ap.add_argument("--act-order", action="store_true",
                     help="process channels by decreasing Hessian diagonal (App. B); adds the gathers to the step")
+    ap.add_argument("--form", choices=["auto", "d", "y"], default="auto",
+                    help="residual form of the sweep (duo_prune_layer's residual_form); auto: the library's choice")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a device-to-device copy of MIB MiB (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -400,7 +402,7 @@ def main():
             duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h)
             info = duo.duo_chol_inv(H, c["damp"], ws=ws_c, sync=check)
             duo.duo_prune_layer(W, H, G, a, c["p_w"], B, ws=ws_p, out=(W_out, lowp, mask, None), nm_n=args.nm,
-                                quant=(args.quant, 128) if args.quant else None)
+                                quant=(args.quant, 128) if args.quant else None, form=args.form)
             return info
         hdiag.zero_()
         duo.duo_hessian_accum(X, H, c["p_x"], G=G, a=a, ws=ws_h, hdiag=hdiag)
@@ -410,7 +412,8 @@ def main():
         duo.duo_permute(a.view(1, k), None, perm, out=ap_)
         duo.duo_permute(W, None, perm, out=Wp)
         info = duo.duo_chol_inv(Hp, c["damp"], ws=ws_c, sync=check)
-        duo.duo_prune_layer(Wp, Hp, Gp, ap_.view(k), c["p_w"], B, ws=ws_p, out=(W_out_p, lowp_p, mask_p, None))
+        duo.duo_prune_layer(Wp, Hp, Gp, ap_.view(k), c["p_w"], B, ws=ws_p, out=(W_out_p, lowp_p, mask_p, None),
+                            form=args.form)
         duo.duo_permute(W_out_p, None, inv, out=W_out)
         duo.duo_permute(lowp_p, None, inv, out=lowp)
         duo.duo_permute_mask(mask_p, k, inv, out=mask)
@@ -473,7 +476,7 @@ def main():
     sweep_gbs = sweep_bytes / (sweep_ms * 1e-3) / 1e9
     # residual form of the sweep: the library's automatic choice (DUO_FORM_AUTO)
     # is the Y form (no D) for the unstructured, unquantised sweep from k = 6144
-    yform = not args.nm and not args.quant and k >= 6144
+    yform = args.form == "y" or (args.form == "auto" and not args.nm and not args.quant and k >= 6144)
     # lazy updates: the two terms (E L^T and W0 D, or (Y - E) L^T and W0 U) of
     # each block over the columns after it, 2 n k (k - B) flop; the Y form adds
     # the block-start products Y[:, blk] L[blk, blk]^T, 2 n B (k - B)
