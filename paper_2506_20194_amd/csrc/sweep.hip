@@ -895,7 +895,10 @@ __global__ void finalize4_kernel(const float* Wo, const uint8_t* bmask, int n, i
 // leaves z = y - e in the E slot; the lazy products become
 // W[:, rest] += Z L[rest, blk]^T and Y[:, rest] += V U[blk, rest].  Same
 // products in count and size as the D form, with the k^3 / 3 of D saved.
-constexpr int kSuper = 512;
+// (1024 columns: at the 70B shape the Y form's two passes over C per
+// super-block cost 4.5 ms less per layer than with 512; 2048 gained 0.8 ms
+// more there and lost at k = 4096 and 11008)
+constexpr int kSuper = 1024;
 
 int super_width(int B) { return B * (kSuper / B > 1 ? kSuper / B : 1); }
 

@@ -283,10 +283,12 @@ def test_sweep_select(duo, n, k, B, p_w):
                                        (50, 160, 32, 0.0), (40, 96, 16, 1.0),
                                        # n, k multiples of 64 but not of 128: the trailing
                                        # products on 64 tiles with 128-grid tiles half outside
-                                       (192, 576, 128, 0.5), (320, 1728, 64, 0.5)])
+                                       (192, 576, 128, 0.5), (320, 1728, 64, 0.5),
+                                       # three 1024-column super-blocks, the last one ragged
+                                       (64, 2304, 128, 0.5), (40, 2200, 16, 0.45)])
 def test_sweep_select_shapes(duo, n, k, B, p_w):
-    """Rows and the last block ragged, several 512-column super-blocks, 8 and
-    32 blocks per super-block, row counts of several selection workgroups'
+    """Rows and the last block ragged, several 1024-column super-blocks, 8 and
+    64 blocks per super-block, row counts of several selection workgroups'
     batches, and no or every weight pruned."""
     say("sweep select shapes", n, k, B, p_w)
     W, X, L, D, fac = _sweep_inputs(n, k, 3 * k, seed=5 * n + k)
@@ -352,7 +354,8 @@ def _layer_terms(n, k, m, seed):
 
 @pytest.mark.parametrize("form", ["d", "y"])
 @pytest.mark.parametrize("n,k,B", [(100, 300, 128), (64, 256, 64), (37, 200, 48), (16, 64, 1), (300, 130, 128),
-                                   (96, 1152, 128), (80, 1344, 64), (192, 576, 128)])
+                                   (96, 1152, 128), (80, 1344, 64), (192, 576, 128), (48, 2304, 128),
+                                   (40, 2200, 32)])
 def test_prune_layer_forced_mask_forms(duo, n, k, B, form):
     say("prune_layer forced", n, k, B, form)
     W, L, G, a, D, fac = _layer_terms(n, k, 3 * k, seed=n + 3 * k)
@@ -370,7 +373,8 @@ def test_prune_layer_forced_mask_forms(duo, n, k, B, form):
 @pytest.mark.parametrize("form", ["d", "y"])
 @pytest.mark.parametrize("n,k,B,p_w", [(200, 336, 128, 0.5), (300, 1152, 128, 0.55), (150, 640, 64, 0.5),
                                        (90, 544, 16, 0.45), (4200, 256, 128, 0.5), (50, 160, 32, 0.0),
-                                       (40, 96, 16, 1.0), (320, 1728, 64, 0.5)])
+                                       (40, 96, 16, 1.0), (320, 1728, 64, 0.5), (64, 2304, 128, 0.5),
+                                       (40, 2200, 16, 0.45)])
 def test_prune_layer_select_forms(duo, n, k, B, p_w, form):
     """Whole stage 3 (Q, fac, selection, sweep) against the oracle's sweep on
     the same L, G, a; several super-blocks, ragged rows and blocks."""
@@ -391,7 +395,7 @@ def test_prune_layer_select_forms(duo, n, k, B, p_w, form):
 
 def test_prune_layer_forms_agree(duo):
     """The two forms on one layer: the same mask and weights within fp32
-    rounding (k = 2048, 4 super-blocks of 512)."""
+    rounding (k = 2048, 2 super-blocks of 1024)."""
     say("prune_layer forms agree")
     n, k, B = 256, 2048, 128
     W, L, G, a, D, fac = _layer_terms(n, k, 3 * k, seed=77)
