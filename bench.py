@@ -31,9 +31,9 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # were taken on: any change to that file makes the figure unknown (null).
 GRAM_TRAFFIC = {
     "source": "paper_2506_20194_amd/csrc/hessian.hip",
-    "sha256": "e730e2ceb5d78a9e9651f63916cc13c7cf9b450e7cd01dde86780a9baf5f2fce",
+    "sha256": "202eba901bef5e1c496d6572f75678682904910e2b08397c71887c8cd76fa3d2",
     "workload": "llama2_70b_down_proj",
-    "fetch_kib": 61316064.8, "fetch_scale": 2.0,
+    "fetch_kib": 173124868.9, "fetch_scale": 2.0,
     "write_kib": 3239936.0, "write_scale": 1.0,
 }
 
