@@ -144,8 +144,8 @@ def test_permute_mask_matches_indexing(duo):
     assert torch.equal(duo.unpack_mask(out, k).cpu(), bits[:, cp.long()])
 
 
-def _layer(duo, W, X, p_x, p_w, B, damp=0.01):
-    out = duo.prune_linear(W.to(DEV), X.to(DEV), p_x, p_w, damp=damp, block=B, act_order=True)
+def _layer(duo, W, X, p_x, p_w, B, damp=0.01, form=None):
+    out = duo.prune_linear(W.to(DEV), X.to(DEV), p_x, p_w, damp=damp, block=B, act_order=True, form=form)
     torch.cuda.synchronize()
     Wn, Xn = W.float().numpy(), X.float().numpy()
     ref = R.prune_layer(Wn, Xn, p_x, p_w, damp=damp, B=B, act_order=True)
@@ -169,12 +169,13 @@ def test_layer_act_order_tiny_linear_config(duo):
     assert (~keep).sum() == int(np.floor(c["p_w"] * c["n"] * c["k"] + 0.5))
 
 
+@pytest.mark.parametrize("form", [None, "y"])
 @pytest.mark.parametrize("n,k,m,B", [(192, 384, 1536, 128), (100, 200, 700, 64)])
-def test_layer_act_order_bf16(duo, n, k, m, B):
-    say("layer act_order bf16", n, k, m, B)
+def test_layer_act_order_bf16(duo, n, k, m, B, form):
+    say("layer act_order bf16", n, k, m, B, form)
     W, X = synth.layer_inputs(n, k, m, torch.bfloat16, torch.bfloat16, seed=n * k + 1, device="cpu", sigma=1.0,
                               outliers=3)
-    out, ref, keep = _layer(duo, W, X, 0.5, 0.5, B)
+    out, ref, keep = _layer(duo, W, X, 0.5, 0.5, B, form=form)
     # outputs come back in the original channel order: the bf16 copy matches
     # the fp32 result column by column
     assert torch.equal(out["W_lowp"].cpu(), out["W_out"].cpu().to(torch.bfloat16))

@@ -393,6 +393,29 @@ def test_prune_layer_select_forms(duo, n, k, B, p_w, form):
         assert relfro(f64(W_out), Wr) < 1e-5, relfro(f64(W_out), Wr)
 
 
+@pytest.mark.parametrize("n,k,B", [(200, 1152, 128), (75, 1000, 64)])
+def test_prune_layer_forms_scores_and_lowp(duo, n, k, B):
+    """The block scores the selection used (S = W^2 fac of the values when a
+    block starts: in the Y form after its start product) and the bf16 copy, in
+    both forms, against the oracle run forced to the GPU's mask; ragged n and
+    k (the dual lazy launch splits into two launches off the fast path)."""
+    say("prune_layer forms: scores, bf16 copy", n, k, B)
+    W, L, G, a, D, fac = _layer_terms(n, k, 3 * k, seed=n * k + 5)
+    Wf = W.float().numpy()
+    t = lambda x: torch.tensor(x, device=DEV)
+    for form in ("d", "y"):
+        W_out, lowp, mask, sc = duo.duo_prune_layer(W.to(DEV), t(L), t(G), t(a), 0.5, B, want_lowp=True,
+                                                    want_scores=True, form=form)
+        keep = duo.unpack_mask(mask, k).cpu().numpy()
+        scores = []
+        Wr, _ = R.sweep_blocked(Wf, L, D, fac, 0.5, B, mask_in=keep, scores_out=scores)
+        S_ref = np.concatenate(scores, axis=1)
+        assert relfro(f64(sc), S_ref) < 1e-5, (form, relfro(f64(sc), S_ref))
+        assert relfro(f64(W_out), Wr) < 1e-5, (form, relfro(f64(W_out), Wr))
+        assert torch.equal(lowp.cpu(), W_out.cpu().to(torch.bfloat16))
+        _attribute(Wf, L, D, fac, 0.5, B, keep)
+
+
 def test_prune_layer_forms_agree(duo):
     """The two forms on one layer: the same mask and weights within fp32
     rounding (k = 2048, 2 super-blocks of 1024)."""
