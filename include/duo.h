@@ -255,8 +255,8 @@ typedef struct {
  *               terms of each column's own block added at the block's start;
  *               two lazy products (W += (Y - E) L^T, Y += W0 U) of the same
  *               total size.  Uses the workspace's D space for Y.  Not with
- *               nm_n or q_bits (DUO_ERR_UNSUPPORTED).
- *   DUO_FORM_AUTO  Y when k >= 6144 and neither nm_n nor q_bits is set, else D.
+ *               q_bits (DUO_ERR_UNSUPPORTED).
+ *   DUO_FORM_AUTO  Y when k >= 6144 and q_bits is not set, else D.
  */
 enum { DUO_FORM_AUTO = 0, DUO_FORM_D = 1, DUO_FORM_Y = 2 };
 

@@ -290,7 +290,7 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   duo_status e = sweep_args(W, w_dtype, n, k, ldw, w_sparsity, opts, block, W_out, &o);
   if (e != DUO_OK) return e;
   if (!L || !G || !a || ldl < k || ldg < k) return DUO_ERR_INVALID_ARG;
-  const bool plain = o.nm_n == 0 && o.q_bits == 0;
+  const bool plain = o.q_bits == 0;  // the Y form takes unstructured and N:4 masks
   if (o.form == DUO_FORM_Y && !plain) return DUO_ERR_UNSUPPORTED;
   const PruneWs pw = carve_prune(nullptr, n, k, block);
   if (!ws_ok(ws, ws_bytes, pw.bytes)) return DUO_ERR_WORKSPACE;
@@ -298,9 +298,10 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   if (d != DUO_OK) return d;
   const PruneWs w = carve_prune(ws, n, k, block);
   const hipStream_t s = (hipStream_t)stream;
-  // The unstructured, unquantised sweep may run in the Y form (no D = U L^T);
-  // N:4 and quantisation read values inside a block that the Y form would
-  // have to rebuild, and keep D.  Automatic choice: the Y form saves the
+  // The unquantised sweep may run in the Y form (no D = U L^T); quantisation
+  // fixes its grids from the values of whole groups of columns inside a block,
+  // which the Y form would have to rebuild, and keeps D.  Automatic choice:
+  // the Y form saves the
   // k^3 / 3 of D but launches two more products per block (measured at
   // n = k = 4096: 0.17 ms slower per layer; k = 11008: 2 ms faster).
   const bool yform = o.form == DUO_FORM_Y || (o.form == DUO_FORM_AUTO && plain && k >= kYFormMinK);

@@ -548,10 +548,13 @@ __device__ __forceinline__ uint32_t row_bcast_u(uint32_t v) {
 // row receives the four columns' current score keys from their owner lanes
 // and derives the same keep bits: the nm_n lowest (equal keys in column
 // order) are pruned.
+// val: this lane's current value of its column in slot G (the Y form adds the
+// y terms the column is still owed inside the block, see ib_step).  Only the
+// group's own four lanes (q = O .. O + 3) record the score they used.
 template <int G, int O>
-__device__ __forceinline__ void nm_select(IbRow& s, int nm_n) {
-  const float S = weight_score(s.w[G], s.f[G]);
-  s.sc[G] = S;
+__device__ __forceinline__ void nm_select(IbRow& s, int nm_n, float val, int q) {
+  const float S = weight_score(val, s.f[G]);
+  if ((q & ~3) == O) s.sc[G] = S;
   const uint32_t key = orderable(S);
   const uint32_t k0 = row_bcast_u<O>(key), k1 = row_bcast_u<O + 1>(key);
   const uint32_t k2 = row_bcast_u<O + 2>(key), k3 = row_bcast_u<O + 3>(key);
@@ -606,7 +609,24 @@ __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* 
                                         const IbOpts& opt, int64_t row, bool rv, int j0, int Bb, int ngroups) {
   constexpr int g = J / IB_Q, o = J % IB_Q;
   ib_load<J + 2>(buf[(J + 2) % 3], lq, dq, il, q);
-  if constexpr (NM && o % 4 == 0) nm_select<g, o>(s, opt.nm_n);
+  if constexpr (NM && o % 4 == 0) {
+    if constexpr (YR) {
+      // the group's columns c = J .. J + 3 as they stand now: w_c plus
+      // L_ci y_i for i = J .. c with the current y (the y terms the column
+      // will still receive inside the block before it is processed); the L
+      // entries of steps J, J + 1, J + 2 are in the ring
+      const int pos = (q - o) & 3;  // position of this lane's column in the group
+      float val = s.w[g] + s.y[g] * il[kMaxBlock + J + pos];
+      const float y0 = row_bcast<o>(s.y[g]), y1 = row_bcast<o + 1>(s.y[g]), y2 = row_bcast<o + 2>(s.y[g]);
+      const IbBuf &b0 = buf[J % 3], &b1 = buf[(J + 1) % 3], &b2 = buf[(J + 2) % 3];
+      if (pos > 0) val = fmaf(b0.l[g] * b0.lj, y0, val);
+      if (pos > 1) val = fmaf(b1.l[g] * b1.lj, y1, val);
+      if (pos > 2) val = fmaf(b2.l[g] * b2.lj, y2, val);
+      nm_select<g, o>(s, opt.nm_n, val, q);
+    } else {
+      nm_select<g, o>(s, opt.nm_n, s.w[g], q);
+    }
+  }
   if constexpr (QUANT && o == 0) {
     // groups start inside the block only (a short last block has no more)
     if (J < Bb && J % opt.q_group == 0) quant_grid<g>(s, opt, row, rv, q, (j0 + J) / opt.q_group, ngroups);
@@ -935,7 +955,7 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
                      void* ws, hipStream_t s, const float* U, int64_t ldu, float* Y) {
   const SweepWs w = carve(ws, n, k, B);
   const bool yr = U != nullptr;  // Y form
-  if (yr && (o.nm_n > 0 || o.q_bits > 0 || !Y)) return DUO_ERR_UNSUPPORTED;
+  if (yr && (o.q_bits > 0 || !Y)) return DUO_ERR_UNSUPPORTED;
   const int64_t nk = n * k;
   const int64_t S = super_width(B);
   auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
@@ -963,7 +983,8 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   const bool qt = o.q_bits > 0;
   const bool wide = !nm && !qt && cdiv(n, IB_ROWS) > 256;  // 32 rows per workgroup
   const int ib_rows = wide ? IB_ROWS2 : IB_ROWS;
-  auto ib_kern = yr ? (wide ? inblock_kernel<false, false, true, IB_ROWS2> : inblock_kernel<false, false, true, IB_ROWS>)
+  auto ib_kern = yr ? (nm ? inblock_kernel<true, false, true, IB_ROWS>
+                          : wide ? inblock_kernel<false, false, true, IB_ROWS2> : inblock_kernel<false, false, true, IB_ROWS>)
                  : nm ? (qt ? inblock_kernel<true, true, false, IB_ROWS> : inblock_kernel<true, false, false, IB_ROWS>)
                  : qt ? inblock_kernel<false, true, false, IB_ROWS>
                       : (wide ? inblock_kernel<false, false, false, IB_ROWS2> : inblock_kernel<false, false, false, IB_ROWS>);

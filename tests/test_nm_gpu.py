@@ -87,6 +87,10 @@ def test_sweep_nm(duo, n, k, B, N):
     _groups_valid(keep, f64(scores), N)
     assert np.mean(keep == keep_r) >= 0.999
     _near_ties(Wn, L, D, fac, B, N, keep)
+    # the scores each group's selection used, against the oracle forced to the GPU's mask
+    S_ref = []
+    R.sweep_blocked(Wn, L, D, fac, 0.5, B, mask_in=keep, scores_out=S_ref, nm=(N, 4))
+    assert relfro(f64(scores), np.concatenate(S_ref, axis=1)) < 1e-5
     assert np.all(f64(W_out)[~keep] == 0.0)
     if np.array_equal(keep, keep_r):
         assert relfro(f64(W_out), Wr) < 1e-5, relfro(f64(W_out), Wr)
@@ -126,6 +130,42 @@ def test_layer_two_four(duo, n, k, m, B):
     J_g, J_r = R.objective(Wn, Wg, Xn, 0.5), R.objective(Wn, ref["W_hat"], Xn, 0.5)
     assert abs(J_g - J_r) <= 1e-3 * J_r
     assert torch.equal(out["W_lowp"].cpu(), out["W_out"].cpu().to(torch.bfloat16))
+
+
+@pytest.mark.parametrize("n,k,B,N", [(48, 2304, 128, 2), (40, 2200, 64, 1), (33, 132, 128, 3)])
+def test_prune_layer_nm_forms(duo, n, k, B, N):
+    """Stage 3 with N:4 groups in both residual forms (in the Y form a group's
+    values are rebuilt from w and y before its selection): the mask a valid
+    N-lowest choice of the GPU's own scores, those scores and W against the
+    oracle forced to the GPU's mask, every difference from the oracle's own
+    choice a near-tie; several super-blocks, ragged rows and blocks."""
+    say("prune_layer N:4 forms", n, k, B, N)
+    W, X = synth.layer_inputs(n, k, 3 * k, torch.bfloat16, torch.bfloat16, seed=n + k + 9, device="cpu", sigma=1.0,
+                              outliers=2)
+    H, G, a = R.hessian_terms(X.float().numpy(), 0.5)
+    L, _ = R.inverse_cholesky(H, 0.01)
+    fac, D, _ = R.score_terms(G, L, a)
+    L32, D32, f32, G32, a32 = (np.ascontiguousarray(x.astype(np.float32)) for x in (L, D, fac, G, a))
+    Wf = W.float().numpy()
+    t = lambda x: torch.tensor(x, device=DEV)
+    outs = {}
+    for form in ("d", "y"):
+        W_out, _, mask, sc = duo.duo_prune_layer(W.to(DEV), t(L32), t(G32), t(a32), 0.5, B, want_scores=True,
+                                                 nm_n=N, form=form)
+        keep = duo.unpack_mask(mask, k).cpu().numpy()
+        S_g = f64(sc)
+        assert np.all((~keep).reshape(n, -1, 4).sum(axis=2) == N), form
+        _groups_valid(keep, S_g, N)
+        scores = []
+        Wr, _ = R.sweep_blocked(Wf, L32, D32, f32, 0.5, B, mask_in=keep, scores_out=scores, nm=(N, 4))
+        S_ref = np.concatenate(scores, axis=1)
+        assert relfro(S_g, S_ref) < 1e-5, (form, relfro(S_g, S_ref))
+        assert relfro(f64(W_out), Wr) < 1e-5, (form, relfro(f64(W_out), Wr))
+        _near_ties(Wf, L32, D32, f32, B, N, keep)
+        outs[form] = (keep, f64(W_out))
+    assert np.mean(outs["d"][0] == outs["y"][0]) >= 0.999
+    if np.array_equal(outs["d"][0], outs["y"][0]):
+        assert relfro(outs["y"][1], outs["d"][1]) < 1e-5
 
 
 def test_nm_refuses_bad_shapes(duo):
