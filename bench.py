@@ -475,8 +475,8 @@ def main():
     sweep_ms = per_step("select") + per_step("inblock")
     sweep_gbs = sweep_bytes / (sweep_ms * 1e-3) / 1e9
     # residual form of the sweep: the library's automatic choice (DUO_FORM_AUTO)
-    # is the Y form (no D) for the unquantised sweep from k = 6144
-    yform = args.form == "y" or (args.form == "auto" and not args.quant and k >= 6144)
+    # is the Y form (no D) from k = 6144 (with quantisation: groups of the block's width)
+    yform = args.form == "y" or (args.form == "auto" and (not args.quant or B == 128) and k >= 6144)
     # lazy updates: the two terms (E L^T and W0 D, or (Y - E) L^T and W0 U) of
     # each block over the columns after it, 2 n k (k - B) flop; the Y form adds
     # the block-start products Y[:, blk] L[blk, blk]^T, 2 n B (k - B)

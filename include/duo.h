@@ -254,9 +254,10 @@ typedef struct {
  *               had when processed) beside W, since W0 D = Y L^T with the
  *               terms of each column's own block added at the block's start;
  *               two lazy products (W += (Y - E) L^T, Y += W0 U) of the same
- *               total size.  Uses the workspace's D space for Y.  Not with
- *               q_bits (DUO_ERR_UNSUPPORTED).
- *   DUO_FORM_AUTO  Y when k >= 6144 and q_bits is not set, else D.
+ *               total size.  Uses the workspace's D space for Y.  With
+ *               q_bits only if q_group == block (grids fixed at a block's
+ *               first column), else DUO_ERR_UNSUPPORTED.
+ *   DUO_FORM_AUTO  Y when k >= 6144 and the Y form applies, else D.
  */
 enum { DUO_FORM_AUTO = 0, DUO_FORM_D = 1, DUO_FORM_Y = 2 };
 

@@ -343,7 +343,7 @@ def _group_grids(Wg, bits: int, qparams_out):
     for r in range(n):
         qs[r], qz[r] = quant_grid(Wg[r], bits)
     if qparams_out is not None:
-        qparams_out.append((qs.copy(), qz.copy()))
+        qparams_out.append((qs.copy(), qz.copy(), _f64(Wg).copy()))
     return qs, qz
 
 
@@ -432,8 +432,9 @@ def _sweep(W, L, D, fac, p_w, B, lazy, mask_in, scores_out, nm, quant, qparams_o
 def sweep_eager(W, L, D, fac, p_w: float, B: int, mask_in=None, scores_out=None, nm=None, quant=None,
                 qparams_out=None, values_in=None, w0_out=None):
     """Column sweep by definition: every column's update reaches all later
-    columns at once (see _sweep).  qparams_out (a list) receives (scale,
-    zero) arrays of shape (n,) per quantisation group.  Test hooks: values_in
+    columns at once (see _sweep).  qparams_out (a list) receives, per
+    quantisation group, the (scale, zero) arrays of shape (n,) and the
+    n x group values the grids were fixed from.  Test hooks: values_in
     (n x k) replaces the value every kept weight takes (as mask_in replaces
     the mask); w0_out (n x k) receives each column's value when it was
     processed.  Returns (W_hat, keep)."""

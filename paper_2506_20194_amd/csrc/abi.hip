@@ -290,7 +290,9 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   duo_status e = sweep_args(W, w_dtype, n, k, ldw, w_sparsity, opts, block, W_out, &o);
   if (e != DUO_OK) return e;
   if (!L || !G || !a || ldl < k || ldg < k) return DUO_ERR_INVALID_ARG;
-  const bool plain = o.q_bits == 0;  // the Y form takes unstructured and N:4 masks
+  // the Y form takes unstructured and N:4 masks, and quantisation with one
+  // grid per row and block (q_group == block: grids fixed at a block's start)
+  const bool plain = o.q_bits == 0 || o.q_group == block;
   if (o.form == DUO_FORM_Y && !plain) return DUO_ERR_UNSUPPORTED;
   const PruneWs pw = carve_prune(nullptr, n, k, block);
   if (!ws_ok(ws, ws_bytes, pw.bytes)) return DUO_ERR_WORKSPACE;
@@ -298,10 +300,10 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   if (d != DUO_OK) return d;
   const PruneWs w = carve_prune(ws, n, k, block);
   const hipStream_t s = (hipStream_t)stream;
-  // The unquantised sweep may run in the Y form (no D = U L^T); quantisation
-  // fixes its grids from the values of whole groups of columns inside a block,
-  // which the Y form would have to rebuild, and keeps D.  Automatic choice:
-  // the Y form saves the
+  // The sweep may run in the Y form (no D = U L^T) unless quantisation
+  // groups start inside a block: their grids come from the values of whole
+  // groups of columns there, which the Y form would have to rebuild, so those
+  // keep D.  Automatic choice: the Y form saves the
   // k^3 / 3 of D but launches two more products per block (measured at
   // n = k = 4096: 0.17 ms slower per layer; k = 11008: 2 ms faster).
   const bool yform = o.form == DUO_FORM_Y || (o.form == DUO_FORM_AUTO && plain && k >= kYFormMinK);

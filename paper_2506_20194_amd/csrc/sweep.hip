@@ -955,7 +955,9 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
                      void* ws, hipStream_t s, const float* U, int64_t ldu, float* Y) {
   const SweepWs w = carve(ws, n, k, B);
   const bool yr = U != nullptr;  // Y form
-  if (yr && (o.q_bits > 0 || !Y)) return DUO_ERR_UNSUPPORTED;
+  // the Y form with quantisation: only grids fixed at a block's first column,
+  // where W[:, blk] holds the values of Algorithm 1 after the start product
+  if (yr && ((o.q_bits > 0 && o.q_group != B) || !Y)) return DUO_ERR_UNSUPPORTED;
   const int64_t nk = n * k;
   const int64_t S = super_width(B);
   auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
@@ -983,7 +985,8 @@ duo_status sweep_run(const void* W, int32_t w_dtype, int64_t n, int64_t k, int64
   const bool qt = o.q_bits > 0;
   const bool wide = !nm && !qt && cdiv(n, IB_ROWS) > 256;  // 32 rows per workgroup
   const int ib_rows = wide ? IB_ROWS2 : IB_ROWS;
-  auto ib_kern = yr ? (nm ? inblock_kernel<true, false, true, IB_ROWS>
+  auto ib_kern = yr ? (nm ? (qt ? inblock_kernel<true, true, true, IB_ROWS> : inblock_kernel<true, false, true, IB_ROWS>)
+                     : qt ? inblock_kernel<false, true, true, IB_ROWS>
                           : wide ? inblock_kernel<false, false, true, IB_ROWS2> : inblock_kernel<false, false, true, IB_ROWS>)
                  : nm ? (qt ? inblock_kernel<true, true, false, IB_ROWS> : inblock_kernel<true, false, false, IB_ROWS>)
                  : qt ? inblock_kernel<false, true, false, IB_ROWS>

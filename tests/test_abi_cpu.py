@@ -114,7 +114,7 @@ def test_chol_and_sweep_argument_errors(duo_lib):
         o = ctypes.byref(SweepOpts(nm, qb, qg, None, None, form)) if (nm or qb or qg or form) else None
         return fn(W, dt, n, k, ldw, FAKE, 64, FAKE, 64, FAKE, p, o, B, None, Wo, None, None, None, WS, big, None)
 
-    # residual form: 0 automatic, 1 D, 2 Y (duo_prune_layer only; not with quantisation)
+    # residual form: 0 automatic, 1 D, 2 Y (duo_prune_layer only; with quantisation only for q_group == block)
     assert sweep(form=1) == NODEV
     assert sweep(form=2) == E
     assert sweep(form=3) == E
@@ -124,7 +124,8 @@ def test_chol_and_sweep_argument_errors(duo_lib):
     assert sweep(fn=P, form=2) == NODEV
     assert sweep(fn=P, form=3) == E
     assert sweep(fn=P, form=2, nm=2) == NODEV
-    assert sweep(fn=P, form=2, qb=4, qg=16) == duo_lib.DUO_ERR_UNSUPPORTED
+    assert sweep(fn=P, form=2, qb=4, qg=16, B=32) == duo_lib.DUO_ERR_UNSUPPORTED  # groups inside a block
+    assert sweep(fn=P, form=2, qb=4, qg=16, B=16) == NODEV  # one grid per row and block
 
     for fn in (L.duo_sweep, L.duo_prune_layer):
         assert sweep(fn=fn) == NODEV

@@ -677,7 +677,7 @@ def test_quant_values_on_grids_fixed_at_group_start(bits, group):
     assert len(qp) == 64 // group
     Wh, keep = out["W_hat"], out["keep"]
     assert np.all(Wh[~keep] == 0)
-    for gi, (s, z) in enumerate(qp):
+    for gi, (s, z, _) in enumerate(qp):
         cols = slice(gi * group, (gi + 1) * group)
         codes = Wh[:, cols] / s[:, None] + z[:, None]
         assert np.allclose(codes, np.round(codes), atol=1e-9)          # on the grid
@@ -715,7 +715,7 @@ def test_quant_last_column_is_ridge_optimum_given_frozen_prefix(quant):
     x = X[:, k - 1]
     v = (r @ x + lam * W[:, k - 1]) / (x @ x + lam)
     if quant is not None:
-        sc, z = qp[-1]
+        sc, z, _ = qp[-1]
         v = sc * (np.clip(np.round(v / sc) + z, 0, 2 ** quant[0] - 1) - z)
     np.testing.assert_allclose(Wh[:, k - 1], np.where(keep, v, 0.0), rtol=0, atol=1e-12)
 
@@ -731,7 +731,7 @@ def test_forced_values_hook_reproduces_the_run():
     Wh, keep = R.sweep_blocked(W, L, D, fac, 0.5, 32, quant=(4, 16), qparams_out=qp, w0_out=w0)
     Wf, _ = R.sweep_blocked(W, L, D, fac, 0.5, 32, mask_in=keep, quant=(4, 16), values_in=Wh)
     np.testing.assert_array_equal(Wf, Wh)
-    for gi, (sc, z) in enumerate(qp):
+    for gi, (sc, z, _) in enumerate(qp):
         cols = slice(16 * gi, 16 * gi + 16)
         want = sc[:, None] * (np.clip(np.round(w0[:, cols] / sc[:, None]) + z[:, None], 0, 15) - z[:, None])
         np.testing.assert_array_equal(np.where(keep[:, cols], want, 0.0), Wh[:, cols])
