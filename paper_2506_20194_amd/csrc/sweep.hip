@@ -628,7 +628,9 @@ __device__ __forceinline__ void ib_step(IbRow& s, IbBuf (&buf)[3], const float* 
     }
   }
   if constexpr (QUANT && o == 0) {
-    // groups start inside the block only (a short last block has no more)
+    // groups start inside the block only (a short last block has no more); the
+    // Y form is run with one group per block only, fixed at J = 0 where the
+    // block's own part of y is still 0 and w holds Algorithm 1's values
     if (J < Bb && J % opt.q_group == 0) quant_grid<g>(s, opt, row, rv, q, (j0 + J) / opt.q_group, ngroups);
   }
   const IbBuf& b = buf[J % 3];
