@@ -6,11 +6,11 @@ bench.py times with --act-order, --nm 2 and --quant 4.
   (each square exact; sums in different orders: 1e-12 relative), the channel
   order bit-identical to the oracle's, and the outputs exactly the permuted
   run's outputs gathered back;
-* 2:4: exact per-group counts, each group's choice the two lowest of the
+* 2:4 (both residual forms): exact per-group counts, each group's choice the two lowest of the
   scores the kernel selected on (ties by column), sampled rows equal to the
   column recurrence of Algorithm 1 in float64 on the kernel's own L, D and
   mask (1e-3 relative);
-* INT4, groups of 128: every kept weight exactly on its reported grid;
+* INT4, groups of 128 (both residual forms): every kept weight exactly on its reported grid;
   sampled rows run through the same recurrence with the kernel's kept values
   forced, whose values at quantisation time must round to the kernel's codes
   except within 1e-3 of a step of a rounding boundary.
@@ -123,15 +123,18 @@ def test_fullsize_act_order(base):
         assert relfro(Wo[r], Wr[i]) < 1e-3, (r, relfro(Wo[r], Wr[i]))
 
 
-def test_fullsize_two_four(base):
+@pytest.mark.parametrize("form", [None, "y"])
+def test_fullsize_two_four(base, form):
+    """form None: the automatic choice (the D form at k = 4096); "y": the Y
+    form, whose group selections rebuild the values from w and y."""
     duo, c = base["duo"], base["c"]
     n, k, B = c["n"], c["k"], c["block"]
-    say("full-size 2:4")
+    say("full-size 2:4", form)
     H, G, a = _stage12(base)
     lam, fail = duo.duo_chol_inv(H, c["damp"], sync=True)
     assert fail == -1
     W_out, lowp, mask, scores = duo.duo_prune_layer(base["W"], H, G, a, c["p_w"], B, want_lowp=True,
-                                                    want_scores=True, nm_n=2)
+                                                    want_scores=True, nm_n=2, form=form)
     D, _ = duo.duo_score_terms(H, G, a)
     torch.cuda.synchronize()
     keep = duo.unpack_mask(mask, k).cpu().numpy()
@@ -153,15 +156,17 @@ def test_fullsize_two_four(base):
         assert relfro(Wo[r], Wr[i]) < 1e-3, (r, relfro(Wo[r], Wr[i]))
 
 
-def test_fullsize_int4(base):
+@pytest.mark.parametrize("form", [None, "y"])
+def test_fullsize_int4(base, form):
     duo, c = base["duo"], base["c"]
     n, k, B = c["n"], c["k"], c["block"]
     bits, group = 4, 128
-    say("full-size int4")
+    say("full-size int4", form)
     H, G, a = _stage12(base)
     lam, fail = duo.duo_chol_inv(H, c["damp"], sync=True)
     assert fail == -1
-    W_out, _, mask, _, qs, qz = duo.duo_prune_layer(base["W"], H, G, a, c["p_w"], B, quant=(bits, group))
+    W_out, _, mask, _, qs, qz = duo.duo_prune_layer(base["W"], H, G, a, c["p_w"], B, quant=(bits, group),
+                                                    form=form)
     D, _ = duo.duo_score_terms(H, G, a)
     torch.cuda.synchronize()
     keep = duo.unpack_mask(mask, k).cpu().numpy()
