@@ -292,8 +292,8 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   if (!L || !G || !a || ldl < k || ldg < k) return DUO_ERR_INVALID_ARG;
   // the Y form takes unstructured and N:4 masks, and quantisation with one
   // grid per row and block (q_group == block: grids fixed at a block's start)
-  const bool plain = o.q_bits == 0 || o.q_group == block;
-  if (o.form == DUO_FORM_Y && !plain) return DUO_ERR_UNSUPPORTED;
+  const bool y_ok = o.q_bits == 0 || o.q_group == block;
+  if (o.form == DUO_FORM_Y && !y_ok) return DUO_ERR_UNSUPPORTED;
   const PruneWs pw = carve_prune(nullptr, n, k, block);
   if (!ws_ok(ws, ws_bytes, pw.bytes)) return DUO_ERR_WORKSPACE;
   duo_status d = device_ok();
@@ -306,7 +306,7 @@ duo_status duo_prune_layer(const void* W, int32_t w_dtype, int64_t n, int64_t k,
   // keep D.  Automatic choice: the Y form saves the
   // k^3 / 3 of D but launches two more products per block (measured at
   // n = k = 4096: 0.17 ms slower per layer; k = 11008: 2 ms faster).
-  const bool yform = o.form == DUO_FORM_Y || (o.form == DUO_FORM_AUTO && plain && k >= kYFormMinK);
+  const bool yform = o.form == DUO_FORM_Y || (o.form == DUO_FORM_AUTO && y_ok && k >= kYFormMinK);
   prof_begin(DUO_PROF_SCORE, s);
   duo_status r = score_run(L, ldl, G, ldg, a, k, yform ? nullptr : w.D, k, w.fac, w.score, s);
   prof_end(DUO_PROF_SCORE, s);
