@@ -876,7 +876,7 @@ __device__ __forceinline__ void lds_barrier() {
 // 1 KB), issued NS - 1 stages ahead (NS = 5 stages of 32 KB, or 3 of 48 KB
 // for the two-stream form, fill the 160 KB of LDS).  LDS layout of one operand tile:
 // [group][256 rows][16 bytes], identical to the packed global layout.
-template <typename T, bool HAS_LO>
+template <typename T, bool HAS_LO, bool SHALLOW>
 __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
   constexpr int EPG = 16 / (int)sizeof(T);
   constexpr int NG = kTokBlk / EPG;
@@ -890,6 +890,11 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
   // fragment reads pipelined half a stage ahead: bf16, one stream (the
   // register budget of the extra fragments is not there for the two-stream form)
   constexpr bool PIPE = MfmaOp<T>::kFrags == 1 && !HAS_LO && NS >= 4;
+  // stages the pipelined form issues ahead of the one being read: NS - 1, or
+  // NS - 2 (SHALLOW; measured faster when the tokens are split into segments,
+  // slower with one long segment per tile)
+  constexpr int AHEAD = PIPE ? (SHALLOW ? NS - 2 : NS - 1) : NS - 1;
+  static_assert(!SHALLOW || PIPE, "the shallow ring is a form of the pipelined loop");
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   const int u = xcd_remap(blockIdx.x, gridDim.x);
@@ -932,7 +937,7 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
 #pragma unroll
     for (int b = 0; b < 4; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
 
-  for (int t = tb0; t < min(tb1, tb0 + NS - 1); ++t) issue(t);
+  for (int t = tb0; t < min(tb1, tb0 + AHEAD); ++t) issue(t);
   if (tb1 <= tb0) {
     // empty segment: the partial tile stays zero
   } else if constexpr (PIPE) {
@@ -958,19 +963,20 @@ __global__ __launch_bounds__(512) void gram_kernel(GramArgs<T> A) {
 #pragma unroll
         for (int b = 0; b < 4; ++b) acc[4 * h2 + a][b] = MfmaOp<T>::mma(Fa[a], Fb[b], acc[4 * h2 + a][b]);
     };
-    // stage t + 1 complete and readable by every wave; stage t + NS - 1 issued
-    // into the slot of stage t - 1, which every wave has finished reading
+    // stage t + 1 complete and readable by every wave; stage t + AHEAD issued
+    // into the slot of stage t + AHEAD - NS (t - 1 or t - 2), which every wave
+    // has finished reading
     auto advance = [&](int t) {
-      switch (min(NS - 3, tb1 - 2 - t)) {
+      switch (min(AHEAD - 2, tb1 - 2 - t)) {
         case 2: wait_vmem<2 * DPW>(); break;
         case 1: wait_vmem<DPW>(); break;
         default: wait_vmem<0>(); break;
       }
       lds_barrier();
-      if (t + NS - 1 < tb1) issue(t + NS - 1);
+      if (t + AHEAD < tb1) issue(t + AHEAD);
     };
     v4u fb[4], fa0[4];
-    switch (min(NS - 2, tb1 - 1 - tb0)) {  // stage tb0 complete
+    switch (min(AHEAD - 1, tb1 - 1 - tb0)) {  // stage tb0 complete
       case 3: wait_vmem<3 * DPW>(); break;
       case 2: wait_vmem<2 * DPW>(); break;
       case 1: wait_vmem<DPW>(); break;
@@ -1358,7 +1364,9 @@ static duo_status launch_gram(const GramArgs<T>& A, hipStream_t s) {
   const size_t stage = NOP * (size_t)GT * kTokBlk * sizeof(T);
   const size_t ns = (160 * 1024) / stage < 5 ? (160 * 1024) / stage : 5;
   const size_t lds = ns * stage;
-  auto kern = gram_kernel<T, LO>;
+  auto kern = gram_kernel<T, LO, false>;
+  if constexpr (sizeof(T) == 2 && !LO)
+    if (A.nseg > 1) kern = gram_kernel<T, LO, true>;  // tokens split into segments: shallow ring
   DUO_HIP_TRY(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   const int grid = (int)rup((int64_t)A.ntiles * A.nseg, 8);
   hipLaunchKernelGGL(kern, dim3(grid), dim3(512), lds, s, A);
